@@ -1,0 +1,400 @@
+"""Pins for the fp64 oracle: it is checked against facts that do not come from
+its own code -- closed forms, invariants, brute force on tiny inputs, exact
+integer arithmetic, and PyTorch CPU float64 library routines (the paper takes
+the PyTorch operator as the reference semantics; Evaluation, Metrics).
+
+Each pin is chosen so that a plausible mistake in the oracle (a dropped term,
+a wrong sign, a swapped index, a transposed operand, a wrong axis) fails it.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2605_30359_amd import inputs
+
+GOLDEN = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "closed_forms.json")))
+
+
+def _t(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
+
+
+# ---------------------------------------------------------------- encodings
+
+def test_decode_e4m3_all_codes_match_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = oracle.decode_e4m3(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert nan.sum() == 2  # 0x7F and 0xFF
+    assert np.array_equal(ours[~nan], ref[~nan])
+
+
+def test_decode_e4m3_closed_forms():
+    for key, code in [("e4m3_max_finite", 0x7E), ("e4m3_min_subnormal", 0x01),
+                      ("e4m3_min_normal", 0x08), ("e4m3_one", 0x38)]:
+        assert oracle.decode_e4m3(np.array([code], np.uint8))[0] == GOLDEN[key]["value"]
+    assert oracle.decode_e4m3(np.array([0xFE], np.uint8))[0] == -448.0
+    assert math.isnan(oracle.decode_e4m3(np.array([0x7F], np.uint8))[0])
+
+
+def test_decode_bf16_matches_torch():
+    bits = np.arange(0, 65536, 7, dtype=np.uint32).astype(np.uint16)
+    ours = oracle.decode_bf16(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], ref[~nan])
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([
+        rng.standard_normal(100000).astype(np.float32) * 10,
+        # exact ties: low 16 bits 0x8000 with even and odd kept lsb
+        (np.arange(1000, dtype=np.uint32) * 0x20000 + 0x3F808000).view(np.float32),
+        (np.arange(1000, dtype=np.uint32) * 0x20000 + 0x3F818000).view(np.float32),
+        np.array([0.0, -0.0, 1e-40, -1e-40, 3.0e38], np.float32),
+    ])
+    ours = inputs.f32_to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+
+
+def test_e4m3_rounding_matches_torch():
+    rng = np.random.default_rng(1)
+    x = np.concatenate([
+        rng.standard_normal(100000).astype(np.float32) * 50,
+        rng.standard_normal(10000).astype(np.float32) * 0.01,
+        # every representable value and every midpoint between neighbours
+        oracle.decode_e4m3(np.arange(0, 0x7F, dtype=np.uint8)).astype(np.float32),
+    ])
+    vals = np.sort(oracle.decode_e4m3(np.arange(0, 0x7F, dtype=np.uint8)))
+    mids = ((vals[1:] + vals[:-1]) / 2).astype(np.float32)
+    x = np.clip(np.concatenate([x, mids, -mids]), -448, 448).astype(np.float32)
+    ours = inputs.f32_to_e4m3_codes(x)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    # +-0 may differ only in the sign bit of zero
+    zero = oracle.decode_e4m3(ours) == 0
+    assert np.array_equal(ours[~zero], ref[~zero])
+    assert np.all(oracle.decode_e4m3(ref[zero]) == 0)
+
+
+def test_e4m3_quantize_scale_and_saturation():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((64, 64)).astype(np.float32)
+    q, s = inputs.quantize_e4m3(x)
+    assert s == np.float32(np.abs(x).max() / np.float32(448))
+    dec = oracle.decode_e4m3(q)
+    assert np.abs(dec).max() == 448.0
+    # relative error of a 3-bit mantissa, RNE: <= 2^-4 for normals
+    xs = x.astype(np.float64) / s
+    big = np.abs(xs) >= 2 ** -6
+    assert np.all(np.abs(dec[big] - xs[big]) <= np.abs(xs[big]) * 2 ** -4 + 1e-12)
+
+
+# -------------------------------------------------------------- contractions
+
+def _brute_gemm(a, b):
+    M, K = a.shape
+    N = b.shape[1]
+    out = [[0.0] * N for _ in range(M)]
+    for i in range(M):
+        for j in range(N):
+            s = 0.0
+            for k in range(K):
+                s += float(a[i, k]) * float(b[k, j])
+            out[i][j] = s
+    return np.array(out)
+
+
+def test_gemm_brute_force_4x4():
+    rng = np.random.default_rng(3)
+    for _ in range(5):
+        a = rng.standard_normal((4, 4))
+        b = rng.standard_normal((4, 4))
+        assert np.allclose(oracle.gemm(a, b), _brute_gemm(a, b), rtol=0, atol=1e-14)
+
+
+def test_gemm_non_square_brute_force_and_layouts():
+    rng = np.random.default_rng(4)
+    a = rng.standard_normal((3, 5))
+    b = rng.standard_normal((5, 7))
+    bf = _brute_gemm(a, b)
+    assert np.allclose(oracle.gemm(a, b, "kn"), bf, atol=1e-14)
+    assert np.allclose(oracle.gemm(a, b.T.copy(), "nk"), bf, atol=1e-14)
+    assert np.allclose(oracle.gemm(a, b, "kn", rows=[2, 0]), bf[[2, 0]], atol=1e-14)
+
+
+def test_gemm_integer_exact_vs_int64():
+    rng = np.random.default_rng(5)
+    a = rng.integers(-8, 9, size=(37, 300))
+    b = rng.integers(-8, 9, size=(300, 45))
+    ref = a.astype(np.int64) @ b.astype(np.int64)
+    assert np.array_equal(oracle.gemm(a.astype(float), b.astype(float)), ref.astype(float))
+
+
+def test_gemm_identity_and_zero():
+    rng = np.random.default_rng(6)
+    a = rng.standard_normal((9, 16))
+    assert np.array_equal(oracle.gemm(a, np.eye(16)), a)
+    assert np.array_equal(oracle.gemm(a, np.zeros((16, 5))), np.zeros((9, 5)))
+
+
+def _brute_conv(x, w):
+    nb, ci, H, W = x.shape
+    co = w.shape[0]
+    out = np.zeros((nb, co, H, W))
+    for n in range(nb):
+        for o in range(co):
+            for i in range(H):
+                for j in range(W):
+                    s = 0.0
+                    for c in range(ci):
+                        for kh in range(3):
+                            for kw in range(3):
+                                ii, jj = i + kh - 1, j + kw - 1
+                                if 0 <= ii < H and 0 <= jj < W:
+                                    s += x[n, c, ii, jj] * w[o, c, kh, kw]
+                    out[n, o, i, j] = s
+    return out
+
+
+def test_conv_brute_force_tiny():
+    rng = np.random.default_rng(7)
+    for shape in [(1, 1, 4, 4), (2, 2, 4, 4)]:
+        x = rng.standard_normal(shape)
+        w = rng.standard_normal((3, shape[1], 3, 3))
+        assert np.allclose(oracle.conv2d_3x3(x, w), _brute_conv(x, w), atol=1e-13)
+
+
+def test_conv_matches_torch_and_image_selection():
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((3, 5, 9, 6))
+    w = rng.standard_normal((7, 5, 3, 3))
+    ref = F.conv2d(_t(x), _t(w), padding=1).numpy()
+    assert np.allclose(oracle.conv2d_3x3(x, w), ref, atol=1e-12)
+    assert np.allclose(oracle.conv2d_3x3(x, w, images=[2, 0]), ref[[2, 0]], atol=1e-12)
+
+
+def test_conv_center_and_corner_taps():
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((2, 4, 6, 8))
+    w = np.zeros((4, 4, 3, 3))
+    for c in range(4):
+        w[c, c, 1, 1] = 1.0
+    assert np.array_equal(oracle.conv2d_3x3(x, w), x)
+    w = np.zeros((4, 4, 3, 3))
+    for c in range(4):
+        w[c, c, 0, 0] = 1.0   # out[oh,ow] = in[oh-1, ow-1], zero at the top/left border
+    out = oracle.conv2d_3x3(x, w)
+    assert np.array_equal(out[:, :, 1:, 1:], x[:, :, :-1, :-1])
+    assert np.all(out[:, :, 0, :] == 0) and np.all(out[:, :, :, 0] == 0)
+
+
+# ------------------------------------------------------------- epilogue ops
+
+def test_elementwise_ops_match_torch():
+    rng = np.random.default_rng(10)
+    h = rng.standard_normal((17, 33)) * 4
+    h[0, :5] = [0.0, -50.0, 50.0, -800.0, 800.0]
+    T = _t(h)
+    assert np.allclose(oracle.op_gelu_tanh(h), F.gelu(T, approximate="tanh").numpy(), rtol=1e-13, atol=1e-14)
+    assert np.allclose(oracle.op_gelu_erf(h), F.gelu(T).numpy(), rtol=1e-13, atol=1e-14)
+    assert np.allclose(oracle.op_swish(h), F.silu(T).numpy(), rtol=1e-13, atol=1e-14)
+    assert np.allclose(oracle.op_sigmoid(h), torch.sigmoid(T).numpy(), rtol=1e-13, atol=1e-14)
+    assert np.allclose(oracle.op_tanh(h), torch.tanh(T).numpy(), rtol=1e-13, atol=1e-14)
+    assert np.array_equal(oracle.op_hardtanh(h, -1, 1), F.hardtanh(T, -1.0, 1.0).numpy())
+    assert np.array_equal(oracle.op_relu(h), F.relu(T).numpy())
+    assert np.all(np.isfinite(oracle.op_swish(h)))
+
+
+def test_elementwise_closed_forms():
+    assert oracle.op_gelu_tanh(np.array([0.0]))[0] == GOLDEN["gelu_tanh_zero"]["value"]
+    assert oracle.op_swish(np.array([0.0]))[0] == GOLDEN["swish_zero"]["value"]
+    assert abs(oracle.op_sigmoid(np.array([math.log(3.0)]))[0] - GOLDEN["sigmoid_ln3"]["value"]) < 1e-15
+    # GELU tends to the identity for large positive input and to 0 for large negative
+    assert oracle.op_gelu_tanh(np.array([30.0]))[0] == 30.0
+    assert oracle.op_gelu_tanh(np.array([-30.0]))[0] == 0.0
+    # odd-part identity of the tanh form: gelu(x) - gelu(-x) = x
+    x = np.linspace(-6, 6, 101)
+    assert np.allclose(oracle.op_gelu_tanh(x) - oracle.op_gelu_tanh(-x), x, atol=1e-14)
+    assert np.allclose(oracle.op_swish(x) - oracle.op_swish(-x), x, atol=1e-14)
+
+
+def test_bias_axis():
+    h = np.zeros((2, 3))
+    assert np.array_equal(oracle.op_bias(h, [1.0, 2.0, 3.0]), [[1, 2, 3], [1, 2, 3]])
+    h4 = np.zeros((1, 2, 2, 2))
+    out = oracle.op_bias(h4, [5.0, 7.0])
+    assert np.all(out[0, 0] == 5) and np.all(out[0, 1] == 7)
+
+
+def test_groupnorm_matches_torch_2d_and_4d():
+    rng = np.random.default_rng(11)
+    h = rng.standard_normal((6, 64)) * 3 + 1
+    g = rng.uniform(0.5, 1.5, 64)
+    b = rng.uniform(-0.1, 0.1, 64)
+    ref = F.group_norm(_t(h), 4, _t(g), _t(b), eps=1e-5).numpy()
+    assert np.allclose(oracle.op_groupnorm(h, 4, 1e-5, g, b), ref, rtol=1e-12, atol=1e-12)
+    h4 = rng.standard_normal((2, 8, 3, 5))
+    g4, b4 = rng.uniform(0.5, 1.5, 8), rng.uniform(-0.1, 0.1, 8)
+    ref4 = F.group_norm(_t(h4), 2, _t(g4), _t(b4), eps=1e-5).numpy()
+    assert np.allclose(oracle.op_groupnorm(h4, 2, 1e-5, g4, b4), ref4, rtol=1e-12, atol=1e-12)
+
+
+def test_groupnorm_invariants():
+    rng = np.random.default_rng(12)
+    h = rng.standard_normal((5, 512)) * 7 - 2
+    n = oracle.op_groupnorm(h, 2, 1e-5)
+    g = n.reshape(5, 2, 256)
+    v = ((h.reshape(5, 2, 256) - h.reshape(5, 2, 256).mean(2, keepdims=True)) ** 2).mean(2)
+    assert np.allclose(g.mean(axis=2), 0, atol=1e-12)
+    assert np.allclose((g ** 2).mean(axis=2), v / (v + 1e-5), rtol=1e-12)
+    # scale invariance up to the eps effect
+    assert np.allclose(oracle.op_groupnorm(2 * h, 2, 0.0), oracle.op_groupnorm(h, 2, 0.0), atol=1e-12)
+
+
+def test_maxpool_matches_torch():
+    rng = np.random.default_rng(13)
+    h = rng.standard_normal((2, 3, 6, 8))
+    ref = F.max_pool2d(_t(h), 2).numpy()
+    assert np.array_equal(oracle.op_maxpool2x2(h), ref)
+    h = rng.standard_normal((1, 1, 5, 7))   # floor mode drops the last row/col
+    assert np.array_equal(oracle.op_maxpool2x2(h), F.max_pool2d(_t(h), 2).numpy())
+
+
+def test_row_softmax_and_logsumexp():
+    rng = np.random.default_rng(14)
+    h = rng.standard_normal((8, 100)) * 20
+    sm = oracle.op_row_softmax(h)
+    assert np.allclose(sm, torch.softmax(_t(h), dim=-1).numpy(), rtol=1e-13, atol=1e-300)
+    assert np.allclose(sm.sum(axis=-1), 1.0, atol=1e-14)
+    lse = oracle.op_row_logsumexp(h)
+    assert np.allclose(lse, torch.logsumexp(_t(h), dim=-1).numpy(), rtol=1e-14)
+    m = h.max(axis=-1)
+    assert np.all(lse >= m) and np.all(lse <= m + math.log(100) + 1e-12)
+    # lse of a constant row is c + ln N
+    assert abs(oracle.op_row_logsumexp(np.zeros((1, 4096)))[0] - GOLDEN["lse_zero_row_4096"]["value"]) < 1e-14
+    assert np.all(oracle.op_row_softmax(np.full((2, 8192), 3.5)) == GOLDEN["softmax_uniform_8192"]["value"])
+
+
+# -------------------------------------------------------------------- chains
+
+def _small(name, **kw):
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=123)
+    return cfg, t
+
+
+def test_chain_c1_zero_and_identity_weights():
+    cfg, t = _small("C1", M=7, N=300, K=256)
+    ch = inputs.chain(cfg)
+    t["b"] = np.zeros_like(t["b"])
+    out = oracle.run_chain(ch, t)
+    assert np.array_equal(out, np.tile(np.maximum(t["bias"].astype(float), 0), (7, 1)))
+    t["b"] = np.eye(256, 300, dtype=np.float32)
+    out = oracle.run_chain(ch, t)
+    x = t["a"].astype(float)
+    bb = t["bias"].astype(float)
+    assert np.allclose(out[:, :256], np.maximum(x + bb[:256], 0), atol=1e-15)
+    assert np.array_equal(out[:, 256:], np.tile(np.maximum(bb[256:], 0), (7, 1)))
+
+
+def test_chain_c1_matches_torch():
+    cfg, t = _small("C1")
+    out = oracle.run_chain(inputs.chain(cfg), t)
+    ref = F.relu(_t(t["a"]) @ _t(t["b"]) + _t(t["bias"])).numpy()
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_chain_c2_closed_forms_and_torch():
+    cfg, t = _small("C2", M=5, N=4096, K=64)
+    ch = inputs.chain(cfg)
+    z = dict(t, b=np.zeros_like(t["b"]), bias=np.zeros_like(t["bias"]))
+    out = oracle.run_chain(ch, z)
+    assert np.allclose(out, GOLDEN["lse_zero_row_4096"]["value"], rtol=0, atol=1e-13)
+    z = dict(t, b=np.zeros_like(t["b"]))
+    out = oracle.run_chain(ch, z)
+    bb = _t(t["bias"])
+    expect = torch.logsumexp(0.5 * F.gelu(bb, approximate="tanh"), 0).item()
+    assert np.allclose(out, expect, rtol=1e-13)
+    out = oracle.run_chain(ch, t)
+    x = _t(oracle.decode_bf16(t["a"]))
+    w = _t(oracle.decode_bf16(t["b"]))
+    ref = torch.logsumexp(0.5 * F.gelu(x @ w + bb, approximate="tanh"), dim=-1).numpy()
+    assert np.allclose(out, ref, rtol=1e-12)
+
+
+def test_chain_c3_zero_weight_and_torch():
+    cfg, t = _small("C3", M=6, N=512, K=96, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
+    ch = inputs.chain(cfg)
+    z = dict(t, b=np.zeros_like(t["b"]))
+    out = oracle.run_chain(ch, z)
+    beta = _t(t["beta"])
+    r = oracle.decode_bf16(t["residual"])
+    assert np.allclose(out, F.silu(beta).numpy()[None, :] + r, rtol=0, atol=1e-15)
+    out = oracle.run_chain(ch, t)
+    x = _t(oracle.decode_bf16(t["a"]))
+    w = _t(oracle.decode_bf16(t["b"]))
+    ref = F.silu(F.group_norm(x @ w, 2, _t(t["gamma"]), beta, eps=1e-5)) + _t(r)
+    assert np.allclose(out, ref.numpy(), rtol=1e-12, atol=1e-12)
+    rows = [5, 1]
+    assert np.allclose(oracle.run_chain(ch, t, rows=rows), ref.numpy()[rows], rtol=1e-12, atol=1e-12)
+
+
+def test_chain_c4_zero_weight_centre_tap_and_torch():
+    cfg, t = _small("C4", batch=2, cin=4, H=6, W=8, cout=6)
+    ch = inputs.chain(cfg)
+    z = dict(t, b=np.zeros_like(t["b"]))
+    out = oracle.run_chain(ch, z)
+    assert out.shape == (2, 6, 3, 4)
+    assert np.array_equal(out, np.broadcast_to(np.maximum(t["bias"].astype(float), 0)[None, :, None, None], out.shape))
+    w = np.zeros((6, 4, 3, 3), np.float32)
+    for c in range(4):
+        w[c, c, 1, 1] = 1.0
+    out = oracle.run_chain(ch, dict(t, b=inputs.f32_to_bf16_bits(w)))
+    x = oracle.decode_bf16(t["a"])
+    bb = t["bias"].astype(float)
+    exp_lo = oracle.op_maxpool2x2(np.maximum(x + bb[None, :4, None, None], 0))
+    assert np.array_equal(out[:, :4], exp_lo)
+    assert np.array_equal(out[:, 4:], np.broadcast_to(np.maximum(bb[4:], 0)[None, :, None, None], out[:, 4:].shape))
+    out = oracle.run_chain(ch, t)
+    ref = F.max_pool2d(F.relu(F.conv2d(_t(x), _t(oracle.decode_bf16(t["b"])), _t(bb), padding=1)), 2)
+    assert np.allclose(out, ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_pool_first_reorder_is_exact():
+    """max-pool commutes with +bias and ReLU (both monotone), the reorder the
+    conv kernel relies on; checked on values rounded like the GPU's fp32."""
+    rng = np.random.default_rng(15)
+    p = rng.standard_normal((2, 5, 8, 8)).astype(np.float32)
+    b = rng.uniform(-0.1, 0.1, 5).astype(np.float32)
+    lhs = oracle.op_maxpool2x2(np.maximum(p + b[None, :, None, None], 0).astype(np.float32))
+    pooled = oracle.op_maxpool2x2(p.astype(np.float64)).astype(np.float32)
+    rhs = np.maximum(pooled + b[None, :, None, None], 0).astype(np.float32)
+    assert np.array_equal(lhs, rhs)
+
+
+def test_chain_c5_uniform_rows_sum_and_torch():
+    cfg, t = _small("C5", M=4, N=8192, K=64)
+    ch = inputs.chain_for(cfg, t)
+    z = dict(t, b=np.zeros_like(t["b"]), bias=np.zeros_like(t["bias"]))
+    out = oracle.run_chain(ch, z)
+    assert np.all(out == GOLDEN["softmax_uniform_8192"]["value"])
+    out = oracle.run_chain(ch, t)
+    assert np.allclose(out.sum(axis=-1), 1.0, atol=1e-12)
+    x = _t(oracle.decode_e4m3(t["a"]) * np.float32(t["scale_a"]))
+    w = _t(oracle.decode_e4m3(t["b"]) * np.float32(t["scale_b"]))
+    ref = torch.softmax(F.hardtanh(x @ w + _t(t["bias"])), dim=-1).numpy()
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-18)
+    # saturated rows (all logits >= 1 after the clamp) are uniform
+    big = dict(t, bias=np.full_like(t["bias"], 1e6))
+    assert np.allclose(oracle.run_chain(ch, big), 1.0 / 8192, rtol=1e-14)
