@@ -1,0 +1,182 @@
+/*
+ * kf.h -- C ABI of libkf.so: fused contraction + epilogue chains on AMD
+ * MI355X (gfx950).
+ *
+ * An operation is a dense contraction followed by an ordered list of
+ * epilogue ops, executed as one kernel (plus, for row-wise softmax and
+ * logsumexp over more columns than one tile holds, a short finishing
+ * kernel).  This is the computation the paper's search turns into single
+ * kernels: a PyTorch operator given as a reference computation (Methodology,
+ * Overview) rewritten by operator fusion -- matmul + activation,
+ * normalisation + activation, softmax -- and by reduced precision and online
+ * softmax (Appendix A, allowed optimisation strategies).  The op descriptor
+ * mirrors that problem statement: the reference module's contraction, its
+ * parameters in module order, and its forward's op sequence.
+ *
+ * Conventions
+ *   - All tensors are device memory (hipMalloc'd or torch-allocated) owned
+ *     by the caller; the library never frees or reallocates them.
+ *   - Strides are in elements.  The innermost stride must be 1 and every
+ *     base pointer 16-byte aligned (the kernels use 128-bit loads).
+ *   - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *     Calls are asynchronous: launch errors are returned, device faults
+ *     surface at the caller's next synchronisation on that stream.
+ *   - No function aborts or throws; every failure returns a kf_status and
+ *     kf_last_error() (thread-local) describes it.
+ *   - Accumulation is always fp32.
+ *   - Nothing in the measured path calls rocBLAS, hipBLASLt, MIOpen or a
+ *     PyTorch op: every step runs in this library's own kernels.
+ */
+#ifndef KF_H_
+#define KF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kf_status {
+  KF_OK = 0,
+  KF_ERR_INVALID_ARG = 1,  /* NULL pointer, bad enum value, bad count        */
+  KF_ERR_SHAPE = 2,        /* tensor shape/dtype/stride disagrees with spec  */
+  KF_ERR_UNSUPPORTED = 3,  /* well-formed but not implemented (e.g. a row op
+                              not last, misaligned pointer, K % 8 != 0)      */
+  KF_ERR_NO_DEVICE = 4,    /* no usable gfx950 device                        */
+  KF_ERR_OOM = 5,          /* workspace allocation failed                    */
+  KF_ERR_HIP = 6           /* a HIP runtime call failed                      */
+} kf_status;
+
+typedef enum kf_contraction {
+  /* h[m][n] = sum_k A[m][k] * B(k, n); A is [M,K] row-major, B is [K,N]
+     (KF_LAYOUT_KN) or [N,K] (KF_LAYOUT_NK, nn.Linear's weight layout). */
+  KF_GEMM = 0,
+  /* PyTorch Conv2d (cross-correlation), 3x3 kernel, stride 1, zero padding
+     1, dilation 1, groups 1.  A = input [batch,cin,H,W] (NCHW), B = weight
+     [cout,cin,3,3] (OIHW); h is [batch,cout,H,W]. */
+  KF_CONV2D_3X3 = 1
+} kf_contraction;
+
+typedef enum kf_dtype {
+  KF_F32 = 0,
+  KF_BF16 = 1,
+  KF_FP8_E4M3 = 2  /* OCP E4M3 (bias 7, max 448, no Inf); GEMM only, with
+                      per-tensor fp32 scales: A_real = dec(A) * scale_a. */
+} kf_dtype;
+
+typedef enum kf_layout { KF_LAYOUT_KN = 0, KF_LAYOUT_NK = 1 } kf_layout;
+
+/* Epilogue ops, applied in list order to the fp32 contraction result.
+   "feature" means the GEMM output column n, or the conv output channel. */
+typedef enum kf_op_kind {
+  KF_OP_BIAS = 1,          /* h += bias[feature]          (input fp32 [F])  */
+  KF_OP_RELU = 2,          /* max(h, 0)                                     */
+  KF_OP_GELU_TANH = 3,     /* 0.5 h (1 + tanh(sqrt(2/pi)(h + 0.044715 h^3))) */
+  KF_OP_GELU_ERF = 4,      /* 0.5 h (1 + erf(h / sqrt 2))                    */
+  KF_OP_SWISH = 5,         /* h * sigmoid(h)                                */
+  KF_OP_SIGMOID = 6,       /* 1 / (1 + e^-h)                                */
+  KF_OP_TANH = 7,          /* tanh(h)                                       */
+  KF_OP_HARDTANH = 8,      /* clamp(h, p0, p1)                              */
+  KF_OP_SCALE = 9,         /* h * p0                                        */
+  KF_OP_GROUPNORM = 10,    /* nn.GroupNorm over features: `groups` groups of
+                              contiguous features per row, biased variance,
+                              eps = p0, then gamma/beta affine
+                              (inputs fp32 [F] each). GEMM only.           */
+  KF_OP_RESIDUAL_ADD = 11, /* h += residual (input, same shape as output;
+                              dtype = spec.residual_dtype)                  */
+  KF_OP_MAXPOOL2X2 = 12,   /* MaxPool2d(2, stride 2) on the conv output;
+                              CONV2D only, H and W even. Output shape
+                              [batch,cout,H/2,W/2].                         */
+  KF_OP_ROW_SOFTMAX = 13,  /* softmax over the last axis; GEMM only; last op */
+  KF_OP_ROW_LOGSUMEXP = 14 /* log sum exp over the last axis; GEMM only; last
+                              op; output becomes fp32 [M]                   */
+} kf_op_kind;
+
+typedef struct kf_op {
+  int32_t kind;    /* kf_op_kind                                            */
+  int32_t groups;  /* GROUPNORM: number of groups                           */
+  float p0;        /* HARDTANH lo, SCALE factor, GROUPNORM eps              */
+  float p1;        /* HARDTANH hi                                           */
+} kf_op;
+
+#define KF_MAX_OPS 8
+
+typedef struct kf_op_spec {
+  int32_t contraction;     /* kf_contraction                                */
+  int32_t in_dtype;        /* kf_dtype of A and B                           */
+  int32_t out_dtype;       /* KF_F32 or KF_BF16 (ROW_LOGSUMEXP: KF_F32)      */
+  int32_t b_layout;        /* kf_layout (GEMM)                              */
+  int64_t M, N, K;         /* GEMM sizes                                    */
+  int64_t batch, cin, height, width, cout; /* CONV2D_3X3 sizes              */
+  float scale_a, scale_b;  /* FP8_E4M3 per-tensor dequantisation scales     */
+  int32_t residual_dtype;  /* KF_F32 or KF_BF16, for RESIDUAL_ADD           */
+  int32_t n_ops;           /* 0..KF_MAX_OPS                                 */
+  kf_op ops[KF_MAX_OPS];
+} kf_op_spec;
+
+typedef struct kf_tensor {
+  void* data;              /* device pointer, 16-byte aligned               */
+  int32_t dtype;           /* kf_dtype                                      */
+  int32_t ndim;            /* 1..4                                          */
+  int64_t shape[4];
+  int64_t stride[4];       /* elements; stride[ndim-1] must be 1            */
+} kf_tensor;
+
+typedef struct kf_desc kf_desc;
+
+/* Validate `spec` and plan the operation: kernel variant, tile shape and a
+   device workspace for cross-tile row partials (owned by the descriptor).
+   Validation happens on the host before any device call, so spec errors are
+   reported (KF_ERR_INVALID_ARG / _SHAPE / _UNSUPPORTED) even with no GPU
+   present; a valid spec with no gfx950 device returns KF_ERR_NO_DEVICE.
+   On any error *out is set to NULL. */
+kf_status kf_create(const kf_op_spec* spec, kf_desc** out);
+
+/* Run the fused operation on `stream`.
+   inputs (in this order): A, B, then one slot per tensor the ops need, in op
+   order -- BIAS: bias; GROUPNORM: gamma, beta; RESIDUAL_ADD: residual.
+   outputs: exactly one tensor (shape from kf_output_shape, dtype
+   spec.out_dtype).  The descriptor's workspace is reused by every call, so
+   at most one call per descriptor may be in flight at a time (use one
+   descriptor per stream). */
+kf_status kf_fused_op(const kf_desc* desc, const kf_tensor* inputs,
+                      kf_tensor* outputs, void* stream);
+
+/* The same operation as an unfused chain, one kernel per op, with every
+   intermediate stored to device memory in bf16 (fp32 for fp32 chains) --
+   the comparator for the fused kernel.  Its intermediate buffers are
+   allocated on the first call and owned by the descriptor. */
+kf_status kf_unfused_op(const kf_desc* desc, const kf_tensor* inputs,
+                        kf_tensor* outputs, void* stream);
+
+/* Free the workspace and the descriptor.  NULL is a no-op.  The caller must
+   make sure no call using `desc` is still running. */
+void kf_destroy(kf_desc* desc);
+
+/* Number of input slots the operation expects. */
+int32_t kf_num_inputs(const kf_desc* desc);
+
+/* Expected dtype / shape of input slot `slot`, and of the single output. */
+kf_status kf_input_info(const kf_desc* desc, int32_t slot, int32_t* dtype,
+                        int32_t* ndim, int64_t shape[4]);
+kf_status kf_output_info(const kf_desc* desc, int32_t* dtype, int32_t* ndim,
+                         int64_t shape[4]);
+
+/* Bytes of device workspace the descriptor owns (fused path). */
+size_t kf_workspace_bytes(const kf_desc* desc);
+
+/* Name of the main (contraction) kernel the plan launches. */
+const char* kf_kernel_name(const kf_desc* desc);
+
+/* Static description of a status code. */
+const char* kf_status_string(kf_status status);
+
+/* Thread-local message for the last failing call on this thread ("" if none). */
+const char* kf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KF_H_ */

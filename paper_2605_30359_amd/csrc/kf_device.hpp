@@ -1,0 +1,179 @@
+// Device-side building blocks shared by the kf kernels (gfx950 only).
+//
+// - raw buffer resources: 128-bit loads/stores whose out-of-range lanes read
+//   zero / are dropped by the hardware, which is how every kernel handles
+//   ragged M, N and K tails without branches;
+// - the epilogue op vocabulary and its fp32 math, written from the
+//   definitions on the hardware exp2 / rcp instructions;
+// - bf16 packing with round-to-nearest-even.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "kf_internal.hpp"
+
+namespace kf {
+
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(8))) uint32_t u32x8;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(8))) int i32x8;
+
+// ---------------------------------------------------------------- buffers
+
+// Word 3 of a gfx9 buffer descriptor for raw (untyped, stride 0) access.
+constexpr int kBufferWord3 = 0x00020000;
+// Any voffset at or above this is outside every descriptor we build
+// (num_records is always < 2^31), so the access reads 0 / is dropped.
+constexpr uint32_t kOOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferWord3);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+__device__ __forceinline__ u32x2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ void buf_store16(u32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 0);
+}
+__device__ __forceinline__ void buf_store8(u32x2 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+}
+__device__ __forceinline__ void buf_store4(uint32_t v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+}
+
+// ------------------------------------------------------------------- bf16
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (inputs here are never NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
+}
+
+// --------------------------------------------------------------- epilogue math
+//
+// exp(x) = 2^(x log2 e) on v_exp_f32; 1/x on v_rcp_f32.  Each composite below
+// is an identity of the function it computes, arranged so that no
+// intermediate overflows to a NaN (large |x| gives +inf in a denominator,
+// whose reciprocal is 0).
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+__device__ __forceinline__ float frcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// sigmoid(x) = 1 / (1 + e^-x)
+__device__ __forceinline__ float f_sigmoid(float x) { return frcp(1.0f + fexp(-x)); }
+// swish(x) = x * sigmoid(x)
+__device__ __forceinline__ float f_swish(float x) { return x * f_sigmoid(x); }
+// tanh(x) = 2 sigmoid(2x) - 1
+__device__ __forceinline__ float f_tanh(float x) { return 2.0f * f_sigmoid(2.0f * x) - 1.0f; }
+// 0.5 x (1 + tanh(u)) = x sigmoid(2u), u = sqrt(2/pi) (x + 0.044715 x^3)
+__device__ __forceinline__ float f_gelu_tanh(float x) {
+  constexpr float c2 = 2.0f * 0.7978845608028654f;  // 2 sqrt(2/pi)
+  const float u2 = c2 * x * fmaf(0.044715f * x, x, 1.0f);
+  return x * f_sigmoid(u2);
+}
+// exact GELU via the device library's erff
+__device__ __forceinline__ float f_gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.7071067811865476f)); }
+
+// One element-wise op (kinds that need no tensor and no reduction).
+__device__ __forceinline__ float apply_elementwise(int kind, float p0, float p1, float x) {
+  switch (kind) {
+    case KF_OP_RELU: return fmaxf(x, 0.0f);
+    case KF_OP_GELU_TANH: return f_gelu_tanh(x);
+    case KF_OP_GELU_ERF: return f_gelu_erf(x);
+    case KF_OP_SWISH: return f_swish(x);
+    case KF_OP_SIGMOID: return f_sigmoid(x);
+    case KF_OP_TANH: return f_tanh(x);
+    case KF_OP_HARDTANH: return fminf(fmaxf(x, p0), p1);
+    case KF_OP_SCALE: return x * p0;
+    default: return x;
+  }
+}
+
+// Apply one element-wise op to a whole register array: the switch is taken
+// once per op (the op kind is uniform across the workgroup) and the loop over
+// the registers is fully unrolled inside each case.
+template <int N>
+__device__ __forceinline__ void apply_elementwise_array(int kind, float p0, float p1, float (&v)[N]) {
+  switch (kind) {
+    case KF_OP_RELU:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], 0.0f);
+      break;
+    case KF_OP_GELU_TANH:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = f_gelu_tanh(v[i]);
+      break;
+    case KF_OP_GELU_ERF:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = f_gelu_erf(v[i]);
+      break;
+    case KF_OP_SWISH:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = f_swish(v[i]);
+      break;
+    case KF_OP_SIGMOID:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = f_sigmoid(v[i]);
+      break;
+    case KF_OP_TANH:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = f_tanh(v[i]);
+      break;
+    case KF_OP_HARDTANH:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = fminf(fmaxf(v[i], p0), p1);
+      break;
+    case KF_OP_SCALE:
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = v[i] * p0;
+      break;
+    default:
+      break;
+  }
+}
+
+__device__ __forceinline__ bool is_elementwise(int kind) {
+  return kind == KF_OP_RELU || kind == KF_OP_GELU_TANH || kind == KF_OP_GELU_ERF ||
+         kind == KF_OP_SWISH || kind == KF_OP_SIGMOID || kind == KF_OP_TANH ||
+         kind == KF_OP_HARDTANH || kind == KF_OP_SCALE;
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
+// register arrays indexed by I never fall back to scratch memory.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// ---------------------------------------------------------- cross-lane ops
+
+__device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
+
+}  // namespace kf

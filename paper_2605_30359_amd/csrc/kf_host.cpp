@@ -1,0 +1,403 @@
+// libkf.so host side: the C ABI declared in include/kf.h.
+//
+// kf_create validates an op descriptor on the host (no device call), then
+// checks for a gfx950 device and allocates the descriptor's workspace.
+// kf_fused_op checks the caller's tensors against the plan and enqueues the
+// kernels on the caller's stream.  Nothing here throws or aborts across the
+// ABI; every failure is a status code plus a thread-local message.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kf.h"
+#include "kf_internal.hpp"
+#include "kf_launch.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kf_status fail(kf_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+kf_status ok() {
+  g_last_error.clear();
+  return KF_OK;
+}
+
+enum Variant { kVarGemmF32 = 0, kVarGemmBf16 = 1, kVarGemmFp8 = 2, kVarConvBf16 = 3 };
+
+struct Slot {
+  int32_t dtype;
+  int32_t ndim;
+  int64_t shape[4];
+  const char* name;
+};
+
+int64_t elem_size(int32_t dt) { return dt == KF_F32 ? 4 : dt == KF_BF16 ? 2 : 1; }
+
+bool is_elementwise_kind(int k) {
+  return k == KF_OP_RELU || k == KF_OP_GELU_TANH || k == KF_OP_GELU_ERF || k == KF_OP_SWISH ||
+         k == KF_OP_SIGMOID || k == KF_OP_TANH || k == KF_OP_HARDTANH || k == KF_OP_SCALE;
+}
+
+}  // namespace
+
+struct kf_desc {
+  kf_op_spec spec;
+  Variant variant;
+  kf::EpiProgram prog;
+  int epi_shape;
+  int red_index;
+  int gn_group;
+  int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / 0
+  std::vector<Slot> inputs;
+  Slot output;
+  int device;
+  void* workspace;
+  size_t workspace_bytes;
+  int tiles_n;
+  std::string kernel_name;
+};
+
+namespace {
+
+kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
+  if (!s) return fail(KF_ERR_INVALID_ARG, "spec is NULL");
+  if (s->contraction != KF_GEMM && s->contraction != KF_CONV2D_3X3)
+    return fail(KF_ERR_INVALID_ARG, "unknown contraction %d", s->contraction);
+  if (s->in_dtype != KF_F32 && s->in_dtype != KF_BF16 && s->in_dtype != KF_FP8_E4M3)
+    return fail(KF_ERR_INVALID_ARG, "unknown in_dtype %d", s->in_dtype);
+  if (s->out_dtype != KF_F32 && s->out_dtype != KF_BF16)
+    return fail(KF_ERR_INVALID_ARG, "out_dtype must be KF_F32 or KF_BF16 (got %d)", s->out_dtype);
+  if (s->n_ops < 0 || s->n_ops > KF_MAX_OPS)
+    return fail(KF_ERR_INVALID_ARG, "n_ops must be in [0, %d] (got %d)", KF_MAX_OPS, s->n_ops);
+
+  memset(&d->prog, 0, sizeof(d->prog));
+  d->prog.n = s->n_ops;
+  d->red_index = s->n_ops;
+  d->epi_shape = kf::kEpiPlain;
+  d->gn_group = 0;
+  d->row_kind = 0;
+  int n_red = 0, n_pool = 0;
+  bool has_bias = false, has_gn = false, has_res = false;
+  for (int i = 0; i < s->n_ops; ++i) {
+    const kf_op& op = s->ops[i];
+    if (op.kind < KF_OP_BIAS || op.kind > KF_OP_ROW_LOGSUMEXP)
+      return fail(KF_ERR_INVALID_ARG, "op %d: unknown kind %d", i, op.kind);
+    d->prog.op[i] = kf::EpiOp{op.kind, op.groups, op.p0, op.p1};
+    switch (op.kind) {
+      case KF_OP_BIAS:
+        if (has_bias) return fail(KF_ERR_UNSUPPORTED, "op %d: at most one BIAS op", i);
+        has_bias = true;
+        break;
+      case KF_OP_HARDTANH:
+        if (!(op.p0 <= op.p1)) return fail(KF_ERR_INVALID_ARG, "op %d: HARDTANH needs lo <= hi", i);
+        break;
+      case KF_OP_GROUPNORM:
+        if (has_gn) return fail(KF_ERR_UNSUPPORTED, "op %d: at most one GROUPNORM op", i);
+        has_gn = true;
+        if (op.groups < 1) return fail(KF_ERR_INVALID_ARG, "op %d: GROUPNORM groups must be >= 1", i);
+        if (!(op.p0 >= 0.0f) || !std::isfinite(op.p0))
+          return fail(KF_ERR_INVALID_ARG, "op %d: GROUPNORM eps must be finite and >= 0", i);
+        ++n_red;
+        d->red_index = i;
+        d->epi_shape = kf::kEpiGroupNorm;
+        break;
+      case KF_OP_RESIDUAL_ADD:
+        if (has_res) return fail(KF_ERR_UNSUPPORTED, "op %d: at most one RESIDUAL_ADD op", i);
+        has_res = true;
+        if (s->residual_dtype != KF_F32 && s->residual_dtype != KF_BF16)
+          return fail(KF_ERR_INVALID_ARG, "residual_dtype must be KF_F32 or KF_BF16");
+        break;
+      case KF_OP_MAXPOOL2X2:
+        ++n_pool;
+        if (s->contraction != KF_CONV2D_3X3) return fail(KF_ERR_UNSUPPORTED, "op %d: MAXPOOL2X2 needs CONV2D_3X3", i);
+        break;
+      case KF_OP_ROW_SOFTMAX:
+      case KF_OP_ROW_LOGSUMEXP:
+        if (i != s->n_ops - 1) return fail(KF_ERR_UNSUPPORTED, "op %d: a row softmax/logsumexp must be the last op", i);
+        if (s->contraction != KF_GEMM) return fail(KF_ERR_UNSUPPORTED, "op %d: row ops need a GEMM", i);
+        ++n_red;
+        d->red_index = i;
+        d->epi_shape = kf::kEpiRow;
+        d->row_kind = op.kind;
+        break;
+      default:
+        break;
+    }
+  }
+  if (n_red > 1) return fail(KF_ERR_UNSUPPORTED, "at most one reduction op (GROUPNORM / ROW_*) per chain");
+  if (n_pool > 1) return fail(KF_ERR_UNSUPPORTED, "at most one MAXPOOL2X2 op");
+  if (d->row_kind == KF_OP_ROW_LOGSUMEXP && s->out_dtype != KF_F32)
+    return fail(KF_ERR_UNSUPPORTED, "ROW_LOGSUMEXP output must be KF_F32");
+
+  const int32_t dt = s->in_dtype;
+  d->inputs.clear();
+  if (s->contraction == KF_GEMM) {
+    if (s->M < 0 || s->N < 1 || s->K < 0) return fail(KF_ERR_SHAPE, "GEMM needs M >= 0, N >= 1, K >= 0");
+    if (s->M > INT32_MAX || s->N > INT32_MAX || s->K > INT32_MAX) return fail(KF_ERR_UNSUPPORTED, "GEMM sizes must be < 2^31");
+    if (s->b_layout != KF_LAYOUT_KN && s->b_layout != KF_LAYOUT_NK) return fail(KF_ERR_INVALID_ARG, "unknown b_layout %d", s->b_layout);
+    const bool nk = s->b_layout == KF_LAYOUT_NK;
+    d->inputs.push_back(Slot{dt, 2, {s->M, s->K, 0, 0}, "A"});
+    d->inputs.push_back(Slot{dt, 2, {nk ? s->N : s->K, nk ? s->K : s->N, 0, 0}, "B"});
+    if (dt == KF_F32) {
+      d->variant = kVarGemmF32;
+      if (d->epi_shape != kf::kEpiPlain)
+        return fail(KF_ERR_UNSUPPORTED, "fp32 GEMM supports element-wise, BIAS and RESIDUAL_ADD ops only");
+      d->kernel_name = "kf_gemm_f32_32x64";
+    } else if (dt == KF_BF16) {
+      d->variant = kVarGemmBf16;
+      if (s->K % 8) return fail(KF_ERR_UNSUPPORTED, "bf16 GEMM needs K %% 8 == 0 (16-byte rows)");
+      if (s->N % 8) return fail(KF_ERR_UNSUPPORTED, "bf16 GEMM needs N %% 8 == 0 (16-byte rows)");
+      d->kernel_name = "kf_gemm_bf16_256x256";
+    } else {
+      return fail(KF_ERR_UNSUPPORTED, "fp8 GEMM is not available in this build");
+    }
+    if (has_gn) {
+      const kf_op& g = s->ops[d->red_index];
+      if (s->N % g.groups) return fail(KF_ERR_SHAPE, "GROUPNORM: N=%lld not divisible by groups=%d", (long long)s->N, g.groups);
+      d->gn_group = (int)(s->N / g.groups);
+      if (d->gn_group != 128 && d->gn_group != 256)
+        return fail(KF_ERR_UNSUPPORTED, "GROUPNORM: fused group width must be 128 or 256 columns (got %d)", d->gn_group);
+    }
+    for (int i = 0; i < s->n_ops; ++i) {
+      const int k = s->ops[i].kind;
+      if (k == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "bias"});
+      if (k == KF_OP_GROUPNORM) {
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "gamma"});
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "beta"});
+      }
+      if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0}, "residual"});
+    }
+    if (d->row_kind == KF_OP_ROW_LOGSUMEXP)
+      d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0}, "out"};
+    else
+      d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0}, "out"};
+    if (d->row_kind) {
+      d->tiles_n = (int)((s->N + kf::gemm_bf16_tile_n() - 1) / kf::gemm_bf16_tile_n());
+      if (d->tiles_n > kf::row_finish_max_tiles())
+        return fail(KF_ERR_UNSUPPORTED, "row softmax/logsumexp supports N <= %d", kf::row_finish_max_tiles() * kf::gemm_bf16_tile_n());
+    }
+  } else {
+    return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 is not available in this build");
+  }
+  return KF_OK;
+}
+
+kf_status check_tensor(const kf_tensor* t, const Slot& s, bool is_output, bool vec16) {
+  const char* what = is_output ? "output" : "input";
+  if (t->dtype != s.dtype) return fail(KF_ERR_SHAPE, "%s '%s': dtype %d, expected %d", what, s.name, t->dtype, s.dtype);
+  if (t->ndim != s.ndim) return fail(KF_ERR_SHAPE, "%s '%s': ndim %d, expected %d", what, s.name, t->ndim, s.ndim);
+  int64_t numel = 1;
+  for (int i = 0; i < s.ndim; ++i) {
+    if (t->shape[i] != s.shape[i])
+      return fail(KF_ERR_SHAPE, "%s '%s': shape[%d] = %lld, expected %lld", what, s.name, i, (long long)t->shape[i], (long long)s.shape[i]);
+    numel *= s.shape[i];
+  }
+  if (numel == 0) return KF_OK;  // never dereferenced
+  if (!t->data) return fail(KF_ERR_INVALID_ARG, "%s '%s': data is NULL", what, s.name);
+  if (t->stride[s.ndim - 1] != 1) return fail(KF_ERR_UNSUPPORTED, "%s '%s': innermost stride must be 1", what, s.name);
+  const int64_t es = elem_size(s.dtype);
+  const int64_t align = vec16 ? 16 : es;
+  if (reinterpret_cast<uintptr_t>(t->data) % align)
+    return fail(KF_ERR_UNSUPPORTED, "%s '%s': data must be %lld-byte aligned", what, s.name, (long long)align);
+  if (s.ndim == 2) {
+    if (t->stride[0] < s.shape[1]) return fail(KF_ERR_SHAPE, "%s '%s': row stride %lld < row length %lld", what, s.name, (long long)t->stride[0], (long long)s.shape[1]);
+    if (vec16 && (t->stride[0] * es) % 16)
+      return fail(KF_ERR_UNSUPPORTED, "%s '%s': row stride must be a multiple of 16 bytes", what, s.name);
+  } else if (s.ndim == 4) {
+    int64_t expect = 1;
+    for (int i = 3; i >= 0; --i) {
+      if (t->stride[i] != expect) return fail(KF_ERR_UNSUPPORTED, "%s '%s': 4-D tensors must be contiguous", what, s.name);
+      expect *= s.shape[i];
+    }
+  }
+  return KF_OK;
+}
+
+// Byte extents addressed through 32-bit buffer offsets must stay below 2^31.
+bool fits_31(int64_t bytes) { return bytes >= 0 && bytes < (int64_t(1) << 31); }
+
+}  // namespace
+
+extern "C" {
+
+const char* kf_status_string(kf_status st) {
+  switch (st) {
+    case KF_OK: return "KF_OK";
+    case KF_ERR_INVALID_ARG: return "KF_ERR_INVALID_ARG: invalid argument";
+    case KF_ERR_SHAPE: return "KF_ERR_SHAPE: tensor shape, dtype or stride does not match the op";
+    case KF_ERR_UNSUPPORTED: return "KF_ERR_UNSUPPORTED: not supported by this library";
+    case KF_ERR_NO_DEVICE: return "KF_ERR_NO_DEVICE: no gfx950 device available";
+    case KF_ERR_OOM: return "KF_ERR_OOM: device workspace allocation failed";
+    case KF_ERR_HIP: return "KF_ERR_HIP: HIP runtime error";
+    default: return "unknown kf_status";
+  }
+}
+
+const char* kf_last_error(void) { return g_last_error.c_str(); }
+
+kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
+  if (!out) return fail(KF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  kf_desc* d = new (std::nothrow) kf_desc();
+  if (!d) return fail(KF_ERR_OOM, "host allocation failed");
+  d->workspace = nullptr;
+  d->workspace_bytes = 0;
+  d->tiles_n = 0;
+  kf_status st = validate_and_plan(spec, d);
+  if (st != KF_OK) {
+    delete d;
+    return st;
+  }
+  d->spec = *spec;
+
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count < 1) {
+    (void)hipGetLastError();
+    delete d;
+    return fail(KF_ERR_NO_DEVICE, "no HIP device present");
+  }
+  int dev = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    delete d;
+    return fail(KF_ERR_NO_DEVICE, "cannot query the current HIP device");
+  }
+  if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+    delete d;
+    return fail(KF_ERR_NO_DEVICE, "device %d is %s; this library is built for gfx950 only", dev, prop.gcnArchName);
+  }
+  d->device = dev;
+
+  if (d->row_kind) {
+    d->workspace_bytes = (size_t)std::max<int64_t>(spec->M, 1) * d->tiles_n * sizeof(float) * 2;
+    if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      delete d;
+      return fail(KF_ERR_OOM, "workspace of %zu bytes could not be allocated", d->workspace_bytes);
+    }
+  }
+  *out = d;
+  return ok();
+}
+
+void kf_destroy(kf_desc* d) {
+  if (!d) return;
+  if (d->workspace) (void)hipFree(d->workspace);
+  delete d;
+}
+
+int32_t kf_num_inputs(const kf_desc* d) { return d ? (int32_t)d->inputs.size() : -1; }
+
+kf_status kf_input_info(const kf_desc* d, int32_t slot, int32_t* dtype, int32_t* ndim, int64_t shape[4]) {
+  if (!d || !dtype || !ndim || !shape) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  if (slot < 0 || slot >= (int32_t)d->inputs.size()) return fail(KF_ERR_INVALID_ARG, "slot %d out of range", slot);
+  const Slot& s = d->inputs[slot];
+  *dtype = s.dtype;
+  *ndim = s.ndim;
+  for (int i = 0; i < 4; ++i) shape[i] = s.shape[i];
+  return ok();
+}
+
+kf_status kf_output_info(const kf_desc* d, int32_t* dtype, int32_t* ndim, int64_t shape[4]) {
+  if (!d || !dtype || !ndim || !shape) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  *dtype = d->output.dtype;
+  *ndim = d->output.ndim;
+  for (int i = 0; i < 4; ++i) shape[i] = d->output.shape[i];
+  return ok();
+}
+
+size_t kf_workspace_bytes(const kf_desc* d) { return d ? d->workspace_bytes : 0; }
+
+const char* kf_kernel_name(const kf_desc* d) { return d ? d->kernel_name.c_str() : ""; }
+
+kf_status kf_fused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
+  if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  for (size_t i = 0; i < d->inputs.size(); ++i) {
+    kf_status st = check_tensor(&inputs[i], d->inputs[i], false, d->variant != kVarGemmF32);
+    if (st != KF_OK) return st;
+  }
+  kf_status st = check_tensor(&outputs[0], d->output, true, d->variant != kVarGemmF32);
+  if (st != KF_OK) return st;
+
+  const kf_op_spec& s = d->spec;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (s.contraction == KF_GEMM) {
+    if (s.M == 0) return ok();
+    kf::GemmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.a = inputs[0].data;
+    a.b = inputs[1].data;
+    a.M = s.M;
+    a.N = s.N;
+    a.K = s.K;
+    a.lda = s.K ? inputs[0].stride[0] : 8;
+    a.ldb = s.K ? inputs[1].stride[0] : 8;
+    a.prog = d->prog;
+    a.scale = 1.0f;
+    a.gn_group = d->gn_group;
+    a.red_index = d->red_index;
+    size_t slot = 2;
+    for (int i = 0; i < s.n_ops; ++i) {
+      const int k = s.ops[i].kind;
+      if (k == KF_OP_BIAS) a.bias = static_cast<const float*>(inputs[slot++].data);
+      if (k == KF_OP_GROUPNORM) {
+        a.gamma = static_cast<const float*>(inputs[slot++].data);
+        a.beta = static_cast<const float*>(inputs[slot++].data);
+      }
+      if (k == KF_OP_RESIDUAL_ADD) {
+        a.residual = inputs[slot].data;
+        a.ldr = inputs[slot].stride[0];
+        a.residual_bf16 = inputs[slot].dtype == KF_BF16;
+        ++slot;
+      }
+    }
+    a.out = outputs[0].data;
+    a.ldo = outputs[0].ndim == 2 ? outputs[0].stride[0] : 1;
+    a.out_bf16 = outputs[0].dtype == KF_BF16;
+    a.partials = d->workspace;
+    const bool nk = s.b_layout == KF_LAYOUT_NK;
+    hipError_t e;
+    if (d->variant == kVarGemmF32) {
+      e = kf::launch_gemm_f32(a, nk, hs);
+    } else {
+      const int64_t es = elem_size(s.in_dtype);
+      if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : std::max<int64_t>(s.K, 1) * a.ldb) * es) ||
+          !fits_31(256 * a.ldo * 4) || (a.residual && !fits_31(256 * a.ldr * 4)))
+        return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
+      e = kf::launch_gemm_bf16(a, d->epi_shape, hs, nk);
+      if (e == hipSuccess && d->row_kind)
+        e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, d->workspace, d->tiles_n, s.M, s.N, a.out,
+                                  a.ldo, a.out_bf16 != 0, hs);
+    }
+    if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return ok();
+  }
+  return fail(KF_ERR_UNSUPPORTED, "contraction not available");
+}
+
+kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
+  (void)inputs;
+  (void)outputs;
+  (void)stream;
+  if (!d) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  return fail(KF_ERR_UNSUPPORTED, "unfused chain not available in this build");
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// Internal types shared by the host planner and the kernels of libkf.so.
+#pragma once
+
+#include <stdint.h>
+
+#include "kf.h"
+
+namespace kf {
+
+struct EpiOp {
+  int32_t kind;
+  int32_t groups;
+  float p0;
+  float p1;
+};
+
+struct EpiProgram {
+  int32_t n;
+  EpiOp op[KF_MAX_OPS];
+};
+
+// Compile-time shape of an epilogue: element-wise ops only, or element-wise
+// ops around one GroupNorm, or element-wise ops followed by a row softmax /
+// logsumexp.
+enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
+
+// Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).
+struct GemmArgs {
+  const void* a;          // [M, lda] row-major
+  const void* b;          // [K, ldb] (KN) or [N, ldb] (NK)
+  int64_t M, N, K;
+  int64_t lda, ldb;
+  EpiProgram prog;
+  const float* bias;      // [N] or null
+  const float* gamma;     // [N] or null
+  const float* beta;      // [N] or null
+  const void* residual;   // [M, ldr] or null
+  int64_t ldr;
+  int32_t residual_bf16;
+  int32_t out_bf16;
+  void* out;              // [M, ldo] (or [M] for a row logsumexp)
+  int64_t ldo;
+  void* partials;         // float2 [M][tiles_n] for row softmax / logsumexp
+  int32_t tiles_m, tiles_n;
+  int32_t gn_group;       // GroupNorm group width in columns (0 = none)
+  int32_t red_index;      // position of the reduction op in prog (n if none)
+  float scale;            // dequantisation factor applied to the accumulator
+};
+
+// Arguments of the implicit-GEMM 3x3 convolution kernels.
+struct ConvArgs {
+  const void* x;          // [batch, cin, H, W]
+  const void* w;          // [cout, cin, 3, 3]
+  int64_t batch, cin, H, W, cout;
+  EpiProgram prog;
+  const float* bias;      // [cout] or null
+  const void* residual;   // output-shaped or null
+  int32_t residual_bf16;
+  int32_t out_bf16;
+  void* out;              // [batch, cout, H(/2), W(/2)]
+  int32_t pool;           // 1 if the op list ends with a 2x2 max-pool
+  int32_t pool_index;     // position of the pool op in prog
+  int32_t tiles;          // number of output tiles
+};
+
+}  // namespace kf

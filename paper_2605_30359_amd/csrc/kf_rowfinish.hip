@@ -1,0 +1,83 @@
+// Row finishing kernels for row-wise softmax / logsumexp wider than a tile.
+//
+// The contraction kernel leaves, per (row m, 256-column tile t), the pair
+// (mu_t, s_t) = (max over the tile of h, sum over the tile of e^(h - mu_t)).
+// The row's statistics follow from the exact identities
+//     mu = max_t mu_t,     S = sum_t s_t e^(mu_t - mu),
+//     logsumexp = mu + ln S,
+//     softmax_j = e^(h_j - mu_t) * e^(mu_t - mu) / S   for column j in tile t,
+// which is the hierarchical, online form of softmax the paper's Appendix A
+// (algorithmic optimisation: online softmax) and Appendix B (hierarchical
+// reductions, normalise before exponentiating) recommend.
+#include "kf_device.hpp"
+#include "kf_launch.hpp"
+
+namespace kf {
+
+__global__ __launch_bounds__(256) void kf_row_logsumexp_finish(const float2* __restrict__ part, int tiles,
+                                                                int64_t M, float* __restrict__ out) {
+  const int64_t m = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (m >= M) return;
+  const float2* pr = part + m * tiles;
+  float mu = -INFINITY;
+  for (int t = 0; t < tiles; ++t) mu = fmaxf(mu, pr[t].x);
+  float s = 0.0f;
+  for (int t = 0; t < tiles; ++t) s += pr[t].y * expf(pr[t].x - mu);
+  out[m] = mu + logf(s);
+}
+
+constexpr int kMaxFinishTiles = 1024;
+
+// One workgroup per row: factors f_t = e^(mu_t - mu) / S, then every 16-byte
+// chunk of the row is scaled by the factor of its tile.
+__global__ __launch_bounds__(256) void kf_row_softmax_rescale(const float2* __restrict__ part, int tiles,
+                                                               int64_t N, void* out, int64_t ldo,
+                                                               int out_bf16) {
+  __shared__ float2 ps[kMaxFinishTiles];
+  __shared__ float fac[kMaxFinishTiles];
+  const int64_t m = blockIdx.x;
+  const int tid = threadIdx.x;
+  for (int t = tid; t < tiles; t += 256) ps[t] = part[m * tiles + t];
+  __syncthreads();
+  float mu = -INFINITY;
+  for (int t = 0; t < tiles; ++t) mu = fmaxf(mu, ps[t].x);
+  float s = 0.0f;
+  for (int t = 0; t < tiles; ++t) s += ps[t].y * expf(ps[t].x - mu);
+  const float inv = 1.0f / s;
+  for (int t = tid; t < tiles; t += 256) fac[t] = expf(ps[t].x - mu) * inv;
+  __syncthreads();
+  if (out_bf16) {
+    uint16_t* row = reinterpret_cast<uint16_t*>(out) + m * ldo;
+    for (int64_t c = tid; c * 8 < N; c += 256) {
+      const float f = fac[(c * 8) >> 8];
+      u32x4 w = *reinterpret_cast<const u32x4*>(row + c * 8);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(bf16_lo(w[e]) * f, bf16_hi(w[e]) * f);
+      *reinterpret_cast<u32x4*>(row + c * 8) = w;
+    }
+  } else {
+    float* row = reinterpret_cast<float*>(out) + m * ldo;
+    for (int64_t c = tid; c * 4 < N; c += 256) {
+      const float f = fac[(c * 4) >> 8];
+      f32x4 v = *reinterpret_cast<const f32x4*>(row + c * 4);
+      *reinterpret_cast<f32x4*>(row + c * 4) = v * f;
+    }
+  }
+}
+
+hipError_t launch_row_finish(bool softmax, const void* partials, int tiles, int64_t M, int64_t N, void* out,
+                             int64_t ldo, bool out_bf16, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  if (softmax) {
+    hipLaunchKernelGGL(kf_row_softmax_rescale, dim3((unsigned)M), dim3(256), 0, stream,
+                       reinterpret_cast<const float2*>(partials), tiles, N, out, ldo, out_bf16 ? 1 : 0);
+  } else {
+    hipLaunchKernelGGL(kf_row_logsumexp_finish, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, stream,
+                       reinterpret_cast<const float2*>(partials), tiles, M, reinterpret_cast<float*>(out));
+  }
+  return hipGetLastError();
+}
+
+int row_finish_max_tiles() { return kMaxFinishTiles; }
+
+}  // namespace kf

@@ -1,0 +1,292 @@
+"""ctypes binding of libkf.so (include/kf.h): argument marshalling only.
+
+Every step of the fused operation runs in the library's HIP kernels; this
+module converts a chain description and torch tensors into the C structs and
+passes ``tensor.data_ptr()`` plus the current HIP stream.  torch is used only
+for device memory and streams.  If the library has not been built the first
+call raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkf.so")
+
+# ---------------------------------------------------------------- C mirror
+
+KF_OK, KF_ERR_INVALID_ARG, KF_ERR_SHAPE, KF_ERR_UNSUPPORTED, KF_ERR_NO_DEVICE, KF_ERR_OOM, KF_ERR_HIP = range(7)
+KF_GEMM, KF_CONV2D_3X3 = 0, 1
+KF_F32, KF_BF16, KF_FP8_E4M3 = 0, 1, 2
+KF_LAYOUT_KN, KF_LAYOUT_NK = 0, 1
+KF_MAX_OPS = 8
+
+OP_KINDS = {
+    "bias": 1, "relu": 2, "gelu_tanh": 3, "gelu_erf": 4, "swish": 5, "sigmoid": 6,
+    "tanh": 7, "hardtanh": 8, "scale": 9, "groupnorm": 10, "residual_add": 11,
+    "maxpool2x2": 12, "row_softmax": 13, "row_logsumexp": 14,
+}
+DTYPES = {"f32": KF_F32, "bf16": KF_BF16, "e4m3": KF_FP8_E4M3}
+DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
+
+EXPORTED = ("kf_create", "kf_fused_op", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
+            "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
+            "kf_status_string", "kf_last_error")
+
+
+class KfOp(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("groups", ctypes.c_int32),
+                ("p0", ctypes.c_float), ("p1", ctypes.c_float)]
+
+
+class KfOpSpec(ctypes.Structure):
+    _fields_ = [("contraction", ctypes.c_int32), ("in_dtype", ctypes.c_int32),
+                ("out_dtype", ctypes.c_int32), ("b_layout", ctypes.c_int32),
+                ("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("batch", ctypes.c_int64), ("cin", ctypes.c_int64), ("height", ctypes.c_int64),
+                ("width", ctypes.c_int64), ("cout", ctypes.c_int64),
+                ("scale_a", ctypes.c_float), ("scale_b", ctypes.c_float),
+                ("residual_dtype", ctypes.c_int32), ("n_ops", ctypes.c_int32),
+                ("ops", KfOp * KF_MAX_OPS)]
+
+
+class KfTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * 4), ("stride", ctypes.c_int64 * 4)]
+
+
+class KFError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)} -- {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libkf.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2605_30359_amd.build` (there is no fallback path)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
+        L.kf_create.argtypes = [ctypes.POINTER(KfOpSpec), ctypes.POINTER(vp)]
+        L.kf_create.restype = i32
+        L.kf_fused_op.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp]
+        L.kf_fused_op.restype = i32
+        L.kf_unfused_op.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp]
+        L.kf_unfused_op.restype = i32
+        L.kf_destroy.argtypes = [vp]
+        L.kf_destroy.restype = None
+        L.kf_num_inputs.argtypes = [vp]
+        L.kf_num_inputs.restype = i32
+        L.kf_input_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.c_int64 * 4]
+        L.kf_input_info.restype = i32
+        L.kf_output_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.c_int64 * 4]
+        L.kf_output_info.restype = i32
+        L.kf_workspace_bytes.argtypes = [vp]
+        L.kf_workspace_bytes.restype = ctypes.c_size_t
+        L.kf_kernel_name.argtypes = [vp]
+        L.kf_kernel_name.restype = ctypes.c_char_p
+        L.kf_status_string.argtypes = [i32]
+        L.kf_status_string.restype = ctypes.c_char_p
+        L.kf_last_error.argtypes = []
+        L.kf_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().kf_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().kf_last_error().decode()
+
+
+def _check(status: int):
+    if status != KF_OK:
+        raise KFError(status, last_error())
+
+
+# ------------------------------------------------------------ spec building
+
+def make_spec(chain: dict, *, M=0, N=0, K=0, batch=0, cin=0, H=0, W=0, cout=0) -> KfOpSpec:
+    """Fill a kf_op_spec from a chain description (see paper_2605_30359_amd.inputs)."""
+    s = KfOpSpec()
+    s.contraction = KF_GEMM if chain["contraction"] == "gemm" else KF_CONV2D_3X3
+    s.in_dtype = DTYPES[chain["in_dtype"]]
+    s.out_dtype = DTYPES[chain.get("out_dtype", "f32")]
+    s.b_layout = KF_LAYOUT_NK if chain.get("b_layout", "kn") == "nk" else KF_LAYOUT_KN
+    s.M, s.N, s.K = M, N, K
+    s.batch, s.cin, s.height, s.width, s.cout = batch, cin, H, W, cout
+    s.scale_a = float(chain.get("scale_a", 1.0))
+    s.scale_b = float(chain.get("scale_b", 1.0))
+    s.residual_dtype = DTYPES[chain.get("residual_dtype", "bf16")]
+    ops = chain["ops"]
+    if len(ops) > KF_MAX_OPS:
+        raise ValueError(f"at most {KF_MAX_OPS} ops")
+    s.n_ops = len(ops)
+    for i, op in enumerate(ops):
+        name, params = op[0], op[1:]
+        s.ops[i].kind = OP_KINDS[name]
+        if name == "hardtanh":
+            s.ops[i].p0, s.ops[i].p1 = float(params[0]), float(params[1])
+        elif name == "scale":
+            s.ops[i].p0 = float(params[0])
+        elif name == "groupnorm":
+            s.ops[i].groups = int(params[0])
+            s.ops[i].p0 = float(params[1])
+    return s
+
+
+def input_names(chain: dict) -> list:
+    """Input slot order: A, B, then the tensors the ops need, in op order."""
+    names = ["a", "b"]
+    for op in chain["ops"]:
+        if op[0] == "bias":
+            names.append("bias")
+        elif op[0] == "groupnorm":
+            names += ["gamma", "beta"]
+        elif op[0] == "residual_add":
+            names.append("residual")
+    return names
+
+
+def sizes_of(cfg: dict) -> dict:
+    if cfg["contraction"] == "gemm":
+        return dict(M=cfg["M"], N=cfg["N"], K=cfg["K"])
+    return dict(batch=cfg["batch"], cin=cfg["cin"], H=cfg["H"], W=cfg["W"], cout=cfg["cout"])
+
+
+# ------------------------------------------------------------ tensors
+
+def _torch():
+    import torch
+    return torch
+
+
+def torch_dtype(code: int):
+    torch = _torch()
+    return {KF_F32: torch.float32, KF_BF16: torch.bfloat16, KF_FP8_E4M3: torch.float8_e4m3fn}[code]
+
+
+def device_tensor(arr: np.ndarray, dtype: str, device="cuda"):
+    """Copy raw storage (float32 / bf16 bits as uint16 / e4m3 codes as uint8)
+    to the device as a tensor of the matching torch dtype."""
+    torch = _torch()
+    arr = np.ascontiguousarray(arr)
+    if dtype == "f32":
+        return torch.from_numpy(arr.astype(np.float32, copy=False)).to(device)
+    if dtype == "bf16":
+        return torch.from_numpy(arr.view(np.int16)).to(device).view(torch.bfloat16)
+    if dtype == "e4m3":
+        return torch.from_numpy(arr.view(np.uint8)).to(device).view(torch.float8_e4m3fn)
+    raise ValueError(dtype)
+
+
+def to_kf_tensor(t) -> KfTensor:
+    torch = _torch()
+    codes = {torch.float32: KF_F32, torch.bfloat16: KF_BF16, torch.float8_e4m3fn: KF_FP8_E4M3}
+    if t.dtype not in codes:
+        raise TypeError(f"unsupported tensor dtype {t.dtype}")
+    if t.dim() < 1 or t.dim() > 4:
+        raise ValueError("tensors must have 1..4 dimensions")
+    k = KfTensor()
+    k.data = t.data_ptr()
+    k.dtype = codes[t.dtype]
+    k.ndim = t.dim()
+    for i in range(t.dim()):
+        k.shape[i] = t.shape[i]
+        k.stride[i] = t.stride(i)
+    return k
+
+
+class FusedOp:
+    """One planned fused operation (kf_create / kf_fused_op / kf_destroy)."""
+
+    def __init__(self, chain: dict, **sizes):
+        self.chain = chain
+        self.sizes = sizes
+        self._spec = make_spec(chain, **sizes)
+        h = ctypes.c_void_p()
+        _check(lib().kf_create(ctypes.byref(self._spec), ctypes.byref(h)))
+        self._h = h
+
+    @classmethod
+    def from_config(cls, cfg: dict, chain: dict | None = None):
+        from . import inputs
+        return cls(chain if chain is not None else inputs.chain(cfg), **sizes_of(cfg))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().kf_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def num_inputs(self) -> int:
+        return lib().kf_num_inputs(self._h)
+
+    def input_info(self, slot: int):
+        dt, nd, shp = ctypes.c_int32(), ctypes.c_int32(), (ctypes.c_int64 * 4)()
+        _check(lib().kf_input_info(self._h, slot, ctypes.byref(dt), ctypes.byref(nd), shp))
+        return DTYPE_NAMES[dt.value], tuple(shp[i] for i in range(nd.value))
+
+    def output_info(self):
+        dt, nd, shp = ctypes.c_int32(), ctypes.c_int32(), (ctypes.c_int64 * 4)()
+        _check(lib().kf_output_info(self._h, ctypes.byref(dt), ctypes.byref(nd), shp))
+        return DTYPE_NAMES[dt.value], tuple(shp[i] for i in range(nd.value))
+
+    def workspace_bytes(self) -> int:
+        return int(lib().kf_workspace_bytes(self._h))
+
+    def kernel_name(self) -> str:
+        return lib().kf_kernel_name(self._h).decode()
+
+    def empty_output(self, device="cuda"):
+        torch = _torch()
+        dt, shp = self.output_info()
+        return torch.empty(shp, dtype=torch_dtype(DTYPES[dt]), device=device)
+
+    def _call(self, fn, inputs, out, stream):
+        torch = _torch()
+        if out is None:
+            out = self.empty_output(inputs[0].device)
+        arr = (KfTensor * max(1, len(inputs)))(*[to_kf_tensor(t) for t in inputs])
+        o = (KfTensor * 1)(to_kf_tensor(out))
+        if stream is None:
+            stream = torch.cuda.current_stream(out.device).cuda_stream
+        elif not isinstance(stream, int):
+            stream = stream.cuda_stream
+        _check(fn(self._h, arr, o, ctypes.c_void_p(stream)))
+        return out
+
+    def __call__(self, inputs, out=None, stream=None):
+        return self._call(lib().kf_fused_op, inputs, out, stream)
+
+    def unfused(self, inputs, out=None, stream=None):
+        return self._call(lib().kf_unfused_op, inputs, out, stream)
+
+    def device_inputs(self, tensors: dict, device="cuda") -> list:
+        """Marshal raw generated storage into the slot order of this op."""
+        out = []
+        for name in input_names(self.chain):
+            if name in ("a", "b"):
+                dt = self.chain["in_dtype"]
+            elif name == "residual":
+                dt = self.chain.get("residual_dtype", "bf16")
+            else:
+                dt = "f32"
+            out.append(device_tensor(tensors[name], dt, device))
+        return out

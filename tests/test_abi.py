@@ -1,0 +1,165 @@
+"""Boundary tests that need no GPU: libkf.so loads, exports every function
+include/kf.h declares, links no vendor math library, and rejects malformed
+op descriptors on the host with the documented status codes."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2605_30359_amd import inputs, kf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kf.h")
+
+
+def _gpu_present():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kf_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_expected_api():
+    names = declared_functions()
+    for required in ("kf_create", "kf_fused_op", "kf_destroy", "kf_status_string", "kf_last_error"):
+        assert required in names
+    assert set(names) == set(kf.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = kf.lib()
+    out = subprocess.run(["nm", "-D", "--defined-only", kf.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (kf_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_library_links_no_vendor_math_or_torch():
+    out = subprocess.run(["ldd", kf.LIB_PATH], capture_output=True, text=True).stdout.lower()
+    for bad in ("rocblas", "hipblas", "miopen", "torch", "rocsolver"):
+        assert bad not in out, out
+
+
+def test_status_strings():
+    for st in range(7):
+        assert kf.status_string(st).startswith("KF_")
+    assert kf.status_string(99) == "unknown kf_status"
+
+
+def test_ctypes_struct_layout_matches_header():
+    # kf_op 16 B; kf_op_spec: 4 ints, 8 int64, 2 floats, 2 ints, 8 ops
+    assert ctypes.sizeof(kf.KfOp) == 16
+    assert ctypes.sizeof(kf.KfOpSpec) == 16 + 64 + 8 + 8 + 8 * 16
+    assert ctypes.sizeof(kf.KfTensor) == 8 + 4 + 4 + 32 + 32
+
+
+def _create(spec):
+    h = ctypes.c_void_p()
+    st = kf.lib().kf_create(ctypes.byref(spec), ctypes.byref(h))
+    return st, h
+
+
+def _spec(name, **kw):
+    cfg = inputs.config(name, **kw)
+    return kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg))
+
+
+def test_create_null_arguments():
+    lib = kf.lib()
+    h = ctypes.c_void_p()
+    assert lib.kf_create(None, ctypes.byref(h)) == kf.KF_ERR_INVALID_ARG
+    assert "NULL" in kf.last_error()
+    spec = _spec("C2")
+    assert lib.kf_create(ctypes.byref(spec), None) == kf.KF_ERR_INVALID_ARG
+    lib.kf_destroy(None)  # NULL-safe
+
+
+@pytest.mark.parametrize("mutate,status,msg", [
+    (lambda s: setattr(s, "contraction", 7), kf.KF_ERR_INVALID_ARG, "contraction"),
+    (lambda s: setattr(s, "in_dtype", 9), kf.KF_ERR_INVALID_ARG, "in_dtype"),
+    (lambda s: setattr(s, "out_dtype", kf.KF_FP8_E4M3), kf.KF_ERR_INVALID_ARG, "out_dtype"),
+    (lambda s: setattr(s, "n_ops", 9), kf.KF_ERR_INVALID_ARG, "n_ops"),
+    (lambda s: setattr(s, "K", 100), kf.KF_ERR_UNSUPPORTED, "K % 8"),
+    (lambda s: setattr(s, "N", 4100), kf.KF_ERR_UNSUPPORTED, "N % 8"),
+    (lambda s: setattr(s, "M", -1), kf.KF_ERR_SHAPE, "M >= 0"),
+    (lambda s: setattr(s, "b_layout", 5), kf.KF_ERR_INVALID_ARG, "b_layout"),
+])
+def test_create_rejects_bad_specs(mutate, status, msg):
+    spec = _spec("C2")
+    mutate(spec)
+    st, h = _create(spec)
+    assert st == status, (st, kf.last_error())
+    assert not h.value
+    assert msg in kf.last_error()
+
+
+def test_row_op_must_be_last():
+    cfg = inputs.config("C2", ops=[("bias",), ("row_logsumexp",), ("relu",)])
+    spec = kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg))
+    st, _ = _create(spec)
+    assert st == kf.KF_ERR_UNSUPPORTED and "last" in kf.last_error()
+
+
+def test_logsumexp_needs_f32_output():
+    cfg = inputs.config("C2", out_dtype="bf16")
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_UNSUPPORTED
+
+
+def test_groupnorm_validation():
+    cfg = inputs.config("C3", ops=[("groupnorm", 3, 1e-5)])
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_SHAPE and "divisible" in kf.last_error()
+    cfg = inputs.config("C3", ops=[("groupnorm", 256, 1e-5)])   # width 32: not fused
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_UNSUPPORTED
+    cfg = inputs.config("C3", ops=[("groupnorm", 32, -1.0)])
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_INVALID_ARG
+
+
+def test_maxpool_needs_conv_and_fp32_limits():
+    cfg = inputs.config("C2", ops=[("maxpool2x2",)], out_dtype="f32")
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_UNSUPPORTED and "CONV" in kf.last_error()
+    cfg = inputs.config("C1", ops=[("row_softmax",)])
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_UNSUPPORTED
+
+
+def test_hardtanh_bounds_validated():
+    cfg = inputs.config("C5", ops=[("hardtanh", 1.0, -1.0)], in_dtype="bf16")
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st == kf.KF_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
+def test_valid_spec_without_device_reports_no_device():
+    for name in ("C1", "C2", "C3"):
+        st, h = _create(_spec(name))
+        assert st == kf.KF_ERR_NO_DEVICE, (name, st, kf.last_error())
+        assert not h.value
+
+
+def test_binding_raises_kferror():
+    cfg = inputs.config("C2", K=100)
+    with pytest.raises(kf.KFError) as ei:
+        kf.FusedOp.from_config(cfg)
+    assert ei.value.status == kf.KF_ERR_UNSUPPORTED
+
+
+def test_input_slot_order():
+    ch = inputs.chain(inputs.config("C3"))
+    assert kf.input_names(ch) == ["a", "b", "gamma", "beta", "residual"]
+    ch = inputs.chain(inputs.config("C2"))
+    assert kf.input_names(ch) == ["a", "b", "bias"]

@@ -1,0 +1,199 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on
+the same seeded inputs.  Small and ragged shapes are compared element by
+element; the full workload sizes are compared on sampled rows, plus a
+bit-exact integer test of the contraction at full size."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2605_30359_amd import inputs, kf
+from parity import TOL, check, parity_error, run_gpu, sample_rows, to_host_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+# ------------------------------------------------------------ C1 (fp32)
+
+def test_c1_full_config():
+    _torch()
+    cfg = inputs.config("C1")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"C1 err {err:.3e}")
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 1, 1), (33, 65, 31), (100, 300, 257), (64, 512, 0)])
+def test_c1_ragged(M, N, K):
+    _torch()
+    cfg = inputs.config("C1", M=M, N=N, K=K)
+    t = inputs.generate(cfg, seed=M + N + K)
+    _, out = run_gpu(cfg, t)
+    check(cfg, t, out)
+
+
+def test_c1_nk_layout_and_gelu_chain():
+    _torch()
+    cfg = inputs.config("C1", M=40, N=96, K=72, b_layout="nk",
+                        ops=[("bias",), ("gelu_erf",), ("scale", -1.5), ("tanh",), ("swish",), ("sigmoid",), ("hardtanh", 0.55, 0.7)])
+    t = inputs.generate(cfg, seed=3)
+    _, out = run_gpu(cfg, t)
+    check(cfg, t, out)
+
+
+# ------------------------------------------------------------ bf16 GEMM
+
+def test_bf16_contraction_bit_exact_full_size():
+    """Integer-valued bf16 operands in [-8, 8]: every partial sum is an
+    integer below 2^24, so the fp32 accumulator must equal the exact product."""
+    torch = _torch()
+    M = N = K = 4096
+    rng = np.random.default_rng(11)
+    a = rng.integers(-8, 9, size=(M, K)).astype(np.float32)
+    b = rng.integers(-8, 9, size=(K, N)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(a), "b": inputs.f32_to_bf16_bits(b)}
+    cfg = inputs.config("C2", out_dtype="f32", ops=[])
+    print("bit-exact 4096^3: launching", flush=True)
+    _, out = run_gpu(cfg, t)
+    g = out.cpu().numpy()
+    # float64 BLAS is exact here: every partial sum is an integer < 2^53
+    ref = a.astype(np.float64) @ b.astype(np.float64)
+    print("bit-exact 4096^3: reference done", flush=True)
+    assert np.array_equal(g.astype(np.float64), ref)
+
+
+def test_bf16_contraction_bit_exact_nk_ragged():
+    torch = _torch()
+    M, N, K = 300, 264, 200
+    rng = np.random.default_rng(12)
+    a = rng.integers(-8, 9, size=(M, K)).astype(np.float32)
+    b = rng.integers(-8, 9, size=(N, K)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(a), "b": inputs.f32_to_bf16_bits(b)}
+    cfg = inputs.config("C2", M=M, N=N, K=K, out_dtype="f32", ops=[], b_layout="nk")
+    _, out = run_gpu(cfg, t)
+    assert np.array_equal(out.cpu().numpy().astype(np.float64), a.astype(np.float64) @ b.astype(np.float64).T)
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 520, 136), (256, 256, 64), (1, 8, 8), (513, 776, 1000)])
+def test_c2_ragged(M, N, K):
+    _torch()
+    cfg = inputs.config("C2", M=M, N=N, K=K)
+    t = inputs.generate(cfg, seed=M * 7 + N + K)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"C2 {M}x{N}x{K} err {err:.3e}")
+
+
+def test_c2_full_config_sampled_rows():
+    _torch()
+    cfg = inputs.config("C2")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    rows = sample_rows(cfg["M"], 48)
+    err = check(cfg, t, out, rows=rows)
+    print(f"C2 full err {err:.3e}")
+    # a property at every row: max_j s_ij <= lse_i <= max_j s_ij + ln N is
+    # implied by the sampled parity; every row must at least be finite
+    assert np.all(np.isfinite(to_host_f64(out)))
+
+
+def test_c2_zero_weights_closed_form():
+    _torch()
+    cfg = inputs.config("C2", M=512, N=4096, K=64)
+    t = inputs.generate(cfg, seed=5)
+    t["b"] = np.zeros_like(t["b"])
+    t["bias"] = np.zeros_like(t["bias"])
+    _, out = run_gpu(cfg, t)
+    g = to_host_f64(out)
+    assert np.max(np.abs(g - np.log(4096.0))) < 1e-5
+
+
+@pytest.mark.parametrize("M,N,K,G", [(300, 512, 136, 2), (256, 1024, 64, 8), (77, 256, 24, 1)])
+def test_c3_ragged(M, N, K, G):
+    _torch()
+    cfg = inputs.config("C3", M=M, N=N, K=K, ops=[("groupnorm", G, 1e-5), ("swish",), ("residual_add",)])
+    t = inputs.generate(cfg, seed=M + N * 3 + K)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"C3 {M}x{N}x{K} G={G} err {err:.3e}")
+
+
+def test_c3_full_config_sampled_rows():
+    _torch()
+    cfg = inputs.config("C3")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    rows = sample_rows(cfg["M"], 32)
+    err = check(cfg, t, out, rows=rows)
+    print(f"C3 full err {err:.3e}")
+
+
+def test_c3_zero_weights_closed_form():
+    _torch()
+    cfg = inputs.config("C3", M=64, N=512, K=32, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
+    t = inputs.generate(cfg, seed=9)
+    t["b"] = np.zeros_like(t["b"])
+    _, out = run_gpu(cfg, t)
+    beta = t["beta"].astype(np.float64)
+    expect = beta / (1 + np.exp(-beta)) + oracle.decode_bf16(t["residual"])
+    assert parity_error(to_host_f64(out), expect, 1.0) < 1e-2
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 1032, 136), (64, 8192, 64)])
+def test_bf16_row_softmax(M, N, K):
+    _torch()
+    cfg = inputs.config("C2", M=M, N=N, K=K, out_dtype="bf16",
+                        ops=[("bias",), ("hardtanh", -1.0, 1.0), ("row_softmax",)])
+    t = inputs.generate(cfg, seed=M + N)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    g = to_host_f64(out)
+    assert np.allclose(g.sum(axis=1), 1.0, atol=2e-2)
+    print(f"bf16 softmax err {err:.3e}")
+
+
+def test_bf16_groupnorm_width_128_and_relu_chain():
+    _torch()
+    cfg = inputs.config("C3", M=130, N=384, K=96,
+                        ops=[("scale", 2.0), ("groupnorm", 3, 1e-5), ("relu",), ("residual_add",)])
+    t = inputs.generate(cfg, seed=21)
+    _, out = run_gpu(cfg, t)
+    check(cfg, t, out)
+
+
+def test_empty_m_is_a_no_op():
+    torch = _torch()
+    cfg = inputs.config("C2", M=0, N=256, K=64)
+    t = inputs.generate(cfg, seed=1)
+    _, out = run_gpu(cfg, t)
+    assert out.numel() == 0
+
+
+def test_repeat_runs_bitwise_identical():
+    torch = _torch()
+    cfg = inputs.config("C3", M=512, N=512, K=256, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
+    t = inputs.generate(cfg, seed=2)
+    op = kf.FusedOp(inputs.chain(cfg), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    o1, o2 = op(ins), op(ins)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
+def test_shape_mismatch_rejected_on_device():
+    torch = _torch()
+    cfg = inputs.config("C2", M=64, N=64, K=64)
+    t = inputs.generate(cfg, seed=1)
+    op = kf.FusedOp(inputs.chain(cfg), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    bad = torch.empty((63,), dtype=torch.float32, device="cuda")
+    with pytest.raises(kf.KFError) as ei:
+        op(ins, bad)
+    assert ei.value.status == kf.KF_ERR_SHAPE
