@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused contraction + epilogue path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C2]
+
+A step is one kf_fused_op call: the whole fused operation (contraction,
+fused epilogue, row finishing kernel) on one batch of seeded synthetic input
+already resident in device memory.  The default workload is the bf16 GEMM
+4096 x 4096 x 4096 + bias + GELU(tanh) + scale 0.5 + row logsumexp -> fp32
+[4096].  One JSON line is printed with:
+
+  value        whole-step throughput in TFLOP/s (2*M*N*K / step time)
+  roofline     the main contraction kernel alone, timed live with HIP events
+               recorded on its stream around each launch, against the dense
+               MFMA peak of its input dtype; `traffic` is the HBM bytes per
+               launch from the committed rocprofv3 counter summary, or null if
+               the kernel source changed since those counters were taken
+  unfused      the same operation as the library's own one-kernel-per-op
+               chain, timed the same way; speedup = unfused / fused time
+  cpu_baseline the fp64 oracle timed on the host cores over a bounded sample
+               of rows of the same workload (every op in the chain is
+               row-local, so a row sample is the same computation per row)
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# Dense peaks of one MI355X (256 CUs at 2.4 GHz), TFLOP/s.
+PEAK_TFLOPS = {"bf16": 2516.6, "e4m3": 5033.2, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+
+
+def _hip():
+    lib = ctypes.CDLL("libamdhip64.so")
+    lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    return lib
+
+
+def _event(hip):
+    e = ctypes.c_void_p()
+    assert hip.hipEventCreate(ctypes.byref(e)) == 0
+    return e.value
+
+
+def _elapsed_ms(hip, a, b) -> float:
+    ms = ctypes.c_float()
+    assert hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) == 0
+    return float(ms.value)
+
+
+def _source_digest(kernel_file: str) -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2605_30359_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name in (kernel_file, "kf_device.hpp", "kf_internal.hpp"):
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_FILES = {"kf_gemm_bf16_256x256": "kf_gemm_bf16.hip", "kf_gemm_f32_32x64": "kf_gemm_f32.hip"}
+
+
+def _traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(f"{kernel}:{workload}")
+    except Exception:
+        return None
+    if not rec or rec.get("source_digest") != _source_digest(KERNEL_FILES.get(kernel, "")):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
+    import numpy as np
+
+    import oracle
+    from paper_2605_30359_amd import inputs
+
+    ch = inputs.chain_for(cfg, tensors)
+    M = cfg["M"]
+    flops_row = 2 * cfg["N"] * cfg["K"]
+    # calibrate on a few rows, then time a sample sized to the budget
+    rows = np.arange(min(8, M), dtype=np.int64)
+    t0 = time.perf_counter()
+    oracle.run_chain(ch, tensors, rows=rows)
+    dt = time.perf_counter() - t0
+    n = int(min(M, max(8, budget_s / max(dt / rows.size, 1e-6))))
+    rng = np.random.default_rng(0)
+    rows = np.sort(rng.choice(M, size=n, replace=False)).astype(np.int64)
+    t0 = time.perf_counter()
+    ref = oracle.run_chain(ch, tensors, rows=rows)
+    dt = time.perf_counter() - t0
+    # parity of the benchmarked output on the same rows
+    import torch
+    g = gpu_out.cpu()
+    if g.dtype == torch.bfloat16:
+        g = oracle.decode_bf16(g.view(torch.int16).numpy().view(np.uint16))
+    else:
+        g = g.numpy().astype(np.float64)
+    g = g[rows]
+    floor = 1.0 / cfg["N"] if cfg["ops"][-1][0] == "row_softmax" else 1.0
+    err = float(np.max(np.abs(g - ref) / np.maximum(np.abs(ref), floor))) if np.all(np.isfinite(g)) else float("inf")
+    return {
+        "value": n * flops_row / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.threads(),
+        "kind": "oracle",
+        "sample": f"{n} of {M} output rows of the same workload (fp64, plain C + OpenMP), {dt:.1f} s",
+        "seconds": dt,
+    }, err
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="C2", help="C1..C5 (default C2)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy 5 times (for scaling HBM byte counters)")
+    args = ap.parse_args(argv)
+
+    if args.copy_calibration:
+        import torch
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda:0")
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": src.numel(), "launches": 5}))
+        return 0
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the fused kernels need no cross-GPU exchange; see DESIGN.md for how the path shards)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2605_30359_amd import inputs, kf
+
+    torch.cuda.set_device(0)
+    cfg = inputs.config(args.workload)
+    tensors = inputs.generate(cfg)
+    chain = inputs.chain_for(cfg, tensors)
+    op = kf.FusedOp(chain, **kf.sizes_of(cfg))
+    ins = op.device_inputs(tensors, "cuda:0")
+    out = op.empty_output("cuda:0")
+    stream = torch.cuda.current_stream()
+    hip = _hip()
+
+    for _ in range(args.warmup):
+        op(ins, out)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [(_event(hip), _event(hip)) for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(K):
+        op.timed(ins, out, evs[i][0], evs[i][1])
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / K
+    kernel_ms = sum(_elapsed_ms(hip, a, b) for a, b in evs) / K
+    for a, b in evs:
+        hip.hipEventDestroy(ctypes.c_void_p(a))
+        hip.hipEventDestroy(ctypes.c_void_p(b))
+
+    flops = inputs.flops(cfg)
+    dt = cfg["in_dtype"]
+    peak = PEAK_TFLOPS[dt]
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    achieved = flops / (kernel_ms * 1e-3) / 1e12
+    kname = op.kernel_name()
+
+    unfused = None
+    if not args.no_unfused:
+        try:
+            u_out = op.empty_output("cuda:0")
+            for _ in range(max(2, args.warmup // 2)):
+                op.unfused(ins, u_out)
+            torch.cuda.synchronize()
+            start.record(stream)
+            for _ in range(K):
+                op.unfused(ins, u_out)
+            end.record(stream)
+            torch.cuda.synchronize()
+            u_ms = start.elapsed_time(end) / K
+            unfused = {"ms_per_step": u_ms, "speedup": u_ms / ms_per_step}
+        except kf.KFError as e:
+            unfused = {"error": str(e)}
+
+    cpu, err = (None, None)
+    if not args.no_cpu_baseline:
+        cpu, err = _cpu_baseline(cfg, tensors, out, args.cpu_budget)
+
+    sizes = kf.sizes_of(cfg)
+    line = {
+        "metric": "fused-op TFLOP/s, % of MFMA peak, speedup vs own unfused kernel chain",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic",
+        "config": dict({"workload": cfg["workload"], "ops": "+".join(o[0] for o in cfg["ops"]),
+                        "out_dtype": cfg["out_dtype"]}, **sizes),
+        "pct_mfma_peak": round(100.0 * value / peak, 2),
+        "speedup_vs_unfused": None if not unfused or "speedup" not in unfused else round(unfused["speedup"], 3),
+        "unfused": unfused,
+        "roofline": {
+            "bound": "mfma",
+            "kernel": kname,
+            "achieved": round(achieved, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "kernel_us": round(kernel_ms * 1e3, 2),
+            "flops_per_launch": flops,
+            "traffic": _traffic(kname, cfg["workload"]),
+        },
+        "cpu_baseline": cpu,
+        "parity_err_sampled_rows": err,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -143,6 +143,15 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out);
 kf_status kf_fused_op(const kf_desc* desc, const kf_tensor* inputs,
                       kf_tensor* outputs, void* stream);
 
+/* kf_fused_op, additionally recording `ev_before` and `ev_after` (hipEvent_t
+   created by the caller, passed as void*) on `stream` immediately before and
+   after the main contraction kernel, so that hipEventElapsedTime gives that
+   kernel's duration alone (finishing kernels fall outside the pair).  Either
+   event may be NULL. */
+kf_status kf_fused_op_timed(const kf_desc* desc, const kf_tensor* inputs,
+                            kf_tensor* outputs, void* stream, void* ev_before,
+                            void* ev_after);
+
 /* The same operation as an unfused chain, one kernel per op, with every
    intermediate stored to device memory in bf16 (fp32 for fp32 chains) --
    the comparator for the fused kernel.  Its intermediate buffers are

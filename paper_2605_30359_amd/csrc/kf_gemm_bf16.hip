@@ -1,28 +1,33 @@
 // bf16 GEMM + fused epilogue on gfx950 matrix cores.
 //
 // h = A * B with A [M,K] bf16 row-major and B either [K,N] ("KN", N
-// contiguous) or [N,K] ("NK", K contiguous), fp32 accumulation, then the
-// op list (bias, activations, scale, GroupNorm, residual add, row softmax /
-// logsumexp partials) on the accumulator registers, then one store.  This is
-// the matmul + epilogue fusion the paper's search produces (Appendix A,
-// "Operator Fusion"; Appendix C, the evolved matmul + activation kernel),
-// laid out for CDNA4:
+// contiguous) or [N,K] ("NK", K contiguous), fp32 accumulation, then the op
+// list (bias, activations, scale, GroupNorm, residual add, row softmax /
+// logsumexp partials) applied to the accumulator registers, then one store.
+// This is the matmul + epilogue fusion the paper's search produces
+// (Appendix A, "Operator Fusion"; Appendix C, the evolved matmul + activation
+// kernel), laid out for CDNA4:
 //
-//   tile        256 x 256 output per workgroup, BK = 64, 4 waves (2 x 2),
-//               each wave 128 x 128 = 8 x 8 blocks of v_mfma_f32_16x16x32_bf16
-//   operands    128-bit buffer loads (out-of-range lanes read 0: ragged M,
-//               N, K need no branches), staged in registers one K-step ahead
-//   LDS         two stages x (A 32 KB + B 32 KB), rows of 64 k (128 B) with
-//               the 16-byte chunk index XOR-swizzled by (row & 7) so both
-//               the staging writes and the fragment reads are conflict-free;
-//               a KN operand is transposed 8x8 in registers (v_perm_b32)
-//               while it is staged, so both operands are k-contiguous in LDS
-//   MFMA order  the B fragment is passed as the MFMA "A" operand, so each
-//               lane's 4 accumulator values are 4 consecutive output
-//               columns of one row: 8-byte bf16 / 16-byte fp32 stores and
-//               row reductions that are lane-local first
-//   raster      workgroups are renumbered so that consecutive tiles land on
-//               the same XCD (its own L2), in groups of 4 tile-rows
+//   tile     256 x 256 outputs per workgroup of 4 waves (2 x 2); each wave
+//            owns 128 x 128 = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16, the
+//            bf16 MFMA shape that sustains the full matrix-core rate (one
+//            instruction per 32 cycles per SIMD); accumulators live in AGPRs
+//   K loop   BK = 32 per step, four LDS stages; operands move global -> LDS
+//            by buffer_load ... lds (LDS DMA), issued three steps ahead, so no
+//            VGPR stages operand data; out-of-range lanes of a DMA write zeros,
+//            which pads ragged M, N and K tails without branches
+//   LDS      A (and B in NK layout) as [rows][32 k] with an XOR swizzle of the
+//            16-byte chunks; B in KN layout kept as [32 k][256 n] with a
+//            padded 544-byte row pitch and read through ds_read_b64_tr_b16,
+//            which transposes 4 x 16 element blocks across each 16-lane group
+//            so every lane receives 8 consecutive k of one column
+//   order    the B fragment is the MFMA "A" operand, so each lane's
+//            accumulators are runs of 4 consecutive output columns of one row:
+//            8-byte bf16 / 16-byte fp32 stores, lane-local row reductions
+//   raster   workgroup ids are renumbered so that consecutive tiles land on
+//            the same XCD (its own L2), in groups of 4 tile-rows
+#include <type_traits>
+
 #include "kf_device.hpp"
 #include "kf_launch.hpp"
 
@@ -32,16 +37,7 @@ namespace {
 
 constexpr int BM = 256;
 constexpr int BN = 256;
-constexpr int BK = 64;
 constexpr int NT = 256;
-constexpr int kStageBytes = (BM + BN) * BK * 2;  // 64 KiB
-constexpr int kOffB = BM * BK * 2;               // B follows A in a stage
-
-// Byte offset of 16-byte chunk `chunk` (0..7) of row `row` in an LDS operand
-// tile whose rows hold 64 bf16.
-__device__ __forceinline__ uint32_t swz(int row, int chunk) {
-  return (uint32_t)(row * 128 + ((chunk ^ (row & 7)) << 4));
-}
 
 __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nwg = tiles_m * tiles_n;
@@ -59,101 +55,96 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
   tn = r / gsize;
 }
 
-__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
-  return __builtin_amdgcn_perm(hi, lo, sel);
-}
-
 template <typename T>
 __device__ __forceinline__ T lds_load(const unsigned char* p) {
   return *reinterpret_cast<const T*>(p);
 }
-template <typename T>
-__device__ __forceinline__ void lds_store(unsigned char* p, T v) {
-  *reinterpret_cast<T*>(p) = v;
-}
 
-typedef f32x4 Acc[8][8];
+// acc[bi][bj][i]: output row    wm*128 + bi*32 + (lane & 31)
+//                 output column wn*128 + bj*32 + (i/4)*8 + (lane >> 5)*4 + i%4
+typedef f32x16 Acc[4][4];
 
 // -------------------------------------------------------------- epilogue
 //
-// Accumulator element (bi, bj, r) of lane `lane` in wave (wm, wn) holds
-// output row  m0 + wm*128 + bi*16 + (lane & 15)
-// and column  n0 + wn*128 + bj*16 + (lane >> 4)*4 + r.
-//
-// The op list is executed in phases separated by its reduction ops
-// (GROUPNORM, ROW_SOFTMAX, ROW_LOGSUMEXP).  Inside a phase each 16-row block
-// bi is taken through all of the phase's element-wise ops at once, so only
-// its 32 values are live in VGPRs while the rest of the tile stays in the
-// accumulator registers.
+// The op list is run in up to two phases around its reduction op (GROUPNORM,
+// ROW_SOFTMAX or ROW_LOGSUMEXP).  Each phase takes one 32-row block bi at a
+// time -- its 64 values per lane in VGPRs, the rest of the tile in AGPRs --
+// through all of the phase's element-wise ops, and the last phase stores.
 
 struct EpiCtx {
   int lane, wm, wn;
   int64_t m0, n0;
-  unsigned char* smem;
+  float* red;  // 2 x 256 floats of LDS for cross-wave row reductions
 };
 
-__device__ __forceinline__ int col_local(const EpiCtx& c, int bj) { return c.wn * 128 + bj * 16 + (c.lane >> 4) * 4; }
-__device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.wm * 128 + bi * 16 + (c.lane & 15); }
-
-__device__ __forceinline__ bool is_reduction(int kind) {
-  return kind == KF_OP_GROUPNORM || kind == KF_OP_ROW_SOFTMAX || kind == KF_OP_ROW_LOGSUMEXP;
+// run g (0..15) of a row = block bj = g / 4, group gi = g % 4
+__device__ __forceinline__ int col_local(const EpiCtx& c, int g) {
+  return c.wn * 128 + (g >> 2) * 32 + (g & 3) * 8 + (c.lane >> 5) * 4;
 }
+__device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.wm * 128 + bi * 32 + (c.lane & 31); }
 
-// 4 consecutive fp32 of a per-column vector (bias, gamma, beta) for block
-// bj; columns >= N read 0.
-__device__ __forceinline__ f32x4 load_col4(const EpiCtx& c, const float* v, int64_t N, int bj) {
-  const __amdgpu_buffer_rsrc_t r = make_rsrc(v + c.n0, (uint32_t)((N - c.n0) * 4));
-  return __builtin_bit_cast(f32x4, buf_load16(r, (uint32_t)col_local(c, bj) * 4u));
-}
+typedef f32x4 Row[16];  // one lane's 64 values of one row
 
-// Reduce one value per 16-row block across the 4 lanes holding each row
-// and then across the two waves that share the rows (through LDS).
-// `red` holds 2 x 256 floats.  Every thread of the workgroup must call it.
-template <bool IS_MAX>
-__device__ __forceinline__ void tile_row_reduce(const EpiCtx& c, float (&v)[8], float* red) {
+__device__ __forceinline__ void get_row(const Acc& acc, int bi, Row& v) {
 #pragma unroll
-  for (int bi = 0; bi < 8; ++bi) {
-    float x = v[bi];
-    float y = shfl_xor(x, 16);
-    x = IS_MAX ? fmaxf(x, y) : x + y;
-    y = shfl_xor(x, 32);
-    v[bi] = IS_MAX ? fmaxf(x, y) : x + y;
+  for (int g = 0; g < 16; ++g) {
+    const f32x16& a = acc[bi][g >> 2];
+    const int o = (g & 3) * 4;
+    v[g] = f32x4{a[o], a[o + 1], a[o + 2], a[o + 3]};
   }
-  if (c.lane < 16) {
+}
+__device__ __forceinline__ void put_row(Acc& acc, int bi, const Row& v) {
 #pragma unroll
-    for (int bi = 0; bi < 8; ++bi) red[c.wn * 256 + row_local(c, bi)] = v[bi];
+  for (int g = 0; g < 16; ++g) {
+    const int o = (g & 3) * 4;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[bi][g >> 2][o + q] = v[g][q];
+  }
+}
+
+// 4 consecutive fp32 of a per-column vector (bias, gamma, beta); columns >= N
+// read as 0.
+__device__ __forceinline__ f32x4 load_col4(const EpiCtx& c, const float* v, int64_t N, int g) {
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(v + c.n0, (uint32_t)((N - c.n0) * 4));
+  return __builtin_bit_cast(f32x4, buf_load16(r, (uint32_t)col_local(c, g) * 4u));
+}
+
+__device__ __forceinline__ float sum4(f32x4 a) { return (a[0] + a[1]) + (a[2] + a[3]); }
+__device__ __forceinline__ float max4(f32x4 a) { return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])); }
+
+// Combine one value per row over the two lanes of the row (lane ^ 32) and, if
+// `cross`, over the two waves that share the rows (through LDS).  Every
+// thread of the workgroup must call it with the same `cross`.
+template <bool IS_MAX>
+__device__ __forceinline__ void row_combine(const EpiCtx& c, float (&v)[4], bool cross) {
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) {
+    const float y = shfl_xor(v[bi], 32);
+    v[bi] = IS_MAX ? fmaxf(v[bi], y) : v[bi] + y;
+  }
+  if (!cross) return;
+  if (c.lane < 32) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) c.red[c.wn * 256 + row_local(c, bi)] = v[bi];
   }
   __syncthreads();
 #pragma unroll
-  for (int bi = 0; bi < 8; ++bi) {
-    const float o = red[(c.wn ^ 1) * 256 + row_local(c, bi)];
+  for (int bi = 0; bi < 4; ++bi) {
+    const float o = c.red[(c.wn ^ 1) * 256 + row_local(c, bi)];
     v[bi] = IS_MAX ? fmaxf(v[bi], o) : v[bi] + o;
   }
   __syncthreads();
 }
 
-// Same, but the second (cross-wave) step is skipped: a group of 128 columns
-// is exactly one wave's half of the tile row.
-__device__ __forceinline__ void wave_row_sum(float (&v)[8]) {
-#pragma unroll
-  for (int bi = 0; bi < 8; ++bi) {
-    float x = v[bi];
-    x += shfl_xor(x, 16);
-    x += shfl_xor(x, 32);
-    v[bi] = x;
-  }
-}
-
-// Element-wise / tensor-reading ops oi..oe-1 on one 16-row block.
-__device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, int bi, int oi, int oe,
-                                            f32x4 (&v)[8]) {
+// Element-wise / tensor-reading ops oi..oe-1 on one row block.
+__device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, int bi, int oi, int oe, Row& v) {
   const int64_t N = p.N;
   for (int o = oi; o < oe; ++o) {
     const EpiOp op = p.prog.op[o];
     switch (op.kind) {
       case KF_OP_BIAS:
 #pragma unroll
-        for (int bj = 0; bj < 8; ++bj) v[bj] += load_col4(c, p.bias, N, bj);
+        for (int g = 0; g < 16; ++g) v[g] += load_col4(c, p.bias, N, g);
         break;
       case KF_OP_RESIDUAL_ADD: {
         const int64_t rows = min<int64_t>(BM, p.M - c.m0);
@@ -162,30 +153,30 @@ __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, 
           const uint16_t* base = reinterpret_cast<const uint16_t*>(p.residual) + c.m0 * p.ldr + c.n0;
           const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 2));
 #pragma unroll
-          for (int bj = 0; bj < 8; ++bj) {
-            const int cl = col_local(c, bj);
+          for (int g = 0; g < 16; ++g) {
+            const int cl = col_local(c, g);
             const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldr + cl) * 2) : kOOB;
             const u32x2 w = buf_load8(r, off);
-            v[bj] += f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+            v[g] += f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
           }
         } else {
           const float* base = reinterpret_cast<const float*>(p.residual) + c.m0 * p.ldr + c.n0;
           const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 4));
 #pragma unroll
-          for (int bj = 0; bj < 8; ++bj) {
-            const int cl = col_local(c, bj);
+          for (int g = 0; g < 16; ++g) {
+            const int cl = col_local(c, g);
             const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldr + cl) * 4) : kOOB;
-            v[bj] += __builtin_bit_cast(f32x4, buf_load16(r, off));
+            v[g] += __builtin_bit_cast(f32x4, buf_load16(r, off));
           }
         }
         break;
       }
 #define KF_EW_CASE(K, EXPR)                          \
   case K:                                            \
-    _Pragma("unroll") for (int bj = 0; bj < 8; ++bj) \
-    _Pragma("unroll") for (int r = 0; r < 4; ++r) {  \
-      const float x = v[bj][r];                      \
-      v[bj][r] = (EXPR);                             \
+    _Pragma("unroll") for (int g = 0; g < 16; ++g)   \
+    _Pragma("unroll") for (int q = 0; q < 4; ++q) {  \
+      const float x = v[g][q];                       \
+      v[g][q] = (EXPR);                              \
     }                                                \
     break;
       KF_EW_CASE(KF_OP_RELU, fmaxf(x, 0.0f))
@@ -203,11 +194,8 @@ __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, 
   }
 }
 
-__device__ __forceinline__ float sum4(f32x4 a) { return (a[0] + a[1]) + (a[2] + a[3]); }
-__device__ __forceinline__ float max4(f32x4 a) { return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])); }
-
-// Store one 16-row block (8 x 4 values per lane) to the output tile.
-__device__ __forceinline__ void store_block(const GemmArgs& p, const EpiCtx& c, int bi, const f32x4 (&v)[8]) {
+// Store one row block (16 runs of 4 values per lane).
+__device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, int bi, const Row& v) {
   const int64_t N = p.N;
   const int64_t rows = min<int64_t>(BM, p.M - c.m0);
   const int64_t rl = row_local(c, bi);
@@ -215,20 +203,19 @@ __device__ __forceinline__ void store_block(const GemmArgs& p, const EpiCtx& c, 
     uint16_t* base = reinterpret_cast<uint16_t*>(p.out) + c.m0 * p.ldo + c.n0;
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 2));
 #pragma unroll
-    for (int bj = 0; bj < 8; ++bj) {
-      const int cl = col_local(c, bj);
+    for (int g = 0; g < 16; ++g) {
+      const int cl = col_local(c, g);
       const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 2) : kOOB;
-      u32x2 w = {pack_bf16x2(v[bj][0], v[bj][1]), pack_bf16x2(v[bj][2], v[bj][3])};
-      buf_store8(w, r, off);
+      buf_store8(u32x2{pack_bf16x2(v[g][0], v[g][1]), pack_bf16x2(v[g][2], v[g][3])}, r, off);
     }
   } else {
     float* base = reinterpret_cast<float*>(p.out) + c.m0 * p.ldo + c.n0;
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 4));
 #pragma unroll
-    for (int bj = 0; bj < 8; ++bj) {
-      const int cl = col_local(c, bj);
+    for (int g = 0; g < 16; ++g) {
+      const int cl = col_local(c, g);
       const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 4) : kOOB;
-      buf_store16(__builtin_bit_cast(u32x4, v[bj]), r, off);
+      buf_store16(__builtin_bit_cast(u32x4, v[g]), r, off);
     }
   }
 }
@@ -238,138 +225,227 @@ __device__ __forceinline__ void store_block(const GemmArgs& p, const EpiCtx& c, 
 template <int EPI>
 __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c, Acc& acc) {
   const int64_t N = p.N;
-  float* red = reinterpret_cast<float*>(c.smem);
   const int nops = p.prog.n;
   const int r = EPI == kEpiPlain ? nops : p.red_index;
 
   if (EPI == kEpiPlain) {
-    static_for<0, 8>([&](auto bi_c) {
+    static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
-      f32x4 v[8];
+      Row v;
+      get_row(acc, bi, v);
 #pragma unroll
-      for (int bj = 0; bj < 8; ++bj) v[bj] = acc[bi][bj] * p.scale;
+      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
       apply_phase(p, c, bi, 0, nops, v);
-      store_block(p, c, bi, v);
+      store_row(p, c, bi, v);
     });
     return;
   }
 
-  // phase A: ops before the reduction, and each row's local statistic
-  float st[8];
-  static_for<0, 8>([&](auto bi_c) {
-    constexpr int bi = decltype(bi_c)::value;
-    f32x4 v[8];
-#pragma unroll
-    for (int bj = 0; bj < 8; ++bj) v[bj] = acc[bi][bj] * p.scale;
-    apply_phase(p, c, bi, 0, r, v);
-    float s;
-    if (EPI == kEpiGroupNorm) {
-      s = 0.0f;
-#pragma unroll
-      for (int bj = 0; bj < 8; ++bj) s += sum4(v[bj]);
-    } else {
-      // columns past N take no part in a row reduction
-#pragma unroll
-      for (int bj = 0; bj < 8; ++bj) {
-        const int64_t n = c.n0 + col_local(c, bj);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[bj][q] = (n + q < N) ? v[bj][q] : -INFINITY;
-      }
-      s = -INFINITY;
-#pragma unroll
-      for (int bj = 0; bj < 8; ++bj) s = fmaxf(s, max4(v[bj]));
-    }
-    st[bi] = s;
-#pragma unroll
-    for (int bj = 0; bj < 8; ++bj) acc[bi][bj] = v[bj];
-  });
-
-  const EpiOp op = p.prog.op[r];
   if (EPI == kEpiGroupNorm) {
-    // group width p.gn_group is 128 (one wave's half of the tile row) or 256
-    const bool whole = p.gn_group == 256;
-    const float inv_n = 1.0f / (float)p.gn_group;
-    if (whole) tile_row_reduce<false>(c, st, red); else wave_row_sum(st);
-    float mean[8], ss[8];
-#pragma unroll
-    for (int bi = 0; bi < 8; ++bi) {
-      mean[bi] = st[bi] * inv_n;
-      float s = 0.0f;
-#pragma unroll
-      for (int bj = 0; bj < 8; ++bj) {
-        const f32x4 d = acc[bi][bj] - mean[bi];
-        s += sum4(d * d);
-      }
-      ss[bi] = s;
-    }
-    if (whole) tile_row_reduce<false>(c, ss, red); else wave_row_sum(ss);
-    static_for<0, 8>([&](auto bi_c) {
+    // Group width gw in {32, 64, 128, 256} columns: each lane holds 16 of
+    // every 32-column block of its rows, so per-block sums are lane-local plus
+    // one exchange with lane ^ 32; wider groups add neighbouring blocks, and a
+    // 256-wide group also the other wave's half of the tile row.
+    const int gw = p.gn_group;
+    const int bpg = gw >> 5;  // 32-column blocks per group (1, 2, 4, 8)
+    const int bw = min(bpg, 4);
+    const float inv_n = 1.0f / (float)gw;
+    float s[4][4];
+    static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
-      const float rs = rsqrtf(ss[bi] * inv_n + op.p0);
-      f32x4 v[8];
+      Row v;
+      get_row(acc, bi, v);
 #pragma unroll
-      for (int bj = 0; bj < 8; ++bj) {
-        const f32x4 g = load_col4(c, p.gamma, N, bj);
-        const f32x4 be = load_col4(c, p.beta, N, bj);
-        v[bj] = (acc[bi][bj] - mean[bi]) * rs * g + be;
+      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+      apply_phase(p, c, bi, 0, r, v);
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj)
+        s[bi][bj] = (sum4(v[bj * 4]) + sum4(v[bj * 4 + 1])) + (sum4(v[bj * 4 + 2]) + sum4(v[bj * 4 + 3]));
+      put_row(acc, bi, v);
+    });
+    auto group_reduce = [&](float (&t)[4][4]) {
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) t[bi][bj] += shfl_xor(t[bi][bj], 32);
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi) {
+        float g2[4];
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) {
+          float a = 0.0f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) a += ((q / bw) == (bj / bw)) ? t[bi][q] : 0.0f;
+          g2[bj] = a;
+        }
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) t[bi][bj] = g2[bj];
+      }
+      if (bpg == 8) {
+        float w[4];
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) w[bi] = t[bi][0];
+        if (c.lane < 32) {
+#pragma unroll
+          for (int bi = 0; bi < 4; ++bi) c.red[c.wn * 256 + row_local(c, bi)] = w[bi];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) {
+          const float o = w[bi] + c.red[(c.wn ^ 1) * 256 + row_local(c, bi)];
+#pragma unroll
+          for (int bj = 0; bj < 4; ++bj) t[bi][bj] = o;
+        }
+        __syncthreads();
+      }
+    };
+    group_reduce(s);
+    float mean[4][4], ss[4][4];
+    static_for<0, 4>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) {
+        mean[bi][bj] = s[bi][bj] * inv_n;
+        float a = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const float d = acc[bi][bj][q] - mean[bi][bj];
+          a += d * d;
+        }
+        ss[bi][bj] = a;
+      }
+    });
+    group_reduce(ss);
+    const float eps = p.prog.op[r].p0;
+    static_for<0, 4>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      get_row(acc, bi, v);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int bj = g >> 2;
+        const float rs = rsqrtf(ss[bi][bj] * inv_n + eps);
+        v[g] = (v[g] - mean[bi][bj]) * rs * load_col4(c, p.gamma, N, g) + load_col4(c, p.beta, N, g);
       }
       apply_phase(p, c, bi, r + 1, nops, v);
-      store_block(p, c, bi, v);
+      store_row(p, c, bi, v);
     });
     return;
   }
 
   // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
   // this 256-column tile goes to the partials buffer.
-  tile_row_reduce<true>(c, st, red);
-  const bool softmax = op.kind == KF_OP_ROW_SOFTMAX;
-  float se[8];
-  static_for<0, 8>([&](auto bi_c) {
+  float mx[4];
+  static_for<0, 4>([&](auto bi_c) {
     constexpr int bi = decltype(bi_c)::value;
-    const float ml = st[bi] * kLog2e;
+    Row v;
+    get_row(acc, bi, v);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+    apply_phase(p, c, bi, 0, r, v);
+    // columns past N take no part in a row reduction
+    float m = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int64_t n = c.n0 + col_local(c, g);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[g][q] = (n + q < N) ? v[g][q] : -INFINITY;
+      m = fmaxf(m, max4(v[g]));
+    }
+    mx[bi] = m;
+    put_row(acc, bi, v);
+  });
+  row_combine<true>(c, mx, true);
+  float se[4];
+  static_for<0, 4>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    const float ml = mx[bi] * kLog2e;
     float s = 0.0f;
 #pragma unroll
-    for (int bj = 0; bj < 8; ++bj) {
-      f32x4 e;
+    for (int q = 0; q < 16; ++q)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) e[q] = __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
-      s += sum4(e);
-    }
+      for (int bj = 0; bj < 4; ++bj) s += __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
     se[bi] = s;
   });
-  tile_row_reduce<false>(c, se, red);
-  if (c.lane < 16 && c.wn == 0) {
+  row_combine<false>(c, se, true);
+  if (c.lane < 32 && c.wn == 0) {
     float2* part = reinterpret_cast<float2*>(p.partials);
     const int tn = (int)(c.n0 / BN);
 #pragma unroll
-    for (int bi = 0; bi < 8; ++bi) {
+    for (int bi = 0; bi < 4; ++bi) {
       const int64_t m = c.m0 + row_local(c, bi);
-      if (m < p.M) part[m * p.tiles_n + tn] = make_float2(st[bi], se[bi]);
+      if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
     }
   }
-  if (!softmax) return;  // logsumexp: the finishing kernel writes the output
+  if (p.prog.op[r].kind != KF_OP_ROW_SOFTMAX) return;  // logsumexp: the finishing kernel writes
   // softmax: store e^(h - tile max); the row-finishing kernel rescales it
-  static_for<0, 8>([&](auto bi_c) {
+  static_for<0, 4>([&](auto bi_c) {
     constexpr int bi = decltype(bi_c)::value;
-    const float ml = st[bi] * kLog2e;
-    f32x4 v[8];
+    const float ml = mx[bi] * kLog2e;
+    Row v;
+    get_row(acc, bi, v);
 #pragma unroll
-    for (int bj = 0; bj < 8; ++bj)
+    for (int g = 0; g < 16; ++g)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[bj][q] = __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
-    store_block(p, c, bi, v);
+      for (int q = 0; q < 4; ++q) v[g][q] = __builtin_amdgcn_exp2f(fmaf(v[g][q], kLog2e, -ml));
+    store_row(p, c, bi, v);
   });
+}
+
+// ---------------------------------------------------------------- main loop
+//
+// One __shared__ array per operand and stage (distinct objects, so the
+// compiler's wait-count analysis can tell the stage being filled by LDS DMA
+// from the stages being read).  An LDS DMA wave instruction writes 16 bytes
+// per lane at M0 + 16 * lane; the swizzles below are therefore applied on the
+// global side, by choosing which chunk each lane fetches.
+//
+//   A (and B-NK): [256 rows][32 k], 64-byte rows; chunk c of row m stored at
+//     chunk c ^ ((m >> 1) & 3), so 8 consecutive rows of a ds_read_b128
+//     fragment read hit 8 distinct 16-byte bank groups.
+//   B-KN: [32 k][256 n] with a 544-byte pitch: the four k-rows a 16-lane
+//     group of ds_read_b64_tr_b16 touches fall in four distinct 32-byte bank
+//     groups.
+
+constexpr int kBK = 32;
+constexpr int kAStage = BM * kBK * 2;    // 16 KiB
+constexpr int kBPitch = 544;             // B-KN row pitch in bytes
+constexpr int kBStage = kBK * kBPitch;   // 17 KiB = 17 DMA blocks of 1 KiB
+constexpr int kBStageNK = BN * kBK * 2;  // 16 KiB
+
+#define LDS3 __attribute__((address_space(3)))
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+// s_waitcnt vmcnt(N), the other counters left alone
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
 
 }  // namespace
 
 template <bool B_NK, int EPI>
 __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * kStageBytes];
+  constexpr int kBS = B_NK ? kBStageNK : kBStage;
+  __shared__ __attribute__((aligned(1024))) unsigned char sA0[kAStage], sA1[kAStage], sA2[kAStage], sA3[kAStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sB0[kBS], sB1[kBS], sB2[kBS], sB3[kBS];
+  __shared__ __attribute__((aligned(1024))) unsigned char sDummy[B_NK ? 16 : 1024];
+  auto stA = [&](auto S_c) -> unsigned char* {
+    constexpr int S = decltype(S_c)::value;
+    return S == 0 ? sA0 : S == 1 ? sA1 : S == 2 ? sA2 : sA3;
+  };
+  auto stB = [&](auto S_c) -> unsigned char* {
+    constexpr int S = decltype(S_c)::value;
+    return S == 0 ? sB0 : S == 1 ? sB1 : S == 2 ? sB2 : sB3;
+  };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1;
   const int wn = wave >> 1;
 
@@ -378,110 +454,172 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
   const int64_t m0 = (int64_t)tm * BM;
   const int64_t n0 = (int64_t)tn * BN;
   const int K = (int)p.K;
+  const int64_t lda = p.lda, ldb = p.ldb;
 
-  // ---- operand descriptors (base at the tile; records end at the last
-  // valid element, so rows past M / N read 0)
+  // operand descriptors: based at the tile, records ending at the last valid
+  // element, so rows past M / N (and past K for B-KN) read as zero
   const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
   const uint16_t* B = reinterpret_cast<const uint16_t*>(p.b);
   const int64_t rows_a = min<int64_t>(BM, p.M - m0);
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * p.lda, (uint32_t)(((rows_a - 1) * p.lda + K) * 2));
-  __amdgpu_buffer_rsrc_t rb;
-  if (B_NK) {
-    const int64_t rows_b = min<int64_t>(BN, p.N - n0);
-    rb = make_rsrc(B + n0 * p.ldb, (uint32_t)(((rows_b - 1) * p.ldb + K) * 2));
-  } else {
-    rb = make_rsrc(B + n0, (uint32_t)((((int64_t)K - 1) * p.ldb + (p.N - n0)) * 2));
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * lda, (uint32_t)(((rows_a - 1) * lda + K) * 2));
+  const int64_t rows_b = min<int64_t>(BN, p.N - n0);
+  const __amdgpu_buffer_rsrc_t rb =
+      B_NK ? make_rsrc(B + n0 * ldb, (uint32_t)(((rows_b - 1) * ldb + K) * 2))
+           : make_rsrc(B + n0, (uint32_t)(((max(K, 1) - 1) * ldb + (p.N - n0)) * 2));
+
+  // ---- DMA source offsets (loop invariant; the K-step enters as soffset)
+  // [rows][32 k] operands: wave w fills rows [64w, 64w + 64) with 4
+  // instructions of 16 rows; lane l -> row 16i + l/4, LDS chunk l%4, which
+  // holds global chunk (l%4) ^ ((l >> 3) & 3).
+  const int dma_lc = (lane & 3) ^ ((lane >> 3) & 3);
+  uint32_t va[4], vbn[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = wave * 64 + i * 16 + (lane >> 2);
+    va[i] = (uint32_t)(((int64_t)row * lda + dma_lc * 8) * 2);
+    vbn[i] = (uint32_t)(((int64_t)row * ldb + dma_lc * 8) * 2);
+  }
+  // B-KN: 17 blocks of 1 KiB per stage, block b = wave + 4 i; byte q of the
+  // stage is row q / 544, chunk (q % 544) / 16 (the pad reads as zero)
+  uint32_t vbk[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    const int b = wave + 4 * i;
+    const int pos = b * 1024 + lane * 16;
+    const int k = pos / kBPitch, col = pos % kBPitch;
+    const bool ok = b < 17 && col < 512 && (n0 + (col / 16) * 8 < p.N);
+    vbk[i] = ok ? (uint32_t)(((int64_t)k * ldb + (col / 16) * 8) * 2) : kOOB;
   }
 
-  // thread -> staging coordinates
-  const int a_row = tid >> 3;   // + 32 i
-  const int a_kc = tid & 7;     // 16-byte chunk within the 64-k row
-  const int b_kb = tid & 7;     // KN: 8-row k block
-  const int b_nb = tid >> 3;    // KN: 8-column n block (0..31)
-  const bool b_ncol_ok = B_NK ? true : (n0 + b_nb * 8 < p.N);
-
-  u32x4 sa[8], sb[8];
-
-  auto load_step = [&](int k0) {
+  auto dma = [&](auto S_c, int t) {
+    const int k0 = t * kBK;
+    const bool kin = k0 + dma_lc * 8 < K;  // K tail of a k-contiguous operand
+    unsigned char* dA = stA(S_c) + wave * 4096;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int gk = k0 + a_kc * 8;
-      const uint32_t off = gk < K ? (uint32_t)(((int64_t)(a_row + 32 * i) * p.lda + gk) * 2) : kOOB;
-      sa[i] = buf_load16(ra, off);
-    }
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (LDS3 void*)(dA + i * 1024), 16, kin ? va[i] : kOOB, k0 * 2, 0, 0);
     if (B_NK) {
+      unsigned char* dB = stB(S_c) + wave * 4096;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int gk = k0 + a_kc * 8;
-        const uint32_t off = gk < K ? (uint32_t)(((int64_t)(a_row + 32 * i) * p.ldb + gk) * 2) : kOOB;
-        sb[i] = buf_load16(rb, off);
-      }
+      for (int i = 0; i < 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(dB + i * 1024), 16, kin ? vbn[i] : kOOB, k0 * 2, 0, 0);
     } else {
+      unsigned char* dB = stB(S_c) + wave * 1024;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int gk = k0 + b_kb * 8 + i;
-        const uint32_t off = (gk < K && b_ncol_ok) ? (uint32_t)(((int64_t)gk * p.ldb + b_nb * 8) * 2) : kOOB;
-        sb[i] = buf_load16(rb, off);
-      }
+      for (int i = 0; i < 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(dB + i * 4096), 16, vbk[i], (int)(k0 * ldb * 2), 0, 0);
+      // block 16 belongs to wave 0; the other waves issue the same
+      // instruction out of range into a 1 KiB dummy region (out-of-range DMA
+      // lanes still write zeros, so they must not target block 16), which
+      // keeps the instruction stream free of branches
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(wave == 0 ? stB(S_c) + 16 * 1024 : sDummy), 16,
+                                                wave == 0 ? vbk[4] : kOOB, (int)(k0 * ldb * 2), 0, 0);
     }
   };
+  // VMEM instructions a wave issues per K-step
+  constexpr int kDmaPerStep = B_NK ? 8 : 9;
 
-  auto store_step = [&](int stage) {
-    unsigned char* sA = smem + stage * kStageBytes;
-    unsigned char* sB = sA + kOffB;
+  // ---- fragment read offsets (32x32x16: lane l holds row / column l & 31 and
+  // the 8-k group l >> 5 of a 16-k sub-step)
+  const int r32 = lane & 31, kg = lane >> 5;
+  uint32_t rA[2], rBn[2], rBk[2][2];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) lds_store(sA + swz(a_row + 32 * i, a_kc), sa[i]);
-    if (B_NK) {
+  for (int kk = 0; kk < 2; ++kk) {
+    const int ch = kk * 2 + kg;
+    rA[kk] = (uint32_t)((wm * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
+    rBn[kk] = (uint32_t)((wn * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
+    // transposed read: in 16-lane group g, lane 4r + q points at k-row
+    // kk*16 + (g>>1)*8 + h*4 + r, columns (g&1)*16 + 4q .. +3 of the block
+    const int g = lane >> 4, rr = (lane >> 2) & 3, q = lane & 3;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) lds_store(sB + swz(a_row + 32 * i, a_kc), sb[i]);
-    } else {
-      // 8x8 transpose of bf16: sb[i] holds k = kb*8+i, n = nb*8 .. nb*8+7.
+    for (int h = 0; h < 2; ++h)
+      rBk[kk][h] = (uint32_t)((kk * 16 + (g >> 1) * 8 + h * 4 + rr) * kBPitch + (wn * 128 + (g & 1) * 16 + q * 4) * 2);
+  }
+
+  bf16x8 fa[2][2][4], fb[2][2][4];  // [buffer][16-k half][block]
+
+  auto read_frags = [&](auto S_c, auto BUF_c) {
+    constexpr int BUF = decltype(BUF_c)::value;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-        u32x4 o;
+    for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = perm(sb[2 * e + 1][j >> 1], sb[2 * e][j >> 1], sel);
-        lds_store(sB + swz(b_nb * 8 + j, b_kb), o);
+      for (int bi = 0; bi < 4; ++bi) fa[BUF][kk][bi] = lds_load<bf16x8>(stA(S_c) + rA[kk] + bi * 2048);
+      if (B_NK) {
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) fb[BUF][kk][bj] = lds_load<bf16x8>(stB(S_c) + rBn[kk] + bj * 2048);
+      } else {
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) {
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[kk][0] + bj * 64));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[kk][1] + bj * 64));
+          fb[BUF][kk][bj] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
       }
     }
   };
 
   Acc acc;
 #pragma unroll
-  for (int bi = 0; bi < 8; ++bi)
+  for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
-    for (int bj = 0; bj < 8; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int bj = 0; bj < 4; ++bj)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
 
-  const int nk = (K + BK - 1) / BK;
-  load_step(0);
-  store_step(0);
+  // K-step t on stage S with fragments in buffer BUF: publish stage S+1 (its
+  // DMA, issued three steps earlier, has landed), refill stage S+3 (= the
+  // stage of step t-1, which every wave has finished reading), then the 32
+  // MFMAs of step t overlapped with the fragment reads of step t+1.
+  auto step = [&](auto S_c, auto BUF_c, int t, int nk) {
+    constexpr int S = decltype(S_c)::value;
+    constexpr int BUF = decltype(BUF_c)::value;
+    wait_vmcnt<kDmaPerStep>();
+    __builtin_amdgcn_s_barrier();
+    // Both unconditional, so that they share one basic block with the MFMAs
+    // they are interleaved with: past the last K-step the DMA lanes are all
+    // out of range (zeros into a stage nobody reads) and the fragment reads
+    // read a stale stage that is never used.
+    dma(IC<(S + 3) & 3>{}, t + 3);
+    read_frags(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{});
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj)
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[BUF][kk][bj], fa[BUF][kk][bi], acc[bi][bj], 0, 0, 0);
+    constexpr int kReads = B_NK ? 16 : 24;
+    constexpr int kDma = B_NK ? 8 : 9;
+#pragma unroll
+    for (int i = 0; i < kReads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // DS read
+      if (i < kDma) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // LDS DMA
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 32 - kReads, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  const int nk = (K + kBK - 1) / kBK;
+  dma(IC<0>{}, 0);
+  if (1 < nk) dma(IC<1>{}, 1);
+  if (2 < nk) dma(IC<2>{}, 2);
+  __syncthreads();  // waits for every DMA issued so far
+  if (nk > 0) read_frags(IC<0>{}, IC<0>{});
+
+  int t = 0;
+  for (; t + 4 <= nk; t += 4) {
+    step(IC<0>{}, IC<0>{}, t, nk);
+    step(IC<1>{}, IC<1>{}, t + 1, nk);
+    step(IC<2>{}, IC<0>{}, t + 2, nk);
+    step(IC<3>{}, IC<1>{}, t + 3, nk);
+  }
+  if (t < nk) step(IC<0>{}, IC<0>{}, t, nk);
+  if (t + 1 < nk) step(IC<1>{}, IC<1>{}, t + 1, nk);
+  if (t + 2 < nk) step(IC<2>{}, IC<0>{}, t + 2, nk);
   __syncthreads();
 
-  for (int t = 0; t < nk; ++t) {
-    const int stage = t & 1;
-    if (t + 1 < nk) load_step((t + 1) * BK);
-    const unsigned char* sA = smem + stage * kStageBytes;
-    const unsigned char* sB = sA + kOffB;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int chunk = kk * 4 + (lane >> 4);
-      bf16x8 fa[8], fb[8];
-#pragma unroll
-      for (int bi = 0; bi < 8; ++bi) fa[bi] = lds_load<bf16x8>(sA + swz(wm * 128 + bi * 16 + (lane & 15), chunk));
-#pragma unroll
-      for (int bj = 0; bj < 8; ++bj) fb[bj] = lds_load<bf16x8>(sB + swz(wn * 128 + bj * 16 + (lane & 15), chunk));
-#pragma unroll
-      for (int bi = 0; bi < 8; ++bi)
-#pragma unroll
-        for (int bj = 0; bj < 8; ++bj)
-          acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[bj], fa[bi], acc[bi][bj], 0, 0, 0);
-    }
-    if (t + 1 < nk) store_step(stage ^ 1);
-    __syncthreads();
-  }
-
-  EpiCtx c{lane, wm, wn, m0, n0, smem};
+  EpiCtx c{lane, wm, wn, m0, n0, reinterpret_cast<float*>(sA0)};
   run_epilogue<EPI>(p, c, acc);
 }
 
@@ -514,7 +652,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& args, int epi, hipStream_t stream, b
   return hipGetLastError();
 }
 
-int gemm_bf16_tile_n() { return BN; }
 int gemm_bf16_tile_m() { return BM; }
+int gemm_bf16_tile_n() { return BN; }
 
 }  // namespace kf

@@ -328,6 +328,11 @@ size_t kf_workspace_bytes(const kf_desc* d) { return d ? d->workspace_bytes : 0;
 const char* kf_kernel_name(const kf_desc* d) { return d ? d->kernel_name.c_str() : ""; }
 
 kf_status kf_fused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
+  return kf_fused_op_timed(d, inputs, outputs, stream, nullptr, nullptr);
+}
+
+kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream,
+                            void* ev_before, void* ev_after) {
   if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
   for (size_t i = 0; i < d->inputs.size(); ++i) {
     kf_status st = check_tensor(&inputs[i], d->inputs[i], false, d->variant != kVarGemmF32);
@@ -373,15 +378,20 @@ kf_status kf_fused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outp
     a.out_bf16 = outputs[0].dtype == KF_BF16;
     a.partials = d->workspace;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
-    hipError_t e;
+    hipError_t e = hipSuccess;
+    if (ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
+    if (e != hipSuccess) return fail(KF_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
     if (d->variant == kVarGemmF32) {
       e = kf::launch_gemm_f32(a, nk, hs);
+      if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
     } else {
       const int64_t es = elem_size(s.in_dtype);
-      if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : std::max<int64_t>(s.K, 1) * a.ldb) * es) ||
+      // the K loop addresses up to three 32-deep steps past K (all out of range)
+      if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : (s.K + 128) * a.ldb) * es) ||
           !fits_31(256 * a.ldo * 4) || (a.residual && !fits_31(256 * a.ldr * 4)))
         return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
       e = kf::launch_gemm_bf16(a, d->epi_shape, hs, nk);
+      if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
       if (e == hipSuccess && d->row_kind)
         e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, d->workspace, d->tiles_n, s.M, s.N, a.out,
                                   a.ldo, a.out_bf16 != 0, hs);

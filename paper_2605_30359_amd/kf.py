@@ -32,7 +32,7 @@ OP_KINDS = {
 DTYPES = {"f32": KF_F32, "bf16": KF_BF16, "e4m3": KF_FP8_E4M3}
 DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 
-EXPORTED = ("kf_create", "kf_fused_op", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
+EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error")
 
@@ -80,6 +80,8 @@ def lib():
         L.kf_create.restype = i32
         L.kf_fused_op.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp]
         L.kf_fused_op.restype = i32
+        L.kf_fused_op_timed.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp, vp, vp]
+        L.kf_fused_op_timed.restype = i32
         L.kf_unfused_op.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp]
         L.kf_unfused_op.restype = i32
         L.kf_destroy.argtypes = [vp]
@@ -259,7 +261,7 @@ class FusedOp:
         dt, shp = self.output_info()
         return torch.empty(shp, dtype=torch_dtype(DTYPES[dt]), device=device)
 
-    def _call(self, fn, inputs, out, stream):
+    def _call(self, fn, inputs, out, stream, events=None):
         torch = _torch()
         if out is None:
             out = self.empty_output(inputs[0].device)
@@ -269,11 +271,19 @@ class FusedOp:
             stream = torch.cuda.current_stream(out.device).cuda_stream
         elif not isinstance(stream, int):
             stream = stream.cuda_stream
-        _check(fn(self._h, arr, o, ctypes.c_void_p(stream)))
+        if events is None:
+            _check(fn(self._h, arr, o, ctypes.c_void_p(stream)))
+        else:
+            _check(fn(self._h, arr, o, ctypes.c_void_p(stream), ctypes.c_void_p(events[0]), ctypes.c_void_p(events[1])))
         return out
 
     def __call__(self, inputs, out=None, stream=None):
         return self._call(lib().kf_fused_op, inputs, out, stream)
+
+    def timed(self, inputs, out, ev_before: int, ev_after: int, stream=None):
+        """Like __call__, recording two caller-created hipEvent_t handles
+        around the main contraction kernel."""
+        return self._call(lib().kf_fused_op_timed, inputs, out, stream, (ev_before, ev_after))
 
     def unfused(self, inputs, out=None, stream=None):
         return self._call(lib().kf_unfused_op, inputs, out, stream)
