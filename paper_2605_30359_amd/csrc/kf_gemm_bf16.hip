@@ -491,23 +491,21 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
     vbk[i] = ok ? (uint32_t)(((int64_t)k * ldb + (col / 16) * 8) * 2) : kOOB;
   }
 
-  auto dma = [&](auto S_c, int t) {
+  // DMA instruction j (0 .. kDma-1) of K-step t into stage S
+  auto dma_one = [&](auto S_c, auto J_c, int t) {
+    constexpr int J = decltype(J_c)::value;
     const int k0 = t * kBK;
     const bool kin = k0 + dma_lc * 8 < K;  // K tail of a k-contiguous operand
-    unsigned char* dA = stA(S_c) + wave * 4096;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (LDS3 void*)(dA + i * 1024), 16, kin ? va[i] : kOOB, k0 * 2, 0, 0);
-    if (B_NK) {
-      unsigned char* dB = stB(S_c) + wave * 4096;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(dB + i * 1024), 16, kin ? vbn[i] : kOOB, k0 * 2, 0, 0);
+    if (J < 4) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (LDS3 void*)(stA(S_c) + wave * 4096 + J * 1024), 16,
+                                                kin ? va[J] : kOOB, k0 * 2, 0, 0);
+    } else if (B_NK) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 4096 + (J - 4) * 1024), 16,
+                                                kin ? vbn[J - 4] : kOOB, k0 * 2, 0, 0);
+    } else if (J < 8) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 1024 + (J - 4) * 4096), 16,
+                                                vbk[J - 4], (int)(k0 * ldb * 2), 0, 0);
     } else {
-      unsigned char* dB = stB(S_c) + wave * 1024;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(dB + i * 4096), 16, vbk[i], (int)(k0 * ldb * 2), 0, 0);
       // block 16 belongs to wave 0; the other waves issue the same
       // instruction out of range into a 1 KiB dummy region (out-of-range DMA
       // lanes still write zeros, so they must not target block 16), which
@@ -516,8 +514,9 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
                                                 wave == 0 ? vbk[4] : kOOB, (int)(k0 * ldb * 2), 0, 0);
     }
   };
-  // VMEM instructions a wave issues per K-step
-  constexpr int kDmaPerStep = B_NK ? 8 : 9;
+  auto dma = [&](auto S_c, int t) {
+    static_for<0, (B_NK ? 8 : 9)>([&](auto J_c) { dma_one(S_c, J_c, t); });
+  };
 
   // ---- fragment read offsets (32x32x16: lane l holds row / column l & 31 and
   // the 8-k group l >> 5 of a 16-k sub-step)
@@ -537,25 +536,34 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
   }
 
   bf16x8 fa[2][2][4], fb[2][2][4];  // [buffer][16-k half][block]
+  i16x4 fbt[2][2][4][2];             // B-KN halves of fb from the transposed reads
 
-  auto read_frags = [&](auto S_c, auto BUF_c) {
+  // Fragment read j of a K-step (in the order the next step consumes them):
+  // per 16-k half, the 4 A fragments then the 4 B fragments (two transposed
+  // reads each for B-KN, one ds_read_b128 for B-NK).
+  constexpr int kReads = B_NK ? 16 : 24;
+  auto read_one = [&](auto S_c, auto BUF_c, auto J_c) {
     constexpr int BUF = decltype(BUF_c)::value;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-      for (int bi = 0; bi < 4; ++bi) fa[BUF][kk][bi] = lds_load<bf16x8>(stA(S_c) + rA[kk] + bi * 2048);
-      if (B_NK) {
-#pragma unroll
-        for (int bj = 0; bj < 4; ++bj) fb[BUF][kk][bj] = lds_load<bf16x8>(stB(S_c) + rBn[kk] + bj * 2048);
-      } else {
-#pragma unroll
-        for (int bj = 0; bj < 4; ++bj) {
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[kk][0] + bj * 64));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[kk][1] + bj * 64));
-          fb[BUF][kk][bj] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        }
-      }
+    constexpr int J = decltype(J_c)::value;
+    constexpr int per = kReads / 2;
+    constexpr int kk = J / per, j = J % per;
+    if (j < 4) {
+      fa[BUF][kk][j] = lds_load<bf16x8>(stA(S_c) + rA[kk] + j * 2048);
+    } else if (B_NK) {
+      fb[BUF][kk][j - 4] = lds_load<bf16x8>(stB(S_c) + rBn[kk] + (j - 4) * 2048);
+    } else {
+      constexpr int bj = (j - 4) / 2, h = (j - 4) % 2;
+      fbt[BUF][kk][bj][h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[kk][h] + bj * 64));
     }
+  };
+  auto read_frags = [&](auto S_c, auto BUF_c) {
+    static_for<0, kReads>([&](auto J_c) { read_one(S_c, BUF_c, J_c); });
+  };
+  auto b_frag = [&](auto BUF_c, int kk, int bj) -> bf16x8 {
+    constexpr int BUF = decltype(BUF_c)::value;
+    if (B_NK) return fb[BUF][kk][bj];
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(fbt[BUF][kk][bj][0], fbt[BUF][kk][bj][1], 0, 1, 2,
+                                                              3, 4, 5, 6, 7));
   };
 
   Acc acc;
@@ -567,56 +575,49 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
       for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
 
   // K-step t on stage S with fragments in buffer BUF: publish stage S+1 (its
-  // DMA, issued three steps earlier, has landed), refill stage S+3 (= the
-  // stage of step t-1, which every wave has finished reading), then the 32
-  // MFMAs of step t overlapped with the fragment reads of step t+1.
-  auto step = [&](auto S_c, auto BUF_c, int t, int nk) {
+  // DMA, issued three steps earlier, has landed), then the 32 MFMAs of step t
+  // in a fixed order, with the fragment reads of step t+1 (from stage S+1)
+  // and the DMA of step t+3 (into stage S+3 = the stage of step t-1, which
+  // every wave has finished reading) placed between them: the reads one per
+  // MFMA from the start, the DMA instructions spread evenly, so that neither
+  // the LDS queue nor the texture address FIFO backs up into the wave's
+  // in-order instruction stream.  Past the last K-step the DMA lanes are all
+  // out of range (zeros into a stage nobody reads) and the reads read a
+  // stale stage that is never used, so nothing here is conditional.
+  constexpr int kDma = B_NK ? 8 : 9;
+  auto step = [&](auto S_c, auto BUF_c, int t) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
-    wait_vmcnt<kDmaPerStep>();
+    wait_vmcnt<kDma>();
     __builtin_amdgcn_s_barrier();
-    // Both unconditional, so that they share one basic block with the MFMAs
-    // they are interleaved with: past the last K-step the DMA lanes are all
-    // out of range (zeros into a stage nobody reads) and the fragment reads
-    // read a stale stage that is never used.
-    dma(IC<(S + 3) & 3>{}, t + 3);
-    read_frags(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{});
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int bi = 0; bi < 4; ++bi)
-#pragma unroll
-        for (int bj = 0; bj < 4; ++bj)
-          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[BUF][kk][bj], fa[BUF][kk][bi], acc[bi][bj], 0, 0, 0);
-    constexpr int kReads = B_NK ? 16 : 24;
-    constexpr int kDma = B_NK ? 8 : 9;
-#pragma unroll
-    for (int i = 0; i < kReads; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // DS read
-      if (i < kDma) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // LDS DMA
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 32 - kReads, 0);
     __builtin_amdgcn_sched_barrier(0);
+    static_for<0, 32>([&](auto I_c) {
+      constexpr int i = decltype(I_c)::value;
+      constexpr int kk = i / 16, bi = (i / 4) % 4, bj = i % 4;
+      acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b_frag(BUF_c, kk, bj), fa[BUF][kk][bi], acc[bi][bj], 0, 0, 0);
+      if constexpr (i < kReads) read_one(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{}, IC<i>{});
+      if constexpr ((i * kDma) / 32 != ((i + 1) * kDma) / 32) dma_one(IC<(S + 3) & 3>{}, IC<(i * kDma) / 32>{}, t + 3);
+      __builtin_amdgcn_sched_barrier(0);
+    });
   };
 
   const int nk = (K + kBK - 1) / kBK;
   dma(IC<0>{}, 0);
-  if (1 < nk) dma(IC<1>{}, 1);
-  if (2 < nk) dma(IC<2>{}, 2);
+  dma(IC<1>{}, 1);
+  dma(IC<2>{}, 2);
   __syncthreads();  // waits for every DMA issued so far
-  if (nk > 0) read_frags(IC<0>{}, IC<0>{});
+  read_frags(IC<0>{}, IC<0>{});
 
   int t = 0;
   for (; t + 4 <= nk; t += 4) {
-    step(IC<0>{}, IC<0>{}, t, nk);
-    step(IC<1>{}, IC<1>{}, t + 1, nk);
-    step(IC<2>{}, IC<0>{}, t + 2, nk);
-    step(IC<3>{}, IC<1>{}, t + 3, nk);
+    step(IC<0>{}, IC<0>{}, t);
+    step(IC<1>{}, IC<1>{}, t + 1);
+    step(IC<2>{}, IC<0>{}, t + 2);
+    step(IC<3>{}, IC<1>{}, t + 3);
   }
-  if (t < nk) step(IC<0>{}, IC<0>{}, t, nk);
-  if (t + 1 < nk) step(IC<1>{}, IC<1>{}, t + 1, nk);
-  if (t + 2 < nk) step(IC<2>{}, IC<0>{}, t + 2, nk);
+  if (t < nk) step(IC<0>{}, IC<0>{}, t);
+  if (t + 1 < nk) step(IC<1>{}, IC<1>{}, t + 1);
+  if (t + 2 < nk) step(IC<2>{}, IC<0>{}, t + 2);
   __syncthreads();
 
   EpiCtx c{lane, wm, wn, m0, n0, reinterpret_cast<float*>(sA0)};
