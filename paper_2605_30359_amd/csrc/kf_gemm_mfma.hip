@@ -1,6 +1,6 @@
-// bf16 GEMM + fused epilogue on gfx950 matrix cores.
+// bf16 / fp8 GEMM + fused epilogue on gfx950 matrix cores.
 //
-// h = A * B with A [M,K] bf16 row-major and B either [K,N] ("KN", N
+// h = A * B with A [M,K] row-major and B either [K,N] ("KN", N
 // contiguous) or [N,K] ("NK", K contiguous), fp32 accumulation, then the op
 // list (bias, activations, scale, GroupNorm, residual add, row softmax /
 // logsumexp partials) applied to the accumulator registers, then one store.
@@ -9,18 +9,20 @@
 // kernel), laid out for CDNA4:
 //
 //   tile     256 x 256 outputs per workgroup of 4 waves (2 x 2); each wave
-//            owns 128 x 128 = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16, the
-//            bf16 MFMA shape that sustains the full matrix-core rate (one
-//            instruction per 32 cycles per SIMD); accumulators live in AGPRs
-//   K loop   BK = 32 per step, four LDS stages; operands move global -> LDS
+//            owns 128 x 128 = 4 x 4 blocks of 32 x 32 MFMA outputs
+//            (v_mfma_f32_32x32x16_bf16, or for OCP fp8 e4m3 operands
+//            v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales and the
+//            per-tensor dequantisation applied to the accumulator), the shapes
+//            that sustain the full matrix-core rate; accumulators in AGPRs
+//   K loop   64 bytes of k per step, four LDS stages; operands move global -> LDS
 //            by buffer_load ... lds (LDS DMA), issued three steps ahead, so no
 //            VGPR stages operand data; out-of-range lanes of a DMA write zeros,
 //            which pads ragged M, N and K tails without branches
-//   LDS      A (and B in NK layout) as [rows][32 k] with an XOR swizzle of the
-//            16-byte chunks; B in KN layout kept as [32 k][256 n] with a
-//            padded 544-byte row pitch and read through ds_read_b64_tr_b16,
-//            which transposes 4 x 16 element blocks across each 16-lane group
-//            so every lane receives 8 consecutive k of one column
+//   LDS      A (and B in NK layout) as [rows][64 bytes of k] with an XOR swizzle
+//            of the 16-byte chunks; B in KN layout kept as [k][256 n] with a
+//            padded row pitch and read through ds_read_b64_tr_b16 / _tr_b8,
+//            which transpose small blocks across each 16-lane group so every
+//            lane receives consecutive k of one column
 //   order    the B fragment is the MFMA "A" operand, so each lane's
 //            accumulators are runs of 4 consecutive output columns of one row:
 //            8-byte bf16 / 16-byte fp32 stores, lane-local row reductions
@@ -400,21 +402,39 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 // per lane at M0 + 16 * lane; the swizzles below are therefore applied on the
 // global side, by choosing which chunk each lane fetches.
 //
-//   A (and B-NK): [256 rows][32 k], 64-byte rows; chunk c of row m stored at
-//     chunk c ^ ((m >> 1) & 3), so 8 consecutive rows of a ds_read_b128
-//     fragment read hit 8 distinct 16-byte bank groups.
-//   B-KN: [32 k][256 n] with a 544-byte pitch: the four k-rows a 16-lane
-//     group of ds_read_b64_tr_b16 touches fall in four distinct 32-byte bank
-//     groups.
+// A K-step covers 64 bytes of k: 32 bf16 or 64 fp8.
+//   A (and B-NK): [256 rows][64 bytes of k]; chunk c of row m stored at chunk
+//     c ^ ((m >> 1) & 3), so 8 consecutive rows of a ds_read_b128 fragment
+//     read hit 8 distinct 16-byte bank groups.
+//   B-KN: [k][256 n] rows with a padded pitch (bf16: 32 rows of 544 bytes,
+//     fp8: 64 rows of 272 bytes; 17 KiB either way), read through the
+//     transposing ds_read_b64_tr_b16 / _b8: in each 16-lane group the lanes
+//     point at 4 (8) k-rows and receive the k values of their own column, and
+//     the pitch puts those rows in distinct bank groups.
+//
+// MFMA: bf16 v_mfma_f32_32x32x16_bf16 (32 per step, two 16-k halves), fp8
+// v_mfma_scale_f32_32x32x64_f8f6f4 with unit block scales (16 per step); both
+// run at the full matrix-core rate and leave the same 32x32 accumulator
+// layout, so the epilogue is shared.
 
-constexpr int kBK = 32;
-constexpr int kAStage = BM * kBK * 2;    // 16 KiB
-constexpr int kBPitch = 544;             // B-KN row pitch in bytes
-constexpr int kBStage = kBK * kBPitch;   // 17 KiB = 17 DMA blocks of 1 KiB
-constexpr int kBStageNK = BN * kBK * 2;  // 16 KiB
+template <bool FP8>
+struct ElemCfg;
+template <>
+struct ElemCfg<false> {  // bf16
+  static constexpr int ES = 2, KSTEP = 32, NMFMA = 32, BPITCH = 544;
+};
+template <>
+struct ElemCfg<true> {  // OCP fp8 e4m3
+  static constexpr int ES = 1, KSTEP = 64, NMFMA = 16, BPITCH = 272;
+};
+
+constexpr int kAStage = BM * 64;           // 16 KiB
+constexpr int kBStageKN = 17 * 1024;       // 17 KiB = 17 DMA blocks of 1 KiB
+constexpr int kBStageNK = BN * 64;         // 16 KiB
 
 #define LDS3 __attribute__((address_space(3)))
 typedef __attribute__((ext_vector_type(4))) short i16x4;
+typedef __attribute__((ext_vector_type(2))) int i32x2;
 
 template <int V>
 using IC = std::integral_constant<int, V>;
@@ -428,9 +448,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 }  // namespace
 
-template <bool B_NK, int EPI>
-__global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
-  constexpr int kBS = B_NK ? kBStageNK : kBStage;
+template <bool FP8, bool B_NK, int EPI>
+__global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
+  using C = ElemCfg<FP8>;
+  constexpr int ES = C::ES;
+  constexpr int kBS = B_NK ? kBStageNK : kBStageKN;
   __shared__ __attribute__((aligned(1024))) unsigned char sA0[kAStage], sA1[kAStage], sA2[kAStage], sA3[kAStage];
   __shared__ __attribute__((aligned(1024))) unsigned char sB0[kBS], sB1[kBS], sB2[kBS], sB3[kBS];
   __shared__ __attribute__((aligned(1024))) unsigned char sDummy[B_NK ? 16 : 1024];
@@ -458,17 +480,17 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
 
   // operand descriptors: based at the tile, records ending at the last valid
   // element, so rows past M / N (and past K for B-KN) read as zero
-  const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
-  const uint16_t* B = reinterpret_cast<const uint16_t*>(p.b);
+  const unsigned char* A = reinterpret_cast<const unsigned char*>(p.a);
+  const unsigned char* B = reinterpret_cast<const unsigned char*>(p.b);
   const int64_t rows_a = min<int64_t>(BM, p.M - m0);
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * lda, (uint32_t)(((rows_a - 1) * lda + K) * 2));
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * lda * ES, (uint32_t)(((rows_a - 1) * lda + K) * ES));
   const int64_t rows_b = min<int64_t>(BN, p.N - n0);
   const __amdgpu_buffer_rsrc_t rb =
-      B_NK ? make_rsrc(B + n0 * ldb, (uint32_t)(((rows_b - 1) * ldb + K) * 2))
-           : make_rsrc(B + n0, (uint32_t)(((max(K, 1) - 1) * ldb + (p.N - n0)) * 2));
+      B_NK ? make_rsrc(B + n0 * ldb * ES, (uint32_t)(((rows_b - 1) * ldb + K) * ES))
+           : make_rsrc(B + n0 * ES, (uint32_t)(((max(K, 1) - 1) * ldb + (p.N - n0)) * ES));
 
-  // ---- DMA source offsets (loop invariant; the K-step enters as soffset)
-  // [rows][32 k] operands: wave w fills rows [64w, 64w + 64) with 4
+  // ---- DMA source byte offsets (loop invariant; the K-step enters as soffset)
+  // [rows][64 B] operands: wave w fills rows [64w, 64w + 64) with 4
   // instructions of 16 rows; lane l -> row 16i + l/4, LDS chunk l%4, which
   // holds global chunk (l%4) ^ ((l >> 3) & 3).
   const int dma_lc = (lane & 3) ^ ((lane >> 3) & 3);
@@ -476,94 +498,118 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = wave * 64 + i * 16 + (lane >> 2);
-    va[i] = (uint32_t)(((int64_t)row * lda + dma_lc * 8) * 2);
-    vbn[i] = (uint32_t)(((int64_t)row * ldb + dma_lc * 8) * 2);
+    va[i] = (uint32_t)((int64_t)row * lda * ES + dma_lc * 16);
+    vbn[i] = (uint32_t)((int64_t)row * ldb * ES + dma_lc * 16);
   }
   // B-KN: 17 blocks of 1 KiB per stage, block b = wave + 4 i; byte q of the
-  // stage is row q / 544, chunk (q % 544) / 16 (the pad reads as zero)
+  // stage is row q / BPITCH, byte (q % BPITCH) of the row (the pad reads as zero)
   uint32_t vbk[5];
 #pragma unroll
   for (int i = 0; i < 5; ++i) {
     const int b = wave + 4 * i;
     const int pos = b * 1024 + lane * 16;
-    const int k = pos / kBPitch, col = pos % kBPitch;
-    const bool ok = b < 17 && col < 512 && (n0 + (col / 16) * 8 < p.N);
-    vbk[i] = ok ? (uint32_t)(((int64_t)k * ldb + (col / 16) * 8) * 2) : kOOB;
+    const int k = pos / C::BPITCH, col = pos % C::BPITCH;
+    const bool ok = b < 17 && col < 256 * ES && (n0 + col / ES < p.N);
+    vbk[i] = ok ? (uint32_t)((int64_t)k * ldb * ES + col) : kOOB;
   }
 
   // DMA instruction j (0 .. kDma-1) of K-step t into stage S
   auto dma_one = [&](auto S_c, auto J_c, int t) {
     constexpr int J = decltype(J_c)::value;
-    const int k0 = t * kBK;
-    const bool kin = k0 + dma_lc * 8 < K;  // K tail of a k-contiguous operand
+    const int k0 = t * C::KSTEP;
+    const bool kin = k0 + dma_lc * (16 / ES) < K;  // K tail of a k-contiguous operand
     if (J < 4) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (LDS3 void*)(stA(S_c) + wave * 4096 + J * 1024), 16,
-                                                kin ? va[J] : kOOB, k0 * 2, 0, 0);
+                                                kin ? va[J] : kOOB, k0 * ES, 0, 0);
     } else if (B_NK) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 4096 + (J - 4) * 1024), 16,
-                                                kin ? vbn[J - 4] : kOOB, k0 * 2, 0, 0);
+                                                kin ? vbn[J - 4] : kOOB, k0 * ES, 0, 0);
     } else if (J < 8) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 1024 + (J - 4) * 4096), 16,
-                                                vbk[J - 4], (int)(k0 * ldb * 2), 0, 0);
+                                                vbk[J - 4], (int)(k0 * ldb * ES), 0, 0);
     } else {
       // block 16 belongs to wave 0; the other waves issue the same
       // instruction out of range into a 1 KiB dummy region (out-of-range DMA
       // lanes still write zeros, so they must not target block 16), which
       // keeps the instruction stream free of branches
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(wave == 0 ? stB(S_c) + 16 * 1024 : sDummy), 16,
-                                                wave == 0 ? vbk[4] : kOOB, (int)(k0 * ldb * 2), 0, 0);
+                                                wave == 0 ? vbk[4] : kOOB, (int)(k0 * ldb * ES), 0, 0);
     }
   };
-  auto dma = [&](auto S_c, int t) {
-    static_for<0, (B_NK ? 8 : 9)>([&](auto J_c) { dma_one(S_c, J_c, t); });
-  };
+  constexpr int kDma = B_NK ? 8 : 9;
+  auto dma = [&](auto S_c, int t) { static_for<0, kDma>([&](auto J_c) { dma_one(S_c, J_c, t); }); };
 
-  // ---- fragment read offsets (32x32x16: lane l holds row / column l & 31 and
-  // the 8-k group l >> 5 of a 16-k sub-step)
+  // ---- fragment read offsets.  32x32 MFMA operand lane l: row / column
+  // l & 31, k-group l >> 5.  bf16: fragment half h is the 16-k sub-step h
+  // (chunk 2h + kg); fp8: the two halves are the 32 bytes of k-group kg
+  // (chunks 2kg, 2kg + 1).
   const int r32 = lane & 31, kg = lane >> 5;
-  uint32_t rA[2], rBn[2], rBk[2][2];
+  uint32_t rA[2], rBn[2];
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int ch = kk * 2 + kg;
-    rA[kk] = (uint32_t)((wm * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
-    rBn[kk] = (uint32_t)((wn * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
-    // transposed read: in 16-lane group g, lane 4r + q points at k-row
-    // kk*16 + (g>>1)*8 + h*4 + r, columns (g&1)*16 + 4q .. +3 of the block
-    const int g = lane >> 4, rr = (lane >> 2) & 3, q = lane & 3;
+  for (int h = 0; h < 2; ++h) {
+    const int ch = FP8 ? kg * 2 + h : h * 2 + kg;
+    rA[h] = (uint32_t)((wm * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
+    rBn[h] = (uint32_t)((wn * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
+  }
+  // transposed B-KN reads, 16-lane group g = lane >> 4 (k-group g >> 1, column
+  // half g & 1).  bf16: read (kk, h) gives k = kk*16 + (g>>1)*8 + h*4 + 0..3,
+  // lane 4r + q points at k-row (.. + r), columns 4q .. 4q+3 of its half.
+  // fp8: read h gives k = (g>>1)*32 + h*8 + 0..7, lane 2r + q points at k-row
+  // (.. + r), columns 8q .. 8q+7 of its half.
+  uint32_t rBk[4];
+  {
+    const int g = lane >> 4;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-      rBk[kk][h] = (uint32_t)((kk * 16 + (g >> 1) * 8 + h * 4 + rr) * kBPitch + (wn * 128 + (g & 1) * 16 + q * 4) * 2);
+    for (int x = 0; x < 4; ++x) {
+      if (FP8) {
+        const int r = (lane >> 1) & 7, q = lane & 1;
+        rBk[x] = (uint32_t)(((g >> 1) * 32 + x * 8 + r) * C::BPITCH + wn * 128 + (g & 1) * 16 + q * 8);
+      } else {
+        const int kk = x >> 1, h = x & 1, r = (lane >> 2) & 3, q = lane & 3;
+        rBk[x] = (uint32_t)((kk * 16 + (g >> 1) * 8 + h * 4 + r) * C::BPITCH + (wn * 128 + (g & 1) * 16 + q * 4) * 2);
+      }
+    }
   }
 
-  bf16x8 fa[2][2][4], fb[2][2][4];  // [buffer][16-k half][block]
-  i16x4 fbt[2][2][4][2];             // B-KN halves of fb from the transposed reads
+  u32x4 fa[2][2][4], fb[2][2][4];  // [buffer][half][block]: A and B-NK fragments
+  i32x2 ft[2][16];                 // [buffer][read]: B-KN transposed reads
 
-  // Fragment read j of a K-step (in the order the next step consumes them):
-  // per 16-k half, the 4 A fragments then the 4 B fragments (two transposed
-  // reads each for B-KN, one ds_read_b128 for B-NK).
+  // Fragment read j of a K-step, in the order the next step consumes them.
+  //   bf16: per 16-k half: 4 A, then B (4 x 2 transposed / 4 b128)
+  //   fp8:  per half of the 32 bytes: 4 A (and 4 B-NK); B-KN: 16 transposed
+  //         reads after the A halves
   constexpr int kReads = B_NK ? 16 : 24;
   auto read_one = [&](auto S_c, auto BUF_c, auto J_c) {
     constexpr int BUF = decltype(BUF_c)::value;
     constexpr int J = decltype(J_c)::value;
-    constexpr int per = kReads / 2;
-    constexpr int kk = J / per, j = J % per;
-    if (j < 4) {
-      fa[BUF][kk][j] = lds_load<bf16x8>(stA(S_c) + rA[kk] + j * 2048);
-    } else if (B_NK) {
-      fb[BUF][kk][j - 4] = lds_load<bf16x8>(stB(S_c) + rBn[kk] + (j - 4) * 2048);
+    if constexpr (!FP8) {
+      constexpr int per = kReads / 2;
+      constexpr int h = J / per, j = J % per;
+      if constexpr (j < 4) {
+        fa[BUF][h][j] = lds_load<u32x4>(stA(S_c) + rA[h] + j * 2048);
+      } else if constexpr (B_NK) {
+        fb[BUF][h][j - 4] = lds_load<u32x4>(stB(S_c) + rBn[h] + (j - 4) * 2048);
+      } else {
+        constexpr int bj = (j - 4) / 2, x = h * 2 + (j - 4) % 2;
+        ft[BUF][(h * 4 + bj) * 2 + (j - 4) % 2] = __builtin_bit_cast(
+            i32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[x] + bj * 64)));
+      }
     } else {
-      constexpr int bj = (j - 4) / 2, h = (j - 4) % 2;
-      fbt[BUF][kk][bj][h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[kk][h] + bj * 64));
+      if constexpr (J < 8) {
+        constexpr int h = J / 4, bi = J % 4;
+        fa[BUF][h][bi] = lds_load<u32x4>(stA(S_c) + rA[h] + bi * 2048);
+      } else if constexpr (B_NK) {
+        constexpr int h = (J - 8) / 4, bj = (J - 8) % 4;
+        fb[BUF][h][bj] = lds_load<u32x4>(stB(S_c) + rBn[h] + bj * 2048);
+      } else {
+        constexpr int bj = (J - 8) / 4, x = (J - 8) % 4;
+        ft[BUF][bj * 4 + x] =
+            __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS3 i32x2*)(stB(S_c) + rBk[x] + bj * 32));
+      }
     }
   };
   auto read_frags = [&](auto S_c, auto BUF_c) {
     static_for<0, kReads>([&](auto J_c) { read_one(S_c, BUF_c, J_c); });
-  };
-  auto b_frag = [&](auto BUF_c, int kk, int bj) -> bf16x8 {
-    constexpr int BUF = decltype(BUF_c)::value;
-    if (B_NK) return fb[BUF][kk][bj];
-    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(fbt[BUF][kk][bj][0], fbt[BUF][kk][bj][1], 0, 1, 2,
-                                                              3, 4, 5, 6, 7));
   };
 
   Acc acc;
@@ -574,34 +620,66 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
 
+  // MFMA i of a K-step on fragment buffer BUF
+  auto mfma_one = [&](auto BUF_c, auto I_c) {
+    constexpr int BUF = decltype(BUF_c)::value;
+    constexpr int i = decltype(I_c)::value;
+    if constexpr (!FP8) {
+      constexpr int kk = i / 16, bi = (i / 4) % 4, bj = i % 4;
+      bf16x8 bfr;
+      if constexpr (B_NK)
+        bfr = __builtin_bit_cast(bf16x8, fb[BUF][kk][bj]);
+      else
+        bfr = __builtin_bit_cast(bf16x8, __builtin_shufflevector(ft[BUF][(kk * 4 + bj) * 2], ft[BUF][(kk * 4 + bj) * 2 + 1], 0, 1, 2, 3));
+      acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr, __builtin_bit_cast(bf16x8, fa[BUF][kk][bi]),
+                                                            acc[bi][bj], 0, 0, 0);
+    } else {
+      constexpr int bi = i / 4, bj = i % 4;
+      const i32x8 afr = __builtin_bit_cast(i32x8, __builtin_shufflevector(fa[BUF][0][bi], fa[BUF][1][bi], 0, 1, 2, 3, 4, 5, 6, 7));
+      i32x8 bfr;
+      if constexpr (B_NK) {
+        bfr = __builtin_bit_cast(i32x8, __builtin_shufflevector(fb[BUF][0][bj], fb[BUF][1][bj], 0, 1, 2, 3, 4, 5, 6, 7));
+      } else {
+        const auto lo = __builtin_shufflevector(ft[BUF][bj * 4], ft[BUF][bj * 4 + 1], 0, 1, 2, 3);
+        const auto hi = __builtin_shufflevector(ft[BUF][bj * 4 + 2], ft[BUF][bj * 4 + 3], 0, 1, 2, 3);
+        bfr = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+      acc[bi][bj] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bfr, afr, acc[bi][bj], 0, 0, 0, 127, 0, 127);
+    }
+  };
+
   // K-step t on stage S with fragments in buffer BUF: publish stage S+1 (its
-  // DMA, issued three steps earlier, has landed), then the 32 MFMAs of step t
-  // in a fixed order, with the fragment reads of step t+1 (from stage S+1)
-  // and the DMA of step t+3 (into stage S+3 = the stage of step t-1, which
-  // every wave has finished reading) placed between them: the reads one per
-  // MFMA from the start, the DMA instructions spread evenly, so that neither
-  // the LDS queue nor the texture address FIFO backs up into the wave's
-  // in-order instruction stream.  Past the last K-step the DMA lanes are all
-  // out of range (zeros into a stage nobody reads) and the reads read a
-  // stale stage that is never used, so nothing here is conditional.
-  constexpr int kDma = B_NK ? 8 : 9;
+  // DMA, issued three steps earlier, has landed), then the MFMAs of step t in
+  // a fixed order, with the fragment reads of step t+1 (from stage S+1) and
+  // the DMA of step t+3 (into stage S+3 = the stage of step t-1, which every
+  // wave has finished reading) placed between them: the reads spread from the
+  // start, the DMA instructions evenly, so that neither the LDS queue nor the
+  // texture address FIFO backs up into the wave's in-order instruction
+  // stream.  Past the last K-step the DMA lanes are all out of range (zeros
+  // into a stage nobody reads) and the reads read a stale stage that is never
+  // used, so nothing here is conditional.
+  constexpr int NM = C::NMFMA;
   auto step = [&](auto S_c, auto BUF_c, int t) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
     wait_vmcnt<kDma>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    static_for<0, 32>([&](auto I_c) {
+    static_for<0, NM>([&](auto I_c) {
       constexpr int i = decltype(I_c)::value;
-      constexpr int kk = i / 16, bi = (i / 4) % 4, bj = i % 4;
-      acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b_frag(BUF_c, kk, bj), fa[BUF][kk][bi], acc[bi][bj], 0, 0, 0);
-      if constexpr (i < kReads) read_one(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{}, IC<i>{});
-      if constexpr ((i * kDma) / 32 != ((i + 1) * kDma) / 32) dma_one(IC<(S + 3) & 3>{}, IC<(i * kDma) / 32>{}, t + 3);
+      mfma_one(BUF_c, I_c);
+      // reads j in [i*R/NM', (i+1)*R/NM') over the first NM' = min(NM, 24) MFMAs
+      constexpr int NR = NM < 24 ? NM : 24;
+      if constexpr (i < NR) {
+        static_for<(i * kReads) / NR, ((i + 1) * kReads) / NR>(
+            [&](auto J_c) { read_one(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{}, J_c); });
+      }
+      if constexpr ((i * kDma) / NM != ((i + 1) * kDma) / NM) dma_one(IC<(S + 3) & 3>{}, IC<(i * kDma) / NM>{}, t + 3);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
 
-  const int nk = (K + kBK - 1) / kBK;
+  const int nk = (K + C::KSTEP - 1) / C::KSTEP;
   dma(IC<0>{}, 0);
   dma(IC<1>{}, 1);
   dma(IC<2>{}, 2);
@@ -626,34 +704,41 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_bf16_256x256(GemmArgs p) {
 
 // ------------------------------------------------------------ host launch
 
-template <bool B_NK>
+template <bool FP8, bool B_NK>
 static void launch_shape(const GemmArgs& p, int epi, dim3 grid, dim3 block, hipStream_t stream) {
   switch (epi) {
     case kEpiGroupNorm:
-      hipLaunchKernelGGL((kf_gemm_bf16_256x256<B_NK, kEpiGroupNorm>), grid, block, 0, stream, p);
+      hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, kEpiGroupNorm>), grid, block, 0, stream, p);
       break;
     case kEpiRow:
-      hipLaunchKernelGGL((kf_gemm_bf16_256x256<B_NK, kEpiRow>), grid, block, 0, stream, p);
+      hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, kEpiRow>), grid, block, 0, stream, p);
       break;
     default:
-      hipLaunchKernelGGL((kf_gemm_bf16_256x256<B_NK, kEpiPlain>), grid, block, 0, stream, p);
+      hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, kEpiPlain>), grid, block, 0, stream, p);
       break;
   }
 }
 
-hipError_t launch_gemm_bf16(const GemmArgs& args, int epi, hipStream_t stream, bool b_nk) {
+hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, hipStream_t stream, bool b_nk) {
   GemmArgs p = args;
   p.tiles_m = (int)((p.M + BM - 1) / BM);
   p.tiles_n = (int)((p.N + BN - 1) / BN);
   const dim3 grid(p.tiles_m * p.tiles_n), block(NT);
-  if (b_nk)
-    launch_shape<true>(p, epi, grid, block, stream);
-  else
-    launch_shape<false>(p, epi, grid, block, stream);
+  if (fp8) {
+    if (b_nk)
+      launch_shape<true, true>(p, epi, grid, block, stream);
+    else
+      launch_shape<true, false>(p, epi, grid, block, stream);
+  } else {
+    if (b_nk)
+      launch_shape<false, true>(p, epi, grid, block, stream);
+    else
+      launch_shape<false, false>(p, epi, grid, block, stream);
+  }
   return hipGetLastError();
 }
 
-int gemm_bf16_tile_m() { return BM; }
-int gemm_bf16_tile_n() { return BN; }
+int gemm_mfma_tile_m() { return BM; }
+int gemm_mfma_tile_n() { return BN; }
 
 }  // namespace kf

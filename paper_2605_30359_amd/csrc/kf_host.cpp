@@ -163,9 +163,16 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       d->variant = kVarGemmBf16;
       if (s->K % 8) return fail(KF_ERR_UNSUPPORTED, "bf16 GEMM needs K %% 8 == 0 (16-byte rows)");
       if (s->N % 8) return fail(KF_ERR_UNSUPPORTED, "bf16 GEMM needs N %% 8 == 0 (16-byte rows)");
-      d->kernel_name = "kf_gemm_bf16_256x256";
+      d->kernel_name = "kf_gemm_mfma_256x256";
     } else {
-      return fail(KF_ERR_UNSUPPORTED, "fp8 GEMM is not available in this build");
+      d->variant = kVarGemmFp8;
+      if (s->K % 16) return fail(KF_ERR_UNSUPPORTED, "fp8 GEMM needs K %% 16 == 0 (16-byte rows)");
+      if (s->N % 16) return fail(KF_ERR_UNSUPPORTED, "fp8 GEMM needs N %% 16 == 0 (16-byte rows)");
+      if (!(s->scale_a > 0.0f) || !(s->scale_b > 0.0f) || !std::isfinite(s->scale_a) || !std::isfinite(s->scale_b))
+        return fail(KF_ERR_INVALID_ARG, "fp8 scale_a / scale_b must be finite and > 0");
+      if (!std::isfinite(s->scale_a * s->scale_b) || s->scale_a * s->scale_b == 0.0f)
+        return fail(KF_ERR_INVALID_ARG, "fp8 scale_a * scale_b must be a finite, nonzero fp32 value");
+      d->kernel_name = "kf_gemm_mfma_256x256";
     }
     if (has_gn) {
       const kf_op& g = s->ops[d->red_index];
@@ -188,9 +195,9 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     else
       d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0}, "out"};
     if (d->row_kind) {
-      d->tiles_n = (int)((s->N + kf::gemm_bf16_tile_n() - 1) / kf::gemm_bf16_tile_n());
+      d->tiles_n = (int)((s->N + kf::gemm_mfma_tile_n() - 1) / kf::gemm_mfma_tile_n());
       if (d->tiles_n > kf::row_finish_max_tiles())
-        return fail(KF_ERR_UNSUPPORTED, "row softmax/logsumexp supports N <= %d", kf::row_finish_max_tiles() * kf::gemm_bf16_tile_n());
+        return fail(KF_ERR_UNSUPPORTED, "row softmax/logsumexp supports N <= %d", kf::row_finish_max_tiles() * kf::gemm_mfma_tile_n());
     }
   } else {
     return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 is not available in this build");
@@ -390,7 +397,8 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
       if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : (s.K + 128) * a.ldb) * es) ||
           !fits_31(256 * a.ldo * 4) || (a.residual && !fits_31(256 * a.ldr * 4)))
         return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
-      e = kf::launch_gemm_bf16(a, d->epi_shape, hs, nk);
+      if (d->variant == kVarGemmFp8) a.scale = s.scale_a * s.scale_b;  // fl(s_a * s_b), applied to the fp32 accumulator
+      e = kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, d->epi_shape, hs, nk);
       if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
       if (e == hipSuccess && d->row_kind)
         e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, d->workspace, d->tiles_n, s.M, s.N, a.out,

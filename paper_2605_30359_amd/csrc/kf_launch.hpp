@@ -8,10 +8,11 @@
 
 namespace kf {
 
-// bf16 GEMM + epilogue; `epi` is an EpiShape.
-hipError_t launch_gemm_bf16(const GemmArgs& args, int epi, hipStream_t stream, bool b_nk);
-int gemm_bf16_tile_m();
-int gemm_bf16_tile_n();
+// bf16 or OCP fp8 e4m3 GEMM + epilogue on the matrix cores; `epi` is an
+// EpiShape.
+hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, hipStream_t stream, bool b_nk);
+int gemm_mfma_tile_m();
+int gemm_mfma_tile_n();
 
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);

@@ -119,25 +119,27 @@ E4M3_MAX = 448.0
 
 def f32_to_e4m3_codes(v: np.ndarray) -> np.ndarray:
     """float32 -> OCP E4M3 codes (uint8): round to nearest even, saturating
-    to +-448 (finite inputs only)."""
-    v = np.asarray(v, dtype=np.float64)  # exact widening of float32
-    s = np.signbit(v)
-    a = np.minimum(np.abs(v), E4M3_MAX)
-    with np.errstate(divide="ignore"):
-        e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
-    e = np.maximum(e, -6.0)                     # subnormal quantum 2^-9
-    quantum = np.exp2(e - 3.0)
-    q = np.rint(a / quantum) * quantum          # np.rint: half to even
-    q = np.minimum(q, E4M3_MAX)
-    with np.errstate(divide="ignore"):
-        E = np.floor(np.log2(np.where(q > 0, q, 1.0)))
-    normal = q >= 2.0 ** -6
-    e_field = np.where(normal, E + 7, 0).astype(np.int64)
-    mant = np.where(normal, (q / np.exp2(E) - 1.0) * 8.0, q / 2.0 ** -9)
-    mant = np.rint(mant).astype(np.int64)
+    to +-448 (finite inputs only).
+
+    Every step is exact in float32: the quantum of a value in [2^E, 2^(E+1))
+    is 2^(E-3) (2^-9 below the normal range), so dividing by it, rounding
+    half to even (np.rint) and multiplying back only rescales by powers of 2.
+    """
+    v = np.asarray(v, dtype=np.float32)
+    sign = np.signbit(v)
+    a = np.minimum(np.abs(v), np.float32(E4M3_MAX))
+    _, e = np.frexp(a)                           # a = m * 2^e, m in [0.5, 1)
+    E = np.maximum(e - 1, -6)                    # floor(log2 a), clamped to the subnormal range
+    q = np.ldexp(np.rint(np.ldexp(a, 3 - E)), E - 3).astype(np.float32)
+    q = np.minimum(q, np.float32(E4M3_MAX))
+    m2, e2 = np.frexp(q)
+    E2 = e2 - 1
+    normal = q >= np.float32(2.0 ** -6)
+    # normal: q = (1 + f/8) * 2^E2, f = 16 m2 - 8; subnormal: q = f * 2^-9
+    mant = np.where(normal, np.rint(m2 * 16 - 8), np.rint(np.ldexp(q, 9))).astype(np.int32)
+    e_field = np.where(normal, E2 + 7, 0).astype(np.int32)
     code = (e_field << 3) | mant
-    code = np.where(q == 0, 0, code)
-    return (code | np.where(s, 0x80, 0)).astype(np.uint8)
+    return (code | np.where(sign & (q > 0), 0x80, 0)).astype(np.uint8)
 
 
 def quantize_e4m3(x: np.ndarray):

@@ -93,6 +93,8 @@ def test_create_null_arguments():
     (lambda s: setattr(s, "N", 4100), kf.KF_ERR_UNSUPPORTED, "N % 8"),
     (lambda s: setattr(s, "M", -1), kf.KF_ERR_SHAPE, "M >= 0"),
     (lambda s: setattr(s, "b_layout", 5), kf.KF_ERR_INVALID_ARG, "b_layout"),
+    (lambda s: (setattr(s, "in_dtype", kf.KF_FP8_E4M3), setattr(s, "scale_a", 0.0)), kf.KF_ERR_INVALID_ARG, "scale"),
+    (lambda s: (setattr(s, "in_dtype", kf.KF_FP8_E4M3), setattr(s, "K", 4104)), kf.KF_ERR_UNSUPPORTED, "K % 16"),
 ])
 def test_create_rejects_bad_specs(mutate, status, msg):
     spec = _spec("C2")

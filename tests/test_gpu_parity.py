@@ -197,3 +197,68 @@ def test_shape_mismatch_rejected_on_device():
     with pytest.raises(kf.KFError) as ei:
         op(ins, bad)
     assert ei.value.status == kf.KF_ERR_SHAPE
+
+
+# ------------------------------------------------------------ fp8 (OCP e4m3)
+
+def _int_e4m3(rng, shape):
+    """Integers in [-16, 16]: all exactly representable in E4M3."""
+    v = rng.integers(-16, 17, size=shape).astype(np.float32)
+    return v, inputs.f32_to_e4m3_codes(v)
+
+
+@pytest.mark.parametrize("layout", ["kn", "nk"])
+def test_fp8_contraction_bit_exact(layout):
+    """Every partial sum is an integer of magnitude < 8192 * 256 = 2^21, so the
+    fp32 accumulator must equal the exact product (unit scales)."""
+    _torch()
+    M, N, K = 2048, 8192, 8192
+    rng = np.random.default_rng(31)
+    a, qa = _int_e4m3(rng, (M, K))
+    b, qb = _int_e4m3(rng, (K, N) if layout == "kn" else (N, K))
+    t = {"a": qa, "b": qb, "scale_a": 1.0, "scale_b": 1.0}
+    cfg = inputs.config("C5", M=M, N=N, K=K, out_dtype="f32", ops=[], b_layout=layout)
+    print(f"fp8 bit-exact {M}x{N}x{K} {layout}", flush=True)
+    _, out = run_gpu(cfg, t)
+    bb = b.astype(np.float64) if layout == "kn" else b.astype(np.float64).T
+    ref = a.astype(np.float64) @ bb
+    assert np.array_equal(out.cpu().numpy().astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("M,N,K,layout", [(300, 1040, 208, "kn"), (257, 272, 64, "nk"), (1, 16, 16, "kn"),
+                                          (520, 4096, 1024, "kn")])
+def test_c5_ragged(M, N, K, layout):
+    _torch()
+    cfg = inputs.config("C5", M=M, N=N, K=K, b_layout=layout)
+    t = inputs.generate(cfg, seed=M + N + K)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    g = to_host_f64(out)
+    assert np.allclose(g.sum(axis=1), 1.0, atol=3e-2)
+    print(f"C5 {M}x{N}x{K} {layout} err {err:.3e}")
+
+
+def test_c5_zero_weights_uniform_bit_exact():
+    """W = 0, b = 0: every logit is 0, so every output is 1/8192 = 2^-13,
+    exactly representable in bf16."""
+    torch = _torch()
+    cfg = inputs.config("C5", M=256, N=8192, K=256)
+    t = inputs.generate(cfg, seed=4)
+    t["b"] = np.zeros_like(t["b"])
+    t["bias"] = np.zeros_like(t["bias"])
+    _, out = run_gpu(cfg, t)
+    bits = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.all(bits == inputs.f32_to_bf16_bits(np.array([2.0 ** -13], np.float32))[0])
+
+
+def test_c5_full_config_sampled_rows():
+    _torch()
+    cfg = inputs.config("C5")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    rows = sample_rows(cfg["M"], 16)
+    err = check(cfg, t, out, rows=rows)
+    g = to_host_f64(out)
+    assert np.all(np.isfinite(g))
+    assert np.allclose(g.sum(axis=1), 1.0, atol=3e-2)
+    print(f"C5 full err {err:.3e}")
