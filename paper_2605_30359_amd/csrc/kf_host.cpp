@@ -200,7 +200,32 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
         return fail(KF_ERR_UNSUPPORTED, "row softmax/logsumexp supports N <= %d", kf::row_finish_max_tiles() * kf::gemm_mfma_tile_n());
     }
   } else {
-    return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 is not available in this build");
+    // 3x3 convolution, stride 1, zero padding 1, NCHW input / OIHW weight
+    if (dt != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 supports bf16 inputs only");
+    if (s->out_dtype != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 writes bf16 outputs only");
+    if (s->batch < 0 || s->cin < 1 || s->height < 1 || s->width < 1 || s->cout < 1)
+      return fail(KF_ERR_SHAPE, "CONV2D_3X3 needs batch >= 0 and positive cin, height, width, cout");
+    if (s->cin != kf::conv_bf16_cin() || s->width != kf::conv_bf16_width() || s->cout != kf::conv_bf16_cout())
+      return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 kernel is built for cin=%d, width=%d, cout=%d",
+                  kf::conv_bf16_cin(), kf::conv_bf16_width(), kf::conv_bf16_cout());
+    if (s->height % 2) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 needs an even height (tiles are row pairs)");
+    if ((int64_t)s->cin * s->height * s->width * 2 >= (int64_t(1) << 31))
+      return fail(KF_ERR_UNSUPPORTED, "one image must be smaller than 2 GiB");
+    for (int i = 0; i < s->n_ops; ++i) {
+      const int k = s->ops[i].kind;
+      if (!(k == KF_OP_BIAS || k == KF_OP_MAXPOOL2X2 || is_elementwise_kind(k)))
+        return fail(KF_ERR_UNSUPPORTED, "op %d: CONV2D_3X3 supports BIAS, element-wise ops and MAXPOOL2X2", i);
+    }
+    d->variant = kVarConvBf16;
+    d->kernel_name = "kf_conv3x3_bf16_256x128";
+    d->inputs.push_back(Slot{dt, 4, {s->batch, s->cin, s->height, s->width}, "A"});
+    d->inputs.push_back(Slot{dt, 4, {s->cout, s->cin, 3, 3}, "B"});
+    for (int i = 0; i < s->n_ops; ++i)
+      if (s->ops[i].kind == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->cout, 0, 0, 0}, "bias"});
+    if (n_pool)
+      d->output = Slot{KF_BF16, 4, {s->batch, s->cout, s->height / 2, s->width / 2}, "out"};
+    else
+      d->output = Slot{KF_BF16, 4, {s->batch, s->cout, s->height, s->width}, "out"};
   }
   return KF_OK;
 }
@@ -292,7 +317,14 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
   }
   d->device = dev;
 
-  if (d->row_kind) {
+  if (d->variant == kVarConvBf16) {
+    d->workspace_bytes = (size_t)9 * spec->cout * spec->cin * 2;  // repacked weights
+    if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      delete d;
+      return fail(KF_ERR_OOM, "workspace of %zu bytes could not be allocated", d->workspace_bytes);
+    }
+  } else if (d->row_kind) {
     d->workspace_bytes = (size_t)std::max<int64_t>(spec->M, 1) * d->tiles_n * sizeof(float) * 2;
     if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
       (void)hipGetLastError();
@@ -407,7 +439,33 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
     if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
   }
-  return fail(KF_ERR_UNSUPPORTED, "contraction not available");
+  // CONV2D_3X3
+  if (s.batch == 0) return ok();
+  kf::ConvArgs c;
+  memset(&c, 0, sizeof(c));
+  c.x = inputs[0].data;
+  c.w = inputs[1].data;
+  c.batch = s.batch;
+  c.cin = s.cin;
+  c.H = s.height;
+  c.W = s.width;
+  c.cout = s.cout;
+  c.prog = d->prog;
+  for (int i = 0; i < s.n_ops; ++i) {
+    if (s.ops[i].kind == KF_OP_BIAS) c.bias = static_cast<const float*>(inputs[2].data);
+    if (s.ops[i].kind == KF_OP_MAXPOOL2X2) {
+      c.pool = 1;
+      c.pool_index = i;
+    }
+  }
+  c.out = outputs[0].data;
+  c.out_bf16 = 1;
+  hipError_t e = kf::launch_conv_pack(c, d->workspace, hs);
+  if (e == hipSuccess && ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
+  if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, hs);
+  if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
+  if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
 }
 
 kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {

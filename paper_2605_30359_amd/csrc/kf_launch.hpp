@@ -23,3 +23,18 @@ hipError_t launch_row_finish(bool softmax, const void* partials, int tiles, int6
 int row_finish_max_tiles();
 
 }  // namespace kf
+
+namespace kf {
+
+// 3x3 conv (bf16, NCHW/OIHW) + fused element-wise ops and 2x2 max-pool:
+// launch_conv_pack repacks the weights into `packed_weights` (device scratch
+// of 9 * cout * cin bf16, layout [tap][co][ci]), launch_conv_bf16 runs the
+// convolution from it.  Supports cin == conv_bf16_cin(), width ==
+// conv_bf16_width(), cout == conv_bf16_cout(), even height.
+hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStream_t stream);
+hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, hipStream_t stream);
+int conv_bf16_cin();
+int conv_bf16_width();
+int conv_bf16_cout();
+
+}  // namespace kf

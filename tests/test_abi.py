@@ -74,6 +74,14 @@ def _spec(name, **kw):
     return kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg))
 
 
+def test_conv_validation():
+    for kw, status in [(dict(cin=32), kf.KF_ERR_UNSUPPORTED), (dict(H=7), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("groupnorm", 2, 1e-5)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(out_dtype="f32"), kf.KF_ERR_UNSUPPORTED), (dict(in_dtype="f32"), kf.KF_ERR_UNSUPPORTED)]:
+        st, _ = _create(_spec("C4", **kw))
+        assert st == status, (kw, st, kf.last_error())
+
+
 def test_create_null_arguments():
     lib = kf.lib()
     h = ctypes.c_void_p()
@@ -147,8 +155,8 @@ def test_hardtanh_bounds_validated():
 
 @pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
 def test_valid_spec_without_device_reports_no_device():
-    for name in ("C1", "C2", "C3"):
-        st, h = _create(_spec(name))
+    for name in ("C1", "C2", "C3", "C4", "C5"):
+        st, h = _create(_spec(name, **({"scale_a": 0.01, "scale_b": 0.01} if name == "C5" else {})))
         assert st == kf.KF_ERR_NO_DEVICE, (name, st, kf.last_error())
         assert not h.value
 

@@ -262,3 +262,65 @@ def test_c5_full_config_sampled_rows():
     assert np.all(np.isfinite(g))
     assert np.allclose(g.sum(axis=1), 1.0, atol=3e-2)
     print(f"C5 full err {err:.3e}")
+
+
+# ------------------------------------------------------------ conv (C4)
+
+@pytest.mark.parametrize("batch,H,ops", [
+    (2, 8, [("bias",), ("relu",), ("maxpool2x2",)]),
+    (1, 2, [("bias",), ("relu",), ("maxpool2x2",)]),
+    (3, 6, [("bias",), ("relu",)]),
+    (1, 4, [("bias",), ("gelu_tanh",), ("maxpool2x2",), ("scale", -2.0), ("swish",)]),
+])
+def test_c4_small(batch, H, ops):
+    _torch()
+    cfg = inputs.config("C4", batch=batch, H=H, ops=ops)
+    t = inputs.generate(cfg, seed=batch * 10 + H)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"C4 batch={batch} H={H} ops={[o[0] for o in ops]} err {err:.3e}")
+
+
+def test_c4_integer_bit_exact():
+    """Integer inputs in [-4, 4] and weights in [-2, 2]: every fp32 partial sum
+    is an exact integer, so the GPU output (no ops) equals the oracle's exact
+    sum rounded to bf16 (round to nearest even), bit for bit."""
+    torch = _torch()
+    cfg = inputs.config("C4", batch=2, H=6, ops=[])
+    rng = np.random.default_rng(41)
+    x = rng.integers(-4, 5, size=(2, 64, 6, 128)).astype(np.float32)
+    w = rng.integers(-2, 3, size=(128, 64, 3, 3)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
+    _, out = run_gpu(cfg, t)
+    ref = oracle.conv2d_3x3(x.astype(np.float64), w.astype(np.float64))
+    assert np.all(np.abs(ref) < 2 ** 24) and np.array_equal(ref, np.round(ref))
+    ref_bits = inputs.f32_to_bf16_bits(ref.astype(np.float32))
+    got_bits = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got_bits, ref_bits)
+
+
+def test_c4_zero_weights_and_centre_tap():
+    _torch()
+    cfg = inputs.config("C4", batch=1, H=4)
+    t = inputs.generate(cfg, seed=3)
+    z = dict(t, b=np.zeros_like(t["b"]))
+    _, out = run_gpu(cfg, z)
+    g = to_host_f64(out)
+    expect = np.maximum(t["bias"].astype(np.float64), 0)[None, :, None, None]
+    assert np.max(np.abs(g - expect)) <= 2.0 ** -8 * np.max(np.abs(expect))
+    w = np.zeros((128, 64, 3, 3), np.float32)
+    for c in range(64):
+        w[c, c, 1, 1] = 1.0
+    t2 = dict(t, b=inputs.f32_to_bf16_bits(w))
+    _, out = run_gpu(cfg, t2)
+    check(cfg, t2, out)
+
+
+def test_c4_full_config_sampled_images():
+    _torch()
+    cfg = inputs.config("C4")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out, images=np.array([0, 37, 63]))
+    assert np.all(np.isfinite(to_host_f64(out)))
+    print(f"C4 full err {err:.3e}")
