@@ -71,6 +71,9 @@ struct kf_desc {
   size_t workspace_bytes;
   int tiles_n;
   std::string kernel_name;
+  // unfused comparator: two intermediate buffers, allocated on first use
+  mutable void* ubuf[2];
+  mutable size_t ubuf_bytes;
 };
 
 namespace {
@@ -291,6 +294,8 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
   d->workspace = nullptr;
   d->workspace_bytes = 0;
   d->tiles_n = 0;
+  d->ubuf[0] = d->ubuf[1] = nullptr;
+  d->ubuf_bytes = 0;
   kf_status st = validate_and_plan(spec, d);
   if (st != KF_OK) {
     delete d;
@@ -339,6 +344,8 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
 void kf_destroy(kf_desc* d) {
   if (!d) return;
   if (d->workspace) (void)hipFree(d->workspace);
+  for (void* b : d->ubuf)
+    if (b) (void)hipFree(b);
   delete d;
 }
 
@@ -469,11 +476,127 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
 }
 
 kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
-  (void)inputs;
-  (void)outputs;
-  (void)stream;
-  if (!d) return fail(KF_ERR_INVALID_ARG, "NULL argument");
-  return fail(KF_ERR_UNSUPPORTED, "unfused chain not available in this build");
+  if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  const bool vec16 = d->variant != kVarGemmF32;
+  for (size_t i = 0; i < d->inputs.size(); ++i) {
+    kf_status st = check_tensor(&inputs[i], d->inputs[i], false, vec16);
+    if (st != KF_OK) return st;
+  }
+  kf_status st = check_tensor(&outputs[0], d->output, true, vec16);
+  if (st != KF_OK) return st;
+  const kf_op_spec& s = d->spec;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const bool gemm = s.contraction == KF_GEMM;
+  if ((gemm && s.M == 0) || (!gemm && s.batch == 0)) return ok();
+
+  // intermediates: bf16 (fp32 for an fp32 chain), full contraction size
+  const bool ibf16 = d->variant != kVarGemmF32;
+  const int64_t n_full = gemm ? s.M * s.N : s.batch * s.cout * s.height * s.width;
+  const size_t need = (size_t)n_full * (ibf16 ? 2 : 4);
+  if (d->ubuf_bytes < need) {
+    for (void*& b : d->ubuf) {
+      if (b) (void)hipFree(b);
+      b = nullptr;
+      if (hipMalloc(&b, need) != hipSuccess) {
+        (void)hipGetLastError();
+        d->ubuf_bytes = 0;
+        return fail(KF_ERR_OOM, "unfused intermediates of %zu bytes could not be allocated", need);
+      }
+    }
+    d->ubuf_bytes = need;
+  }
+
+  // 1. the contraction alone (empty op list), into the first buffer -- or
+  //    straight into the output when there are no ops
+  void* out = outputs[0].data;
+  const bool out_bf16 = outputs[0].dtype == KF_BF16;
+  void* cur = s.n_ops ? d->ubuf[0] : out;
+  bool cur_bf16 = s.n_ops ? ibf16 : out_bf16;
+  hipError_t e = hipSuccess;
+  size_t slot = 2;
+  if (gemm) {
+    kf::GemmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.a = inputs[0].data;
+    a.b = inputs[1].data;
+    a.M = s.M;
+    a.N = s.N;
+    a.K = s.K;
+    a.lda = s.K ? inputs[0].stride[0] : 8;
+    a.ldb = s.K ? inputs[1].stride[0] : 8;
+    a.scale = d->variant == kVarGemmFp8 ? s.scale_a * s.scale_b : 1.0f;
+    a.out = cur;
+    a.ldo = s.n_ops ? s.N : (outputs[0].ndim == 2 ? outputs[0].stride[0] : 1);
+    a.out_bf16 = cur_bf16;
+    a.red_index = 0;
+    const bool nk = s.b_layout == KF_LAYOUT_NK;
+    e = d->variant == kVarGemmF32 ? kf::launch_gemm_f32(a, nk, hs)
+                                  : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, hs, nk);
+  } else {
+    kf::ConvArgs c;
+    memset(&c, 0, sizeof(c));
+    c.x = inputs[0].data;
+    c.w = inputs[1].data;
+    c.batch = s.batch;
+    c.cin = s.cin;
+    c.H = s.height;
+    c.W = s.width;
+    c.cout = s.cout;
+    c.out = cur;
+    c.out_bf16 = 1;
+    e = kf::launch_conv_pack(c, d->workspace, hs);
+    if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, hs);
+  }
+  if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+
+  // 2. one kernel per op, ping-ponging between the buffers; the last op
+  //    writes the output
+  int64_t n = n_full;
+  int64_t hh = s.height, ww = s.width;
+  int which = 0;
+  for (int i = 0; i < s.n_ops && e == hipSuccess; ++i) {
+    const kf_op& op = s.ops[i];
+    const bool last = i == s.n_ops - 1;
+    void* dst = last ? out : d->ubuf[which ^ 1];
+    const bool dst_bf16 = last ? out_bf16 : ibf16;
+    switch (op.kind) {
+      case KF_OP_BIAS: {
+        const float* bias = static_cast<const float*>(inputs[slot++].data);
+        const int64_t fdiv = gemm ? 1 : hh * ww, fmod = gemm ? s.N : s.cout;
+        e = kf::launch_unfused_elementwise(cur, cur_bf16, dst, dst_bf16, n, op.kind, 0.f, 0.f, bias, fdiv, fmod, hs);
+        break;
+      }
+      case KF_OP_RESIDUAL_ADD: {
+        const kf_tensor& r = inputs[slot++];
+        e = kf::launch_unfused_residual(cur, cur_bf16, r.data, r.dtype == KF_BF16, dst, dst_bf16, n, hs);
+        break;
+      }
+      case KF_OP_GROUPNORM: {
+        const float* gamma = static_cast<const float*>(inputs[slot++].data);
+        const float* beta = static_cast<const float*>(inputs[slot++].data);
+        e = kf::launch_unfused_groupnorm(cur, cur_bf16, dst, dst_bf16, s.M, s.N, op.groups, op.p0, gamma, beta, hs);
+        break;
+      }
+      case KF_OP_ROW_SOFTMAX:
+      case KF_OP_ROW_LOGSUMEXP:
+        e = kf::launch_unfused_rowop(cur, cur_bf16, dst, dst_bf16, s.M, s.N, op.kind == KF_OP_ROW_SOFTMAX, hs);
+        break;
+      case KF_OP_MAXPOOL2X2:
+        e = kf::launch_unfused_maxpool(cur, cur_bf16, dst, dst_bf16, s.batch * s.cout, (int)hh, (int)ww, hs);
+        hh /= 2;
+        ww /= 2;
+        n = s.batch * s.cout * hh * ww;
+        break;
+      default:
+        e = kf::launch_unfused_elementwise(cur, cur_bf16, dst, dst_bf16, n, op.kind, op.p0, op.p1, nullptr, 1, 1, hs);
+        break;
+    }
+    cur = dst;
+    cur_bf16 = dst_bf16;
+    which ^= 1;
+  }
+  if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
 }
 
 }  // extern "C"

@@ -38,3 +38,21 @@ int conv_bf16_width();
 int conv_bf16_cout();
 
 }  // namespace kf
+
+namespace kf {
+
+// Unfused comparator kernels (one per op, memory-bound).  `fdiv` / `fmod`
+// map a flat element index to its feature for BIAS: (i / fdiv) % fmod.
+hipError_t launch_unfused_elementwise(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t n, int kind,
+                                      float p0, float p1, const float* bias, int64_t fdiv, int64_t fmod,
+                                      hipStream_t stream);
+hipError_t launch_unfused_residual(const void* in, bool in_bf16, const void* res, bool res_bf16, void* out,
+                                   bool out_bf16, int64_t n, hipStream_t stream);
+hipError_t launch_unfused_groupnorm(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t rows, int64_t N,
+                                    int groups, float eps, const float* gamma, const float* beta, hipStream_t stream);
+hipError_t launch_unfused_rowop(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t rows, int64_t N,
+                                bool softmax, hipStream_t stream);
+hipError_t launch_unfused_maxpool(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t planes, int H,
+                                  int W, hipStream_t stream);
+
+}  // namespace kf

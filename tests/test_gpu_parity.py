@@ -324,3 +324,36 @@ def test_c4_full_config_sampled_images():
     err = check(cfg, t, out, images=np.array([0, 37, 63]))
     assert np.all(np.isfinite(to_host_f64(out)))
     print(f"C4 full err {err:.3e}")
+
+
+# ------------------------------------------------------------ unfused chain
+
+@pytest.mark.parametrize("name,kw", [
+    ("C1", {}),
+    ("C2", dict(M=300, N=520, K=136)),
+    ("C3", dict(M=300, N=512, K=136, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
+    ("C4", dict(batch=2, H=8)),
+    ("C5", dict(M=300, N=1040, K=208)),
+])
+def test_unfused_chain_parity(name, kw):
+    """The one-kernel-per-op comparator must compute the same chain.  Its
+    intermediates are stored in bf16 (as a bf16 eager chain stores them), so
+    every op adds one more rounding of up to 2^-9 relative on values of
+    magnitude up to ~5 (C3: GEMM output, GroupNorm output and swish output
+    before the residual add): the bound is the fused tolerance per rounding,
+    i.e. 3x for bf16/fp8 chains."""
+    _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=77)
+    _, out = run_gpu(cfg, t, unfused=True)
+    tol = TOL[cfg["in_dtype"]] * (1 if cfg["in_dtype"] == "f32" else 3)
+    err = check(cfg, t, out, tol=tol)
+    print(f"unfused {name} err {err:.3e}")
+
+
+def test_unfused_c2_full_config_sampled_rows():
+    _torch()
+    cfg = inputs.config("C2")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t, unfused=True)
+    check(cfg, t, out, rows=sample_rows(cfg["M"], 16), tol=3 * TOL["bf16"])
