@@ -69,7 +69,7 @@ def _source_digest(kernel_file: str) -> str:
     return h.hexdigest()[:16]
 
 
-KERNEL_FILES = {"kf_gemm_mfma_256x256": "kf_gemm_mfma.hip", "kf_gemm_f32_32x64": "kf_gemm_f32.hip"}
+KERNEL_FILES = {"kf_gemm_mfma_256x256": "kf_gemm_mfma.hip", "kf_gemm_f32_8x8": "kf_gemm_f32.hip", "kf_conv3x3_bf16_256x128": "kf_conv_bf16.hip"}
 
 
 def _traffic(kernel: str, workload: str):

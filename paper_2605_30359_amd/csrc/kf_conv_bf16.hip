@@ -22,7 +22,12 @@
 //              with a shifted pixel index.
 //   weights    repacked per call by kf_conv_pack_weights to [tap][co][ci],
 //              then streamed per K-step (one tap, 32 channels = 8 KiB) into
-//              four LDS stages by LDS DMA, three steps ahead.
+//              six LDS stages by LDS DMA, six steps ahead.
+//   schedule   persistent: one workgroup per compute unit walks the tiles
+//              with a stride of the grid size.  The next tile's halo is
+//              loaded into registers during the last K-steps and the
+//              epilogue of the current one, and the weight stream runs on
+//              across tiles, so neither waits at a tile boundary.
 //   order      A fragment = MFMA "A" operand: each lane's accumulators are
 //              runs of 4 consecutive output pixels of one channel.
 #include <type_traits>
@@ -43,17 +48,20 @@ constexpr int HALO_ROWS = 4;         // ih = oh0 - 1 .. oh0 + 2
 constexpr int PIX_BYTES = CIN * 2;   // 128 bytes of channels per pixel
 constexpr int kHalo = HALO_ROWS * HALO_COLS * PIX_BYTES;  // 66560 bytes
 constexpr int kWStage = COUT * 64;   // [128 co][32 ci] bf16 = 8 KiB
-constexpr int kSteps = 9 * (CIN / 32);  // 18 K-steps of 32
+constexpr int kWS = 6;               // weight stages = prefetch distance in K-steps
+constexpr int kSteps = 9 * (CIN / 32);  // 18 K-steps of 32 per tile
+static_assert(kSteps % kWS == 0 && kSteps >= 2 * kWS, "the tile loop unrolls kWS steps at a time");
 
 #define LDS3 __attribute__((address_space(3)))
 
 template <int V>
 using IC = std::integral_constant<int, V>;
 
+// s_waitcnt vmcnt(N) lgkmcnt(0), expcnt left alone
 template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0x0 << 8) | ((N >> 4) << 14));
 }
 
 template <typename T>
@@ -61,26 +69,31 @@ __device__ __forceinline__ T lds_load(const unsigned char* p) {
   return *reinterpret_cast<const T*>(p);
 }
 
-// byte offset of channel chunk c (8 channels) of halo pixel p
-__device__ __forceinline__ uint32_t halo_off(int p, int c) { return (uint32_t)(p * PIX_BYTES + ((c ^ (p & 7)) << 4)); }
+// byte offset of channel chunk c (8 channels) of halo pixel p: a 16-lane
+// fragment read covers 16 consecutive pixels, whose chunks land on the 16
+// distinct 16-byte slots of a 256-byte bank line (pixel parity picks the
+// half, bits 1-3 of the pixel the chunk swizzle)
+__device__ __forceinline__ uint32_t halo_off(int p, int c) {
+  return (uint32_t)(p * PIX_BYTES + ((c ^ ((p >> 1) & 7)) << 4));
+}
 
 // acc[bi][bj][i]: pixel row  (bi >> 1), column wm*64 + (bi & 1)*32 + (i/4)*8 + (lane >> 5)*4 + i%4
 //                 channel    wn*64 + bj*32 + (lane & 31)
 typedef f32x16 CAcc[4][2];
 
 // Element-wise ops oi..oe-1 (BIAS and the activations) on one lane's values
-// of output channel `co`: the op kind is uniform, so the switch is taken once
-// per op and the loop over the registers is unrolled inside each case.
+// of one output channel, whose bias is b: the op kind is uniform, so the
+// switch is taken once per op and the loop over the registers is unrolled
+// inside each case.
 template <int N>
-__device__ __forceinline__ void conv_apply_phase(const ConvArgs& p, int oi, int oe, int co, float (&v)[N]) {
+__device__ __forceinline__ void conv_apply_phase(const OpTable& ops, int oi, int oe, float b, float (&v)[N]) {
   for (int o = oi; o < oe; ++o) {
-    const EpiOp op = p.prog.op[o];
-    if (op.kind == KF_OP_BIAS) {
-      const float b = p.bias[co];
+    const int kind = op_kind(ops, o);
+    if (kind == KF_OP_BIAS) {
 #pragma unroll
       for (int i = 0; i < N; ++i) v[i] += b;
     } else {
-      apply_elementwise_array(op.kind, op.p0, op.p1, v);
+      apply_elementwise_array(kind, op_p0(ops, o), op_p1(ops, o), v);
     }
   }
 }
@@ -101,10 +114,11 @@ __global__ __launch_bounds__(256) void kf_conv_pack_weights(const uint16_t* __re
 
 __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, const uint16_t* __restrict__ wp) {
   __shared__ __attribute__((aligned(1024))) unsigned char sHalo[kHalo];
-  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage], sW3[kWStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage], sW3[kWStage],
+      sW4[kWStage], sW5[kWStage];
   auto stW = [&](auto S_c) -> unsigned char* {
     constexpr int S = decltype(S_c)::value;
-    return S == 0 ? sW0 : S == 1 ? sW1 : S == 2 ? sW2 : sW3;
+    return S == 0 ? sW0 : S == 1 ? sW1 : S == 2 ? sW2 : S == 3 ? sW3 : S == 4 ? sW4 : sW5;
   };
 
   const int tid = threadIdx.x;
@@ -114,33 +128,44 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   const int wn = wave >> 1;
   const int H = (int)p.H;
   const int rows_per_img = H / 2;
-  const int n_img = blockIdx.x / rows_per_img;
-  const int ph = blockIdx.x % rows_per_img;  // tile = output rows 2 ph, 2 ph + 1
-  const int oh0 = 2 * ph;
+  const int64_t img_elems = (int64_t)CIN * H * WID;
 
-  // ---- stage the halo: x[n][ci][oh0-1+hr][iw] -> sHalo[(hr*130 + iw+1)][ci]
-  {
-    const uint16_t* X = reinterpret_cast<const uint16_t*>(p.x) + (int64_t)n_img * CIN * H * WID;
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, (uint32_t)((int64_t)CIN * H * WID * 2));
+  // ---- halo of a tile: x[n][ci][oh0-1+hr][iw] -> sHalo[(hr*130 + iw+1)][ci].
+  // Thread t owns blocks t and t + 256 (8 channels x 8 pixels of one row):
+  // 16 x 16-byte loads into registers, then an 8 x 8 bf16 transpose by
+  // v_perm_b32 on the way into LDS.
+  u32x4 hv[2][8];
+  // (a tile past the end issues the same 16 loads, all out of range, so the
+  // number of loads in flight is the same in every pass)
+  auto halo_load = [&](int tile, bool live) {
+    const int n_img = live ? tile / rows_per_img : 0;
+    const int oh0 = 2 * (tile % rows_per_img);
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(reinterpret_cast<const uint16_t*>(p.x) + n_img * img_elems, (uint32_t)(img_elems * 2));
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      const int b = tid + half * 256;  // block: 8 channels x 8 pixels of one row
+      const int b = tid + half * 256;
       const int cg = b & 7, pg = (b >> 3) & 15, hr = b >> 7;
       const int ih = oh0 - 1 + hr;
-      const bool row_ok = ih >= 0 && ih < H;
-      u32x4 v[8];
+      const bool row_ok = live && ih >= 0 && ih < H;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint32_t off = row_ok ? (uint32_t)((((int64_t)(cg * 8 + j) * H + ih) * WID + pg * 8) * 2) : kOOB;
-        v[j] = buf_load16(rx, off);
+        const uint32_t off = row_ok ? (uint32_t)((((cg * 8 + j) * H + ih) * WID + pg * 8) * 2) : kOOB;
+        hv[half][j] = buf_load16(rx, off);
       }
-      // 8x8 transpose of bf16: v[j] = channel cg*8+j, pixels pg*8 .. +7
+    }
+  };
+  auto halo_write = [&]() {
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int b = tid + half * 256;
+      const int cg = b & 7, pg = (b >> 3) & 15, hr = b >> 7;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const uint32_t sel = (k & 1) ? 0x07060302u : 0x05040100u;
         u32x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(v[2 * e + 1][k >> 1], v[2 * e][k >> 1], sel);
+        for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(hv[half][2 * e + 1][k >> 1], hv[half][2 * e][k >> 1], sel);
         const int pix = hr * HALO_COLS + pg * 8 + k + 1;
         *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = o;
       }
@@ -151,23 +176,27 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
       const int pix = hr * HALO_COLS + (side ? HALO_COLS - 1 : 0);
       *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = u32x4{0u, 0u, 0u, 0u};
     }
-  }
+  };
 
   // ---- weight stream: step s = (tap s/2, channel half s%2) -> [co][32 ci]
-  // stage with chunk c of row co stored at c ^ ((co >> 1) & 3); wave w fills
-  // rows [32w, 32w + 32) with 2 DMA instructions of 16 rows
+  // stage with chunk c of row co stored at c ^ ((co >> 2) & 3) (16
+  // consecutive rows of a fragment read on 16 distinct bank slots); wave w fills
+  // rows [32w, 32w + 32) with 2 DMA instructions of 16 rows.  The weights
+  // are the same for every tile, so the stream runs on across tiles: the
+  // DMA issued in step s of a tile fetches step (s + 6) mod 18, for this tile
+  // or the next.
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp, (uint32_t)(9 * COUT * CIN * 2));
-  const int dma_lc = (lane & 3) ^ ((lane >> 3) & 3);
+  const int dma_lc = (lane & 3) ^ ((lane >> 4) & 3);
   uint32_t vw[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int co = wave * 32 + i * 16 + (lane >> 2);
     vw[i] = (uint32_t)((co * CIN + dma_lc * 8) * 2);
   }
-  auto dma_one = [&](auto S_c, auto J_c, int s) {
+  auto dma_one = [&](auto S_c, auto J_c, int s, bool live) {
     constexpr int J = decltype(J_c)::value;
-    const bool live = s < kSteps;
-    const int soff = live ? ((s >> 1) * COUT * CIN + (s & 1) * 32) * 2 : 0;
+    const int sw = s >= kSteps ? s - kSteps : s;
+    const int soff = ((sw >> 1) * COUT * CIN + (sw & 1) * 32) * 2;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS3 void*)(stW(S_c) + wave * 2048 + J * 1024), 16,
                                               live ? vw[J] : kOOB, soff, 0, 0);
   };
@@ -178,7 +207,7 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) {
     const int ch = kk * 2 + kg;
-    rB[kk] = (uint32_t)((wn * 64 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
+    rB[kk] = (uint32_t)((wn * 64 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
   }
   u32x4 fa[2][2][4], fb[2][2][2];  // [buffer][16-k half][block]
   constexpr int kReads = 12;       // per step: 8 A (4 blocks x 2 halves), 4 B
@@ -187,7 +216,7 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
     constexpr int J = decltype(J_c)::value;
     constexpr int kk = J / 6, j = J % 6;
     if constexpr (j < 4) {
-      // past the last step (the prefetch of step kSteps) read the last tap
+      // past the last step (the read ahead of step kSteps) read the last tap
       // again: the values are never used, and the halo index stays in range
       const int sc = s < kSteps ? s : kSteps - 1;
       const int tap = sc >> 1, kh = tap / 3, kw = tap - kh * 3;
@@ -199,108 +228,185 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
     }
   };
 
-  CAcc acc;
+  // bias of this lane's two output channels, once for all tiles
+  float bias_v[2] = {0.0f, 0.0f};
+  if (p.bias) {
 #pragma unroll
-  for (int bi = 0; bi < 4; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
+    for (int bj = 0; bj < 2; ++bj) bias_v[bj] = p.bias[wn * 64 + bj * 32 + (lane & 31)];
+  }
 
+  CAcc acc;
   constexpr int kDma = 2;
-  // K-step s on weight stage S (same pipeline as the GEMM kernel): publish
-  // stage S+1, then 16 MFMAs with the fragment reads of step s+1 and the
-  // weight DMA of step s+3 interleaved in a fixed order.
-  auto step = [&](auto S_c, auto BUF_c, int s) {
+  constexpr int kHaloStep = kSteps - kWS;  // step that loads the next tile's halo
+  // K-step s of a tile on weight stage S = s % 6: every wave has read its
+  // fragments of stage S (during step s-1) once it passes the barrier, so the
+  // DMA of step s+6 goes into stage S; the barrier also publishes stage S+1
+  // (DMA issued during step s-5), read during this step.  WAIT is the number
+  // of younger loads allowed in flight: the DMA of the 4 steps in between,
+  // plus the 16 halo loads of the next tile, which follow the MFMAs of step
+  // 12 and are older than the DMA awaited in steps 13-17.
+  auto step = [&](auto S_c, auto BUF_c, auto WAIT_c, auto HALO_c, int s, bool next_live, int next_tile) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
-    wait_vmcnt<kDma>();
+    constexpr int WAIT = decltype(WAIT_c)::value;
+    constexpr bool HALO = decltype(HALO_c)::value;
+    wait_vmcnt_lgkm0<WAIT>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    const bool live = s + kWS < kSteps || next_live;
     static_for<0, 16>([&](auto I_c) {
       constexpr int i = decltype(I_c)::value;
       constexpr int kk = i / 8, bi = (i / 2) % 4, bj = i % 2;
       acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[BUF][kk][bi]),
                                                             __builtin_bit_cast(bf16x8, fb[BUF][kk][bj]), acc[bi][bj], 0,
                                                             0, 0);
-      if constexpr (i < kReads) read_one(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{}, I_c, s + 1);
-      if constexpr (i == 3 || i == 11) dma_one(IC<(S + 3) & 3>{}, IC<(i == 3 ? 0 : 1)>{}, s + 3);
+      if constexpr (i < kReads) read_one(IC<(S + 1) % kWS>{}, IC<BUF ^ 1>{}, I_c, s + 1);
+      if constexpr (i == 3 || i == 11) dma_one(S_c, IC<(i == 3 ? 0 : 1)>{}, s + kWS, live);
       __builtin_amdgcn_sched_barrier(0);
     });
+    if (HALO) halo_load(next_tile, next_live);
   };
 
-  dma_one(IC<0>{}, IC<0>{}, 0);
-  dma_one(IC<0>{}, IC<1>{}, 0);
-  dma_one(IC<1>{}, IC<0>{}, 1);
-  dma_one(IC<1>{}, IC<1>{}, 1);
-  dma_one(IC<2>{}, IC<0>{}, 2);
-  dma_one(IC<2>{}, IC<1>{}, 2);
-  __syncthreads();  // halo written, first three weight stages landed
-  static_for<0, kReads>([&](auto J_c) { read_one(IC<0>{}, IC<0>{}, J_c, 0); });
-
-  // 18 steps = 4 x 4 + 2
-#pragma unroll 1
-  for (int s = 0; s < 16; s += 4) {
-    step(IC<0>{}, IC<0>{}, s);
-    step(IC<1>{}, IC<1>{}, s + 1);
-    step(IC<2>{}, IC<0>{}, s + 2);
-    step(IC<3>{}, IC<1>{}, s + 3);
-  }
-  step(IC<0>{}, IC<0>{}, 16);
-  step(IC<1>{}, IC<1>{}, 17);
-  __syncthreads();
-
-  // ---- epilogue: ops before the pool on every pre-pool value, the pool in
-  // registers, ops after it on the pooled values, one store
   const int nops = p.prog.n;
+  const OpTable ops = load_op_table(p.prog, lane);
   const int pidx = p.pool ? p.pool_index : nops;
   const int64_t plane_out = p.pool ? (int64_t)(H / 2) * (WID / 2) : (int64_t)H * WID;
   uint16_t* out = reinterpret_cast<uint16_t*>(p.out);
-  static_for<0, 2>([&](auto bj_c) {
-    constexpr int bj = decltype(bj_c)::value;
-    const int co = wn * 64 + bj * 32 + (lane & 31);
-    uint16_t* oc = out + ((int64_t)n_img * COUT + co) * plane_out;
-    float v[64];  // v[bi * 16 + i] = acc[bi][bj][i]
+
+  int tile = blockIdx.x;
+  // prologue: the first tile's halo, then the weight stages of steps 0-5
+  halo_load(tile, true);
+  static_for<0, kWS>([&](auto S_c) {
+    dma_one(S_c, IC<0>{}, decltype(S_c)::value, true);
+    dma_one(S_c, IC<1>{}, decltype(S_c)::value, true);
+  });
+
+  for (; tile < p.tiles; tile += gridDim.x) {
+    const int n_img = tile / rows_per_img;
+    const int ph = tile % rows_per_img;  // tile = output rows 2 ph, 2 ph + 1
+    const int oh0 = 2 * ph;
+    const int next_tile = tile + (int)gridDim.x;
+    const bool next_live = next_tile < p.tiles;
+
+    // this tile's halo registers and weight stage 0 have landed (the stages
+    // of steps 1-5 may still be in flight); every wave is past its last read
+    // of the previous halo
+    wait_vmcnt_lgkm0<(kWS - 1) * kDma>();
+    __syncthreads();
+    halo_write();
+    __syncthreads();
+    static_for<0, kReads>([&](auto J_c) { read_one(IC<0>{}, IC<0>{}, J_c, 0); });
+
 #pragma unroll
     for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) v[bi * 16 + i] = acc[bi][bj][i];
-    conv_apply_phase(p, 0, pidx, co, v);
-    if (p.pool) {
-      // window (bc, q, h2): columns i, i+1 (i = 4q + 2 h2) of row blocks bc
-      // (output row 0) and bc + 2 (output row 1)
-      float pv[16];
+      for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
-      for (int bc = 0; bc < 2; ++bc)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int h2 = 0; h2 < 2; ++h2) {
-            const int i = q * 4 + h2 * 2;
-            pv[bc * 8 + q * 2 + h2] = fmaxf(fmaxf(v[bc * 16 + i], v[bc * 16 + i + 1]),
-                                            fmaxf(v[(bc + 2) * 16 + i], v[(bc + 2) * 16 + i + 1]));
-          }
-      conv_apply_phase(p, pidx + 1, nops, co, pv);
-#pragma unroll
-      for (int bc = 0; bc < 2; ++bc)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int pw = wm * 32 + bc * 16 + q * 4 + (lane >> 5) * 2;
-          *reinterpret_cast<uint32_t*>(oc + (int64_t)ph * (WID / 2) + pw) =
-              pack_bf16x2(pv[bc * 8 + q * 2], pv[bc * 8 + q * 2 + 1]);
-        }
-    } else {
-#pragma unroll
-      for (int bi = 0; bi < 4; ++bi)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int oh = oh0 + (bi >> 1);
-          const int ow = wm * 64 + (bi & 1) * 32 + q * 8 + (lane >> 5) * 4;
-          const float* x = &v[bi * 16 + q * 4];
-          *reinterpret_cast<u32x2*>(oc + (int64_t)oh * WID + ow) = u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
-        }
+        for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
+
+    // 18 steps = 2 x 6 + 6 (stage s % 6, fragment buffer s % 2)
+    constexpr int W = (kWS - 2) * kDma, WH = W + 16;
+#pragma unroll 1
+    for (int s = 0; s < kHaloStep; s += kWS) {
+      step(IC<0>{}, IC<0>{}, IC<W>{}, IC<0>{}, s, next_live, next_tile);
+      step(IC<1>{}, IC<1>{}, IC<W>{}, IC<0>{}, s + 1, next_live, next_tile);
+      step(IC<2>{}, IC<0>{}, IC<W>{}, IC<0>{}, s + 2, next_live, next_tile);
+      step(IC<3>{}, IC<1>{}, IC<W>{}, IC<0>{}, s + 3, next_live, next_tile);
+      step(IC<4>{}, IC<0>{}, IC<W>{}, IC<0>{}, s + 4, next_live, next_tile);
+      step(IC<5>{}, IC<1>{}, IC<W>{}, IC<0>{}, s + 5, next_live, next_tile);
     }
-  });
+    step(IC<0>{}, IC<0>{}, IC<W>{}, IC<1>{}, 12, next_live, next_tile);
+    step(IC<1>{}, IC<1>{}, IC<WH>{}, IC<0>{}, 13, next_live, next_tile);
+    step(IC<2>{}, IC<0>{}, IC<WH>{}, IC<0>{}, 14, next_live, next_tile);
+    step(IC<3>{}, IC<1>{}, IC<WH>{}, IC<0>{}, 15, next_live, next_tile);
+    step(IC<4>{}, IC<0>{}, IC<WH>{}, IC<0>{}, 16, next_live, next_tile);
+    step(IC<5>{}, IC<1>{}, IC<WH>{}, IC<0>{}, 17, next_live, next_tile);
+
+    // ---- epilogue, per output channel block bj and column half bc (the
+    // two output rows of the tile): ops before the pool on the pre-pool
+    // values, the pool in registers, ops after it on the pooled values.  The
+    // bf16 results are staged in LDS (the halo region: after the barrier of
+    // step 17 no wave reads halo data it uses) as [channel][row][pixels], a
+    // 16-byte chunk q of row (co, r) at chunk q ^ (co & 15), then written out
+    // with 16-byte stores, so that each store instruction covers whole
+    // 128-byte lines of the output rows instead of 32 scattered channels.
+    unsigned char* const stage = sHalo;
+    static_for<0, 2>([&](auto bj_c) {
+      constexpr int bj = decltype(bj_c)::value;
+      const int co = wn * 64 + bj * 32 + (lane & 31);
+      static_for<0, 2>([&](auto bc_c) {
+        constexpr int bc = decltype(bc_c)::value;
+        float v[32];  // v[r * 16 + i] = acc[2 r + bc][bj][i]: output row r
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          v[i] = acc[bc][bj][i];
+          v[16 + i] = acc[bc + 2][bj][i];
+        }
+        conv_apply_phase(ops, 0, pidx, bias_v[bj], v);
+        if (p.pool) {
+          // window (q, h2): columns i, i + 1 (i = 4q + 2 h2) of both rows
+          float pv[8];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+              const int i = q * 4 + h2 * 2;
+              pv[q * 2 + h2] = fmaxf(fmaxf(v[i], v[i + 1]), fmaxf(v[16 + i], v[16 + i + 1]));
+            }
+          conv_apply_phase(ops, pidx + 1, nops, bias_v[bj], pv);
+          // pooled row of channel co: 64 pixels = 8 chunks of 16 bytes
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int pw = wm * 32 + bc * 16 + q * 4 + (lane >> 5) * 2;
+            const int ch = pw >> 3;
+            *reinterpret_cast<uint32_t*>(stage + co * 128 + ((ch ^ (co & 7)) << 4) + (pw & 7) * 2) =
+                pack_bf16x2(pv[q * 2], pv[q * 2 + 1]);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int ow = wm * 64 + bc * 32 + q * 8 + (lane >> 5) * 4;
+              const float* x = &v[r * 16 + q * 4];
+              *reinterpret_cast<u32x2*>(stage + (co * 2 + r) * 256 + (((ow >> 3) ^ (co & 15)) << 4) + (ow & 7) * 2) =
+                  u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+            }
+        }
+      });
+    });
+    __syncthreads();
+    {
+      // output rows of this tile: channel co's row starts at
+      // img_out + co * plane_out + row_off (+ WID for the second pre-pool row)
+      const __amdgpu_buffer_rsrc_t ro =
+          make_rsrc(out + (int64_t)n_img * COUT * plane_out, (uint32_t)(COUT * plane_out * 2));
+      if (p.pool) {
+        // 128 channels x 8 chunks
+        const uint32_t row_off = (uint32_t)(ph * (WID / 2) * 2);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int idx = tid + 256 * k;
+          const int co = idx >> 3, ch = idx & 7;
+          const u32x4 w = *reinterpret_cast<const u32x4*>(stage + co * 128 + ((ch ^ (co & 7)) << 4));
+          buf_store16(w, ro, (uint32_t)(co * plane_out * 2) + row_off + ch * 16);
+        }
+      } else {
+        // 128 channels x 2 rows x 16 chunks
+        const uint32_t row_off = (uint32_t)(oh0 * WID * 2);
+#pragma unroll 4
+        for (int k = 0; k < 16; ++k) {
+          const int idx = tid + 256 * k;
+          const int row = idx >> 4, ch = idx & 15;
+          const int co = row >> 1, r = row & 1;
+          const u32x4 w = *reinterpret_cast<const u32x4*>(stage + row * 256 + ((ch ^ (co & 15)) << 4));
+          buf_store16(w, ro, (uint32_t)(co * plane_out * 2) + row_off + (uint32_t)(r * WID * 2) + ch * 16);
+        }
+      }
+    }
+  }
+  // nothing may land in LDS after the workgroup ends
+  wait_vmcnt_lgkm0<0>();
 }
 
 hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStream_t stream) {
@@ -311,7 +417,8 @@ hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStrea
 }
 
 hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, hipStream_t stream) {
-  const dim3 grid((unsigned)(args.batch * (args.H / 2)));
+  if (args.tiles <= 0) return hipSuccess;
+  const dim3 grid((unsigned)(args.grid < args.tiles ? args.grid : args.tiles));
   hipLaunchKernelGGL(kf_conv3x3_bf16_256x128, grid, dim3(NT), 0, stream, args,
                      reinterpret_cast<const uint16_t*>(packed_weights));
   return hipGetLastError();

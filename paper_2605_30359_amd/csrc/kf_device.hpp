@@ -61,14 +61,14 @@ __device__ __forceinline__ void buf_store4(uint32_t v, __amdgpu_buffer_rsrc_t r,
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fp32 -> bf16 bits, round to nearest even (inputs here are never NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
+// fp32 -> bf16 bits, round to nearest even: gfx950's v_cvt_pk_bf16_f32
+// (the conversion honours the default round-to-nearest-even mode).
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) { return pack_bf16x2(f, 0.0f) & 0xffffu; }
 
 // --------------------------------------------------------------- epilogue math
 //
@@ -160,6 +160,31 @@ __device__ __forceinline__ bool is_elementwise(int kind) {
   return kind == KF_OP_RELU || kind == KF_OP_GELU_TANH || kind == KF_OP_GELU_ERF ||
          kind == KF_OP_SWISH || kind == KF_OP_SIGMOID || kind == KF_OP_TANH ||
          kind == KF_OP_HARDTANH || kind == KF_OP_SCALE;
+}
+
+// The op program held one op per lane (3 VGPRs), loaded once per kernel.  A
+// wave-uniform op index then reads the op's fields with v_readlane, where an
+// access through the kernel-argument pointer would cost one scalar-memory
+// round trip per field and per use.
+struct OpTable {
+  int kind;
+  float p0, p1;
+};
+__device__ __forceinline__ OpTable load_op_table(const EpiProgram& prog, int lane) {
+  OpTable t{0, 0.0f, 0.0f};
+  if (lane < KF_MAX_OPS) {
+    t.kind = prog.op[lane].kind;
+    t.p0 = prog.op[lane].p0;
+    t.p1 = prog.op[lane].p1;
+  }
+  return t;
+}
+__device__ __forceinline__ int op_kind(const OpTable& t, int o) { return __builtin_amdgcn_readlane(t.kind, o); }
+__device__ __forceinline__ float op_p0(const OpTable& t, int o) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t.p0), o));
+}
+__device__ __forceinline__ float op_p1(const OpTable& t, int o) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t.p1), o));
 }
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so

@@ -62,6 +62,13 @@ __device__ __forceinline__ T lds_load(const unsigned char* p) {
   return *reinterpret_cast<const T*>(p);
 }
 
+// s_waitcnt vmcnt(N) lgkmcnt(0), expcnt left alone
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0x0 << 8) | ((N >> 4) << 14));
+}
+
 // acc[bi][bj][i]: output row    wm*128 + bi*32 + (lane & 31)
 //                 output column wn*128 + bj*32 + (i/4)*8 + (lane >> 5)*4 + i%4
 typedef f32x16 Acc[4][4];
@@ -76,7 +83,11 @@ typedef f32x16 Acc[4][4];
 struct EpiCtx {
   int lane, wm, wn;
   int64_t m0, n0;
-  float* red;  // 2 x 256 floats of LDS for cross-wave row reductions
+  float* red;                    // 2 x 256 floats of LDS for cross-wave row reductions
+  const float* col;              // LDS: bias, gamma, beta of the tile's 256 columns
+  bool res_lds;                  // the bf16 residual tile sits in LDS (see the kernel's residual staging)
+  const unsigned char* res[4];   // LDS rows of row block bi of this wave's residual
+  OpTable ops;                   // the op program, one op per lane
 };
 
 // run g (0..15) of a row = block bj = g / 4, group gi = g % 4
@@ -104,11 +115,28 @@ __device__ __forceinline__ void put_row(Acc& acc, int bi, const Row& v) {
   }
 }
 
-// 4 consecutive fp32 of a per-column vector (bias, gamma, beta); columns >= N
-// read as 0.
-__device__ __forceinline__ f32x4 load_col4(const EpiCtx& c, const float* v, int64_t N, int g) {
-  const __amdgpu_buffer_rsrc_t r = make_rsrc(v + c.n0, (uint32_t)((N - c.n0) * 4));
-  return __builtin_bit_cast(f32x4, buf_load16(r, (uint32_t)col_local(c, g) * 4u));
+// 4 consecutive fp32 of a per-column vector (0 bias, 1 gamma, 2 beta), staged
+// in LDS at kernel start; columns >= N read as 0.
+__device__ __forceinline__ f32x4 col4(const EpiCtx& c, int which, int g) {
+  return *reinterpret_cast<const f32x4*>(c.col + which * 256 + col_local(c, g));
+}
+
+// The bf16 residual tile in LDS: row m of the tile at row (m & 31) of array
+// res[(m >> 5) & 3] of the wave that owns it, 512 bytes per row, 16-byte
+// chunk q of the row stored at chunk q ^ (m & 15).
+__device__ __forceinline__ f32x4 res4(const EpiCtx& c, int bi, int g) {
+  const int r = c.lane & 31;
+  const int q = c.wn * 16 + (g >> 2) * 4 + (g & 3);
+  const u32x2 w = *reinterpret_cast<const u32x2*>(c.res[bi] + r * 512 + ((q ^ (r & 15)) << 4) + (c.lane >> 5) * 8);
+  return f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+}
+
+// Wait until every wave's share of the residual tile has landed in LDS.
+__device__ __forceinline__ void res_wait(const EpiCtx& c) {
+  if (c.res_lds) {
+    wait_vmcnt_lgkm0<0>();
+    __syncthreads();
+  }
 }
 
 __device__ __forceinline__ float sum4(f32x4 a) { return (a[0] + a[1]) + (a[2] + a[3]); }
@@ -142,16 +170,20 @@ __device__ __forceinline__ void row_combine(const EpiCtx& c, float (&v)[4], bool
 __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, int bi, int oi, int oe, Row& v) {
   const int64_t N = p.N;
   for (int o = oi; o < oe; ++o) {
-    const EpiOp op = p.prog.op[o];
-    switch (op.kind) {
+    const int kind = op_kind(c.ops, o);
+    const float p0 = op_p0(c.ops, o), p1 = op_p1(c.ops, o);
+    switch (kind) {
       case KF_OP_BIAS:
 #pragma unroll
-        for (int g = 0; g < 16; ++g) v[g] += load_col4(c, p.bias, N, g);
+        for (int g = 0; g < 16; ++g) v[g] += col4(c, 0, g);
         break;
       case KF_OP_RESIDUAL_ADD: {
         const int64_t rows = min<int64_t>(BM, p.M - c.m0);
         const int64_t rl = row_local(c, bi);
-        if (p.residual_bf16) {
+        if (c.res_lds) {
+#pragma unroll
+          for (int g = 0; g < 16; ++g) v[g] += res4(c, bi, g);
+        } else if (p.residual_bf16) {
           const uint16_t* base = reinterpret_cast<const uint16_t*>(p.residual) + c.m0 * p.ldr + c.n0;
           const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 2));
 #pragma unroll
@@ -187,8 +219,8 @@ __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, 
       KF_EW_CASE(KF_OP_SWISH, f_swish(x))
       KF_EW_CASE(KF_OP_SIGMOID, f_sigmoid(x))
       KF_EW_CASE(KF_OP_TANH, f_tanh(x))
-      KF_EW_CASE(KF_OP_HARDTANH, fminf(fmaxf(x, op.p0), op.p1))
-      KF_EW_CASE(KF_OP_SCALE, x * op.p0)
+      KF_EW_CASE(KF_OP_HARDTANH, fminf(fmaxf(x, p0), p1))
+      KF_EW_CASE(KF_OP_SCALE, x * p0)
 #undef KF_EW_CASE
       default:
         break;
@@ -231,6 +263,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
   const int r = EPI == kEpiPlain ? nops : p.red_index;
 
   if (EPI == kEpiPlain) {
+    res_wait(c);
     static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
       Row v;
@@ -248,6 +281,11 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     // every 32-column block of its rows, so per-block sums are lane-local plus
     // one exchange with lane ^ 32; wider groups add neighbouring blocks, and a
     // 256-wide group also the other wave's half of the tile row.
+    int res_at = -1;
+    for (int o = 0; o < nops; ++o)
+      if (op_kind(c.ops, o) == KF_OP_RESIDUAL_ADD) res_at = o;
+    const bool res_early = res_at < r;  // the residual is added before the statistics
+    if (res_early) res_wait(c);
     const int gw = p.gn_group;
     const int bpg = gw >> 5;  // 32-column blocks per group (1, 2, 4, 8)
     const int bw = min(bpg, 4);
@@ -318,7 +356,8 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       }
     });
     group_reduce(ss);
-    const float eps = p.prog.op[r].p0;
+    const float eps = op_p0(c.ops, r);
+    if (!res_early) res_wait(c);
     static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
       Row v;
@@ -327,7 +366,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       for (int g = 0; g < 16; ++g) {
         const int bj = g >> 2;
         const float rs = rsqrtf(ss[bi][bj] * inv_n + eps);
-        v[g] = (v[g] - mean[bi][bj]) * rs * load_col4(c, p.gamma, N, g) + load_col4(c, p.beta, N, g);
+        v[g] = (v[g] - mean[bi][bj]) * rs * col4(c, 1, g) + col4(c, 2, g);
       }
       apply_phase(p, c, bi, r + 1, nops, v);
       store_row(p, c, bi, v);
@@ -337,6 +376,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 
   // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
   // this 256-column tile goes to the partials buffer.
+  res_wait(c);
   float mx[4];
   static_for<0, 4>([&](auto bi_c) {
     constexpr int bi = decltype(bi_c)::value;
@@ -379,7 +419,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
     }
   }
-  if (p.prog.op[r].kind != KF_OP_ROW_SOFTMAX) return;  // logsumexp: the finishing kernel writes
+  if (op_kind(c.ops, r) != KF_OP_ROW_SOFTMAX) return;  // logsumexp: the finishing kernel writes
   // softmax: store e^(h - tile max); the row-finishing kernel rescales it
   static_for<0, 4>([&](auto bi_c) {
     constexpr int bi = decltype(bi_c)::value;
@@ -403,14 +443,19 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 // global side, by choosing which chunk each lane fetches.
 //
 // A K-step covers 64 bytes of k: 32 bf16 or 64 fp8.
+// The LDS serves 256 bytes per clock, so a 16-byte-per-lane read is taken 16
+// lanes at a time and an 8-byte one 32 lanes at a time; the layouts below
+// give every such lane group 16 (32) distinct 16-byte (8-byte) bank slots.
 //   A (and B-NK): [256 rows][64 bytes of k]; chunk c of row m stored at chunk
-//     c ^ ((m >> 1) & 3), so 8 consecutive rows of a ds_read_b128 fragment
-//     read hit 8 distinct 16-byte bank groups.
-//   B-KN: [k][256 n] rows with a padded pitch (bf16: 32 rows of 544 bytes,
-//     fp8: 64 rows of 272 bytes; 17 KiB either way), read through the
+//     c ^ ((m >> 2) & 3): the 16 consecutive rows of a ds_read_b128 lane
+//     group fall on 4 row positions x 4 chunk positions of a 256-byte line.
+//   B-KN: [k][256 n] rows with a padded pitch (bf16: 32 rows of 576 bytes,
+//     fp8: 64 rows of 288 bytes; 18 KiB either way), read through the
 //     transposing ds_read_b64_tr_b16 / _b8: in each 16-lane group the lanes
-//     point at 4 (8) k-rows and receive the k values of their own column, and
-//     the pitch puts those rows in distinct bank groups.
+//     point at 4 (8) k-rows and receive the k values of their own column.  A
+//     pitch of 64 (32) bytes past 256-byte alignment puts one group's rows in
+//     alternate 32 (16) byte slots and the other column half of the same
+//     32-lane read in the slots between.
 //
 // MFMA: bf16 v_mfma_f32_32x32x16_bf16 (32 per step, two 16-k halves), fp8
 // v_mfma_scale_f32_32x32x64_f8f6f4 with unit block scales (16 per step); both
@@ -421,15 +466,15 @@ template <bool FP8>
 struct ElemCfg;
 template <>
 struct ElemCfg<false> {  // bf16
-  static constexpr int ES = 2, KSTEP = 32, NMFMA = 32, BPITCH = 544;
+  static constexpr int ES = 2, KSTEP = 32, NMFMA = 32, BPITCH = 576;
 };
 template <>
 struct ElemCfg<true> {  // OCP fp8 e4m3
-  static constexpr int ES = 1, KSTEP = 64, NMFMA = 16, BPITCH = 272;
+  static constexpr int ES = 1, KSTEP = 64, NMFMA = 16, BPITCH = 288;
 };
 
 constexpr int kAStage = BM * 64;           // 16 KiB
-constexpr int kBStageKN = 17 * 1024;       // 17 KiB = 17 DMA blocks of 1 KiB
+constexpr int kBStageKN = 18 * 1024;       // 18 KiB = 18 DMA blocks of 1 KiB
 constexpr int kBStageNK = BN * 64;         // 16 KiB
 
 #define LDS3 __attribute__((address_space(3)))
@@ -439,12 +484,6 @@ typedef __attribute__((ext_vector_type(2))) int i32x2;
 template <int V>
 using IC = std::integral_constant<int, V>;
 
-// s_waitcnt vmcnt(N), the other counters left alone
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
-}
 
 }  // namespace
 
@@ -456,6 +495,8 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   __shared__ __attribute__((aligned(1024))) unsigned char sA0[kAStage], sA1[kAStage], sA2[kAStage], sA3[kAStage];
   __shared__ __attribute__((aligned(1024))) unsigned char sB0[kBS], sB1[kBS], sB2[kBS], sB3[kBS];
   __shared__ __attribute__((aligned(1024))) unsigned char sDummy[B_NK ? 16 : 1024];
+  __shared__ __attribute__((aligned(16))) float sCol[3 * 256];  // bias, gamma, beta of the tile's columns
+  __shared__ float sRed[2 * 256];                              // cross-wave row reductions
   auto stA = [&](auto S_c) -> unsigned char* {
     constexpr int S = decltype(S_c)::value;
     return S == 0 ? sA0 : S == 1 ? sA1 : S == 2 ? sA2 : sA3;
@@ -489,11 +530,24 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
       B_NK ? make_rsrc(B + n0 * ldb * ES, (uint32_t)(((rows_b - 1) * ldb + K) * ES))
            : make_rsrc(B + n0 * ES, (uint32_t)(((max(K, 1) - 1) * ldb + (p.N - n0)) * ES));
 
+  const OpTable ops = load_op_table(p.prog, lane);
+
+  // The tile's per-column epilogue vectors (bias, gamma, beta) go to LDS with
+  // one DMA instruction each (waves 0, 1, 2; columns past N read as zero),
+  // ahead of the operand DMA, so they have landed long before the epilogue.
+  {
+    const float* vec = wave == 0 ? p.bias : wave == 1 ? p.gamma : p.beta;
+    if (wave < 3 && vec != nullptr) {
+      const __amdgpu_buffer_rsrc_t rv = make_rsrc(vec + n0, (uint32_t)((p.N - n0) * 4));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (LDS3 void*)(sCol + wave * 256), 16, (uint32_t)lane * 16u, 0, 0, 0);
+    }
+  }
+
   // ---- DMA source byte offsets (loop invariant; the K-step enters as soffset)
   // [rows][64 B] operands: wave w fills rows [64w, 64w + 64) with 4
   // instructions of 16 rows; lane l -> row 16i + l/4, LDS chunk l%4, which
-  // holds global chunk (l%4) ^ ((l >> 3) & 3).
-  const int dma_lc = (lane & 3) ^ ((lane >> 3) & 3);
+  // holds global chunk (l%4) ^ ((l >> 4) & 3).
+  const int dma_lc = (lane & 3) ^ ((lane >> 4) & 3);
   uint32_t va[4], vbn[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -501,7 +555,7 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
     va[i] = (uint32_t)((int64_t)row * lda * ES + dma_lc * 16);
     vbn[i] = (uint32_t)((int64_t)row * ldb * ES + dma_lc * 16);
   }
-  // B-KN: 17 blocks of 1 KiB per stage, block b = wave + 4 i; byte q of the
+  // B-KN: 18 blocks of 1 KiB per stage, block b = wave + 4 i; byte q of the
   // stage is row q / BPITCH, byte (q % BPITCH) of the row (the pad reads as zero)
   uint32_t vbk[5];
 #pragma unroll
@@ -509,11 +563,14 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
     const int b = wave + 4 * i;
     const int pos = b * 1024 + lane * 16;
     const int k = pos / C::BPITCH, col = pos % C::BPITCH;
-    const bool ok = b < 17 && col < 256 * ES && (n0 + col / ES < p.N);
+    const bool ok = b < 18 && col < 256 * ES && (n0 + col / ES < p.N);
     vbk[i] = ok ? (uint32_t)((int64_t)k * ldb * ES + col) : kOOB;
   }
 
-  // DMA instruction j (0 .. kDma-1) of K-step t into stage S
+  // DMA instruction j (0 .. kDma-1) of K-step t into stage S.  The K-step
+  // enters as the scalar offset; the descriptor's range check applies to the
+  // sum of vector and scalar offsets, so k-rows of B-KN past K (and every
+  // lane of the steps past the end that the pipeline issues) read as zero.
   auto dma_one = [&](auto S_c, auto J_c, int t) {
     constexpr int J = decltype(J_c)::value;
     const int k0 = t * C::KSTEP;
@@ -528,12 +585,12 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 1024 + (J - 4) * 4096), 16,
                                                 vbk[J - 4], (int)(k0 * ldb * ES), 0, 0);
     } else {
-      // block 16 belongs to wave 0; the other waves issue the same
-      // instruction out of range into a 1 KiB dummy region (out-of-range DMA
-      // lanes still write zeros, so they must not target block 16), which
-      // keeps the instruction stream free of branches
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(wave == 0 ? stB(S_c) + 16 * 1024 : sDummy), 16,
-                                                wave == 0 ? vbk[4] : kOOB, (int)(k0 * ldb * ES), 0, 0);
+      // blocks 16 and 17 belong to waves 0 and 1; the other waves issue the
+      // same instruction out of range into a 1 KiB dummy region (out-of-range
+      // DMA lanes still write zeros, so they must not target a live block),
+      // which keeps the instruction stream free of branches
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(wave < 2 ? stB(S_c) + (16 + wave) * 1024 : sDummy), 16,
+                                                wave < 2 ? vbk[4] : kOOB, (int)(k0 * ldb * ES), 0, 0);
     }
   };
   constexpr int kDma = B_NK ? 8 : 9;
@@ -548,8 +605,8 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int ch = FP8 ? kg * 2 + h : h * 2 + kg;
-    rA[h] = (uint32_t)((wm * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
-    rBn[h] = (uint32_t)((wn * 128 + r32) * 64 + ((ch ^ ((r32 >> 1) & 3)) << 4));
+    rA[h] = (uint32_t)((wm * 128 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
+    rBn[h] = (uint32_t)((wn * 128 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
   }
   // transposed B-KN reads, 16-lane group g = lane >> 4 (k-group g >> 1, column
   // half g & 1).  bf16: read (kk, h) gives k = kk*16 + (g>>1)*8 + h*4 + 0..3,
@@ -648,21 +705,23 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
     }
   };
 
-  // K-step t on stage S with fragments in buffer BUF: publish stage S+1 (its
-  // DMA, issued three steps earlier, has landed), then the MFMAs of step t in
-  // a fixed order, with the fragment reads of step t+1 (from stage S+1) and
-  // the DMA of step t+3 (into stage S+3 = the stage of step t-1, which every
-  // wave has finished reading) placed between them: the reads spread from the
-  // start, the DMA instructions evenly, so that neither the LDS queue nor the
-  // texture address FIFO backs up into the wave's in-order instruction
-  // stream.  Past the last K-step the DMA lanes are all out of range (zeros
-  // into a stage nobody reads) and the reads read a stale stage that is never
-  // used, so nothing here is conditional.
+  // K-step t on stage S with fragments in buffer BUF.  The fragments of step
+  // t were read from stage S during step t-1, so once every wave has passed
+  // the barrier at the top of step t (each having waited for its own reads),
+  // stage S is free: the DMA of step t+4 goes there, four steps ahead of its
+  // use.  The same barrier publishes stage S+1 (DMA issued during step t-3),
+  // whose fragments are read during this step.  The MFMAs run in a fixed
+  // order with the reads spread from the start and the DMA instructions
+  // evenly, so that neither the LDS queue nor the texture address FIFO backs
+  // up into the wave's in-order instruction stream.  Past the last K-step the
+  // DMA lanes are all out of range (zeros into a stage nobody reads) and the
+  // reads read a stale stage that is never used, so nothing here is
+  // conditional.
   constexpr int NM = C::NMFMA;
   auto step = [&](auto S_c, auto BUF_c, int t) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
-    wait_vmcnt<kDma>();
+    wait_vmcnt_lgkm0<2 * kDma>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     static_for<0, NM>([&](auto I_c) {
@@ -674,7 +733,7 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
         static_for<(i * kReads) / NR, ((i + 1) * kReads) / NR>(
             [&](auto J_c) { read_one(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{}, J_c); });
       }
-      if constexpr ((i * kDma) / NM != ((i + 1) * kDma) / NM) dma_one(IC<(S + 3) & 3>{}, IC<(i * kDma) / NM>{}, t + 3);
+      if constexpr ((i * kDma) / NM != ((i + 1) * kDma) / NM) dma_one(S_c, IC<(i * kDma) / NM>{}, t + 4);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
@@ -683,7 +742,9 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   dma(IC<0>{}, 0);
   dma(IC<1>{}, 1);
   dma(IC<2>{}, 2);
-  __syncthreads();  // waits for every DMA issued so far
+  dma(IC<3>{}, 3);
+  wait_vmcnt_lgkm0<3 * kDma>();  // stage 0 has landed
+  __builtin_amdgcn_s_barrier();
   read_frags(IC<0>{}, IC<0>{});
 
   int t = 0;
@@ -696,9 +757,36 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   if (t < nk) step(IC<0>{}, IC<0>{}, t);
   if (t + 1 < nk) step(IC<1>{}, IC<1>{}, t + 1);
   if (t + 2 < nk) step(IC<2>{}, IC<0>{}, t + 2);
+  // the zero fills past the end may still be in flight: drain them before
+  // the epilogue reuses the stage memory
+  wait_vmcnt_lgkm0<0>();
   __syncthreads();
 
-  EpiCtx c{lane, wm, wn, m0, n0, reinterpret_cast<float*>(sA0)};
+  // A bf16 residual tile (256 x 256 = 128 KiB) moves into the free stages by
+  // LDS DMA now, so its latency overlaps whatever the epilogue computes
+  // before the add.  Wave w fetches tile rows [64w, 64w + 64): rows 0-31 of
+  // that quarter into sA<w>, rows 32-63 into sB<w>, 512 bytes per row, the
+  // 16-byte chunk q of row m at chunk q ^ (m & 15) (so the epilogue's
+  // 32-lane column reads spread over 16 chunk slots).
+  const bool res_lds = p.residual != nullptr && p.residual_bf16;
+  if (res_lds) {
+    const uint16_t* R = reinterpret_cast<const uint16_t*>(p.residual) + m0 * p.ldr + n0;
+    const int64_t rows_r = min<int64_t>(BM, p.M - m0);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(R, (uint32_t)(((rows_r - 1) * p.ldr + (p.N - n0)) * 2));
+    unsigned char* const da = wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sA2 : sA3;
+    unsigned char* const db = wave == 0 ? sB0 : wave == 1 ? sB1 : wave == 2 ? sB2 : sB3;
+    static_for<0, 32>([&](auto J_c) {
+      constexpr int j = decltype(J_c)::value;
+      const int m = wave * 64 + 2 * j + (lane >> 5);
+      const int q = (lane & 31) ^ (m & 15);
+      const bool ok = m < rows_r && n0 + q * 8 < p.N;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (LDS3 void*)((j < 16 ? da : db) + ((2 * j) & 31) * 512), 16,
+                                                ok ? (uint32_t)((m * p.ldr + q * 8) * 2) : kOOB, 0, 0, 0);
+    });
+  }
+
+  EpiCtx c{lane, wm, wn, m0, n0, sRed, sCol, res_lds,
+           {wm ? sA2 : sA0, wm ? sB2 : sB0, wm ? sA3 : sA1, wm ? sB3 : sB1}, ops};
   run_epilogue<EPI>(p, c, acc);
 }
 

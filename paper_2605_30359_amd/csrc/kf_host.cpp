@@ -57,6 +57,7 @@ bool is_elementwise_kind(int k) {
 }  // namespace
 
 struct kf_desc {
+  int num_cu = 1;  // compute units of the device (persistent launch width)
   kf_op_spec spec;
   Variant variant;
   kf::EpiProgram prog;
@@ -161,7 +162,8 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       d->variant = kVarGemmF32;
       if (d->epi_shape != kf::kEpiPlain)
         return fail(KF_ERR_UNSUPPORTED, "fp32 GEMM supports element-wise, BIAS and RESIDUAL_ADD ops only");
-      d->kernel_name = "kf_gemm_f32_32x64";
+      if ((s->M + 7) / 8 > 65535) return fail(KF_ERR_UNSUPPORTED, "fp32 GEMM supports M <= 524280");
+      d->kernel_name = "kf_gemm_f32_8x8";
     } else if (dt == KF_BF16) {
       d->variant = kVarGemmBf16;
       if (s->K % 8) return fail(KF_ERR_UNSUPPORTED, "bf16 GEMM needs K %% 8 == 0 (16-byte rows)");
@@ -212,8 +214,10 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 kernel is built for cin=%d, width=%d, cout=%d",
                   kf::conv_bf16_cin(), kf::conv_bf16_width(), kf::conv_bf16_cout());
     if (s->height % 2) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 needs an even height (tiles are row pairs)");
-    if ((int64_t)s->cin * s->height * s->width * 2 >= (int64_t(1) << 31))
-      return fail(KF_ERR_UNSUPPORTED, "one image must be smaller than 2 GiB");
+    if ((int64_t)std::max(s->cin, s->cout) * s->height * s->width * 2 >= (int64_t(1) << 31))
+      return fail(KF_ERR_UNSUPPORTED, "one input or output image must be smaller than 2 GiB");
+    if ((int64_t)s->batch * (s->height / 2) > INT32_MAX)
+      return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 supports at most 2^31 - 1 row-pair tiles");
     for (int i = 0; i < s->n_ops; ++i) {
       const int k = s->ops[i].kind;
       if (!(k == KF_OP_BIAS || k == KF_OP_MAXPOOL2X2 || is_elementwise_kind(k)))
@@ -321,6 +325,7 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
     return fail(KF_ERR_NO_DEVICE, "device %d is %s; this library is built for gfx950 only", dev, prop.gcnArchName);
   }
   d->device = dev;
+  d->num_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
 
   if (d->variant == kVarConvBf16) {
     d->workspace_bytes = (size_t)9 * spec->cout * spec->cin * 2;  // repacked weights
@@ -432,8 +437,8 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
       if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
     } else {
       const int64_t es = elem_size(s.in_dtype);
-      // the K loop addresses up to three 32-deep steps past K (all out of range)
-      if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : (s.K + 128) * a.ldb) * es) ||
+      // the K loop addresses up to four K-steps (at most 256 k) past K, all out of range
+      if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : (s.K + 256) * a.ldb) * es) ||
           !fits_31(256 * a.ldo * 4) || (a.residual && !fits_31(256 * a.ldr * 4)))
         return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
       if (d->variant == kVarGemmFp8) a.scale = s.scale_a * s.scale_b;  // fl(s_a * s_b), applied to the fp32 accumulator
@@ -457,6 +462,8 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
   c.H = s.height;
   c.W = s.width;
   c.cout = s.cout;
+  c.tiles = (int32_t)(s.batch * (s.height / 2));
+  c.grid = d->num_cu;
   c.prog = d->prog;
   for (int i = 0; i < s.n_ops; ++i) {
     if (s.ops[i].kind == KF_OP_BIAS) c.bias = static_cast<const float*>(inputs[2].data);
@@ -542,6 +549,8 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     c.H = s.height;
     c.W = s.width;
     c.cout = s.cout;
+    c.tiles = (int32_t)(s.batch * (s.height / 2));
+    c.grid = d->num_cu;
     c.out = cur;
     c.out_bf16 = 1;
     e = kf::launch_conv_pack(c, d->workspace, hs);

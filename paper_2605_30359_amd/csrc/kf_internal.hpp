@@ -60,7 +60,8 @@ struct ConvArgs {
   void* out;              // [batch, cout, H(/2), W(/2)]
   int32_t pool;           // 1 if the op list ends with a 2x2 max-pool
   int32_t pool_index;     // position of the pool op in prog
-  int32_t tiles;          // number of output tiles
+  int32_t tiles;          // number of output tiles (batch x H/2 row pairs)
+  int32_t grid;           // workgroups of the persistent launch (at most tiles)
 };
 
 }  // namespace kf

@@ -357,3 +357,33 @@ def test_unfused_c2_full_config_sampled_rows():
     t = inputs.generate(cfg)
     _, out = run_gpu(cfg, t, unfused=True)
     check(cfg, t, out, rows=sample_rows(cfg["M"], 16), tol=3 * TOL["bf16"])
+
+
+# ------------------------------------------------- epilogue operand paths
+
+_ALL_DIST = dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1),
+                 gamma=("uniform", 0.5, 1.5), beta=("uniform", -0.1, 0.1), residual=("normal", 1.0))
+
+
+@pytest.mark.parametrize("name,kw,res_f32", [
+    # residual in a plain epilogue, ragged M and N (tile tails), bf16 and fp32 residual
+    ("C2", dict(M=300, N=520, K=136, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("relu",)]), False),
+    ("C2", dict(M=300, N=520, K=136, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("relu",)]), True),
+    # residual before the GroupNorm statistics, 256-wide groups across both waves
+    ("C3", dict(M=260, N=512, K=64, ops=[("bias",), ("residual_add",), ("groupnorm", 2, 1e-5), ("swish",)]), False),
+    # residual feeding a row softmax, columns past N masked out
+    ("C2", dict(M=77, N=520, K=40, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("row_softmax",)]), False),
+    # fp8 contraction with a residual
+    ("C5", dict(M=300, N=528, K=160, ops=[("bias",), ("residual_add",), ("hardtanh", -1.0, 1.0)]), False),
+    # NK layout with every column vector present
+    ("C3", dict(M=100, N=256, K=48, b_layout="nk", ops=[("bias",), ("groupnorm", 1, 1e-5), ("residual_add",)]), False),
+])
+def test_epilogue_operand_paths(name, kw, res_f32):
+    _torch()
+    cfg = inputs.config(name, dist=_ALL_DIST, residual_dtype="f32" if res_f32 else "bf16", **kw)
+    t = inputs.generate(cfg, seed=21)
+    if res_f32:
+        t["residual"] = oracle.decode_bf16(t["residual"]).astype(np.float32) * np.float32(1.25)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"{name} {kw['ops']} err {err:.3e}")
