@@ -60,16 +60,24 @@ def _elapsed_ms(hip, a, b) -> float:
     return float(ms.value)
 
 
-def _source_digest(kernel_file: str) -> str:
+def _source_digest(kernel_files) -> str:
+    """Digest of a kernel's sources (its files plus the shared device headers),
+    so that a counter summary taken on other sources is not reported."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2605_30359_amd", "csrc")
+    files = set(kernel_files) | {"kf_device.hpp", "kf_internal.hpp"}
     for name in sorted(os.listdir(csrc)):
-        if name in (kernel_file, "kf_device.hpp", "kf_internal.hpp"):
+        if name in files:
             h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()[:16]
 
 
-KERNEL_FILES = {"kf_gemm_mfma_256x256": "kf_gemm_mfma.hip", "kf_gemm_f32_8x8": "kf_gemm_f32.hip", "kf_conv3x3_bf16_256x128": "kf_conv_bf16.hip"}
+KERNEL_FILES = {
+    "kf_gemm_mfma_256x256": ["kf_gemm_mfma.hpp", "kf_gemm_mfma.hip", "kf_gemm_mfma_bf16_nk.hip",
+                             "kf_gemm_mfma_fp8_kn.hip", "kf_gemm_mfma_fp8_nk.hip"],
+    "kf_gemm_f32_8x8": ["kf_gemm_f32.hip"],
+    "kf_conv3x3_bf16_256x128": ["kf_conv_bf16.hip"],
+}
 
 
 def _traffic(kernel: str, workload: str):
@@ -82,7 +90,7 @@ def _traffic(kernel: str, workload: str):
         rec = json.load(open(path)).get(f"{kernel}:{workload}")
     except Exception:
         return None
-    if not rec or rec.get("source_digest") != _source_digest(KERNEL_FILES.get(kernel, "")):
+    if not rec or rec.get("source_digest") != _source_digest(KERNEL_FILES.get(kernel, [])):
         return None
     return rec.get("hbm_bytes_per_launch")
 

@@ -3,7 +3,10 @@
     python -m paper_2605_30359_amd.build        # or build() from Python
 
 Every .hip file under csrc/ is compiled by hipcc for gfx950 only, with packed
-fp32 instructions disabled, then linked with the host code into
+fp32 instructions disabled and no implicit contraction of a multiply and an
+add into one fma (the kernels write each fma they want explicitly, so the
+specialised and the interpreted epilogues round alike), then linked with the
+host code into
 paper_2605_30359_amd/libkf.so.  Object files go to _build/ at the repo root.
 """
 from __future__ import annotations
@@ -25,7 +28,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-Wno-unused-function"]
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-ffp-contract=off"]
 
 
 def _compile(src: str) -> str:

@@ -86,16 +86,38 @@ typedef f32x16 CAcc[4][2];
 // switch is taken once per op and the loop over the registers is unrolled
 // inside each case.
 template <int N>
-__device__ __forceinline__ void conv_apply_phase(const OpTable& ops, int oi, int oe, float b, float (&v)[N]) {
-  for (int o = oi; o < oe; ++o) {
-    const int kind = op_kind(ops, o);
-    if (kind == KF_OP_BIAS) {
+__device__ __forceinline__ void conv_apply_op(const OpTable& ops, int kind, int o, float b, float (&v)[N]) {
+  if (kind == KF_OP_BIAS) {
 #pragma unroll
-      for (int i = 0; i < N; ++i) v[i] += b;
-    } else {
-      apply_elementwise_array(kind, op_p0(ops, o), op_p1(ops, o), v);
-    }
+    for (int i = 0; i < N; ++i) v[i] += b;
+  } else {
+    apply_elementwise_array(kind, op_p0(ops, o), op_p1(ops, o), v);
   }
+}
+template <int CH, int N>
+__device__ __forceinline__ void conv_apply_phase(const OpTable& ops, int oi, int oe, float b, float (&v)[N]) {
+  if constexpr (CH == 0) {
+    for (int o = oi; o < oe; ++o) conv_apply_op(ops, op_kind(ops, o), o, b, v);
+  } else {
+    static_for<0, kChainLen[CH]>([&](auto O_c) {
+      constexpr int o = decltype(O_c)::value;
+      if (o >= oi && o < oe) conv_apply_op(ops, kChainOps[CH][o], o, b, v);
+    });
+  }
+}
+
+// A compile-time chain whose ops before the pool are all non-decreasing and
+// exact in floating point (bias add, ReLU, hardtanh) can pool first: max
+// commutes with each of them, so the result is the same bit for bit, and
+// the ops run on a quarter of the values.
+constexpr bool chain_pools_first(int ch) {
+  if (ch == 0) return false;
+  for (int o = 0; o < kChainLen[ch]; ++o) {
+    const int k = kChainOps[ch][o];
+    if (k == KF_OP_MAXPOOL2X2) return true;
+    if (k != KF_OP_BIAS && k != KF_OP_RELU && k != KF_OP_HARDTANH) return false;
+  }
+  return false;
 }
 
 }  // namespace
@@ -112,6 +134,7 @@ __global__ __launch_bounds__(256) void kf_conv_pack_weights(const uint16_t* __re
   }
 }
 
+template <int CH>
 __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, const uint16_t* __restrict__ wp) {
   __shared__ __attribute__((aligned(1024))) unsigned char sHalo[kHalo];
   __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage], sW3[kWStage],
@@ -342,7 +365,8 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
           v[i] = acc[bc][bj][i];
           v[16 + i] = acc[bc + 2][bj][i];
         }
-        conv_apply_phase(ops, 0, pidx, bias_v[bj], v);
+        constexpr bool kPoolFirst = chain_pools_first(CH);
+        if constexpr (!kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias_v[bj], v);
         if (p.pool) {
           // window (q, h2): columns i, i + 1 (i = 4q + 2 h2) of both rows
           float pv[8];
@@ -353,7 +377,8 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
               const int i = q * 4 + h2 * 2;
               pv[q * 2 + h2] = fmaxf(fmaxf(v[i], v[i + 1]), fmaxf(v[16 + i], v[16 + i + 1]));
             }
-          conv_apply_phase(ops, pidx + 1, nops, bias_v[bj], pv);
+          if constexpr (kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias_v[bj], pv);
+          conv_apply_phase<CH>(ops, pidx + 1, nops, bias_v[bj], pv);
           // pooled row of channel co: 64 pixels = 8 chunks of 16 bytes
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -416,11 +441,14 @@ hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStrea
   return hipGetLastError();
 }
 
-hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, hipStream_t stream) {
+hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, int chain, hipStream_t stream) {
   if (args.tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)(args.grid < args.tiles ? args.grid : args.tiles));
-  hipLaunchKernelGGL(kf_conv3x3_bf16_256x128, grid, dim3(NT), 0, stream, args,
-                     reinterpret_cast<const uint16_t*>(packed_weights));
+  const uint16_t* wp = reinterpret_cast<const uint16_t*>(packed_weights);
+  if (chain == 7)
+    hipLaunchKernelGGL(kf_conv3x3_bf16_256x128<7>, grid, dim3(NT), 0, stream, args, wp);
+  else
+    hipLaunchKernelGGL(kf_conv3x3_bf16_256x128<0>, grid, dim3(NT), 0, stream, args, wp);
   return hipGetLastError();
 }
 

@@ -1,0 +1,864 @@
+// bf16 / fp8 GEMM + fused epilogue on gfx950 matrix cores.
+//
+// h = A * B with A [M,K] row-major and B either [K,N] ("KN", N
+// contiguous) or [N,K] ("NK", K contiguous), fp32 accumulation, then the op
+// list (bias, activations, scale, GroupNorm, residual add, row softmax /
+// logsumexp partials) applied to the accumulator registers, then one store.
+// This is the matmul + epilogue fusion the paper's search produces
+// (Appendix A, "Operator Fusion"; Appendix C, the evolved matmul + activation
+// kernel), laid out for CDNA4:
+//
+//   tile     256 x 256 outputs per workgroup of 4 waves (2 x 2); each wave
+//            owns 128 x 128 = 4 x 4 blocks of 32 x 32 MFMA outputs
+//            (v_mfma_f32_32x32x16_bf16, or for OCP fp8 e4m3 operands
+//            v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales and the
+//            per-tensor dequantisation applied to the accumulator), the shapes
+//            that sustain the full matrix-core rate; accumulators in AGPRs
+//   K loop   64 bytes of k per step, four LDS stages; operands move global -> LDS
+//            by buffer_load ... lds (LDS DMA), issued three steps ahead, so no
+//            VGPR stages operand data; out-of-range lanes of a DMA write zeros,
+//            which pads ragged M, N and K tails without branches
+//   LDS      A (and B in NK layout) as [rows][64 bytes of k] with an XOR swizzle
+//            of the 16-byte chunks; B in KN layout kept as [k][256 n] with a
+//            padded row pitch and read through ds_read_b64_tr_b16 / _tr_b8,
+//            which transpose small blocks across each 16-lane group so every
+//            lane receives consecutive k of one column
+//   order    the B fragment is the MFMA "A" operand, so each lane's
+//            accumulators are runs of 4 consecutive output columns of one row:
+//            8-byte bf16 / 16-byte fp32 stores, lane-local row reductions
+//   raster   workgroup ids are renumbered so that consecutive tiles land on
+//            the same XCD (its own L2), in groups of 4 tile-rows
+#pragma once
+
+#include <type_traits>
+
+#include "kf_device.hpp"
+#include "kf_launch.hpp"
+
+namespace kf {
+
+namespace {
+
+constexpr int BM = 256;
+constexpr int BN = 256;
+constexpr int NT = 256;
+
+__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nwg = tiles_m * tiles_n;
+  int lid = bid;
+  // Workgroups are dispatched round-robin over the 8 XCDs; renumber so that
+  // each XCD receives a contiguous range of logical tiles.
+  if ((nwg & 7) == 0) lid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  constexpr int G = 4;
+  const int per_group = G * tiles_n;
+  const int group = lid / per_group;
+  const int first_m = group * G;
+  const int gsize = min(tiles_m - first_m, G);
+  const int r = lid - group * per_group;
+  tm = first_m + r % gsize;
+  tn = r / gsize;
+}
+
+template <typename T>
+__device__ __forceinline__ T lds_load(const unsigned char* p) {
+  return *reinterpret_cast<const T*>(p);
+}
+
+// s_waitcnt vmcnt(N) lgkmcnt(0), expcnt left alone
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0x0 << 8) | ((N >> 4) << 14));
+}
+
+// acc[bi][bj][i]: output row    wm*128 + bi*32 + (lane & 31)
+//                 output column wn*128 + bj*32 + (i/4)*8 + (lane >> 5)*4 + i%4
+typedef f32x16 Acc[4][4];
+
+// -------------------------------------------------------------- epilogue
+//
+// The op list is run in up to two phases around its reduction op (GROUPNORM,
+// ROW_SOFTMAX or ROW_LOGSUMEXP).  Each phase takes one 32-row block bi at a
+// time -- its 64 values per lane in VGPRs, the rest of the tile in AGPRs --
+// through all of the phase's element-wise ops, and the last phase stores.
+
+struct EpiCtx {
+  int lane, wm, wn;
+  int64_t m0, n0;
+  float* red;                    // 2 x 256 floats of LDS for cross-wave row reductions
+  const float* col;              // LDS: bias, gamma, beta of the tile's 256 columns
+  bool res_lds;                  // the bf16 residual tile sits in LDS (see the kernel's residual staging)
+  const unsigned char* res[4];   // LDS rows of row block bi of this wave's residual
+  OpTable ops;                   // the op program, one op per lane
+};
+
+// run g (0..15) of a row = block bj = g / 4, group gi = g % 4
+__device__ __forceinline__ int col_local(const EpiCtx& c, int g) {
+  return c.wn * 128 + (g >> 2) * 32 + (g & 3) * 8 + (c.lane >> 5) * 4;
+}
+__device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.wm * 128 + bi * 32 + (c.lane & 31); }
+
+typedef f32x4 Row[16];  // one lane's 64 values of one row
+
+__device__ __forceinline__ void get_row(const Acc& acc, int bi, Row& v) {
+#pragma unroll
+  for (int g = 0; g < 16; ++g) {
+    const f32x16& a = acc[bi][g >> 2];
+    const int o = (g & 3) * 4;
+    v[g] = f32x4{a[o], a[o + 1], a[o + 2], a[o + 3]};
+  }
+}
+__device__ __forceinline__ void put_row(Acc& acc, int bi, const Row& v) {
+#pragma unroll
+  for (int g = 0; g < 16; ++g) {
+    const int o = (g & 3) * 4;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[bi][g >> 2][o + q] = v[g][q];
+  }
+}
+
+// 4 consecutive fp32 of a per-column vector (0 bias, 1 gamma, 2 beta), staged
+// in LDS at kernel start; columns >= N read as 0.
+__device__ __forceinline__ f32x4 col4(const EpiCtx& c, int which, int g) {
+  return *reinterpret_cast<const f32x4*>(c.col + which * 256 + col_local(c, g));
+}
+
+// The bf16 residual tile in LDS: row m of the tile at row (m & 31) of array
+// res[(m >> 5) & 3] of the wave that owns it, 512 bytes per row, 16-byte
+// chunk q of the row stored at chunk q ^ (m & 15).
+__device__ __forceinline__ f32x4 res4(const EpiCtx& c, int bi, int g) {
+  const int r = c.lane & 31;
+  const int q = c.wn * 16 + (g >> 2) * 4 + (g & 3);
+  const u32x2 w = *reinterpret_cast<const u32x2*>(c.res[bi] + r * 512 + ((q ^ (r & 15)) << 4) + (c.lane >> 5) * 8);
+  return f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+}
+
+// Wait until every wave's share of the residual tile has landed in LDS.
+__device__ __forceinline__ void res_wait(const EpiCtx& c) {
+  if (c.res_lds) {
+    wait_vmcnt_lgkm0<0>();
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ float sum4(f32x4 a) { return (a[0] + a[1]) + (a[2] + a[3]); }
+__device__ __forceinline__ float max4(f32x4 a) { return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])); }
+
+// Combine one value per row over the two lanes of the row (lane ^ 32) and, if
+// `cross`, over the two waves that share the rows (through LDS).  Every
+// thread of the workgroup must call it with the same `cross`.
+template <bool IS_MAX>
+__device__ __forceinline__ void row_combine(const EpiCtx& c, float (&v)[4], bool cross) {
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) {
+    const float y = shfl_xor(v[bi], 32);
+    v[bi] = IS_MAX ? fmaxf(v[bi], y) : v[bi] + y;
+  }
+  if (!cross) return;
+  if (c.lane < 32) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) c.red[c.wn * 256 + row_local(c, bi)] = v[bi];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) {
+    const float o = c.red[(c.wn ^ 1) * 256 + row_local(c, bi)];
+    v[bi] = IS_MAX ? fmaxf(v[bi], o) : v[bi] + o;
+  }
+  __syncthreads();
+}
+
+// One element-wise / tensor-reading op (kind, at position o of the list) on
+// one row block.  With a compile-time kind the switch folds away.
+__device__ __forceinline__ void apply_op(const GemmArgs& p, const EpiCtx& c, int bi, int kind, int o, Row& v) {
+  const int64_t N = p.N;
+  {
+    const float p0 = op_p0(c.ops, o), p1 = op_p1(c.ops, o);
+    switch (kind) {
+      case KF_OP_BIAS:
+#pragma unroll
+        for (int g = 0; g < 16; ++g) v[g] += col4(c, 0, g);
+        break;
+      case KF_OP_RESIDUAL_ADD: {
+        const int64_t rows = min<int64_t>(BM, p.M - c.m0);
+        const int64_t rl = row_local(c, bi);
+        if (c.res_lds) {
+#pragma unroll
+          for (int g = 0; g < 16; ++g) v[g] += res4(c, bi, g);
+        } else if (p.residual_bf16) {
+          const uint16_t* base = reinterpret_cast<const uint16_t*>(p.residual) + c.m0 * p.ldr + c.n0;
+          const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 2));
+#pragma unroll
+          for (int g = 0; g < 16; ++g) {
+            const int cl = col_local(c, g);
+            const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldr + cl) * 2) : kOOB;
+            const u32x2 w = buf_load8(r, off);
+            v[g] += f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+          }
+        } else {
+          const float* base = reinterpret_cast<const float*>(p.residual) + c.m0 * p.ldr + c.n0;
+          const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 4));
+#pragma unroll
+          for (int g = 0; g < 16; ++g) {
+            const int cl = col_local(c, g);
+            const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldr + cl) * 4) : kOOB;
+            v[g] += __builtin_bit_cast(f32x4, buf_load16(r, off));
+          }
+        }
+        break;
+      }
+#define KF_EW_CASE(K, EXPR)                          \
+  case K:                                            \
+    _Pragma("unroll") for (int g = 0; g < 16; ++g)   \
+    _Pragma("unroll") for (int q = 0; q < 4; ++q) {  \
+      const float x = v[g][q];                       \
+      v[g][q] = (EXPR);                              \
+    }                                                \
+    break;
+      KF_EW_CASE(KF_OP_RELU, fmaxf(x, 0.0f))
+      KF_EW_CASE(KF_OP_GELU_TANH, f_gelu_tanh(x))
+      KF_EW_CASE(KF_OP_GELU_ERF, f_gelu_erf(x))
+      KF_EW_CASE(KF_OP_SWISH, f_swish(x))
+      KF_EW_CASE(KF_OP_SIGMOID, f_sigmoid(x))
+      KF_EW_CASE(KF_OP_TANH, f_tanh(x))
+      KF_EW_CASE(KF_OP_HARDTANH, fminf(fmaxf(x, p0), p1))
+      KF_EW_CASE(KF_OP_SCALE, x * p0)
+#undef KF_EW_CASE
+      default:
+        break;
+    }
+  }
+}
+
+// Ops oi..oe-1 of chain CH on one row block: interpreted (chain 0), or
+// unrolled over the chain's compile-time op kinds.
+template <int CH>
+__device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, int bi, int oi, int oe, Row& v) {
+  if constexpr (CH == 0) {
+#pragma nounroll
+    for (int o = oi; o < oe; ++o) apply_op(p, c, bi, op_kind(c.ops, o), o, v);
+  } else {
+    static_for<0, kChainLen[CH]>([&](auto O_c) {
+      constexpr int o = decltype(O_c)::value;
+      if (o >= oi && o < oe) apply_op(p, c, bi, kChainOps[CH][o], o, v);
+    });
+  }
+}
+
+// Store one row block (16 runs of 4 values per lane).
+__device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, int bi, const Row& v) {
+  const int64_t N = p.N;
+  const int64_t rows = min<int64_t>(BM, p.M - c.m0);
+  const int64_t rl = row_local(c, bi);
+  if (p.out_bf16) {
+    uint16_t* base = reinterpret_cast<uint16_t*>(p.out) + c.m0 * p.ldo + c.n0;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 2));
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int cl = col_local(c, g);
+      const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 2) : kOOB;
+      buf_store8(u32x2{pack_bf16x2(v[g][0], v[g][1]), pack_bf16x2(v[g][2], v[g][3])}, r, off);
+    }
+  } else {
+    float* base = reinterpret_cast<float*>(p.out) + c.m0 * p.ldo + c.n0;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 4));
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int cl = col_local(c, g);
+      const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 4) : kOOB;
+      buf_store16(__builtin_bit_cast(u32x4, v[g]), r, off);
+    }
+  }
+}
+
+// Epilogue of shape EPI (see EpiShape): ops [0, r) element-wise, op r the
+// reduction (if any), ops (r, n) element-wise, then the store.
+template <int EPI, int CH, bool FP8>
+__device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c, Acc& acc) {
+  const int64_t N = p.N;
+  const int nops = p.prog.n;
+  const int r = EPI == kEpiPlain ? nops : p.red_index;
+
+  if (EPI == kEpiPlain) {
+    res_wait(c);
+    static_for<0, 4>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      get_row(acc, bi, v);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+      apply_phase<CH>(p, c, bi, 0, nops, v);
+      store_row(p, c, bi, v);
+    });
+    return;
+  }
+
+  if (EPI == kEpiGroupNorm) {
+    // Group width gw in {32, 64, 128, 256} columns: each lane holds 16 of
+    // every 32-column block of its rows, so per-block sums are lane-local plus
+    // one exchange with lane ^ 32; wider groups add neighbouring blocks, and a
+    // 256-wide group also the other wave's half of the tile row.
+    int res_at = -1;
+    for (int o = 0; o < nops; ++o)
+      if (op_kind(c.ops, o) == KF_OP_RESIDUAL_ADD) res_at = o;
+    const bool res_early = res_at < r;  // the residual is added before the statistics
+    if (res_early) res_wait(c);
+    const int gw = p.gn_group;
+    const int bpg = gw >> 5;  // 32-column blocks per group (1, 2, 4, 8)
+    const int bw = min(bpg, 4);
+    const float inv_n = 1.0f / (float)gw;
+    float s[4][4];
+    static_for<0, 4>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      get_row(acc, bi, v);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+      apply_phase<CH>(p, c, bi, 0, r, v);
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj)
+        s[bi][bj] = (sum4(v[bj * 4]) + sum4(v[bj * 4 + 1])) + (sum4(v[bj * 4 + 2]) + sum4(v[bj * 4 + 3]));
+      put_row(acc, bi, v);
+    });
+    auto group_reduce = [&](float (&t)[4][4]) {
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) t[bi][bj] += shfl_xor(t[bi][bj], 32);
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi) {
+        float g2[4];
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) {
+          float a = 0.0f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) a += ((q / bw) == (bj / bw)) ? t[bi][q] : 0.0f;
+          g2[bj] = a;
+        }
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) t[bi][bj] = g2[bj];
+      }
+      if (bpg == 8) {
+        float w[4];
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) w[bi] = t[bi][0];
+        if (c.lane < 32) {
+#pragma unroll
+          for (int bi = 0; bi < 4; ++bi) c.red[c.wn * 256 + row_local(c, bi)] = w[bi];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) {
+          const float o = w[bi] + c.red[(c.wn ^ 1) * 256 + row_local(c, bi)];
+#pragma unroll
+          for (int bj = 0; bj < 4; ++bj) t[bi][bj] = o;
+        }
+        __syncthreads();
+      }
+    };
+    group_reduce(s);
+    float mean[4][4], ss[4][4];
+    static_for<0, 4>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) {
+        mean[bi][bj] = s[bi][bj] * inv_n;
+        float a = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const float d = acc[bi][bj][q] - mean[bi][bj];
+          a += d * d;
+        }
+        ss[bi][bj] = a;
+      }
+    });
+    group_reduce(ss);
+    const float eps = op_p0(c.ops, r);
+    if (!res_early) res_wait(c);
+    static_for<0, 4>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      get_row(acc, bi, v);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int bj = g >> 2;
+        const float rs = rsqrtf(ss[bi][bj] * inv_n + eps);
+        const f32x4 gm = col4(c, 1, g), bt = col4(c, 2, g);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[g][q] = fmaf((v[g][q] - mean[bi][bj]) * rs, gm[q], bt[q]);
+      }
+      apply_phase<CH>(p, c, bi, r + 1, nops, v);
+      store_row(p, c, bi, v);
+    });
+    return;
+  }
+
+  // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
+  // this 256-column tile goes to the partials buffer.
+  res_wait(c);
+  float mx[4];
+  static_for<0, 4>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    Row v;
+    get_row(acc, bi, v);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+    apply_phase<CH>(p, c, bi, 0, r, v);
+    // columns past N take no part in a row reduction (only the last column
+    // tile can have any)
+    if (c.n0 + BN > N) {
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int64_t n = c.n0 + col_local(c, g);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[g][q] = (n + q < N) ? v[g][q] : -INFINITY;
+      }
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) m = fmaxf(m, max4(v[g]));
+    mx[bi] = m;
+    put_row(acc, bi, v);
+  });
+  row_combine<true>(c, mx, true);
+  float se[4];
+  static_for<0, 4>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    const float ml = mx[bi] * kLog2e;
+    float s = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) s += __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
+    se[bi] = s;
+  });
+  row_combine<false>(c, se, true);
+  if (c.lane < 32 && c.wn == 0) {
+    float2* part = reinterpret_cast<float2*>(p.partials);
+    const int tn = (int)(c.n0 / BN);
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) {
+      const int64_t m = c.m0 + row_local(c, bi);
+      if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
+    }
+  }
+  if (op_kind(c.ops, r) != KF_OP_ROW_SOFTMAX) return;  // logsumexp: the finishing kernel writes
+  // softmax: store e^(h - tile max); the row-finishing kernel rescales it
+  static_for<0, 4>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    const float ml = mx[bi] * kLog2e;
+    Row v;
+    get_row(acc, bi, v);
+#pragma unroll
+    for (int g = 0; g < 16; ++g)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[g][q] = __builtin_amdgcn_exp2f(fmaf(v[g][q], kLog2e, -ml));
+    store_row(p, c, bi, v);
+  });
+}
+
+// ---------------------------------------------------------------- main loop
+//
+// One __shared__ array per operand and stage (distinct objects, so the
+// compiler's wait-count analysis can tell the stage being filled by LDS DMA
+// from the stages being read).  An LDS DMA wave instruction writes 16 bytes
+// per lane at M0 + 16 * lane; the swizzles below are therefore applied on the
+// global side, by choosing which chunk each lane fetches.
+//
+// A K-step covers 64 bytes of k: 32 bf16 or 64 fp8.
+// The LDS serves 256 bytes per clock, so a 16-byte-per-lane read is taken 16
+// lanes at a time and an 8-byte one 32 lanes at a time; the layouts below
+// give every such lane group 16 (32) distinct 16-byte (8-byte) bank slots.
+//   A (and B-NK): [256 rows][64 bytes of k]; chunk c of row m stored at chunk
+//     c ^ ((m >> 2) & 3): the 16 consecutive rows of a ds_read_b128 lane
+//     group fall on 4 row positions x 4 chunk positions of a 256-byte line.
+//   B-KN: [k][256 n] rows with a padded pitch (bf16: 32 rows of 576 bytes,
+//     fp8: 64 rows of 288 bytes; 18 KiB either way), read through the
+//     transposing ds_read_b64_tr_b16 / _b8: in each 16-lane group the lanes
+//     point at 4 (8) k-rows and receive the k values of their own column.  A
+//     pitch of 64 (32) bytes past 256-byte alignment puts one group's rows in
+//     alternate 32 (16) byte slots and the other column half of the same
+//     32-lane read in the slots between.
+//
+// MFMA: bf16 v_mfma_f32_32x32x16_bf16 (32 per step, two 16-k halves), fp8
+// v_mfma_scale_f32_32x32x64_f8f6f4 with unit block scales (16 per step); both
+// run at the full matrix-core rate and leave the same 32x32 accumulator
+// layout, so the epilogue is shared.
+
+template <bool FP8>
+struct ElemCfg;
+template <>
+struct ElemCfg<false> {  // bf16
+  static constexpr int ES = 2, KSTEP = 32, NMFMA = 32, BPITCH = 576;
+};
+template <>
+struct ElemCfg<true> {  // OCP fp8 e4m3
+  static constexpr int ES = 1, KSTEP = 64, NMFMA = 16, BPITCH = 288;
+};
+
+constexpr int kAStage = BM * 64;           // 16 KiB
+constexpr int kBStageKN = 18 * 1024;       // 18 KiB = 18 DMA blocks of 1 KiB
+constexpr int kBStageNK = BN * 64;         // 16 KiB
+
+#define LDS3 __attribute__((address_space(3)))
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+typedef __attribute__((ext_vector_type(2))) int i32x2;
+
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+
+}  // namespace
+
+template <bool FP8, bool B_NK, int EPI, int CH>
+__global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
+  using C = ElemCfg<FP8>;
+  constexpr int ES = C::ES;
+  constexpr int kBS = B_NK ? kBStageNK : kBStageKN;
+  __shared__ __attribute__((aligned(1024))) unsigned char sA0[kAStage], sA1[kAStage], sA2[kAStage], sA3[kAStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sB0[kBS], sB1[kBS], sB2[kBS], sB3[kBS];
+  __shared__ __attribute__((aligned(1024))) unsigned char sDummy[B_NK ? 16 : 1024];
+  __shared__ __attribute__((aligned(16))) float sCol[3 * 256];  // bias, gamma, beta of the tile's columns
+  __shared__ float sRed[2 * 256];                              // cross-wave row reductions
+  auto stA = [&](auto S_c) -> unsigned char* {
+    constexpr int S = decltype(S_c)::value;
+    return S == 0 ? sA0 : S == 1 ? sA1 : S == 2 ? sA2 : sA3;
+  };
+  auto stB = [&](auto S_c) -> unsigned char* {
+    constexpr int S = decltype(S_c)::value;
+    return S == 0 ? sB0 : S == 1 ? sB1 : S == 2 ? sB2 : sB3;
+  };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1;
+  const int wn = wave >> 1;
+
+  int tm, tn;
+  tile_coords(blockIdx.x, p.tiles_m, p.tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM;
+  const int64_t n0 = (int64_t)tn * BN;
+  const int K = (int)p.K;
+  const int64_t lda = p.lda, ldb = p.ldb;
+
+  // operand descriptors: based at the tile, records ending at the last valid
+  // element, so rows past M / N (and past K for B-KN) read as zero
+  const unsigned char* A = reinterpret_cast<const unsigned char*>(p.a);
+  const unsigned char* B = reinterpret_cast<const unsigned char*>(p.b);
+  const int64_t rows_a = min<int64_t>(BM, p.M - m0);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * lda * ES, (uint32_t)(((rows_a - 1) * lda + K) * ES));
+  const int64_t rows_b = min<int64_t>(BN, p.N - n0);
+  const __amdgpu_buffer_rsrc_t rb =
+      B_NK ? make_rsrc(B + n0 * ldb * ES, (uint32_t)(((rows_b - 1) * ldb + K) * ES))
+           : make_rsrc(B + n0 * ES, (uint32_t)(((max(K, 1) - 1) * ldb + (p.N - n0)) * ES));
+
+  const OpTable ops = load_op_table(p.prog, lane);
+
+  // The tile's per-column epilogue vectors (bias, gamma, beta) go to LDS with
+  // one DMA instruction each (waves 0, 1, 2; columns past N read as zero),
+  // ahead of the operand DMA, so they have landed long before the epilogue.
+  {
+    const float* vec = wave == 0 ? p.bias : wave == 1 ? p.gamma : p.beta;
+    if (wave < 3 && vec != nullptr) {
+      const __amdgpu_buffer_rsrc_t rv = make_rsrc(vec + n0, (uint32_t)((p.N - n0) * 4));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (LDS3 void*)(sCol + wave * 256), 16, (uint32_t)lane * 16u, 0, 0, 0);
+    }
+  }
+
+  // ---- DMA source byte offsets (loop invariant; the K-step enters as soffset)
+  // [rows][64 B] operands: wave w fills rows [64w, 64w + 64) with 4
+  // instructions of 16 rows; lane l -> row 16i + l/4, LDS chunk l%4, which
+  // holds global chunk (l%4) ^ ((l >> 4) & 3).
+  const int dma_lc = (lane & 3) ^ ((lane >> 4) & 3);
+  uint32_t va[4], vbn[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = wave * 64 + i * 16 + (lane >> 2);
+    va[i] = (uint32_t)((int64_t)row * lda * ES + dma_lc * 16);
+    vbn[i] = (uint32_t)((int64_t)row * ldb * ES + dma_lc * 16);
+  }
+  // B-KN: 18 blocks of 1 KiB per stage, block b = wave + 4 i; byte q of the
+  // stage is row q / BPITCH, byte (q % BPITCH) of the row (the pad reads as zero)
+  uint32_t vbk[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    const int b = wave + 4 * i;
+    const int pos = b * 1024 + lane * 16;
+    const int k = pos / C::BPITCH, col = pos % C::BPITCH;
+    const bool ok = b < 18 && col < 256 * ES && (n0 + col / ES < p.N);
+    vbk[i] = ok ? (uint32_t)((int64_t)k * ldb * ES + col) : kOOB;
+  }
+
+  // DMA instruction j (0 .. kDma-1) of K-step t into stage S.  The K-step
+  // enters as the scalar offset; the descriptor's range check applies to the
+  // sum of vector and scalar offsets, so k-rows of B-KN past K (and every
+  // lane of the steps past the end that the pipeline issues) read as zero.
+  auto dma_one = [&](auto S_c, auto J_c, int t) {
+    constexpr int J = decltype(J_c)::value;
+    const int k0 = t * C::KSTEP;
+    const bool kin = k0 + dma_lc * (16 / ES) < K;  // K tail of a k-contiguous operand
+    if (J < 4) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (LDS3 void*)(stA(S_c) + wave * 4096 + J * 1024), 16,
+                                                kin ? va[J] : kOOB, k0 * ES, 0, 0);
+    } else if (B_NK) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 4096 + (J - 4) * 1024), 16,
+                                                kin ? vbn[J - 4] : kOOB, k0 * ES, 0, 0);
+    } else if (J < 8) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(stB(S_c) + wave * 1024 + (J - 4) * 4096), 16,
+                                                vbk[J - 4], (int)(k0 * ldb * ES), 0, 0);
+    } else {
+      // blocks 16 and 17 belong to waves 0 and 1; the other waves issue the
+      // same instruction out of range into a 1 KiB dummy region (out-of-range
+      // DMA lanes still write zeros, so they must not target a live block),
+      // which keeps the instruction stream free of branches
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (LDS3 void*)(wave < 2 ? stB(S_c) + (16 + wave) * 1024 : sDummy), 16,
+                                                wave < 2 ? vbk[4] : kOOB, (int)(k0 * ldb * ES), 0, 0);
+    }
+  };
+  constexpr int kDma = B_NK ? 8 : 9;
+  auto dma = [&](auto S_c, int t) { static_for<0, kDma>([&](auto J_c) { dma_one(S_c, J_c, t); }); };
+
+  // ---- fragment read offsets.  32x32 MFMA operand lane l: row / column
+  // l & 31, k-group l >> 5.  bf16: fragment half h is the 16-k sub-step h
+  // (chunk 2h + kg); fp8: the two halves are the 32 bytes of k-group kg
+  // (chunks 2kg, 2kg + 1).
+  const int r32 = lane & 31, kg = lane >> 5;
+  uint32_t rA[2], rBn[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int ch = FP8 ? kg * 2 + h : h * 2 + kg;
+    rA[h] = (uint32_t)((wm * 128 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
+    rBn[h] = (uint32_t)((wn * 128 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
+  }
+  // transposed B-KN reads, 16-lane group g = lane >> 4 (k-group g >> 1, column
+  // half g & 1).  bf16: read (kk, h) gives k = kk*16 + (g>>1)*8 + h*4 + 0..3,
+  // lane 4r + q points at k-row (.. + r), columns 4q .. 4q+3 of its half.
+  // fp8: read h gives k = (g>>1)*32 + h*8 + 0..7, lane 2r + q points at k-row
+  // (.. + r), columns 8q .. 8q+7 of its half.
+  uint32_t rBk[4];
+  {
+    const int g = lane >> 4;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      if (FP8) {
+        const int r = (lane >> 1) & 7, q = lane & 1;
+        rBk[x] = (uint32_t)(((g >> 1) * 32 + x * 8 + r) * C::BPITCH + wn * 128 + (g & 1) * 16 + q * 8);
+      } else {
+        const int kk = x >> 1, h = x & 1, r = (lane >> 2) & 3, q = lane & 3;
+        rBk[x] = (uint32_t)((kk * 16 + (g >> 1) * 8 + h * 4 + r) * C::BPITCH + (wn * 128 + (g & 1) * 16 + q * 4) * 2);
+      }
+    }
+  }
+
+  u32x4 fa[2][2][4], fb[2][2][4];  // [buffer][half][block]: A and B-NK fragments
+  i32x2 ft[2][16];                 // [buffer][read]: B-KN transposed reads
+
+  // Fragment read j of a K-step, in the order the next step consumes them.
+  //   bf16: per 16-k half: 4 A, then B (4 x 2 transposed / 4 b128)
+  //   fp8:  per half of the 32 bytes: 4 A (and 4 B-NK); B-KN: 16 transposed
+  //         reads after the A halves
+  constexpr int kReads = B_NK ? 16 : 24;
+  auto read_one = [&](auto S_c, auto BUF_c, auto J_c) {
+    constexpr int BUF = decltype(BUF_c)::value;
+    constexpr int J = decltype(J_c)::value;
+    if constexpr (!FP8) {
+      constexpr int per = kReads / 2;
+      constexpr int h = J / per, j = J % per;
+      if constexpr (j < 4) {
+        fa[BUF][h][j] = lds_load<u32x4>(stA(S_c) + rA[h] + j * 2048);
+      } else if constexpr (B_NK) {
+        fb[BUF][h][j - 4] = lds_load<u32x4>(stB(S_c) + rBn[h] + (j - 4) * 2048);
+      } else {
+        constexpr int bj = (j - 4) / 2, x = h * 2 + (j - 4) % 2;
+        ft[BUF][(h * 4 + bj) * 2 + (j - 4) % 2] = __builtin_bit_cast(
+            i32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS3 i16x4*)(stB(S_c) + rBk[x] + bj * 64)));
+      }
+    } else {
+      if constexpr (J < 8) {
+        constexpr int h = J / 4, bi = J % 4;
+        fa[BUF][h][bi] = lds_load<u32x4>(stA(S_c) + rA[h] + bi * 2048);
+      } else if constexpr (B_NK) {
+        constexpr int h = (J - 8) / 4, bj = (J - 8) % 4;
+        fb[BUF][h][bj] = lds_load<u32x4>(stB(S_c) + rBn[h] + bj * 2048);
+      } else {
+        constexpr int bj = (J - 8) / 4, x = (J - 8) % 4;
+        ft[BUF][bj * 4 + x] =
+            __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS3 i32x2*)(stB(S_c) + rBk[x] + bj * 32));
+      }
+    }
+  };
+  auto read_frags = [&](auto S_c, auto BUF_c) {
+    static_for<0, kReads>([&](auto J_c) { read_one(S_c, BUF_c, J_c); });
+  };
+
+  Acc acc;
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
+
+  // MFMA i of a K-step on fragment buffer BUF
+  auto mfma_one = [&](auto BUF_c, auto I_c) {
+    constexpr int BUF = decltype(BUF_c)::value;
+    constexpr int i = decltype(I_c)::value;
+    if constexpr (!FP8) {
+      constexpr int kk = i / 16, bi = (i / 4) % 4, bj = i % 4;
+      bf16x8 bfr;
+      if constexpr (B_NK)
+        bfr = __builtin_bit_cast(bf16x8, fb[BUF][kk][bj]);
+      else
+        bfr = __builtin_bit_cast(bf16x8, __builtin_shufflevector(ft[BUF][(kk * 4 + bj) * 2], ft[BUF][(kk * 4 + bj) * 2 + 1], 0, 1, 2, 3));
+      acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr, __builtin_bit_cast(bf16x8, fa[BUF][kk][bi]),
+                                                            acc[bi][bj], 0, 0, 0);
+    } else {
+      constexpr int bi = i / 4, bj = i % 4;
+      const i32x8 afr = __builtin_bit_cast(i32x8, __builtin_shufflevector(fa[BUF][0][bi], fa[BUF][1][bi], 0, 1, 2, 3, 4, 5, 6, 7));
+      i32x8 bfr;
+      if constexpr (B_NK) {
+        bfr = __builtin_bit_cast(i32x8, __builtin_shufflevector(fb[BUF][0][bj], fb[BUF][1][bj], 0, 1, 2, 3, 4, 5, 6, 7));
+      } else {
+        const auto lo = __builtin_shufflevector(ft[BUF][bj * 4], ft[BUF][bj * 4 + 1], 0, 1, 2, 3);
+        const auto hi = __builtin_shufflevector(ft[BUF][bj * 4 + 2], ft[BUF][bj * 4 + 3], 0, 1, 2, 3);
+        bfr = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+      acc[bi][bj] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bfr, afr, acc[bi][bj], 0, 0, 0, 127, 0, 127);
+    }
+  };
+
+  // K-step t on stage S with fragments in buffer BUF.  The fragments of step
+  // t were read from stage S during step t-1, so once every wave has passed
+  // the barrier at the top of step t (each having waited for its own reads),
+  // stage S is free: the DMA of step t+4 goes there, four steps ahead of its
+  // use.  The same barrier publishes stage S+1 (DMA issued during step t-3),
+  // whose fragments are read during this step.  The MFMAs run in a fixed
+  // order with the reads spread from the start and the DMA instructions
+  // evenly, so that neither the LDS queue nor the texture address FIFO backs
+  // up into the wave's in-order instruction stream.  Past the last K-step the
+  // DMA lanes are all out of range (zeros into a stage nobody reads) and the
+  // reads read a stale stage that is never used, so nothing here is
+  // conditional.
+  constexpr int NM = C::NMFMA;
+  auto step = [&](auto S_c, auto BUF_c, int t) {
+    constexpr int S = decltype(S_c)::value;
+    constexpr int BUF = decltype(BUF_c)::value;
+    wait_vmcnt_lgkm0<2 * kDma>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, NM>([&](auto I_c) {
+      constexpr int i = decltype(I_c)::value;
+      mfma_one(BUF_c, I_c);
+      // reads j in [i*R/NM', (i+1)*R/NM') over the first NM' = min(NM, 24) MFMAs
+      constexpr int NR = NM < 24 ? NM : 24;
+      if constexpr (i < NR) {
+        static_for<(i * kReads) / NR, ((i + 1) * kReads) / NR>(
+            [&](auto J_c) { read_one(IC<(S + 1) & 3>{}, IC<BUF ^ 1>{}, J_c); });
+      }
+      if constexpr ((i * kDma) / NM != ((i + 1) * kDma) / NM) dma_one(S_c, IC<(i * kDma) / NM>{}, t + 4);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  const int nk = (K + C::KSTEP - 1) / C::KSTEP;
+  dma(IC<0>{}, 0);
+  dma(IC<1>{}, 1);
+  dma(IC<2>{}, 2);
+  dma(IC<3>{}, 3);
+  wait_vmcnt_lgkm0<3 * kDma>();  // stage 0 has landed
+  __builtin_amdgcn_s_barrier();
+  read_frags(IC<0>{}, IC<0>{});
+
+  int t = 0;
+  for (; t + 4 <= nk; t += 4) {
+    step(IC<0>{}, IC<0>{}, t);
+    step(IC<1>{}, IC<1>{}, t + 1);
+    step(IC<2>{}, IC<0>{}, t + 2);
+    step(IC<3>{}, IC<1>{}, t + 3);
+  }
+  if (t < nk) step(IC<0>{}, IC<0>{}, t);
+  if (t + 1 < nk) step(IC<1>{}, IC<1>{}, t + 1);
+  if (t + 2 < nk) step(IC<2>{}, IC<0>{}, t + 2);
+  // the zero fills past the end may still be in flight: drain them before
+  // the epilogue reuses the stage memory
+  wait_vmcnt_lgkm0<0>();
+  __syncthreads();
+
+  // A bf16 residual tile (256 x 256 = 128 KiB) moves into the free stages by
+  // LDS DMA now, so its latency overlaps whatever the epilogue computes
+  // before the add.  Wave w fetches tile rows [64w, 64w + 64): rows 0-31 of
+  // that quarter into sA<w>, rows 32-63 into sB<w>, 512 bytes per row, the
+  // 16-byte chunk q of row m at chunk q ^ (m & 15) (so the epilogue's
+  // 32-lane column reads spread over 16 chunk slots).
+  const bool res_lds = p.residual != nullptr && p.residual_bf16;
+  if (res_lds) {
+    const uint16_t* R = reinterpret_cast<const uint16_t*>(p.residual) + m0 * p.ldr + n0;
+    const int64_t rows_r = min<int64_t>(BM, p.M - m0);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(R, (uint32_t)(((rows_r - 1) * p.ldr + (p.N - n0)) * 2));
+    unsigned char* const da = wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sA2 : sA3;
+    unsigned char* const db = wave == 0 ? sB0 : wave == 1 ? sB1 : wave == 2 ? sB2 : sB3;
+    static_for<0, 32>([&](auto J_c) {
+      constexpr int j = decltype(J_c)::value;
+      const int m = wave * 64 + 2 * j + (lane >> 5);
+      const int q = (lane & 31) ^ (m & 15);
+      const bool ok = m < rows_r && n0 + q * 8 < p.N;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (LDS3 void*)((j < 16 ? da : db) + ((2 * j) & 31) * 512), 16,
+                                                ok ? (uint32_t)((m * p.ldr + q * 8) * 2) : kOOB, 0, 0, 0);
+    });
+  }
+
+  EpiCtx c{lane, wm, wn, m0, n0, sRed, sCol, res_lds,
+           {wm ? sA2 : sA0, wm ? sB2 : sB0, wm ? sA3 : sA1, wm ? sB3 : sB1}, ops};
+  run_epilogue<EPI, CH, FP8>(p, c, acc);
+}
+
+// ------------------------------------------------------------ host launch
+//
+// Each (FP8, B_NK) combination is instantiated by its own translation unit
+// (kf_gemm_mfma_<in>_<layout>.hip), so the kernels compile in parallel.
+
+// Epilogue shape of a compile-time chain.
+constexpr int chain_epi(int ch) {
+  for (int o = 0; o < kChainLen[ch]; ++o) {
+    if (kChainOps[ch][o] == KF_OP_GROUPNORM) return kEpiGroupNorm;
+    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kEpiRow;
+  }
+  return kEpiPlain;
+}
+
+template <bool FP8, bool B_NK, int CH>
+inline void launch_chain(const GemmArgs& p, dim3 grid, dim3 block, hipStream_t stream) {
+  hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, chain_epi(CH), CH>), grid, block, 0, stream, p);
+}
+
+template <bool FP8, bool B_NK>
+inline void launch_shape(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream) {
+  switch (chain) {
+    case 1: launch_chain<FP8, B_NK, 1>(p, grid, block, stream); return;
+    case 2: launch_chain<FP8, B_NK, 2>(p, grid, block, stream); return;
+    case 3: launch_chain<FP8, B_NK, 3>(p, grid, block, stream); return;
+    case 4: launch_chain<FP8, B_NK, 4>(p, grid, block, stream); return;
+    case 5: launch_chain<FP8, B_NK, 5>(p, grid, block, stream); return;
+    case 6: launch_chain<FP8, B_NK, 6>(p, grid, block, stream); return;
+    default: break;
+  }
+  switch (epi) {
+    case kEpiGroupNorm:
+      hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, kEpiGroupNorm, 0>), grid, block, 0, stream, p);
+      break;
+    case kEpiRow:
+      hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, kEpiRow, 0>), grid, block, 0, stream, p);
+      break;
+    default:
+      hipLaunchKernelGGL((kf_gemm_mfma_256x256<FP8, B_NK, kEpiPlain, 0>), grid, block, 0, stream, p);
+      break;
+  }
+}
+
+void launch_gemm_bf16_kn(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+void launch_gemm_bf16_nk(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+void launch_gemm_fp8_kn(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+void launch_gemm_fp8_nk(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+
+}  // namespace kf

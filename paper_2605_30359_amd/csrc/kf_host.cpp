@@ -65,6 +65,7 @@ struct kf_desc {
   int red_index;
   int gn_group;
   int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / 0
+  int chain = 0;  // compile-time epilogue chain matching the op list (0: interpreted)
   std::vector<Slot> inputs;
   Slot output;
   int device;
@@ -78,6 +79,19 @@ struct kf_desc {
 };
 
 namespace {
+
+// The compile-time chain whose op kinds equal the spec's (GEMM chains 1-6,
+// the conv chain 7), else 0.
+int match_chain(const kf_op_spec* s) {
+  const bool conv = s->contraction == KF_CONV2D_3X3;
+  for (int ch = 1; ch < kf::kNumChains; ++ch) {
+    if ((ch == 7) != conv || kf::kChainLen[ch] != s->n_ops) continue;
+    bool same = true;
+    for (int o = 0; o < s->n_ops; ++o) same = same && s->ops[o].kind == kf::kChainOps[ch][o];
+    if (same) return ch;
+  }
+  return 0;
+}
 
 kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   if (!s) return fail(KF_ERR_INVALID_ARG, "spec is NULL");
@@ -306,6 +320,7 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
     return st;
   }
   d->spec = *spec;
+  d->chain = match_chain(spec);
 
   int count = 0;
   if (hipGetDeviceCount(&count) != hipSuccess || count < 1) {
@@ -442,7 +457,7 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
           !fits_31(256 * a.ldo * 4) || (a.residual && !fits_31(256 * a.ldr * 4)))
         return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
       if (d->variant == kVarGemmFp8) a.scale = s.scale_a * s.scale_b;  // fl(s_a * s_b), applied to the fp32 accumulator
-      e = kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, d->epi_shape, hs, nk);
+      e = kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, d->epi_shape, d->chain, hs, nk);
       if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
       if (e == hipSuccess && d->row_kind)
         e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, d->workspace, d->tiles_n, s.M, s.N, a.out,
@@ -476,7 +491,7 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
   c.out_bf16 = 1;
   hipError_t e = kf::launch_conv_pack(c, d->workspace, hs);
   if (e == hipSuccess && ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
-  if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, hs);
+  if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, d->chain, hs);
   if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
   if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
@@ -538,7 +553,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     a.red_index = 0;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
     e = d->variant == kVarGemmF32 ? kf::launch_gemm_f32(a, nk, hs)
-                                  : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, hs, nk);
+                                  : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk);
   } else {
     kf::ConvArgs c;
     memset(&c, 0, sizeof(c));
@@ -554,7 +569,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     c.out = cur;
     c.out_bf16 = 1;
     e = kf::launch_conv_pack(c, d->workspace, hs);
-    if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, hs);
+    if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, 0, hs);
   }
   if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
 

@@ -24,6 +24,24 @@ struct EpiProgram {
 // logsumexp.
 enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
 
+// Op chains with an epilogue generated for exactly that op sequence (the op
+// parameters stay run-time values).  Chain 0 is the general one: the op list
+// is interpreted at run time.  The paper turns each operator into its own
+// specialised kernel; these are the chains of the benchmarked operators and
+// the plain building blocks, and every other chain runs interpreted.
+constexpr int kNumChains = 8;
+constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3};
+constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
+    {},                                                                         // 0: interpreted
+    {},                                                                         // 1: contraction only
+    {KF_OP_BIAS},                                                               // 2
+    {KF_OP_BIAS, KF_OP_RELU},                                                   // 3
+    {KF_OP_BIAS, KF_OP_GELU_TANH, KF_OP_SCALE, KF_OP_ROW_LOGSUMEXP},           // 4: GEMM, GELU, logsumexp
+    {KF_OP_GROUPNORM, KF_OP_SWISH, KF_OP_RESIDUAL_ADD},                        // 5: GEMM, GroupNorm, swish
+    {KF_OP_BIAS, KF_OP_HARDTANH, KF_OP_ROW_SOFTMAX},                           // 6: GEMM, hardtanh, softmax
+    {KF_OP_BIAS, KF_OP_RELU, KF_OP_MAXPOOL2X2},                                // 7: conv, ReLU, max-pool
+};
+
 // Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).
 struct GemmArgs {
   const void* a;          // [M, lda] row-major

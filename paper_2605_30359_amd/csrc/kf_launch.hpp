@@ -9,8 +9,8 @@
 namespace kf {
 
 // bf16 or OCP fp8 e4m3 GEMM + epilogue on the matrix cores; `epi` is an
-// EpiShape.
-hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, hipStream_t stream, bool b_nk);
+// EpiShape, `chain` a compile-time chain id (0: the op list is interpreted).
+hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, hipStream_t stream, bool b_nk);
 int gemm_mfma_tile_m();
 int gemm_mfma_tile_n();
 
@@ -32,7 +32,7 @@ namespace kf {
 // convolution from it.  Supports cin == conv_bf16_cin(), width ==
 // conv_bf16_width(), cout == conv_bf16_cout(), even height.
 hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStream_t stream);
-hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, hipStream_t stream);
+hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, int chain, hipStream_t stream);
 int conv_bf16_cin();
 int conv_bf16_width();
 int conv_bf16_cout();

@@ -387,3 +387,29 @@ def test_epilogue_operand_paths(name, kw, res_f32):
     _, out = run_gpu(cfg, t)
     err = check(cfg, t, out)
     print(f"{name} {kw['ops']} err {err:.3e}")
+
+
+# ------------------------------------- specialised vs interpreted epilogues
+
+@pytest.mark.parametrize("name,kw", [
+    ("C2", dict(M=300, N=520, K=136)),                                     # bias, GELU(tanh), scale, logsumexp
+    ("C3", dict(M=300, N=512, K=136, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
+    ("C5", dict(M=300, N=528, K=160)),                                     # fp8, bias, hardtanh, softmax
+    ("C4", dict(batch=2, H=10)),                                           # conv, bias, ReLU, pool (pool first)
+])
+def test_specialised_chain_matches_interpreted(name, kw):
+    """The benchmarked op lists run an epilogue generated for that exact
+    chain; prefixing a scale by 1.0 (exact) makes the same list run through
+    the interpreted epilogue.  Both must agree bit for bit, and the conv one
+    shows that pooling before the monotone bias and ReLU changes nothing."""
+    torch = _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=31)
+    _, out_spec = run_gpu(cfg, t)
+    cfg2 = dict(cfg, ops=[("scale", 1.0)] + list(cfg["ops"]))
+    _, out_gen = run_gpu(cfg2, t)
+    a, b = out_spec, out_gen
+    if a.dtype == torch.bfloat16:
+        a, b = a.view(torch.int16), b.view(torch.int16)
+    assert torch.equal(a, b), f"{name}: specialised and interpreted epilogues differ"
+    check(cfg, t, out_spec)
