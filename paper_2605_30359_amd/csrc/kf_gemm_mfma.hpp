@@ -37,6 +37,8 @@
 
 namespace kf {
 
+#define LDS3 __attribute__((address_space(3)))
+
 namespace {
 
 constexpr int BM = 256;
@@ -271,15 +273,47 @@ __device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, in
   }
 }
 
+// The bf16 residual tile (256 x 256 = 128 KiB) moves into the free stage
+// memory by LDS DMA during the epilogue: wave w fetches tile rows [64w,
+// 64w + 64), rows 0-31 of that quarter into sA<w>, rows 32-63 into sB<w>,
+// 512 bytes per row, the 16-byte chunk q of row m at chunk q ^ (m & 15) (so
+// the epilogue's 32-lane column reads spread over 16 chunk slots).  The 32
+// DMA instructions per wave are issued in groups between epilogue
+// computations that do not need the residual, because every workgroup
+// reaches this point at about the same time and the burst is bound by HBM
+// bandwidth: a wave that issued them back to back would stall on the full
+// address queue instead of computing.
+struct ResDma {
+  __amdgpu_buffer_rsrc_t rr;
+  unsigned char* da;
+  unsigned char* db;
+  int wave, lane, rows_r;
+  int64_t n0, N, ldr;
+  bool active;
+  template <int J0, int J1>
+  __device__ __forceinline__ void issue() const {
+    if (!active) return;
+    static_for<J0, J1>([&](auto J_c) {
+      constexpr int j = decltype(J_c)::value;
+      const int m = wave * 64 + 2 * j + (lane >> 5);
+      const int q = (lane & 31) ^ (m & 15);
+      const bool ok = m < rows_r && n0 + q * 8 < N;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (LDS3 void*)((j < 16 ? da : db) + ((2 * j) & 31) * 512), 16,
+                                                ok ? (uint32_t)((m * ldr + q * 8) * 2) : kOOB, 0, 0, 0);
+    });
+  }
+};
+
 // Epilogue of shape EPI (see EpiShape): ops [0, r) element-wise, op r the
 // reduction (if any), ops (r, n) element-wise, then the store.
 template <int EPI, int CH, bool FP8>
-__device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c, Acc& acc) {
+__device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c, Acc& acc, const ResDma& rd) {
   const int64_t N = p.N;
   const int nops = p.prog.n;
   const int r = EPI == kEpiPlain ? nops : p.red_index;
 
   if (EPI == kEpiPlain) {
+    rd.issue<0, 32>();
     res_wait(c);
     static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
@@ -302,7 +336,10 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     for (int o = 0; o < nops; ++o)
       if (op_kind(c.ops, o) == KF_OP_RESIDUAL_ADD) res_at = o;
     const bool res_early = res_at < r;  // the residual is added before the statistics
-    if (res_early) res_wait(c);
+    if (res_early) {
+      rd.issue<0, 32>();
+      res_wait(c);
+    }
     const int gw = p.gn_group;
     const int bpg = gw >> 5;  // 32-column blocks per group (1, 2, 4, 8)
     const int bw = min(bpg, 4);
@@ -310,6 +347,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     float s[4][4];
     static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
+      if (!res_early) rd.issue<4 * bi, 4 * bi + 4>();
       Row v;
       get_row(acc, bi, v);
 #pragma unroll
@@ -360,6 +398,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     float mean[4][4], ss[4][4];
     static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
+      if (!res_early) rd.issue<16 + 4 * bi, 20 + 4 * bi>();
 #pragma unroll
       for (int bj = 0; bj < 4; ++bj) {
         mean[bi][bj] = s[bi][bj] * inv_n;
@@ -395,6 +434,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 
   // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
   // this 256-column tile goes to the partials buffer.
+  rd.issue<0, 32>();
   res_wait(c);
   float mx[4];
   static_for<0, 4>([&](auto bi_c) {
@@ -500,7 +540,6 @@ constexpr int kAStage = BM * 64;           // 16 KiB
 constexpr int kBStageKN = 18 * 1024;       // 18 KiB = 18 DMA blocks of 1 KiB
 constexpr int kBStageNK = BN * 64;         // 16 KiB
 
-#define LDS3 __attribute__((address_space(3)))
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(2))) int i32x2;
 
@@ -785,32 +824,23 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   wait_vmcnt_lgkm0<0>();
   __syncthreads();
 
-  // A bf16 residual tile (256 x 256 = 128 KiB) moves into the free stages by
-  // LDS DMA now, so its latency overlaps whatever the epilogue computes
-  // before the add.  Wave w fetches tile rows [64w, 64w + 64): rows 0-31 of
-  // that quarter into sA<w>, rows 32-63 into sB<w>, 512 bytes per row, the
-  // 16-byte chunk q of row m at chunk q ^ (m & 15) (so the epilogue's
-  // 32-lane column reads spread over 16 chunk slots).
   const bool res_lds = p.residual != nullptr && p.residual_bf16;
-  if (res_lds) {
-    const uint16_t* R = reinterpret_cast<const uint16_t*>(p.residual) + m0 * p.ldr + n0;
-    const int64_t rows_r = min<int64_t>(BM, p.M - m0);
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(R, (uint32_t)(((rows_r - 1) * p.ldr + (p.N - n0)) * 2));
-    unsigned char* const da = wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sA2 : sA3;
-    unsigned char* const db = wave == 0 ? sB0 : wave == 1 ? sB1 : wave == 2 ? sB2 : sB3;
-    static_for<0, 32>([&](auto J_c) {
-      constexpr int j = decltype(J_c)::value;
-      const int m = wave * 64 + 2 * j + (lane >> 5);
-      const int q = (lane & 31) ^ (m & 15);
-      const bool ok = m < rows_r && n0 + q * 8 < p.N;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (LDS3 void*)((j < 16 ? da : db) + ((2 * j) & 31) * 512), 16,
-                                                ok ? (uint32_t)((m * p.ldr + q * 8) * 2) : kOOB, 0, 0, 0);
-    });
-  }
+  ResDma rd;
+  rd.active = res_lds;
+  rd.wave = wave;
+  rd.lane = lane;
+  rd.rows_r = (int)min<int64_t>(BM, p.M - m0);
+  rd.n0 = n0;
+  rd.N = p.N;
+  rd.ldr = p.ldr;
+  rd.da = wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sA2 : sA3;
+  rd.db = wave == 0 ? sB0 : wave == 1 ? sB1 : wave == 2 ? sB2 : sB3;
+  rd.rr = make_rsrc(reinterpret_cast<const uint16_t*>(res_lds ? p.residual : p.a) + (res_lds ? m0 * p.ldr + n0 : 0),
+                    res_lds ? (uint32_t)(((rd.rows_r - 1) * p.ldr + (p.N - n0)) * 2) : 0u);
 
   EpiCtx c{lane, wm, wn, m0, n0, sRed, sCol, res_lds,
            {wm ? sA2 : sA0, wm ? sB2 : sB0, wm ? sA3 : sA1, wm ? sB3 : sB1}, ops};
-  run_epilogue<EPI, CH, FP8>(p, c, acc);
+  run_epilogue<EPI, CH, FP8>(p, c, acc, rd);
 }
 
 // ------------------------------------------------------------ host launch
