@@ -42,15 +42,21 @@ HBM_PEAK_GBS = 8000.0
 def _hip():
     lib = ctypes.CDLL("libamdhip64.so")
     lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
     lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
     lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
     lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
     return lib
 
 
+# Timing-only events: no system-scope fence (no cache writeback and
+# invalidation around the kernel they bracket).
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
 def _event(hip):
     e = ctypes.c_void_p()
-    assert hip.hipEventCreate(ctypes.byref(e)) == 0
+    assert hip.hipEventCreateWithFlags(ctypes.byref(e), HIP_EVENT_DISABLE_SYSTEM_FENCE) == 0
     return e.value
 
 

@@ -122,15 +122,18 @@ constexpr bool chain_pools_first(int ch) {
 
 }  // namespace
 
-// wp[tap][co][ci] = w[co][ci][kh][kw]
+// wp[tap][co][ci] = w[co][ci][kh][kw]: one thread per (co, ci) reads its 9
+// contiguous taps and writes them to the 9 tap planes, so that a wave's reads
+// and each of its writes cover contiguous memory.
 __global__ __launch_bounds__(256) void kf_conv_pack_weights(const uint16_t* __restrict__ w, uint16_t* __restrict__ wp,
                                                             int cout, int cin) {
-  const int64_t total = (int64_t)cout * cin * 9;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int ci = (int)(e % cin);
-    const int co = (int)((e / cin) % cout);
-    const int tap = (int)(e / ((int64_t)cin * cout));
-    wp[e] = w[((int64_t)co * cin + ci) * 9 + tap];
+  const int64_t pairs = (int64_t)cout * cin;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < pairs; e += (int64_t)gridDim.x * 256) {
+    uint16_t t[9];
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) t[tap] = w[e * 9 + tap];
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) wp[tap * pairs + e] = t[tap];
   }
 }
 
@@ -435,7 +438,9 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
 }
 
 hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStream_t stream) {
-  hipLaunchKernelGGL(kf_conv_pack_weights, dim3(288), dim3(256), 0, stream,
+  const int64_t pairs = args.cout * args.cin;
+  const unsigned blocks = (unsigned)((pairs + 255) / 256 < 1024 ? (pairs + 255) / 256 : 1024);
+  hipLaunchKernelGGL(kf_conv_pack_weights, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, stream,
                      reinterpret_cast<const uint16_t*>(args.w), reinterpret_cast<uint16_t*>(packed_weights),
                      (int)args.cout, (int)args.cin);
   return hipGetLastError();
