@@ -22,11 +22,11 @@
 //              with a shifted pixel index.
 //   weights    repacked per call by kf_conv_pack_weights to [tap][co][ci],
 //              then streamed per K-step (one tap, 32 channels = 8 KiB) into
-//              six LDS stages by LDS DMA, six steps ahead.
+//              three LDS stages by LDS DMA, three steps ahead.
 //   schedule   persistent: one workgroup per compute unit walks the tiles
-//              with a stride of the grid size.  The next tile's halo is
-//              loaded into registers during the last K-steps and the
-//              epilogue of the current one, and the weight stream runs on
+//              with a stride of the grid size.  The next tile's halo rows
+//              arrive by LDS DMA spread over the current tile's K-steps and
+//              are transposed at the boundary, and the weight stream runs on
 //              across tiles, so neither waits at a tile boundary.
 //   order      A fragment = MFMA "A" operand: each lane's accumulators are
 //              runs of 4 consecutive output pixels of one channel.
@@ -48,9 +48,10 @@ constexpr int HALO_ROWS = 4;         // ih = oh0 - 1 .. oh0 + 2
 constexpr int PIX_BYTES = CIN * 2;   // 128 bytes of channels per pixel
 constexpr int kHalo = HALO_ROWS * HALO_COLS * PIX_BYTES;  // 66560 bytes
 constexpr int kWStage = COUT * 64;   // [128 co][32 ci] bf16 = 8 KiB
-constexpr int kWS = 6;               // weight stages = prefetch distance in K-steps
+constexpr int kWS = 3;               // weight stages = prefetch distance in K-steps
+constexpr int kRaw = CIN * 4 * WID * 2;  // the next tile's halo as loaded: [ci][4 rows][128 px] = 64 KiB
 constexpr int kSteps = 9 * (CIN / 32);  // 18 K-steps of 32 per tile
-static_assert(kSteps % kWS == 0 && kSteps >= 2 * kWS, "the tile loop unrolls kWS steps at a time");
+static_assert(kSteps % 6 == 0 && kSteps >= 16, "the tile loop unrolls 6 steps; 16 carry halo DMA");
 
 #define LDS3 __attribute__((address_space(3)))
 
@@ -140,11 +141,12 @@ __global__ __launch_bounds__(256) void kf_conv_pack_weights(const uint16_t* __re
 template <int CH>
 __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, const uint16_t* __restrict__ wp) {
   __shared__ __attribute__((aligned(1024))) unsigned char sHalo[kHalo];
-  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage], sW3[kWStage],
-      sW4[kWStage], sW5[kWStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sRaw[kRaw];
+  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sDummy[1024];
   auto stW = [&](auto S_c) -> unsigned char* {
     constexpr int S = decltype(S_c)::value;
-    return S == 0 ? sW0 : S == 1 ? sW1 : S == 2 ? sW2 : S == 3 ? sW3 : S == 4 ? sW4 : sW5;
+    return S == 0 ? sW0 : S == 1 ? sW1 : sW2;
   };
 
   const int tid = threadIdx.x;
@@ -157,41 +159,44 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   const int64_t img_elems = (int64_t)CIN * H * WID;
 
   // ---- halo of a tile: x[n][ci][oh0-1+hr][iw] -> sHalo[(hr*130 + iw+1)][ci].
-  // Thread t owns blocks t and t + 256 (8 channels x 8 pixels of one row):
-  // 16 x 16-byte loads into registers, then an 8 x 8 bf16 transpose by
-  // v_perm_b32 on the way into LDS.
-  u32x4 hv[2][8];
-  // (a tile past the end issues the same 16 loads, all out of range, so the
-  // number of loads in flight is the same in every pass)
-  auto halo_load = [&](int tile, bool live) {
-    const int n_img = live ? tile / rows_per_img : 0;
-    const int oh0 = 2 * (tile % rows_per_img);
+  // The next tile's four input rows of every channel arrive by LDS DMA,
+  // spread over the K-steps of the current tile, into sRaw as [ci][hr][128
+  // px] (row (ci, hr) = 256 bytes, its 16-byte chunk q stored at q ^
+  // rsw(ci)); at the tile boundary each thread transposes 2 blocks of 8
+  // channels x 8 pixels from sRaw into sHalo with v_perm_b32.  Wave w's DMA i
+  // (i < 16) fetches channel 16 w + i, lane l its row l >> 4, chunk
+  // position l & 15; past i = 15 the instruction is a zero fill of a dummy
+  // block, so every K-step issues the same number of DMA instructions.
+  auto rsw = [](int c) { return ((c >> 3) << 1) & 15; };
+  auto raw_dma = [&](int i, int tile, bool live) {
+    const bool on = live && i < 16;
+    const int c = wave * 16 + (i < 16 ? i : 0);
+    const int n_img = on ? tile / rows_per_img : 0;
+    const int ih = 2 * (tile % rows_per_img) - 1 + (lane >> 4);
     const __amdgpu_buffer_rsrc_t rx =
         make_rsrc(reinterpret_cast<const uint16_t*>(p.x) + n_img * img_elems, (uint32_t)(img_elems * 2));
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int b = tid + half * 256;
-      const int cg = b & 7, pg = (b >> 3) & 15, hr = b >> 7;
-      const int ih = oh0 - 1 + hr;
-      const bool row_ok = live && ih >= 0 && ih < H;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t off = row_ok ? (uint32_t)((((cg * 8 + j) * H + ih) * WID + pg * 8) * 2) : kOOB;
-        hv[half][j] = buf_load16(rx, off);
-      }
-    }
+    const int q = (lane & 15) ^ rsw(c);
+    const bool ok = on && ih >= 0 && ih < H;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS3 void*)(on ? sRaw + c * 1024 : sDummy), 16,
+                                              ok ? (uint32_t)(((c * H + ih) * WID + q * 8) * 2) : kOOB, 0, 0, 0);
   };
   auto halo_write = [&]() {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       const int b = tid + half * 256;
       const int cg = b & 7, pg = (b >> 3) & 15, hr = b >> 7;
+      u32x4 hv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = cg * 8 + j;
+        hv[j] = *reinterpret_cast<const u32x4*>(sRaw + c * 1024 + hr * 256 + ((pg ^ rsw(c)) << 4));
+      }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const uint32_t sel = (k & 1) ? 0x07060302u : 0x05040100u;
         u32x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(hv[half][2 * e + 1][k >> 1], hv[half][2 * e][k >> 1], sel);
+        for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(hv[2 * e + 1][k >> 1], hv[2 * e][k >> 1], sel);
         const int pix = hr * HALO_COLS + pg * 8 + k + 1;
         *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = o;
       }
@@ -262,21 +267,16 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   }
 
   CAcc acc;
-  constexpr int kDma = 2;
-  constexpr int kHaloStep = kSteps - kWS;  // step that loads the next tile's halo
-  // K-step s of a tile on weight stage S = s % 6: every wave has read its
+  constexpr int kDma = 3;  // DMA instructions per K-step: 2 weight blocks, 1 halo (or dummy)
+  // K-step s of a tile on weight stage S = s % 3: every wave has read its
   // fragments of stage S (during step s-1) once it passes the barrier, so the
-  // DMA of step s+6 goes into stage S; the barrier also publishes stage S+1
-  // (DMA issued during step s-5), read during this step.  WAIT is the number
-  // of younger loads allowed in flight: the DMA of the 4 steps in between,
-  // plus the 16 halo loads of the next tile, which follow the MFMAs of step
-  // 12 and are older than the DMA awaited in steps 13-17.
-  auto step = [&](auto S_c, auto BUF_c, auto WAIT_c, auto HALO_c, int s, bool next_live, int next_tile) {
+  // DMA of step s+3 goes into stage S; the barrier also publishes stage S+1
+  // (DMA issued during step s-2), read during this step.  The wait allows the
+  // 3 DMA instructions of step s-1 in flight.
+  auto step = [&](auto S_c, auto BUF_c, int s, bool next_live, int next_tile) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
-    constexpr int WAIT = decltype(WAIT_c)::value;
-    constexpr bool HALO = decltype(HALO_c)::value;
-    wait_vmcnt_lgkm0<WAIT>();
+    wait_vmcnt_lgkm0<kDma>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     const bool live = s + kWS < kSteps || next_live;
@@ -288,9 +288,9 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
                                                             0, 0);
       if constexpr (i < kReads) read_one(IC<(S + 1) % kWS>{}, IC<BUF ^ 1>{}, I_c, s + 1);
       if constexpr (i == 3 || i == 11) dma_one(S_c, IC<(i == 3 ? 0 : 1)>{}, s + kWS, live);
+      if constexpr (i == 7) raw_dma(s, next_tile, next_live);
       __builtin_amdgcn_sched_barrier(0);
     });
-    if (HALO) halo_load(next_tile, next_live);
   };
 
   const int nops = p.prog.n;
@@ -300,10 +300,12 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   uint16_t* out = reinterpret_cast<uint16_t*>(p.out);
 
   int tile = blockIdx.x;
-  // prologue: the first tile's halo, then the weight stages of steps 0-5
-  halo_load(tile, true);
+  // prologue: the first tile's halo, then the weight stages of steps 0-2
+  // (each followed by a dummy, as in a K-step)
+  for (int i = 0; i < 16; ++i) raw_dma(i, tile, true);
   static_for<0, kWS>([&](auto S_c) {
     dma_one(S_c, IC<0>{}, decltype(S_c)::value, true);
+    raw_dma(16, tile, false);
     dma_one(S_c, IC<1>{}, decltype(S_c)::value, true);
   });
 
@@ -314,9 +316,9 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
     const int next_tile = tile + (int)gridDim.x;
     const bool next_live = next_tile < p.tiles;
 
-    // this tile's halo registers and weight stage 0 have landed (the stages
-    // of steps 1-5 may still be in flight); every wave is past its last read
-    // of the previous halo
+    // this tile's raw halo and weight stage 0 have landed (the DMA of the
+    // last two K-steps, stages 1 and 2, may still be in flight); every wave
+    // is past its last read of the previous halo
     wait_vmcnt_lgkm0<(kWS - 1) * kDma>();
     __syncthreads();
     halo_write();
@@ -330,23 +332,16 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
 
-    // 18 steps = 2 x 6 + 6 (stage s % 6, fragment buffer s % 2)
-    constexpr int W = (kWS - 2) * kDma, WH = W + 16;
+    // 18 steps = 3 x 6 (stage s % 3, fragment buffer s % 2)
 #pragma unroll 1
-    for (int s = 0; s < kHaloStep; s += kWS) {
-      step(IC<0>{}, IC<0>{}, IC<W>{}, IC<0>{}, s, next_live, next_tile);
-      step(IC<1>{}, IC<1>{}, IC<W>{}, IC<0>{}, s + 1, next_live, next_tile);
-      step(IC<2>{}, IC<0>{}, IC<W>{}, IC<0>{}, s + 2, next_live, next_tile);
-      step(IC<3>{}, IC<1>{}, IC<W>{}, IC<0>{}, s + 3, next_live, next_tile);
-      step(IC<4>{}, IC<0>{}, IC<W>{}, IC<0>{}, s + 4, next_live, next_tile);
-      step(IC<5>{}, IC<1>{}, IC<W>{}, IC<0>{}, s + 5, next_live, next_tile);
+    for (int s = 0; s < kSteps; s += 6) {
+      step(IC<0>{}, IC<0>{}, s, next_live, next_tile);
+      step(IC<1>{}, IC<1>{}, s + 1, next_live, next_tile);
+      step(IC<2>{}, IC<0>{}, s + 2, next_live, next_tile);
+      step(IC<0>{}, IC<1>{}, s + 3, next_live, next_tile);
+      step(IC<1>{}, IC<0>{}, s + 4, next_live, next_tile);
+      step(IC<2>{}, IC<1>{}, s + 5, next_live, next_tile);
     }
-    step(IC<0>{}, IC<0>{}, IC<W>{}, IC<1>{}, 12, next_live, next_tile);
-    step(IC<1>{}, IC<1>{}, IC<WH>{}, IC<0>{}, 13, next_live, next_tile);
-    step(IC<2>{}, IC<0>{}, IC<WH>{}, IC<0>{}, 14, next_live, next_tile);
-    step(IC<3>{}, IC<1>{}, IC<WH>{}, IC<0>{}, 15, next_live, next_tile);
-    step(IC<4>{}, IC<0>{}, IC<WH>{}, IC<0>{}, 16, next_live, next_tile);
-    step(IC<5>{}, IC<1>{}, IC<WH>{}, IC<0>{}, 17, next_live, next_tile);
 
     // ---- epilogue, per output channel block bj and column half bc (the
     // two output rows of the tile): ops before the pool on the pre-pool

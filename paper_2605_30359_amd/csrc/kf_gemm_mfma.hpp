@@ -345,18 +345,30 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     const int bw = min(bpg, 4);
     const float inv_n = 1.0f / (float)gw;
     float s[4][4];
+    // A bf16 chain that starts with the GroupNorm sums the accumulators as
+    // they are (the dequantisation factor is 1), in the same order as below.
+    constexpr bool kSumAcc = !FP8 && CH != 0 && kChainOps[CH][0] == KF_OP_GROUPNORM;
     static_for<0, 4>([&](auto bi_c) {
       constexpr int bi = decltype(bi_c)::value;
       if (!res_early) rd.issue<4 * bi, 4 * bi + 4>();
-      Row v;
-      get_row(acc, bi, v);
+      if constexpr (kSumAcc) {
 #pragma unroll
-      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
-      apply_phase<CH>(p, c, bi, 0, r, v);
+        for (int bj = 0; bj < 4; ++bj) {
+          const f32x16& a = acc[bi][bj];
+          auto s4 = [&](int o) { return (a[o] + a[o + 1]) + (a[o + 2] + a[o + 3]); };
+          s[bi][bj] = (s4(0) + s4(4)) + (s4(8) + s4(12));
+        }
+      } else {
+        Row v;
+        get_row(acc, bi, v);
 #pragma unroll
-      for (int bj = 0; bj < 4; ++bj)
-        s[bi][bj] = (sum4(v[bj * 4]) + sum4(v[bj * 4 + 1])) + (sum4(v[bj * 4 + 2]) + sum4(v[bj * 4 + 3]));
-      put_row(acc, bi, v);
+        for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+        apply_phase<CH>(p, c, bi, 0, r, v);
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj)
+          s[bi][bj] = (sum4(v[bj * 4]) + sum4(v[bj * 4 + 1])) + (sum4(v[bj * 4 + 2]) + sum4(v[bj * 4 + 3]));
+        put_row(acc, bi, v);
+      }
     });
     auto group_reduce = [&](float (&t)[4][4]) {
 #pragma unroll
@@ -779,6 +791,13 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   // DMA lanes are all out of range (zeros into a stage nobody reads) and the
   // reads read a stale stage that is never used, so nothing here is
   // conditional.
+  const int nk = (K + C::KSTEP - 1) / C::KSTEP;
+  const bool res_bf16 = p.residual != nullptr && p.residual_bf16;  // the residual tile goes through LDS
+  const int rows_r = (int)min<int64_t>(BM, p.M - m0);
+  const __amdgpu_buffer_rsrc_t rres =
+      make_rsrc(reinterpret_cast<const uint16_t*>(res_bf16 ? p.residual : p.a) + (res_bf16 ? m0 * p.ldr + n0 : 0),
+                res_bf16 ? (uint32_t)(((rows_r - 1) * p.ldr + (p.N - n0)) * 2) : 0u);
+
   constexpr int NM = C::NMFMA;
   auto step = [&](auto S_c, auto BUF_c, int t) {
     constexpr int S = decltype(S_c)::value;
@@ -800,7 +819,6 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
     });
   };
 
-  const int nk = (K + C::KSTEP - 1) / C::KSTEP;
   dma(IC<0>{}, 0);
   dma(IC<1>{}, 1);
   dma(IC<2>{}, 2);
@@ -824,19 +842,18 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   wait_vmcnt_lgkm0<0>();
   __syncthreads();
 
-  const bool res_lds = p.residual != nullptr && p.residual_bf16;
+  const bool res_lds = res_bf16;
   ResDma rd;
   rd.active = res_lds;
   rd.wave = wave;
   rd.lane = lane;
-  rd.rows_r = (int)min<int64_t>(BM, p.M - m0);
+  rd.rows_r = rows_r;
   rd.n0 = n0;
   rd.N = p.N;
   rd.ldr = p.ldr;
   rd.da = wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sA2 : sA3;
   rd.db = wave == 0 ? sB0 : wave == 1 ? sB1 : wave == 2 ? sB2 : sB3;
-  rd.rr = make_rsrc(reinterpret_cast<const uint16_t*>(res_lds ? p.residual : p.a) + (res_lds ? m0 * p.ldr + n0 : 0),
-                    res_lds ? (uint32_t)(((rd.rows_r - 1) * p.ldr + (p.N - n0)) * 2) : 0u);
+  rd.rr = rres;
 
   EpiCtx c{lane, wm, wn, m0, n0, sRed, sCol, res_lds,
            {wm ? sA2 : sA0, wm ? sB2 : sB0, wm ? sA3 : sA1, wm ? sB3 : sB1}, ops};
