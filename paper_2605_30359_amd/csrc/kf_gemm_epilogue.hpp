@@ -1,0 +1,513 @@
+// Shared pieces of the bf16 / fp8 GEMM kernels: the element types, LDS
+// helpers and the fused epilogue that runs on the accumulator registers.
+//
+// A wave owns RB x 4 blocks of 32 x 32 outputs (RB row blocks of 32 rows,
+// four column blocks of 32 columns; two waves side by side cover a
+// 256-column tile row).  After the K loop the op list is applied to these
+// accumulators and the result stored once.
+#pragma once
+
+#include <type_traits>
+
+#include "kf_device.hpp"
+#include "kf_launch.hpp"
+
+namespace kf {
+
+#define LDS3 __attribute__((address_space(3)))
+
+namespace {
+
+constexpr int BN = 256;  // columns of a tile (and of a row-reduction partial)
+constexpr int NT = 256;  // threads of a workgroup
+
+template <typename T>
+__device__ __forceinline__ T lds_load(const unsigned char* p) {
+  return *reinterpret_cast<const T*>(p);
+}
+
+// s_waitcnt vmcnt(N) lgkmcnt(0), expcnt left alone
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0x0 << 8) | ((N >> 4) << 14));
+}
+
+// The accumulators of one wave, RB row blocks x 4 column blocks:
+// acc[bi][bj][i]: output row    row_base + bi*32 + (lane & 31)
+//                 output column wn*128 + bj*32 + (i/4)*8 + (lane >> 5)*4 + i%4
+template <int RB>
+using AccT = f32x16[RB][4];
+
+// -------------------------------------------------------------- epilogue
+//
+// The op list is run in up to two phases around its reduction op (GROUPNORM,
+// ROW_SOFTMAX or ROW_LOGSUMEXP).  Each phase takes one 32-row block bi at a
+// time -- its 64 values per lane in VGPRs, the rest of the tile in AGPRs --
+// through all of the phase's element-wise ops, and the last phase stores.
+
+struct EpiCtx {
+  int lane, wm, wn;
+  int row_base;                  // first tile row of this wave's row blocks
+  int rows;                      // rows of the tile inside the output (min(tile rows, M - m0))
+  int64_t m0, n0;
+  float* red;                    // 2 x 256 floats of LDS for cross-wave row reductions
+  const float* col;              // LDS: bias, gamma, beta of the tile's 256 columns
+  bool res_lds;                  // the bf16 residual tile sits in LDS (see the kernel's residual staging)
+  const unsigned char* res[4];   // LDS: this lane's residual row (lane & 31) of row block bi
+  OpTable ops;                   // the op program, one op per lane
+};
+
+// run g (0..15) of a row = block bj = g / 4, group gi = g % 4
+__device__ __forceinline__ int col_local(const EpiCtx& c, int g) {
+  return c.wn * 128 + (g >> 2) * 32 + (g & 3) * 8 + (c.lane >> 5) * 4;
+}
+__device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.row_base + bi * 32 + (c.lane & 31); }
+
+typedef f32x4 Row[16];  // one lane's 64 values of one row
+
+template <int RB>
+__device__ __forceinline__ void get_row(const AccT<RB>& acc, int bi, Row& v) {
+#pragma unroll
+  for (int g = 0; g < 16; ++g) {
+    const f32x16& a = acc[bi][g >> 2];
+    const int o = (g & 3) * 4;
+    v[g] = f32x4{a[o], a[o + 1], a[o + 2], a[o + 3]};
+  }
+}
+template <int RB>
+__device__ __forceinline__ void put_row(AccT<RB>& acc, int bi, const Row& v) {
+#pragma unroll
+  for (int g = 0; g < 16; ++g) {
+    const int o = (g & 3) * 4;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[bi][g >> 2][o + q] = v[g][q];
+  }
+}
+
+// 4 consecutive fp32 of a per-column vector (0 bias, 1 gamma, 2 beta), staged
+// in LDS at kernel start; columns >= N read as 0.
+__device__ __forceinline__ f32x4 col4(const EpiCtx& c, int which, int g) {
+  return *reinterpret_cast<const f32x4*>(c.col + which * 256 + col_local(c, g));
+}
+
+// The bf16 residual tile in LDS: 512 bytes per tile row, the 16-byte chunk q
+// of row m stored at chunk q ^ (m & 15); where each row sits is up to the
+// kernel (c.res).
+__device__ __forceinline__ f32x4 res4(const EpiCtx& c, int bi, int g) {
+  const int r = c.lane & 31;
+  const int q = c.wn * 16 + (g >> 2) * 4 + (g & 3);
+  const u32x2 w = *reinterpret_cast<const u32x2*>(c.res[bi] + ((q ^ (r & 15)) << 4) + (c.lane >> 5) * 8);
+  return f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+}
+
+// Wait until every wave's share of the residual tile has landed in LDS.
+__device__ __forceinline__ void res_wait(const EpiCtx& c) {
+  if (c.res_lds) {
+    wait_vmcnt_lgkm0<0>();
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ float sum4(f32x4 a) { return (a[0] + a[1]) + (a[2] + a[3]); }
+__device__ __forceinline__ float max4(f32x4 a) { return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])); }
+
+// Combine one value per row over the two lanes of the row (lane ^ 32) and, if
+// `cross`, over the two waves that share the rows (through LDS).  Every
+// thread of the workgroup must call it with the same `cross`.
+template <bool IS_MAX, int RB>
+__device__ __forceinline__ void row_combine(const EpiCtx& c, float (&v)[RB], bool cross) {
+#pragma unroll
+  for (int bi = 0; bi < RB; ++bi) {
+    const float y = shfl_xor(v[bi], 32);
+    v[bi] = IS_MAX ? fmaxf(v[bi], y) : v[bi] + y;
+  }
+  if (!cross) return;
+  if (c.lane < 32) {
+#pragma unroll
+    for (int bi = 0; bi < RB; ++bi) c.red[c.wn * 256 + row_local(c, bi)] = v[bi];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int bi = 0; bi < RB; ++bi) {
+    const float o = c.red[(c.wn ^ 1) * 256 + row_local(c, bi)];
+    v[bi] = IS_MAX ? fmaxf(v[bi], o) : v[bi] + o;
+  }
+  __syncthreads();
+}
+
+// One element-wise / tensor-reading op (kind, at position o of the list) on
+// one row block.  With a compile-time kind the switch folds away.
+__device__ __forceinline__ void apply_op(const GemmArgs& p, const EpiCtx& c, int bi, int kind, int o, Row& v) {
+  const int64_t N = p.N;
+  {
+    const float p0 = op_p0(c.ops, o), p1 = op_p1(c.ops, o);
+    switch (kind) {
+      case KF_OP_BIAS:
+#pragma unroll
+        for (int g = 0; g < 16; ++g) v[g] += col4(c, 0, g);
+        break;
+      case KF_OP_RESIDUAL_ADD: {
+        const int64_t rows = c.rows;
+        const int64_t rl = row_local(c, bi);
+        if (c.res_lds) {
+#pragma unroll
+          for (int g = 0; g < 16; ++g) v[g] += res4(c, bi, g);
+        } else if (p.residual_bf16) {
+          const uint16_t* base = reinterpret_cast<const uint16_t*>(p.residual) + c.m0 * p.ldr + c.n0;
+          const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 2));
+#pragma unroll
+          for (int g = 0; g < 16; ++g) {
+            const int cl = col_local(c, g);
+            const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldr + cl) * 2) : kOOB;
+            const u32x2 w = buf_load8(r, off);
+            v[g] += f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+          }
+        } else {
+          const float* base = reinterpret_cast<const float*>(p.residual) + c.m0 * p.ldr + c.n0;
+          const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldr + (N - c.n0)) * 4));
+#pragma unroll
+          for (int g = 0; g < 16; ++g) {
+            const int cl = col_local(c, g);
+            const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldr + cl) * 4) : kOOB;
+            v[g] += __builtin_bit_cast(f32x4, buf_load16(r, off));
+          }
+        }
+        break;
+      }
+#define KF_EW_CASE(K, EXPR)                          \
+  case K:                                            \
+    _Pragma("unroll") for (int g = 0; g < 16; ++g)   \
+    _Pragma("unroll") for (int q = 0; q < 4; ++q) {  \
+      const float x = v[g][q];                       \
+      v[g][q] = (EXPR);                              \
+    }                                                \
+    break;
+      KF_EW_CASE(KF_OP_RELU, fmaxf(x, 0.0f))
+      KF_EW_CASE(KF_OP_GELU_TANH, f_gelu_tanh(x))
+      KF_EW_CASE(KF_OP_GELU_ERF, f_gelu_erf(x))
+      KF_EW_CASE(KF_OP_SWISH, f_swish(x))
+      KF_EW_CASE(KF_OP_SIGMOID, f_sigmoid(x))
+      KF_EW_CASE(KF_OP_TANH, f_tanh(x))
+      KF_EW_CASE(KF_OP_HARDTANH, fminf(fmaxf(x, p0), p1))
+      KF_EW_CASE(KF_OP_SCALE, x * p0)
+#undef KF_EW_CASE
+      default:
+        break;
+    }
+  }
+}
+
+// Ops oi..oe-1 of chain CH on one row block: interpreted (chain 0), or
+// unrolled over the chain's compile-time op kinds.
+template <int CH>
+__device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, int bi, int oi, int oe, Row& v) {
+  if constexpr (CH == 0) {
+#pragma nounroll
+    for (int o = oi; o < oe; ++o) apply_op(p, c, bi, op_kind(c.ops, o), o, v);
+  } else {
+    static_for<0, kChainLen[CH]>([&](auto O_c) {
+      constexpr int o = decltype(O_c)::value;
+      if (o >= oi && o < oe) apply_op(p, c, bi, kChainOps[CH][o], o, v);
+    });
+  }
+}
+
+// Store one row block (16 runs of 4 values per lane).
+__device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, int bi, const Row& v) {
+  const int64_t N = p.N;
+  const int64_t rows = c.rows;
+  const int64_t rl = row_local(c, bi);
+  if (p.out_bf16) {
+    uint16_t* base = reinterpret_cast<uint16_t*>(p.out) + c.m0 * p.ldo + c.n0;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 2));
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int cl = col_local(c, g);
+      const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 2) : kOOB;
+      buf_store8(u32x2{pack_bf16x2(v[g][0], v[g][1]), pack_bf16x2(v[g][2], v[g][3])}, r, off);
+    }
+  } else {
+    float* base = reinterpret_cast<float*>(p.out) + c.m0 * p.ldo + c.n0;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 4));
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int cl = col_local(c, g);
+      const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 4) : kOOB;
+      buf_store16(__builtin_bit_cast(u32x4, v[g]), r, off);
+    }
+  }
+}
+
+// The bf16 residual tile (RB * 64 rows x 256 columns) moves into the free
+// stage memory by LDS DMA during the epilogue: wave w fetches the RB * 16
+// tile rows [w * RB * 16, (w + 1) * RB * 16), the first half of them to `da`
+// and the second half to `db`, 512 bytes per row, the 16-byte chunk q of row
+// m at chunk q ^ (m & 15) (so the epilogue's 32-lane column reads spread over
+// 16 chunk slots); one DMA instruction moves two rows, 8 * RB per wave.  The
+// instructions are issued in groups between epilogue computations that do
+// not need the residual: when workgroups reach this point together the burst
+// is bound by HBM bandwidth, and a wave that issued them back to back would
+// stall on the full address queue instead of computing.
+template <int RB>
+struct ResDma {
+  static constexpr int kRows = RB * 16;  // tile rows fetched by one wave
+  static constexpr int kInstr = kRows / 2;
+  __amdgpu_buffer_rsrc_t rr;
+  unsigned char* da;
+  unsigned char* db;
+  int wave, lane, rows_r;
+  int64_t n0, N, ldr;
+  bool active;
+  template <int J0, int J1>
+  __device__ __forceinline__ void issue() const {
+    if (!active) return;
+    static_for<J0, J1>([&](auto J_c) {
+      constexpr int j = decltype(J_c)::value;
+      const int m = wave * kRows + 2 * j + (lane >> 5);
+      const int q = (lane & 31) ^ (m & 15);
+      const bool ok = m < rows_r && n0 + q * 8 < N;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rr, (LDS3 void*)((j < kInstr / 2 ? da : db) + ((2 * j) & (kRows / 2 - 1)) * 512), 16,
+          ok ? (uint32_t)((m * ldr + q * 8) * 2) : kOOB, 0, 0, 0);
+    });
+  }
+};
+
+// Epilogue of shape EPI (see EpiShape): ops [0, r) element-wise, op r the
+// reduction (if any), ops (r, n) element-wise, then the store.
+template <int EPI, int CH, bool FP8, int RB>
+__device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c, AccT<RB>& acc, const ResDma<RB>& rd) {
+  constexpr int kRes = ResDma<RB>::kInstr;  // residual DMA instructions per wave
+  static_assert(kRes == 8 * RB, "the GroupNorm passes issue 4 residual DMAs per row block each");
+  const int64_t N = p.N;
+  const int nops = p.prog.n;
+  const int r = EPI == kEpiPlain ? nops : p.red_index;
+
+  if (EPI == kEpiPlain) {
+    rd.template issue<0, kRes>();
+    res_wait(c);
+    static_for<0, RB>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      get_row(acc, bi, v);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+      apply_phase<CH>(p, c, bi, 0, nops, v);
+      store_row(p, c, bi, v);
+    });
+    return;
+  }
+
+  if (EPI == kEpiGroupNorm) {
+    // Group width gw in {32, 64, 128, 256} columns: each lane holds 16 of
+    // every 32-column block of its rows, so per-block sums are lane-local plus
+    // one exchange with lane ^ 32; wider groups add neighbouring blocks, and a
+    // 256-wide group also the other wave's half of the tile row.
+    int res_at = -1;
+    for (int o = 0; o < nops; ++o)
+      if (op_kind(c.ops, o) == KF_OP_RESIDUAL_ADD) res_at = o;
+    const bool res_early = res_at < r;  // the residual is added before the statistics
+    if (res_early) {
+      rd.template issue<0, kRes>();
+      res_wait(c);
+    }
+    const int gw = p.gn_group;
+    const int bpg = gw >> 5;  // 32-column blocks per group (1, 2, 4, 8)
+    const int bw = min(bpg, 4);
+    const float inv_n = 1.0f / (float)gw;
+    float s[RB][4];
+    // A bf16 chain that starts with the GroupNorm sums the accumulators as
+    // they are (the dequantisation factor is 1), in the same order as below.
+    constexpr bool kSumAcc = !FP8 && CH != 0 && kChainOps[CH][0] == KF_OP_GROUPNORM;
+    static_for<0, RB>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      if (!res_early) rd.template issue<4 * bi, 4 * bi + 4>();
+      if constexpr (kSumAcc) {
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) {
+          const f32x16& a = acc[bi][bj];
+          auto s4 = [&](int o) { return (a[o] + a[o + 1]) + (a[o + 2] + a[o + 3]); };
+          s[bi][bj] = (s4(0) + s4(4)) + (s4(8) + s4(12));
+        }
+      } else {
+        Row v;
+        get_row(acc, bi, v);
+#pragma unroll
+        for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+        apply_phase<CH>(p, c, bi, 0, r, v);
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj)
+          s[bi][bj] = (sum4(v[bj * 4]) + sum4(v[bj * 4 + 1])) + (sum4(v[bj * 4 + 2]) + sum4(v[bj * 4 + 3]));
+        put_row(acc, bi, v);
+      }
+    });
+    auto group_reduce = [&](float (&t)[RB][4]) {
+#pragma unroll
+      for (int bi = 0; bi < RB; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) t[bi][bj] += shfl_xor(t[bi][bj], 32);
+#pragma unroll
+      for (int bi = 0; bi < RB; ++bi) {
+        float g2[4];
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) {
+          float a = 0.0f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) a += ((q / bw) == (bj / bw)) ? t[bi][q] : 0.0f;
+          g2[bj] = a;
+        }
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) t[bi][bj] = g2[bj];
+      }
+      if (bpg == 8) {
+        float w[RB];
+#pragma unroll
+        for (int bi = 0; bi < RB; ++bi) w[bi] = t[bi][0];
+        if (c.lane < 32) {
+#pragma unroll
+          for (int bi = 0; bi < RB; ++bi) c.red[c.wn * 256 + row_local(c, bi)] = w[bi];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int bi = 0; bi < RB; ++bi) {
+          const float o = w[bi] + c.red[(c.wn ^ 1) * 256 + row_local(c, bi)];
+#pragma unroll
+          for (int bj = 0; bj < 4; ++bj) t[bi][bj] = o;
+        }
+        __syncthreads();
+      }
+    };
+    group_reduce(s);
+    float mean[RB][4], ss[RB][4];
+    static_for<0, RB>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      if (!res_early) rd.template issue<kRes / 2 + 4 * bi, kRes / 2 + 4 * bi + 4>();
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) {
+        mean[bi][bj] = s[bi][bj] * inv_n;
+        float a = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const float d = acc[bi][bj][q] - mean[bi][bj];
+          a += d * d;
+        }
+        ss[bi][bj] = a;
+      }
+    });
+    group_reduce(ss);
+    const float eps = op_p0(c.ops, r);
+    if (!res_early) res_wait(c);
+    static_for<0, RB>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      get_row(acc, bi, v);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int bj = g >> 2;
+        const float rs = rsqrtf(ss[bi][bj] * inv_n + eps);
+        const f32x4 gm = col4(c, 1, g), bt = col4(c, 2, g);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[g][q] = fmaf((v[g][q] - mean[bi][bj]) * rs, gm[q], bt[q]);
+      }
+      apply_phase<CH>(p, c, bi, r + 1, nops, v);
+      store_row(p, c, bi, v);
+    });
+    return;
+  }
+
+  // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
+  // this 256-column tile goes to the partials buffer.
+  rd.template issue<0, kRes>();
+  res_wait(c);
+  float mx[RB];
+  static_for<0, RB>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    Row v;
+    get_row(acc, bi, v);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+    apply_phase<CH>(p, c, bi, 0, r, v);
+    // columns past N take no part in a row reduction (only the last column
+    // tile can have any)
+    if (c.n0 + BN > N) {
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int64_t n = c.n0 + col_local(c, g);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[g][q] = (n + q < N) ? v[g][q] : -INFINITY;
+      }
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) m = fmaxf(m, max4(v[g]));
+    mx[bi] = m;
+    put_row(acc, bi, v);
+  });
+  row_combine<true>(c, mx, true);
+  float se[RB];
+  static_for<0, RB>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    const float ml = mx[bi] * kLog2e;
+    float s = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) s += __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
+    se[bi] = s;
+  });
+  row_combine<false>(c, se, true);
+  if (c.lane < 32 && c.wn == 0) {
+    float2* part = reinterpret_cast<float2*>(p.partials);
+    const int tn = (int)(c.n0 / BN);
+#pragma unroll
+    for (int bi = 0; bi < RB; ++bi) {
+      const int64_t m = c.m0 + row_local(c, bi);
+      if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
+    }
+  }
+  if (op_kind(c.ops, r) != KF_OP_ROW_SOFTMAX) return;  // logsumexp: the finishing kernel writes
+  // softmax: store e^(h - tile max); the row-finishing kernel rescales it
+  static_for<0, RB>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    const float ml = mx[bi] * kLog2e;
+    Row v;
+    get_row(acc, bi, v);
+#pragma unroll
+    for (int g = 0; g < 16; ++g)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[g][q] = __builtin_amdgcn_exp2f(fmaf(v[g][q], kLog2e, -ml));
+    store_row(p, c, bi, v);
+  });
+}
+
+
+template <bool FP8>
+struct ElemCfg;
+template <>
+struct ElemCfg<false> {  // bf16
+  static constexpr int ES = 2, KSTEP = 32, NMFMA = 32, BPITCH = 576;
+};
+template <>
+struct ElemCfg<true> {  // OCP fp8 e4m3
+  static constexpr int ES = 1, KSTEP = 64, NMFMA = 16, BPITCH = 288;
+};
+
+// Epilogue shape of a compile-time chain.
+constexpr int chain_epi(int ch) {
+  for (int o = 0; o < kChainLen[ch]; ++o) {
+    if (kChainOps[ch][o] == KF_OP_GROUPNORM) return kEpiGroupNorm;
+    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kEpiRow;
+  }
+  return kEpiPlain;
+}
+
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+typedef __attribute__((ext_vector_type(2))) int i32x2;
+
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+}  // namespace
+
+}  // namespace kf

@@ -173,3 +173,27 @@ def test_input_slot_order():
     assert kf.input_names(ch) == ["a", "b", "gamma", "beta", "residual"]
     ch = inputs.chain(inputs.config("C2"))
     assert kf.input_names(ch) == ["a", "b", "bias"]
+
+
+def test_struct_offsets_match_c_compiler(tmp_path):
+    # the ctypes mirror against what a C compiler makes of include/kf.h
+    import shutil
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = [("kf_op", kf.KfOp), ("kf_op_spec", kf.KfOpSpec), ("kf_tensor", kf.KfTensor)]
+    lines, want = [], []
+    for cname, py in structs:
+        for f in py._fields_:
+            lines.append(f'  printf("%zu\\n", offsetof({cname}, {f[0]}));\n')
+            want.append(getattr(py, f[0]).offset)
+        lines.append(f'  printf("%zu\\n", sizeof({cname}));\n')
+        want.append(ctypes.sizeof(py))
+    src = tmp_path / "off.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "kf.h"\nint main(void) {\n'
+                   + "".join(lines) + "  return 0;\n}\n")
+    exe = tmp_path / "off"
+    subprocess.check_call([cc, "-std=c99", f"-I{os.path.join(ROOT, 'include')}", str(src), "-o", str(exe)])
+    got = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert got == want
+
