@@ -39,6 +39,22 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 template <int RB>
 using AccT = f32x16[RB][4];
 
+// The row softmax / logsumexp op of a compile-time chain (0: none, or chain 0).
+constexpr int chain_row_op(int ch) {
+  for (int o = 0; o < kChainLen[ch]; ++o)
+    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kChainOps[ch][o];
+  return 0;
+}
+
+// Epilogue shape of a compile-time chain.
+constexpr int chain_epi(int ch) {
+  for (int o = 0; o < kChainLen[ch]; ++o) {
+    if (kChainOps[ch][o] == KF_OP_GROUPNORM) return kEpiGroupNorm;
+    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kEpiRow;
+  }
+  return kEpiPlain;
+}
+
 // -------------------------------------------------------------- epilogue
 //
 // The op list is run in up to two phases around its reduction op (GROUPNORM,
@@ -58,9 +74,11 @@ struct EpiCtx {
   OpTable ops;                   // the op program, one op per lane
 };
 
-// run g (0..15) of a row = block bj = g / 4, group gi = g % 4
+// run g (0..15) of a row = block bj = g / 4, group gi = g % 4: columns
+// col_local(c, 0) + run_offset(g) + 0..3
+constexpr int run_offset(int g) { return (g >> 2) * 32 + (g & 3) * 8; }
 __device__ __forceinline__ int col_local(const EpiCtx& c, int g) {
-  return c.wn * 128 + (g >> 2) * 32 + (g & 3) * 8 + (c.lane >> 5) * 4;
+  return c.wn * 128 + run_offset(g) + (c.lane >> 5) * 4;
 }
 __device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.row_base + bi * 32 + (c.lane & 31); }
 
@@ -218,23 +236,42 @@ __device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, in
   const int64_t N = p.N;
   const int64_t rows = c.rows;
   const int64_t rl = row_local(c, bi);
+  // Rows past M fall outside the descriptor's range.  Columns past N exist
+  // only in the last column tile; in every other tile the 16 runs of a row
+  // sit at fixed distances from the first, which become immediate offsets.
+  const bool full = c.n0 + BN <= N;
+  const int cl0 = col_local(c, 0);
   if (p.out_bf16) {
     uint16_t* base = reinterpret_cast<uint16_t*>(p.out) + c.m0 * p.ldo + c.n0;
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 2));
+    u32x2 w[16];
 #pragma unroll
-    for (int g = 0; g < 16; ++g) {
-      const int cl = col_local(c, g);
-      const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 2) : kOOB;
-      buf_store8(u32x2{pack_bf16x2(v[g][0], v[g][1]), pack_bf16x2(v[g][2], v[g][3])}, r, off);
+    for (int g = 0; g < 16; ++g) w[g] = u32x2{pack_bf16x2(v[g][0], v[g][1]), pack_bf16x2(v[g][2], v[g][3])};
+    if (full) {
+      const uint32_t off0 = (uint32_t)((rl * p.ldo + cl0) * 2);
+#pragma unroll
+      for (int g = 0; g < 16; ++g) buf_store8(w[g], r, off0 + (uint32_t)(run_offset(g) * 2));
+    } else {
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int cl = col_local(c, g);
+        buf_store8(w[g], r, (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 2) : kOOB);
+      }
     }
   } else {
     float* base = reinterpret_cast<float*>(p.out) + c.m0 * p.ldo + c.n0;
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 4));
+    if (full) {
+      const uint32_t off0 = (uint32_t)((rl * p.ldo + cl0) * 4);
 #pragma unroll
-    for (int g = 0; g < 16; ++g) {
-      const int cl = col_local(c, g);
-      const uint32_t off = (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 4) : kOOB;
-      buf_store16(__builtin_bit_cast(u32x4, v[g]), r, off);
+      for (int g = 0; g < 16; ++g)
+        buf_store16(__builtin_bit_cast(u32x4, v[g]), r, off0 + (uint32_t)(run_offset(g) * 4));
+    } else {
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        const int cl = col_local(c, g);
+        buf_store16(__builtin_bit_cast(u32x4, v[g]), r, (c.n0 + cl < N) ? (uint32_t)((rl * p.ldo + cl) * 4) : kOOB);
+      }
     }
   }
 }
@@ -445,17 +482,29 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     put_row(acc, bi, v);
   });
   row_combine<true>(c, mx, true);
+  // softmax keeps e^(h - max) in the accumulators for the store below
+  const bool softmax = chain_row_op(CH) ? chain_row_op(CH) == KF_OP_ROW_SOFTMAX : op_kind(c.ops, r) == KF_OP_ROW_SOFTMAX;
   float se[RB];
-  static_for<0, RB>([&](auto bi_c) {
-    constexpr int bi = decltype(bi_c)::value;
-    const float ml = mx[bi] * kLog2e;
-    float s = 0.0f;
+  auto exp_sums = [&](auto KEEP_c) {
+    static_for<0, RB>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      const float ml = mx[bi] * kLog2e;
+      float s = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 16; ++q)
+      for (int q = 0; q < 16; ++q)
 #pragma unroll
-      for (int bj = 0; bj < 4; ++bj) s += __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
-    se[bi] = s;
-  });
+        for (int bj = 0; bj < 4; ++bj) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
+          if constexpr (decltype(KEEP_c)::value) acc[bi][bj][q] = e;
+          s += e;
+        }
+      se[bi] = s;
+    });
+  };
+  if (softmax)
+    exp_sums(std::true_type{});
+  else
+    exp_sums(std::false_type{});
   row_combine<false>(c, se, true);
   if (c.lane < 32 && c.wn == 0) {
     float2* part = reinterpret_cast<float2*>(p.partials);
@@ -466,17 +515,12 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
     }
   }
-  if (op_kind(c.ops, r) != KF_OP_ROW_SOFTMAX) return;  // logsumexp: the finishing kernel writes
+  if (!softmax) return;  // logsumexp: the finishing kernel writes
   // softmax: store e^(h - tile max); the row-finishing kernel rescales it
   static_for<0, RB>([&](auto bi_c) {
     constexpr int bi = decltype(bi_c)::value;
-    const float ml = mx[bi] * kLog2e;
     Row v;
     get_row(acc, bi, v);
-#pragma unroll
-    for (int g = 0; g < 16; ++g)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[g][q] = __builtin_amdgcn_exp2f(fmaf(v[g][q], kLog2e, -ml));
     store_row(p, c, bi, v);
   });
 }
@@ -492,15 +536,6 @@ template <>
 struct ElemCfg<true> {  // OCP fp8 e4m3
   static constexpr int ES = 1, KSTEP = 64, NMFMA = 16, BPITCH = 288;
 };
-
-// Epilogue shape of a compile-time chain.
-constexpr int chain_epi(int ch) {
-  for (int o = 0; o < kChainLen[ch]; ++o) {
-    if (kChainOps[ch][o] == KF_OP_GROUPNORM) return kEpiGroupNorm;
-    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kEpiRow;
-  }
-  return kEpiPlain;
-}
 
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(2))) int i32x2;

@@ -29,7 +29,11 @@ __global__ __launch_bounds__(256) void kf_row_logsumexp_finish(const float2* __r
 constexpr int kMaxFinishTiles = 1024;
 
 // One workgroup per row: factors f_t = e^(mu_t - mu) / S, then every 16-byte
-// chunk of the row is scaled by the factor of its tile.
+// chunk of the row is scaled by the factor of its tile.  The row is taken in
+// passes of 4 chunks per thread (16 KiB per workgroup for bf16), all four
+// loads issued before any store, so that each thread keeps several reads in
+// flight: the kernel only moves data, and its speed is the number of bytes
+// in flight per CU.
 __global__ __launch_bounds__(256) void kf_row_softmax_rescale(const float2* __restrict__ part, int tiles,
                                                                int64_t N, void* out, int64_t ldo,
                                                                int out_bf16) {
@@ -46,21 +50,42 @@ __global__ __launch_bounds__(256) void kf_row_softmax_rescale(const float2* __re
   const float inv = 1.0f / s;
   for (int t = tid; t < tiles; t += 256) fac[t] = expf(ps[t].x - mu) * inv;
   __syncthreads();
+  constexpr int U = 4;
   if (out_bf16) {
     uint16_t* row = reinterpret_cast<uint16_t*>(out) + m * ldo;
-    for (int64_t c = tid; c * 8 < N; c += 256) {
-      const float f = fac[(c * 8) >> 8];
-      u32x4 w = *reinterpret_cast<const u32x4*>(row + c * 8);
+    const int64_t chunks = N / 8;  // N % 8 == 0 for bf16 outputs
+    for (int64_t c0 = 0; c0 < chunks; c0 += 256 * U) {
+      u32x4 w[U];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(bf16_lo(w[e]) * f, bf16_hi(w[e]) * f);
-      *reinterpret_cast<u32x4*>(row + c * 8) = w;
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 256 + tid;
+        if (c < chunks) w[u] = *reinterpret_cast<const u32x4*>(row + c * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 256 + tid;
+        if (c >= chunks) continue;
+        const float f = fac[(c * 8) >> 8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[u][e] = pack_bf16x2(bf16_lo(w[u][e]) * f, bf16_hi(w[u][e]) * f);
+        *reinterpret_cast<u32x4*>(row + c * 8) = w[u];
+      }
     }
   } else {
     float* row = reinterpret_cast<float*>(out) + m * ldo;
-    for (int64_t c = tid; c * 4 < N; c += 256) {
-      const float f = fac[(c * 4) >> 8];
-      f32x4 v = *reinterpret_cast<const f32x4*>(row + c * 4);
-      *reinterpret_cast<f32x4*>(row + c * 4) = v * f;
+    const int64_t chunks = N / 4;  // N % 4 == 0 for fp32 outputs of the matrix-core GEMMs
+    for (int64_t c0 = 0; c0 < chunks; c0 += 256 * U) {
+      f32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 256 + tid;
+        if (c < chunks) v[u] = *reinterpret_cast<const f32x4*>(row + c * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 256 + tid;
+        if (c < chunks) *reinterpret_cast<f32x4*>(row + c * 4) = v[u] * fac[(c * 4) >> 8];
+      }
     }
   }
 }
