@@ -44,14 +44,17 @@ constexpr int CIN = 64;              // channels the halo holds
 constexpr int WID = 128;             // image width (= tile width)
 constexpr int COUT = 128;            // output channels (= tile width in N)
 constexpr int HALO_COLS = WID + 2;   // iw = -1 .. WID
-constexpr int HALO_ROWS = 4;         // ih = oh0 - 1 .. oh0 + 2
+constexpr int HALO_SLOTS = 4;        // input rows the halo holds (a ring)
 constexpr int PIX_BYTES = CIN * 2;   // 128 bytes of channels per pixel
-constexpr int kHalo = HALO_ROWS * HALO_COLS * PIX_BYTES;  // 66560 bytes
+constexpr int kSlot = HALO_COLS * PIX_BYTES;  // one input row of the halo: 16640 bytes
+constexpr int kHalo = HALO_SLOTS * kSlot;     // 66560 bytes
 constexpr int kWStage = COUT * 64;   // [128 co][32 ci] bf16 = 8 KiB
-constexpr int kWS = 3;               // weight stages = prefetch distance in K-steps
-constexpr int kRaw = CIN * 4 * WID * 2;  // the next tile's halo as loaded: [ci][4 rows][128 px] = 64 KiB
+constexpr int kWS = 6;               // weight stages = prefetch distance in K-steps
+constexpr int kRaw = CIN * 2 * WID * 2;  // two input rows as loaded: [ci][2 rows][128 px] = 32 KiB
+constexpr int kRawDma = kRaw / 1024 / 4;  // DMA instructions per wave for two input rows
 constexpr int kSteps = 9 * (CIN / 32);  // 18 K-steps of 32 per tile
-static_assert(kSteps % 6 == 0 && kSteps >= 16, "the tile loop unrolls 6 steps; 16 carry halo DMA");
+static_assert(kSteps % kWS == 0 && kSteps % 2 == 0, "a tile's steps cycle whole weight stages and fragment buffers");
+static_assert(kRawDma <= kSteps - kWS, "the next tile's rows are requested before its first weight stage");
 
 #define LDS3 __attribute__((address_space(3)))
 
@@ -142,11 +145,12 @@ template <int CH>
 __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, const uint16_t* __restrict__ wp) {
   __shared__ __attribute__((aligned(1024))) unsigned char sHalo[kHalo];
   __shared__ __attribute__((aligned(1024))) unsigned char sRaw[kRaw];
-  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage], sW3[kWStage],
+      sW4[kWStage], sW5[kWStage];
   __shared__ __attribute__((aligned(1024))) unsigned char sDummy[1024];
   auto stW = [&](auto S_c) -> unsigned char* {
     constexpr int S = decltype(S_c)::value;
-    return S == 0 ? sW0 : S == 1 ? sW1 : sW2;
+    return S == 0 ? sW0 : S == 1 ? sW1 : S == 2 ? sW2 : S == 3 ? sW3 : S == 4 ? sW4 : sW5;
   };
 
   const int tid = threadIdx.x;
@@ -158,38 +162,41 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   const int rows_per_img = H / 2;
   const int64_t img_elems = (int64_t)CIN * H * WID;
 
-  // ---- halo of a tile: x[n][ci][oh0-1+hr][iw] -> sHalo[(hr*130 + iw+1)][ci].
-  // The next tile's four input rows of every channel arrive by LDS DMA,
-  // spread over the K-steps of the current tile, into sRaw as [ci][hr][128
-  // px] (row (ci, hr) = 256 bytes, its 16-byte chunk q stored at q ^
-  // rsw(ci)); at the tile boundary each thread transposes 2 blocks of 8
-  // channels x 8 pixels from sRaw into sHalo with v_perm_b32.  Wave w's DMA i
-  // (i < 16) fetches channel 16 w + i, lane l its row l >> 4, chunk
-  // position l & 15; past i = 15 the instruction is a zero fill of a dummy
-  // block, so every K-step issues the same number of DMA instructions.
+  // ---- halo: a ring of 4 input rows, slot k at sHalo + k * kSlot, each as
+  // [130 pixels (iw = -1 .. WID)][64 channels].  Logical row lr (input row
+  // oh0 - 1 + lr) of the current tile sits in slot (rb + lr) & 3.  A
+  // workgroup walks a contiguous range of tiles; the next tile of the same
+  // image shares two input rows with this one, so only two new rows are
+  // loaded per tile (rb advances by 2), and only at the start of the range
+  // or of an image are all four loaded.
+  //
+  // Two input rows of every channel arrive by LDS DMA into sRaw as [ci][2
+  // rows][128 px] (row (ci, r) = 256 bytes, its 16-byte chunk q stored at q ^
+  // rsw(ci)); at the tile boundary each thread transposes one block of 8
+  // channels x 8 pixels from sRaw into its halo slot with v_perm_b32.  Wave
+  // w's DMA i (0 .. 7) fetches channels 2 (8 w + i) and 2 (8 w + i) + 1, lane
+  // l channel 2 (8 w + i) + (l >> 5), row (l >> 4) & 1, chunk position l & 15.
   auto rsw = [](int c) { return ((c >> 3) << 1) & 15; };
-  auto raw_dma = [&](int i, int tile, bool live) {
-    const bool on = live && i < 16;
-    const int c = wave * 16 + (i < 16 ? i : 0);
-    const int n_img = on ? tile / rows_per_img : 0;
-    const int ih = 2 * (tile % rows_per_img) - 1 + (lane >> 4);
+  auto raw_dma = [&](int i, int n_img, int ih0, bool live) {
+    const int c = 2 * (wave * kRawDma + i) + (lane >> 5);
+    const int ih = ih0 + ((lane >> 4) & 1);
     const __amdgpu_buffer_rsrc_t rx =
-        make_rsrc(reinterpret_cast<const uint16_t*>(p.x) + n_img * img_elems, (uint32_t)(img_elems * 2));
+        make_rsrc(reinterpret_cast<const uint16_t*>(p.x) + (live ? n_img : 0) * img_elems, (uint32_t)(img_elems * 2));
     const int q = (lane & 15) ^ rsw(c);
-    const bool ok = on && ih >= 0 && ih < H;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS3 void*)(on ? sRaw + c * 1024 : sDummy), 16,
+    const bool ok = live && ih >= 0 && ih < H;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS3 void*)(live ? sRaw + (wave * kRawDma + i) * 1024 : sDummy), 16,
                                               ok ? (uint32_t)(((c * H + ih) * WID + q * 8) * 2) : kOOB, 0, 0, 0);
   };
-  auto halo_write = [&]() {
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int b = tid + half * 256;
-      const int cg = b & 7, pg = (b >> 3) & 15, hr = b >> 7;
+  // sRaw -> halo slots s0 (its row 0) and s1 (row 1), zero padding columns
+  auto halo_write = [&](int s0, int s1) {
+    {
+      const int cg = tid & 7, pg = (tid >> 3) & 15, r = tid >> 7;
+      const int slot = r ? s1 : s0;
       u32x4 hv[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int c = cg * 8 + j;
-        hv[j] = *reinterpret_cast<const u32x4*>(sRaw + c * 1024 + hr * 256 + ((pg ^ rsw(c)) << 4));
+        hv[j] = *reinterpret_cast<const u32x4*>(sRaw + c * 512 + r * 256 + ((pg ^ rsw(c)) << 4));
       }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -197,14 +204,13 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
         u32x4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(hv[2 * e + 1][k >> 1], hv[2 * e][k >> 1], sel);
-        const int pix = hr * HALO_COLS + pg * 8 + k + 1;
+        const int pix = slot * HALO_COLS + pg * 8 + k + 1;
         *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = o;
       }
     }
-    // zero padding columns iw = -1 and iw = WID of every halo row
-    if (tid < 64) {
-      const int hr = tid >> 4, side = (tid >> 3) & 1, cg = tid & 7;
-      const int pix = hr * HALO_COLS + (side ? HALO_COLS - 1 : 0);
+    if (tid < 32) {
+      const int r = tid >> 4, side = (tid >> 3) & 1, cg = tid & 7;
+      const int pix = (r ? s1 : s0) * HALO_COLS + (side ? HALO_COLS - 1 : 0);
       *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = u32x4{0u, 0u, 0u, 0u};
     }
   };
@@ -240,6 +246,7 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
     const int ch = kk * 2 + kg;
     rB[kk] = (uint32_t)((wn * 64 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
   }
+  int rb = 0;                      // ring slot of logical halo row 0
   u32x4 fa[2][2][4], fb[2][2][2];  // [buffer][16-k half][block]
   constexpr int kReads = 12;       // per step: 8 A (4 blocks x 2 halves), 4 B
   auto read_one = [&](auto S_c, auto BUF_c, auto J_c, int s) {
@@ -251,7 +258,8 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
       // again: the values are never used, and the halo index stays in range
       const int sc = s < kSteps ? s : kSteps - 1;
       const int tap = sc >> 1, kh = tap / 3, kw = tap - kh * 3;
-      const int pix = ((j >> 1) + kh) * HALO_COLS + wm * 64 + (j & 1) * 32 + r32 + kw;
+      const int slot = (rb + (j >> 1) + kh) & 3;
+      const int pix = slot * HALO_COLS + wm * 64 + (j & 1) * 32 + r32 + kw;
       const int ch = (sc & 1) * 4 + kk * 2 + kg;
       fa[BUF][kk][j] = lds_load<u32x4>(sHalo + halo_off(pix, ch));
     } else {
@@ -267,16 +275,21 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   }
 
   CAcc acc;
-  constexpr int kDma = 3;  // DMA instructions per K-step: 2 weight blocks, 1 halo (or dummy)
-  // K-step s of a tile on weight stage S = s % 3: every wave has read its
+  constexpr int kDma = 3;  // DMA instructions per K-step: 2 weight blocks, then 1 row block (or dummy)
+  // K-step s of a tile on weight stage S = s % 6: every wave has read its
   // fragments of stage S (during step s-1) once it passes the barrier, so the
-  // DMA of step s+3 goes into stage S; the barrier also publishes stage S+1
-  // (DMA issued during step s-2), read during this step.  The wait allows the
-  // 3 DMA instructions of step s-1 in flight.
-  auto step = [&](auto S_c, auto BUF_c, int s, bool next_live, int next_tile) {
+  // DMA of step s+6 goes into stage S; the barrier also publishes stage S+1
+  // (DMA issued during step s-5), read during this step.  A wave's loads
+  // complete in issue order, so that wait also covers the input rows it
+  // requested up to step s-6: the HBM latency of a row request is hidden
+  // behind five K-steps.  The wait allows the row DMA of step s-5 and the
+  // 3 DMA instructions of each of steps s-4 .. s-1 in flight.
+  constexpr int kStepWait = 1 + 4 * kDma;
+  // the next tile's rows: image n_next, first input row ih_next (rows_live: any)
+  auto step = [&](auto S_c, auto BUF_c, int s, bool next_live, bool rows_live, int n_next, int ih_next) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
-    wait_vmcnt_lgkm0<kDma>();
+    wait_vmcnt_lgkm0<kStepWait>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     const bool live = s + kWS < kSteps || next_live;
@@ -287,8 +300,8 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
                                                             __builtin_bit_cast(bf16x8, fb[BUF][kk][bj]), acc[bi][bj], 0,
                                                             0, 0);
       if constexpr (i < kReads) read_one(IC<(S + 1) % kWS>{}, IC<BUF ^ 1>{}, I_c, s + 1);
-      if constexpr (i == 3 || i == 11) dma_one(S_c, IC<(i == 3 ? 0 : 1)>{}, s + kWS, live);
-      if constexpr (i == 7) raw_dma(s, next_tile, next_live);
+      if constexpr (i == 1 || i == 3) dma_one(S_c, IC<(i == 1 ? 0 : 1)>{}, s + kWS, live);
+      if constexpr (i == 5) raw_dma(s < kRawDma ? s : 0, n_next, ih_next, rows_live && s < kRawDma);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
@@ -299,29 +312,53 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   const int64_t plane_out = p.pool ? (int64_t)(H / 2) * (WID / 2) : (int64_t)H * WID;
   uint16_t* out = reinterpret_cast<uint16_t*>(p.out);
 
-  int tile = blockIdx.x;
-  // prologue: the first tile's halo, then the weight stages of steps 0-2
-  // (each followed by a dummy, as in a K-step)
-  for (int i = 0; i < 16; ++i) raw_dma(i, tile, true);
+  // this workgroup's tiles (the grid never exceeds the tile count)
+  const int t_begin = (int)((int64_t)blockIdx.x * p.tiles / gridDim.x);
+  const int t_end = (int)((int64_t)(blockIdx.x + 1) * p.tiles / gridDim.x);
+  // tile t continues tile t-1 (same image, next row pair) inside the range
+  auto continues = [&](int t) { return t > t_begin && t % rows_per_img != 0; };
+
+  // prologue: input rows 0-1 of the first tile, then the weight stages of
+  // steps 0-5 (each followed by a dummy, as in a K-step)
+  for (int i = 0; i < kRawDma; ++i) raw_dma(i, t_begin / rows_per_img, 2 * (t_begin % rows_per_img) - 1, true);
   static_for<0, kWS>([&](auto S_c) {
     dma_one(S_c, IC<0>{}, decltype(S_c)::value, true);
-    raw_dma(16, tile, false);
     dma_one(S_c, IC<1>{}, decltype(S_c)::value, true);
+    raw_dma(0, 0, 0, false);
   });
 
-  for (; tile < p.tiles; tile += gridDim.x) {
+  for (int tile = t_begin; tile < t_end; ++tile) {
     const int n_img = tile / rows_per_img;
     const int ph = tile % rows_per_img;  // tile = output rows 2 ph, 2 ph + 1
     const int oh0 = 2 * ph;
-    const int next_tile = tile + (int)gridDim.x;
-    const bool next_live = next_tile < p.tiles;
+    const bool cont = continues(tile);
+    const int next_tile = tile + 1;
+    const bool next_live = next_tile < t_end;
+    // rows the next tile needs from sRaw: its rows 2-3 if it continues this
+    // one, else its rows 0-1 (rows 2-3 follow at its boundary)
+    const bool next_cont = next_live && continues(next_tile);
+    const int n_next = next_tile / rows_per_img;
+    const int ih_next = 2 * (next_tile % rows_per_img) + (next_cont ? 1 : -1);
 
-    // this tile's raw halo and weight stage 0 have landed (the DMA of the
-    // last two K-steps, stages 1 and 2, may still be in flight); every wave
-    // is past its last read of the previous halo
-    wait_vmcnt_lgkm0<(kWS - 1) * kDma>();
+    // This tile's new input rows and weight stage 0 have landed (the DMA of
+    // the last five K-steps may still be in flight; the row requests are all
+    // older); every wave is past its last read of the slots rewritten here
+    // and of the previous tile's output staging.
+    wait_vmcnt_lgkm0<1 + 5 * kDma>();
     __syncthreads();
-    halo_write();
+    rb = cont ? (rb + 2) & 3 : 0;
+    if (cont) {
+      halo_write((rb + 2) & 3, (rb + 3) & 3);
+    } else {
+      // start of the range or of an image: rows 0-1 are in sRaw; rows 2-3
+      // are requested now and waited for
+      halo_write(0, 1);
+      __syncthreads();
+      for (int i = 0; i < kRawDma; ++i) raw_dma(i, n_img, oh0 + 1, true);
+      wait_vmcnt_lgkm0<0>();
+      __syncthreads();
+      halo_write(2, 3);
+    }
     __syncthreads();
     static_for<0, kReads>([&](auto J_c) { read_one(IC<0>{}, IC<0>{}, J_c, 0); });
 
@@ -332,26 +369,34 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
 
-    // 18 steps = 3 x 6 (stage s % 3, fragment buffer s % 2)
+    // 18 steps = 3 x 6 (stage s % 6, fragment buffer s % 2)
 #pragma unroll 1
     for (int s = 0; s < kSteps; s += 6) {
-      step(IC<0>{}, IC<0>{}, s, next_live, next_tile);
-      step(IC<1>{}, IC<1>{}, s + 1, next_live, next_tile);
-      step(IC<2>{}, IC<0>{}, s + 2, next_live, next_tile);
-      step(IC<0>{}, IC<1>{}, s + 3, next_live, next_tile);
-      step(IC<1>{}, IC<0>{}, s + 4, next_live, next_tile);
-      step(IC<2>{}, IC<1>{}, s + 5, next_live, next_tile);
+      step(IC<0>{}, IC<0>{}, s, next_live, next_live, n_next, ih_next);
+      step(IC<1>{}, IC<1>{}, s + 1, next_live, next_live, n_next, ih_next);
+      step(IC<2>{}, IC<0>{}, s + 2, next_live, next_live, n_next, ih_next);
+      step(IC<3>{}, IC<1>{}, s + 3, next_live, next_live, n_next, ih_next);
+      step(IC<4>{}, IC<0>{}, s + 4, next_live, next_live, n_next, ih_next);
+      step(IC<5>{}, IC<1>{}, s + 5, next_live, next_live, n_next, ih_next);
     }
 
     // ---- epilogue, per output channel block bj and column half bc (the
     // two output rows of the tile): ops before the pool on the pre-pool
     // values, the pool in registers, ops after it on the pooled values.  The
-    // bf16 results are staged in LDS (the halo region: after the barrier of
-    // step 17 no wave reads halo data it uses) as [channel][row][pixels], a
+    // bf16 results are staged in LDS, in the halo slots of this tile's input
+    // rows 0 and 1 (last read in step 11), as [channel][row][pixels], a
     // 16-byte chunk q of row (co, r) at chunk q ^ (co & 15), then written out
     // with 16-byte stores, so that each store instruction covers whole
     // 128-byte lines of the output rows instead of 32 scattered channels.
-    unsigned char* const stage = sHalo;
+    // Pooled, the whole tile (128 channels x 64 pixels) fits one slot; else
+    // each channel block bj (64 channels x 2 rows x 128 pixels) fills both
+    // slots and is stored before the next is staged.
+    unsigned char* const slot_a = sHalo + rb * kSlot;
+    unsigned char* const slot_b = sHalo + ((rb + 1) & 3) * kSlot;
+    // staging row (64 channels x 2 rows of 256 bytes, unpooled)
+    auto stage_row = [&](int row) { return row < 64 ? slot_a + row * 256 : slot_b + (row - 64) * 256; };
+    const __amdgpu_buffer_rsrc_t ro =
+        make_rsrc(out + (int64_t)n_img * COUT * plane_out, (uint32_t)(COUT * plane_out * 2));
     static_for<0, 2>([&](auto bj_c) {
       constexpr int bj = decltype(bj_c)::value;
       const int co = wn * 64 + bj * 32 + (lane & 31);
@@ -382,49 +427,48 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
           for (int q = 0; q < 4; ++q) {
             const int pw = wm * 32 + bc * 16 + q * 4 + (lane >> 5) * 2;
             const int ch = pw >> 3;
-            *reinterpret_cast<uint32_t*>(stage + co * 128 + ((ch ^ (co & 7)) << 4) + (pw & 7) * 2) =
+            *reinterpret_cast<uint32_t*>(slot_a + co * 128 + ((ch ^ (co & 7)) << 4) + (pw & 7) * 2) =
                 pack_bf16x2(pv[q * 2], pv[q * 2 + 1]);
           }
         } else {
+          const int col = wn * 32 + (lane & 31);  // channel within block bj
 #pragma unroll
           for (int r = 0; r < 2; ++r)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int ow = wm * 64 + bc * 32 + q * 8 + (lane >> 5) * 4;
               const float* x = &v[r * 16 + q * 4];
-              *reinterpret_cast<u32x2*>(stage + (co * 2 + r) * 256 + (((ow >> 3) ^ (co & 15)) << 4) + (ow & 7) * 2) =
+              *reinterpret_cast<u32x2*>(stage_row(col * 2 + r) + (((ow >> 3) ^ (co & 15)) << 4) + (ow & 7) * 2) =
                   u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
             }
         }
       });
-    });
-    __syncthreads();
-    {
-      // output rows of this tile: channel co's row starts at
-      // img_out + co * plane_out + row_off (+ WID for the second pre-pool row)
-      const __amdgpu_buffer_rsrc_t ro =
-          make_rsrc(out + (int64_t)n_img * COUT * plane_out, (uint32_t)(COUT * plane_out * 2));
-      if (p.pool) {
-        // 128 channels x 8 chunks
-        const uint32_t row_off = (uint32_t)(ph * (WID / 2) * 2);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int idx = tid + 256 * k;
-          const int co = idx >> 3, ch = idx & 7;
-          const u32x4 w = *reinterpret_cast<const u32x4*>(stage + co * 128 + ((ch ^ (co & 7)) << 4));
-          buf_store16(w, ro, (uint32_t)(co * plane_out * 2) + row_off + ch * 16);
-        }
-      } else {
-        // 128 channels x 2 rows x 16 chunks
+      if (!p.pool) {
+        // channel block bj: 64 channels x 2 rows x 16 chunks
+        __syncthreads();
         const uint32_t row_off = (uint32_t)(oh0 * WID * 2);
-#pragma unroll 4
-        for (int k = 0; k < 16; ++k) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
           const int idx = tid + 256 * k;
           const int row = idx >> 4, ch = idx & 15;
-          const int co = row >> 1, r = row & 1;
-          const u32x4 w = *reinterpret_cast<const u32x4*>(stage + row * 256 + ((ch ^ (co & 15)) << 4));
+          const int col = row >> 1, r = row & 1;
+          const int co = (col >> 5) * 64 + bj * 32 + (col & 31);
+          const u32x4 w = *reinterpret_cast<const u32x4*>(stage_row(row) + ((ch ^ (co & 15)) << 4));
           buf_store16(w, ro, (uint32_t)(co * plane_out * 2) + row_off + (uint32_t)(r * WID * 2) + ch * 16);
         }
+        __syncthreads();
+      }
+    });
+    if (p.pool) {
+      // 128 channels x 8 chunks
+      __syncthreads();
+      const uint32_t row_off = (uint32_t)(ph * (WID / 2) * 2);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int idx = tid + 256 * k;
+        const int co = idx >> 3, ch = idx & 7;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(slot_a + co * 128 + ((ch ^ (co & 7)) << 4));
+        buf_store16(w, ro, (uint32_t)(co * plane_out * 2) + row_off + ch * 16);
       }
     }
   }

@@ -326,6 +326,38 @@ def test_c4_full_config_sampled_images():
     print(f"C4 full err {err:.3e}")
 
 
+
+@pytest.mark.parametrize("batch,H,ops", [
+    (5, 120, [("bias",), ("relu",), ("maxpool2x2",)]),   # 300 row-pair tiles, 60 per image
+    (3, 200, [("bias",), ("relu",)]),                    # unpooled
+])
+def test_c4_tile_ranges(batch, H, ops):
+    """More tiles than workgroups: each workgroup walks a contiguous range of
+    row pairs, reusing two halo rows from one tile to the next and reloading
+    all four at the start of an image; ranges here cross image boundaries."""
+    _torch()
+    cfg = inputs.config("C4", batch=batch, H=H, ops=ops)
+    t = inputs.generate(cfg, seed=batch + H)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out, images=np.arange(batch))
+    print(f"C4 batch={batch} H={H} err {err:.3e}")
+
+
+def test_c4_integer_bit_exact_tile_ranges():
+    """The integer test of the contraction with several tiles per workgroup."""
+    torch = _torch()
+    batch, H = 3, 200
+    cfg = inputs.config("C4", batch=batch, H=H, ops=[])
+    rng = np.random.default_rng(43)
+    x = rng.integers(-4, 5, size=(batch, 64, H, 128)).astype(np.float32)
+    w = rng.integers(-2, 3, size=(128, 64, 3, 3)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
+    _, out = run_gpu(cfg, t)
+    got_bits = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    for n in range(batch):
+        ref = oracle.conv2d_3x3(x[n:n + 1].astype(np.float64), w.astype(np.float64))
+        assert np.array_equal(got_bits[n:n + 1], inputs.f32_to_bf16_bits(ref.astype(np.float32))), f"image {n}"
+
 # ------------------------------------------------------------ unfused chain
 
 @pytest.mark.parametrize("name,kw", [
