@@ -80,7 +80,7 @@ struct kf_desc {
 
 namespace {
 
-// The compile-time chain whose op kinds equal the spec's (GEMM chains 1-6,
+// The compile-time chain whose op kinds equal the spec's (GEMM chains 1-6 and 8,
 // the conv chain 7), else 0.
 int match_chain(const kf_op_spec* s) {
   const bool conv = s->contraction == KF_CONV2D_3X3;

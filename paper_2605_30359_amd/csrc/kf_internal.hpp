@@ -29,8 +29,8 @@ enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
 // is interpreted at run time.  The paper turns each operator into its own
 // specialised kernel; these are the chains of the benchmarked operators and
 // the plain building blocks, and every other chain runs interpreted.
-constexpr int kNumChains = 8;
-constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3};
+constexpr int kNumChains = 9;
+constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5};
 constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {},                                                                         // 0: interpreted
     {},                                                                         // 1: contraction only
@@ -40,6 +40,7 @@ constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {KF_OP_GROUPNORM, KF_OP_SWISH, KF_OP_RESIDUAL_ADD},                        // 5: GEMM, GroupNorm, swish
     {KF_OP_BIAS, KF_OP_HARDTANH, KF_OP_ROW_SOFTMAX},                           // 6: GEMM, hardtanh, softmax
     {KF_OP_BIAS, KF_OP_RELU, KF_OP_MAXPOOL2X2},                                // 7: conv, ReLU, max-pool
+    {KF_OP_BIAS, KF_OP_SWISH, KF_OP_TANH, KF_OP_GELU_ERF, KF_OP_HARDTANH},     // 8: GEMM + activation chain
 };
 
 // Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).

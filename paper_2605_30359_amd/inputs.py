@@ -65,13 +65,23 @@ CONFIGS = {
         ops=[("bias",), ("hardtanh", -1.0, 1.0), ("row_softmax",)],
         dist=dict(a=("normal", 1.0), b=("normal", 1.0), bias=("uniform", -0.1, 0.1)),
     ),
+    # the paper's worked matmul + activation fusion (Appendix C): a GEMM
+    # followed by bias, swish, tanh, exact GELU and hardtanh, at the C2 size
+    "F1": dict(
+        workload="gemm_bias_swish_tanh_geluerf_hardtanh_bf16",
+        contraction="gemm", in_dtype="bf16", out_dtype="bf16", b_layout="kn",
+        M=4096, N=4096, K=4096,
+        ops=[("bias",), ("swish",), ("tanh",), ("gelu_erf",), ("hardtanh", -1.0, 1.0)],
+        dist=dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1)),
+    ),
 }
 
 BASE_SEED = 260530359
 
 
 def default_seed(name: str) -> int:
-    return BASE_SEED + int(name[1:])
+    # C1..C5: BASE_SEED + k; the F workloads (the next chains) from + 100
+    return BASE_SEED + int(name[1:]) + (100 if name.startswith("F") else 0)
 
 
 def config(name: str, **overrides) -> dict:

@@ -264,6 +264,33 @@ def test_c5_full_config_sampled_rows():
     print(f"C5 full err {err:.3e}")
 
 
+
+# ------------------------------------------------ GEMM + activation chain (F1)
+
+@pytest.mark.parametrize("M,N,K,in_dtype", [(300, 520, 136, "bf16"), (1, 8, 8, "bf16"), (257, 272, 64, "e4m3"),
+                                            (33, 65, 31, "f32")])
+def test_f1_ragged(M, N, K, in_dtype):
+    _torch()
+    kw = dict(M=M, N=N, K=K, in_dtype=in_dtype)
+    if in_dtype == "f32":
+        kw["out_dtype"] = "f32"
+    if in_dtype == "e4m3":
+        kw["dist"] = dict(a=("normal", 1.0), b=("normal", 1.0), bias=("uniform", -0.1, 0.1))
+    cfg = inputs.config("F1", **kw)
+    t = inputs.generate(cfg, seed=M + N + K)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"F1 {M}x{N}x{K} {in_dtype} err {err:.3e}")
+
+
+def test_f1_full_config_sampled_rows():
+    _torch()
+    cfg = inputs.config("F1")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out, rows=sample_rows(cfg["M"], 48))
+    print(f"F1 full err {err:.3e}")
+
 # ------------------------------------------------------------ conv (C4)
 
 @pytest.mark.parametrize("batch,H,ops", [
@@ -428,6 +455,7 @@ def test_epilogue_operand_paths(name, kw, res_f32):
     ("C3", dict(M=300, N=512, K=136, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
     ("C5", dict(M=300, N=528, K=160)),                                     # fp8, bias, hardtanh, softmax
     ("C4", dict(batch=2, H=10)),                                           # conv, bias, ReLU, pool (pool first)
+    ("F1", dict(M=300, N=520, K=136)),                                     # bias, swish, tanh, GELU(erf), hardtanh
 ])
 def test_specialised_chain_matches_interpreted(name, kw):
     """The benchmarked op lists run an epilogue generated for that exact

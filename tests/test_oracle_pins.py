@@ -333,6 +333,33 @@ def test_chain_c2_closed_forms_and_torch():
     assert np.allclose(out, ref, rtol=1e-12)
 
 
+
+def test_chain_f1_zero_weight_and_torch():
+    """The GEMM + activation chain (bias, swish, tanh, exact GELU, hardtanh):
+    W = 0 makes every row the chain applied to the bias; the full chain agrees
+    with torch's CPU float64 composition of the same modules."""
+    cfg, t = _small("F1", M=6, N=520, K=64)
+    ch = inputs.chain(cfg)
+    bb = _t(t["bias"])
+
+    def torch_chain(h):
+        return F.hardtanh(F.gelu(torch.tanh(F.silu(h))), -1.0, 1.0)
+
+    z = dict(t, b=np.zeros_like(t["b"]))
+    out = oracle.run_chain(ch, z)
+    assert np.allclose(out, np.tile(torch_chain(bb).numpy(), (6, 1)), rtol=1e-13, atol=1e-15)
+    out = oracle.run_chain(ch, t)
+    x = _t(oracle.decode_bf16(t["a"]))
+    w = _t(oracle.decode_bf16(t["b"]))
+    ref = torch_chain(x @ w + bb).numpy()
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-14)
+    # swish >= -0.2785, so the GELU input tanh(swish) lies in (-0.2716, 1),
+    # where gelu is increasing (its minimum is at -0.75): the output lies in
+    # (gelu(-0.2716), gelu(1)) = (-0.1068, 0.8414) and hardtanh never clips
+    lo = F.gelu(torch.tanh(F.silu(torch.tensor(-1.2784645427610738, dtype=torch.float64)))).item()
+    assert -0.1068 < lo < -0.1066
+    assert out.min() >= lo and out.max() < 0.8414
+
 def test_chain_c3_zero_weight_and_torch():
     cfg, t = _small("C3", M=6, N=512, K=96, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
     ch = inputs.chain(cfg)
