@@ -117,16 +117,18 @@ def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
     from paper_2605_30359_amd import inputs
 
     ch = inputs.chain_for(cfg, tensors)
-    gemm = cfg["contraction"] == "gemm"
+    rowwise = cfg["contraction"] == "rowwise"
+    gemm = cfg["contraction"] == "gemm" or rowwise  # a sample is a set of rows
     units = cfg["M"] if gemm else cfg["batch"]
-    flops_unit = inputs.flops(cfg) // max(units, 1)
+    work = inputs.rowwise_bytes(cfg) if rowwise else inputs.flops(cfg)
+    work_unit = work / max(units, 1)
     unit_name = "output rows" if gemm else "images"
 
     import torch
     g_all = gpu_out.cpu()
     bf16_out = g_all.dtype == torch.bfloat16
     g_all = g_all.view(torch.int16).numpy().view(np.uint16) if bf16_out else g_all.numpy()
-    floor = 1.0 / cfg["N"] if cfg["ops"][-1][0] == "row_softmax" else 1.0
+    floor = 1.0 / cfg["N"] if cfg["ops"] and cfg["ops"][-1][0] == "row_softmax" else 1.0
 
     perm = np.random.default_rng(0).permutation(units).astype(np.int64)
     pos, done, elapsed, err = 0, 0, 0.0, 0.0
@@ -152,8 +154,8 @@ def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
         chunk = int(max(1, min(4 * chunk, units, rate * (budget_s - elapsed) + 1)))
     passes = done / units
     return {
-        "value": done * flops_unit / elapsed / 1e12,
-        "unit": "TFLOP/s",
+        "value": done * work_unit / elapsed / (1e9 if rowwise else 1e12),
+        "unit": "GB/s" if rowwise else "TFLOP/s",
         "cores": oracle.threads(),
         "kind": "oracle",
         "sample": (f"{done} {unit_name} ({passes:.2f} x the {units} of the full workload, seeded random order) "
@@ -167,7 +169,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="C2", help="C1..C5, F1 (default C2)")
+    ap.add_argument("--workload", default="C2", help="C1..C5, F1, F3, F4 (default C2)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
@@ -225,11 +227,16 @@ def main(argv=None):
         hip.hipEventDestroy(ctypes.c_void_p(a))
         hip.hipEventDestroy(ctypes.c_void_p(b))
 
-    flops = inputs.flops(cfg)
+    # contraction chains are measured in FLOP/s against the MFMA (or fp32)
+    # peak; the row-wise chains, which have no contraction, in bytes per
+    # second against HBM bandwidth
+    rowwise = cfg["contraction"] == "rowwise"
     dt = cfg["in_dtype"]
-    peak = PEAK_TFLOPS[dt]
-    value = flops / (ms_per_step * 1e-3) / 1e12
-    achieved = flops / (kernel_ms * 1e-3) / 1e12
+    work = inputs.rowwise_bytes(cfg) if rowwise else inputs.flops(cfg)
+    peak = HBM_PEAK_GBS if rowwise else PEAK_TFLOPS[dt]
+    scale = 1e9 if rowwise else 1e12
+    value = work / (ms_per_step * 1e-3) / scale
+    achieved = work / (kernel_ms * 1e-3) / scale
     kname = op.kernel_name()
 
     unfused = None
@@ -255,9 +262,10 @@ def main(argv=None):
 
     sizes = kf.sizes_of(cfg)
     line = {
-        "metric": "fused-op TFLOP/s, % of MFMA peak, speedup vs own unfused kernel chain",
+        "metric": ("fused-op GB/s, % of HBM peak, speedup vs own unfused kernel chain" if rowwise else
+                   "fused-op TFLOP/s, % of MFMA peak, speedup vs own unfused kernel chain"),
         "value": round(value, 2),
-        "unit": "TFLOP/s",
+        "unit": "GB/s" if rowwise else "TFLOP/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
@@ -269,18 +277,18 @@ def main(argv=None):
         "data": "synthetic",
         "config": dict({"workload": cfg["workload"], "ops": "+".join(o[0] for o in cfg["ops"]),
                         "out_dtype": cfg["out_dtype"]}, **sizes),
-        "pct_mfma_peak": round(100.0 * value / peak, 2),
+        ("pct_hbm_peak" if rowwise else "pct_mfma_peak"): round(100.0 * value / peak, 2),
         "speedup_vs_unfused": None if not unfused or "speedup" not in unfused else round(unfused["speedup"], 3),
         "unfused": unfused,
         "roofline": {
-            "bound": "mfma",
+            "bound": "hbm" if rowwise else "mfma",
             "kernel": kname,
             "achieved": round(achieved, 2),
             "peak": peak,
-            "unit": "TFLOP/s",
+            "unit": "GB/s" if rowwise else "TFLOP/s",
             "frac": round(achieved / peak, 4),
             "kernel_us": round(kernel_ms * 1e3, 2),
-            "flops_per_launch": flops,
+            ("bytes_per_launch" if rowwise else "flops_per_launch"): work,
             "traffic": _traffic(kname, cfg["workload"]),
         },
         "cpu_baseline": cpu,

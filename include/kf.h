@@ -55,7 +55,13 @@ typedef enum kf_contraction {
   /* PyTorch Conv2d (cross-correlation), 3x3 kernel, stride 1, zero padding
      1, dilation 1, groups 1.  A = input [batch,cin,H,W] (NCHW), B = weight
      [cout,cin,3,3] (OIHW); h is [batch,cout,H,W]. */
-  KF_CONV2D_3X3 = 1
+  KF_CONV2D_3X3 = 1,
+  /* No contraction: h = A, an [M,N] row-major tensor (fp32 or bf16, any row
+     stride), and the op list runs over its rows -- the memory-bound
+     reduction chains (softmax, logsumexp, GroupNorm with their element-wise
+     neighbours).  No B input; K is ignored.  N <= 16384, N % 8 == 0;
+     GROUPNORM needs (N / groups) % 8 == 0. */
+  KF_ROWWISE = 2
 } kf_contraction;
 
 typedef enum kf_dtype {
@@ -82,15 +88,16 @@ typedef enum kf_op_kind {
   KF_OP_GROUPNORM = 10,    /* nn.GroupNorm over features: `groups` groups of
                               contiguous features per row, biased variance,
                               eps = p0, then gamma/beta affine
-                              (inputs fp32 [F] each). GEMM only.           */
+                              (inputs fp32 [F] each). GEMM or ROWWISE.     */
   KF_OP_RESIDUAL_ADD = 11, /* h += residual (input, same shape as output;
                               dtype = spec.residual_dtype)                  */
   KF_OP_MAXPOOL2X2 = 12,   /* MaxPool2d(2, stride 2) on the conv output;
                               CONV2D only, H and W even. Output shape
                               [batch,cout,H/2,W/2].                         */
-  KF_OP_ROW_SOFTMAX = 13,  /* softmax over the last axis; GEMM only; last op */
-  KF_OP_ROW_LOGSUMEXP = 14 /* log sum exp over the last axis; GEMM only; last
-                              op; output becomes fp32 [M]                   */
+  KF_OP_ROW_SOFTMAX = 13,  /* softmax over the last axis; GEMM or ROWWISE;
+                              last op                                       */
+  KF_OP_ROW_LOGSUMEXP = 14 /* log sum exp over the last axis; GEMM or
+                              ROWWISE; last op; output becomes fp32 [M]     */
 } kf_op_kind;
 
 typedef struct kf_op {
@@ -134,8 +141,9 @@ typedef struct kf_desc kf_desc;
 kf_status kf_create(const kf_op_spec* spec, kf_desc** out);
 
 /* Run the fused operation on `stream`.
-   inputs (in this order): A, B, then one slot per tensor the ops need, in op
-   order -- BIAS: bias; GROUPNORM: gamma, beta; RESIDUAL_ADD: residual.
+   inputs (in this order): A, B (no B for KF_ROWWISE), then one slot per
+   tensor the ops need, in op order -- BIAS: bias; GROUPNORM: gamma, beta;
+   RESIDUAL_ADD: residual.
    outputs: exactly one tensor (shape from kf_output_shape, dtype
    spec.out_dtype).  The descriptor's workspace is reused by every call, so
    at most one call per descriptor may be in flight at a time (use one

@@ -266,32 +266,9 @@ def op_row_logsumexp(h):
 # Chains
 # --------------------------------------------------------------------------
 
-def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
-    """Evaluate one fused chain in float64.
-
-    chain:   {"contraction": "gemm" | "conv2d_3x3", "in_dtype": "f32" | "bf16"
-              | "e4m3", "b_layout": "kn" | "nk", "scale_a": s_x, "scale_b": s_w,
-              "ops": [(name, *params), ...]}
-    tensors: raw storage: "a", "b" (in_dtype), "bias", "gamma", "beta" (f32),
-             "residual" (its own dtype given by chain["residual_dtype"]).
-    rows / images: evaluate only these output rows (GEMM) or batch entries
-             (conv); every op in scope is local to a row (GEMM) or to one
-             image (conv), so the selected slice is exact.
-    """
-    dt = chain["in_dtype"]
-    a = to_f64(tensors["a"], dt)
-    b = to_f64(tensors["b"], dt)
-    if dt == "e4m3":
-        a = a * float(np.float32(chain["scale_a"]))
-        b = b * float(np.float32(chain["scale_b"]))
-    if chain["contraction"] == "gemm":
-        h = gemm(a, b, chain.get("b_layout", "kn"), rows)
-        sel = rows
-    elif chain["contraction"] == "conv2d_3x3":
-        h = conv2d_3x3(a, b, images)
-        sel = images
-    else:
-        raise ValueError(chain["contraction"])
+def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel) -> np.ndarray:
+    """The op list of `chain`, in order, on the float64 contraction result h
+    (rows / images `sel` of the full result, or all of it)."""
     for op in chain["ops"]:
         name, params = op[0], op[1:]
         if name == "bias":
@@ -330,3 +307,38 @@ def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
         else:
             raise ValueError(f"unknown op {name!r}")
     return h
+
+
+def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
+    """Evaluate one fused chain in float64.
+
+    chain:   {"contraction": "gemm" | "conv2d_3x3" | "rowwise", "in_dtype": "f32" | "bf16"
+              | "e4m3", "b_layout": "kn" | "nk", "scale_a": s_x, "scale_b": s_w,
+              "ops": [(name, *params), ...]}
+    tensors: raw storage: "a", "b" (in_dtype; no "b" for "rowwise", whose h is
+             A itself), "bias", "gamma", "beta" (f32),
+             "residual" (its own dtype given by chain["residual_dtype"]).
+    rows / images: evaluate only these output rows (GEMM) or batch entries
+             (conv); every op in scope is local to a row (GEMM) or to one
+             image (conv), so the selected slice is exact.
+    """
+    dt = chain["in_dtype"]
+    a = to_f64(tensors["a"], dt)
+    if chain["contraction"] == "rowwise":
+        # no contraction: the ops run over the rows of A
+        h = a if rows is None else a[np.asarray(rows, dtype=np.int64)]
+        sel = rows
+        return _apply_ops(chain, tensors, h, sel)
+    b = to_f64(tensors["b"], dt)
+    if dt == "e4m3":
+        a = a * float(np.float32(chain["scale_a"]))
+        b = b * float(np.float32(chain["scale_b"]))
+    if chain["contraction"] == "gemm":
+        h = gemm(a, b, chain.get("b_layout", "kn"), rows)
+        sel = rows
+    elif chain["contraction"] == "conv2d_3x3":
+        h = conv2d_3x3(a, b, images)
+        sel = images
+    else:
+        raise ValueError(chain["contraction"])
+    return _apply_ops(chain, tensors, h, sel)

@@ -38,7 +38,7 @@ kf_status ok() {
   return KF_OK;
 }
 
-enum Variant { kVarGemmF32 = 0, kVarGemmBf16 = 1, kVarGemmFp8 = 2, kVarConvBf16 = 3 };
+enum Variant { kVarGemmF32 = 0, kVarGemmBf16 = 1, kVarGemmFp8 = 2, kVarConvBf16 = 3, kVarRowwise = 4 };
 
 struct Slot {
   int32_t dtype;
@@ -95,7 +95,7 @@ int match_chain(const kf_op_spec* s) {
 
 kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   if (!s) return fail(KF_ERR_INVALID_ARG, "spec is NULL");
-  if (s->contraction != KF_GEMM && s->contraction != KF_CONV2D_3X3)
+  if (s->contraction != KF_GEMM && s->contraction != KF_CONV2D_3X3 && s->contraction != KF_ROWWISE)
     return fail(KF_ERR_INVALID_ARG, "unknown contraction %d", s->contraction);
   if (s->in_dtype != KF_F32 && s->in_dtype != KF_BF16 && s->in_dtype != KF_FP8_E4M3)
     return fail(KF_ERR_INVALID_ARG, "unknown in_dtype %d", s->in_dtype);
@@ -148,7 +148,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       case KF_OP_ROW_SOFTMAX:
       case KF_OP_ROW_LOGSUMEXP:
         if (i != s->n_ops - 1) return fail(KF_ERR_UNSUPPORTED, "op %d: a row softmax/logsumexp must be the last op", i);
-        if (s->contraction != KF_GEMM) return fail(KF_ERR_UNSUPPORTED, "op %d: row ops need a GEMM", i);
+        if (s->contraction == KF_CONV2D_3X3) return fail(KF_ERR_UNSUPPORTED, "op %d: row ops need a GEMM or ROWWISE", i);
         ++n_red;
         d->red_index = i;
         d->epi_shape = kf::kEpiRow;
@@ -218,6 +218,35 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       if (d->tiles_n > kf::row_finish_max_tiles())
         return fail(KF_ERR_UNSUPPORTED, "row softmax/logsumexp supports N <= %d", kf::row_finish_max_tiles() * kf::gemm_mfma_tile_n());
     }
+  } else if (s->contraction == KF_ROWWISE) {
+    // no contraction: the op list over the rows of A [M, N]
+    if (dt != KF_F32 && dt != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "ROWWISE supports fp32 and bf16 inputs");
+    if (s->M < 0 || s->N < 1) return fail(KF_ERR_SHAPE, "ROWWISE needs M >= 0, N >= 1");
+    if (s->M > INT32_MAX) return fail(KF_ERR_UNSUPPORTED, "ROWWISE supports M < 2^31");
+    if (s->N > kf::rowwise_max_cols() || s->N % 8)
+      return fail(KF_ERR_UNSUPPORTED, "ROWWISE needs N %% 8 == 0 and N <= %d", kf::rowwise_max_cols());
+    if (has_gn) {
+      const kf_op& g = s->ops[d->red_index];
+      if (s->N % g.groups || (s->N / g.groups) % 8)
+        return fail(KF_ERR_UNSUPPORTED, "GROUPNORM (ROWWISE): N / groups must be a whole multiple of 8 columns");
+      d->gn_group = (int)(s->N / g.groups);
+    }
+    d->variant = kVarRowwise;
+    d->kernel_name = "kf_rowwise";
+    d->inputs.push_back(Slot{dt, 2, {s->M, s->N, 0, 0}, "A"});
+    for (int i = 0; i < s->n_ops; ++i) {
+      const int k = s->ops[i].kind;
+      if (k == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "bias"});
+      if (k == KF_OP_GROUPNORM) {
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "gamma"});
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "beta"});
+      }
+      if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0}, "residual"});
+    }
+    if (d->row_kind == KF_OP_ROW_LOGSUMEXP)
+      d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0}, "out"};
+    else
+      d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0}, "out"};
   } else {
     // 3x3 convolution, stride 1, zero padding 1, NCHW input / OIHW weight
     if (dt != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 supports bf16 inputs only");
@@ -349,7 +378,7 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
       delete d;
       return fail(KF_ERR_OOM, "workspace of %zu bytes could not be allocated", d->workspace_bytes);
     }
-  } else if (d->row_kind) {
+  } else if (d->row_kind && d->variant != kVarRowwise) {
     d->workspace_bytes = (size_t)std::max<int64_t>(spec->M, 1) * d->tiles_n * sizeof(float) * 2;
     if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
       (void)hipGetLastError();
@@ -409,6 +438,42 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
 
   const kf_op_spec& s = d->spec;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (s.contraction == KF_ROWWISE) {
+    if (s.M == 0) return ok();
+    kf::RowArgs r;
+    memset(&r, 0, sizeof(r));
+    r.a = inputs[0].data;
+    r.M = s.M;
+    r.N = s.N;
+    r.lda = inputs[0].stride[0];
+    r.in_bf16 = s.in_dtype == KF_BF16;
+    r.prog = d->prog;
+    r.gn_group = d->gn_group;
+    size_t slot = 1;
+    for (int i = 0; i < s.n_ops; ++i) {
+      const int k = s.ops[i].kind;
+      if (k == KF_OP_BIAS) r.bias = static_cast<const float*>(inputs[slot++].data);
+      if (k == KF_OP_GROUPNORM) {
+        r.gamma = static_cast<const float*>(inputs[slot++].data);
+        r.beta = static_cast<const float*>(inputs[slot++].data);
+      }
+      if (k == KF_OP_RESIDUAL_ADD) {
+        r.residual = inputs[slot].data;
+        r.ldr = inputs[slot].stride[0];
+        r.residual_bf16 = inputs[slot].dtype == KF_BF16;
+        ++slot;
+      }
+    }
+    r.out = outputs[0].data;
+    r.ldo = outputs[0].ndim == 2 ? outputs[0].stride[0] : 1;
+    r.out_bf16 = outputs[0].dtype == KF_BF16;
+    hipError_t e = hipSuccess;
+    if (ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
+    if (e == hipSuccess) e = kf::launch_rowwise(r, d->chain, hs);
+    if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
+    if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return ok();
+  }
   if (s.contraction == KF_GEMM) {
     if (s.M == 0) return ok();
     kf::GemmArgs a;
@@ -509,11 +574,16 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   const kf_op_spec& s = d->spec;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   const bool gemm = s.contraction == KF_GEMM;
-  if ((gemm && s.M == 0) || (!gemm && s.batch == 0)) return ok();
+  const bool rowwise = s.contraction == KF_ROWWISE;
+  const bool rows = gemm || rowwise;  // an [M, N] intermediate
+  if ((rows && s.M == 0) || (!rows && s.batch == 0)) return ok();
+  // the per-op kernels index [M, N] tensors as contiguous rows
+  if (rowwise && inputs[0].stride[0] != s.N)
+    return fail(KF_ERR_UNSUPPORTED, "the unfused ROWWISE chain needs A with row stride N");
 
   // intermediates: bf16 (fp32 for an fp32 chain), full contraction size
-  const bool ibf16 = d->variant != kVarGemmF32;
-  const int64_t n_full = gemm ? s.M * s.N : s.batch * s.cout * s.height * s.width;
+  const bool ibf16 = rowwise ? s.in_dtype == KF_BF16 : d->variant != kVarGemmF32;
+  const int64_t n_full = rows ? s.M * s.N : s.batch * s.cout * s.height * s.width;
   const size_t need = (size_t)n_full * (ibf16 ? 2 : 4);
   if (d->ubuf_bytes < need) {
     for (void*& b : d->ubuf) {
@@ -536,7 +606,13 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   bool cur_bf16 = s.n_ops ? ibf16 : out_bf16;
   hipError_t e = hipSuccess;
   size_t slot = 2;
-  if (gemm) {
+  if (rowwise) {
+    // no contraction: the first op reads A itself (an empty list copies it)
+    slot = 1;
+    cur = inputs[0].data;
+    cur_bf16 = s.in_dtype == KF_BF16;
+    if (!s.n_ops) e = kf::launch_unfused_elementwise(cur, cur_bf16, out, out_bf16, n_full, 0, 0.f, 0.f, nullptr, 1, 1, hs);
+  } else if (gemm) {
     kf::GemmArgs a;
     memset(&a, 0, sizeof(a));
     a.a = inputs[0].data;
@@ -586,7 +662,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     switch (op.kind) {
       case KF_OP_BIAS: {
         const float* bias = static_cast<const float*>(inputs[slot++].data);
-        const int64_t fdiv = gemm ? 1 : hh * ww, fmod = gemm ? s.N : s.cout;
+        const int64_t fdiv = rows ? 1 : hh * ww, fmod = rows ? s.N : s.cout;
         e = kf::launch_unfused_elementwise(cur, cur_bf16, dst, dst_bf16, n, op.kind, 0.f, 0.f, bias, fdiv, fmod, hs);
         break;
       }

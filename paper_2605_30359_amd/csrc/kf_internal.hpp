@@ -29,8 +29,8 @@ enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
 // is interpreted at run time.  The paper turns each operator into its own
 // specialised kernel; these are the chains of the benchmarked operators and
 // the plain building blocks, and every other chain runs interpreted.
-constexpr int kNumChains = 9;
-constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5};
+constexpr int kNumChains = 10;
+constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1};
 constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {},                                                                         // 0: interpreted
     {},                                                                         // 1: contraction only
@@ -41,6 +41,7 @@ constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {KF_OP_BIAS, KF_OP_HARDTANH, KF_OP_ROW_SOFTMAX},                           // 6: GEMM, hardtanh, softmax
     {KF_OP_BIAS, KF_OP_RELU, KF_OP_MAXPOOL2X2},                                // 7: conv, ReLU, max-pool
     {KF_OP_BIAS, KF_OP_SWISH, KF_OP_TANH, KF_OP_GELU_ERF, KF_OP_HARDTANH},     // 8: GEMM + activation chain
+    {KF_OP_ROW_SOFTMAX},                                                        // 9: softmax rows
 };
 
 // Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).
@@ -64,6 +65,24 @@ struct GemmArgs {
   int32_t gn_group;       // GroupNorm group width in columns (0 = none)
   int32_t red_index;      // position of the reduction op in prog (n if none)
   float scale;            // dequantisation factor applied to the accumulator
+};
+
+// Arguments of the row-wise kernel (no contraction: h = A).
+struct RowArgs {
+  const void* a;          // [M, lda]
+  int64_t M, N, lda;
+  int32_t in_bf16;
+  EpiProgram prog;
+  const float* bias;      // [N] or null
+  const float* gamma;     // [N] or null
+  const float* beta;      // [N] or null
+  const void* residual;   // [M, ldr] or null
+  int64_t ldr;
+  int32_t residual_bf16;
+  int32_t out_bf16;
+  void* out;              // [M, ldo] (or [M] for a row logsumexp)
+  int64_t ldo;
+  int32_t gn_group;       // GroupNorm group width in columns (0 = none)
 };
 
 // Arguments of the implicit-GEMM 3x3 convolution kernels.

@@ -14,6 +14,11 @@ hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, 
 int gemm_mfma_tile_m();
 int gemm_mfma_tile_n();
 
+// Row-wise op chain with no contraction (h = A), one workgroup per row;
+// N <= rowwise_max_cols(); `chain` as for the GEMM (0: interpreted).
+hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream);
+int rowwise_max_cols();
+
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);
 

@@ -74,6 +74,25 @@ CONFIGS = {
         ops=[("bias",), ("swish",), ("tanh",), ("gelu_erf",), ("hardtanh", -1.0, 1.0)],
         dist=dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1)),
     ),
+    # memory-bound reduction chains with no contraction (the paper's
+    # reduction-dominated category, Table 2): C3's epilogue and C5's softmax
+    # over stored [8192, 8192] bf16 activations
+    "F3": dict(
+        workload="rows_groupnorm_swish_residual_bf16",
+        contraction="rowwise", in_dtype="bf16", out_dtype="bf16",
+        M=8192, N=8192,
+        ops=[("groupnorm", 32, 1e-5), ("swish",), ("residual_add",)],
+        residual_dtype="bf16",
+        dist=dict(a=("normal", 1.0), gamma=("uniform", 0.5, 1.5), beta=("uniform", -0.1, 0.1),
+                  residual=("normal", 1.0)),
+    ),
+    "F4": dict(
+        workload="rows_softmax_bf16",
+        contraction="rowwise", in_dtype="bf16", out_dtype="bf16",
+        M=8192, N=8192,
+        ops=[("row_softmax",)],
+        dist=dict(a=("normal", 1.0)),
+    ),
 }
 
 BASE_SEED = 260530359
@@ -102,7 +121,10 @@ def chain(cfg: dict) -> dict:
 
 def flops(cfg: dict) -> int:
     """Algorithmic FLOPs: 2 per multiply-add of the contraction only (conv:
-    at every pre-pool output position).  Epilogue arithmetic is not counted."""
+    at every pre-pool output position).  Epilogue arithmetic is not counted
+    (a row-wise chain has none)."""
+    if cfg["contraction"] == "rowwise":
+        return 0
     if cfg["contraction"] == "gemm":
         return 2 * cfg["M"] * cfg["N"] * cfg["K"]
     return 2 * cfg["batch"] * cfg["H"] * cfg["W"] * cfg["cout"] * cfg["cin"] * 9
@@ -175,7 +197,24 @@ def _draw(rng, spec, shape, k_fan_in):
     raise ValueError(kind)
 
 
+def rowwise_bytes(cfg: dict) -> int:
+    """Algorithmic HBM bytes of a row-wise chain: A and each tensor input read
+    once, the output written once."""
+    M, N = cfg["M"], cfg["N"]
+    es = {"f32": 4, "bf16": 2}
+    names = [op[0] for op in cfg["ops"]]
+    b = M * N * es[cfg["in_dtype"]]
+    b += 4 * N * (("bias" in names) + 2 * ("groupnorm" in names))
+    if "residual_add" in names:
+        b += M * N * es[cfg.get("residual_dtype", "bf16")]
+    b += 4 * M if names and names[-1] == "row_logsumexp" else M * N * es[cfg["out_dtype"]]
+    return b
+
+
 def shapes(cfg: dict) -> dict:
+    if cfg["contraction"] == "rowwise":
+        M, N = cfg["M"], cfg["N"]
+        return dict(a=(M, N), bias=(N,), gamma=(N,), beta=(N,), residual=(M, N), fan_in=N)
     if cfg["contraction"] == "gemm":
         M, N, K = cfg["M"], cfg["N"], cfg["K"]
         b = (K, N) if cfg.get("b_layout", "kn") == "kn" else (N, K)
@@ -201,7 +240,7 @@ def generate(cfg: dict, seed: int | None = None) -> dict:
     names = [op[0] for op in cfg["ops"]]
     out = {}
     raw_a = _draw(rng, dist["a"], shp["a"], shp["fan_in"])
-    raw_b = _draw(rng, dist["b"], shp["b"], shp["fan_in"])
+    raw_b = _draw(rng, dist["b"], shp["b"], shp["fan_in"]) if "b" in shp else None
     if "bias" in names:
         out["bias"] = _draw(rng, dist["bias"], shp["bias"], shp["fan_in"])
     if "groupnorm" in names:
@@ -210,7 +249,11 @@ def generate(cfg: dict, seed: int | None = None) -> dict:
     if "residual_add" in names:
         out["residual"] = f32_to_bf16_bits(_draw(rng, dist["residual"], shp["residual"], shp["fan_in"]))
     dt = cfg["in_dtype"]
-    if dt == "f32":
+    if raw_b is None:  # a row-wise chain: A only
+        if dt not in ("f32", "bf16"):
+            raise ValueError(dt)
+        out["a"] = raw_a if dt == "f32" else f32_to_bf16_bits(raw_a)
+    elif dt == "f32":
         out["a"], out["b"] = raw_a, raw_b
     elif dt == "bf16":
         out["a"], out["b"] = f32_to_bf16_bits(raw_a), f32_to_bf16_bits(raw_b)

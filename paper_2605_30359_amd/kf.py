@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_PKG, "libkf.so")
 # ---------------------------------------------------------------- C mirror
 
 KF_OK, KF_ERR_INVALID_ARG, KF_ERR_SHAPE, KF_ERR_UNSUPPORTED, KF_ERR_NO_DEVICE, KF_ERR_OOM, KF_ERR_HIP = range(7)
-KF_GEMM, KF_CONV2D_3X3 = 0, 1
+KF_GEMM, KF_CONV2D_3X3, KF_ROWWISE = 0, 1, 2
+CONTRACTIONS = {"gemm": KF_GEMM, "conv2d_3x3": KF_CONV2D_3X3, "rowwise": KF_ROWWISE}
 KF_F32, KF_BF16, KF_FP8_E4M3 = 0, 1, 2
 KF_LAYOUT_KN, KF_LAYOUT_NK = 0, 1
 KF_MAX_OPS = 8
@@ -122,7 +123,7 @@ def _check(status: int):
 def make_spec(chain: dict, *, M=0, N=0, K=0, batch=0, cin=0, H=0, W=0, cout=0) -> KfOpSpec:
     """Fill a kf_op_spec from a chain description (see paper_2605_30359_amd.inputs)."""
     s = KfOpSpec()
-    s.contraction = KF_GEMM if chain["contraction"] == "gemm" else KF_CONV2D_3X3
+    s.contraction = CONTRACTIONS[chain["contraction"]]
     s.in_dtype = DTYPES[chain["in_dtype"]]
     s.out_dtype = DTYPES[chain.get("out_dtype", "f32")]
     s.b_layout = KF_LAYOUT_NK if chain.get("b_layout", "kn") == "nk" else KF_LAYOUT_KN
@@ -149,8 +150,9 @@ def make_spec(chain: dict, *, M=0, N=0, K=0, batch=0, cin=0, H=0, W=0, cout=0) -
 
 
 def input_names(chain: dict) -> list:
-    """Input slot order: A, B, then the tensors the ops need, in op order."""
-    names = ["a", "b"]
+    """Input slot order: A, B (no B for a row-wise chain), then the tensors
+    the ops need, in op order."""
+    names = ["a"] if chain["contraction"] == "rowwise" else ["a", "b"]
     for op in chain["ops"]:
         if op[0] == "bias":
             names.append("bias")
@@ -164,6 +166,8 @@ def input_names(chain: dict) -> list:
 def sizes_of(cfg: dict) -> dict:
     if cfg["contraction"] == "gemm":
         return dict(M=cfg["M"], N=cfg["N"], K=cfg["K"])
+    if cfg["contraction"] == "rowwise":
+        return dict(M=cfg["M"], N=cfg["N"])
     return dict(batch=cfg["batch"], cin=cfg["cin"], H=cfg["H"], W=cfg["W"], cout=cfg["cout"])
 
 

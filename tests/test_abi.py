@@ -197,3 +197,28 @@ def test_struct_offsets_match_c_compiler(tmp_path):
     got = [int(x) for x in subprocess.check_output([str(exe)]).split()]
     assert got == want
 
+
+
+
+def test_rowwise_validation():
+    base = dict(M=64, N=1024)
+    cases = [
+        (dict(N=1020), kf.KF_ERR_UNSUPPORTED),                              # N % 8
+        (dict(N=16392), kf.KF_ERR_UNSUPPORTED),                             # too wide
+        (dict(ops=[("groupnorm", 3, 1e-5)]), kf.KF_ERR_UNSUPPORTED),        # N % groups
+        (dict(ops=[("groupnorm", 256, 1e-5)]), kf.KF_ERR_UNSUPPORTED),      # 4-column groups
+        (dict(ops=[("maxpool2x2",)]), kf.KF_ERR_UNSUPPORTED),
+        (dict(ops=[("row_softmax",), ("relu",)]), kf.KF_ERR_UNSUPPORTED),   # row op not last
+        (dict(in_dtype="e4m3"), kf.KF_ERR_UNSUPPORTED),
+        (dict(M=-1), kf.KF_ERR_SHAPE),
+    ]
+    for kw, status in cases:
+        cfg = inputs.config("F3", **dict(base, **kw))
+        st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+        assert st == status, (kw, st, kf.last_error())
+
+
+def test_rowwise_input_slots():
+    ch = inputs.chain(inputs.config("F3"))
+    assert kf.input_names(ch) == ["a", "gamma", "beta", "residual"]
+    assert kf.input_names(inputs.chain(inputs.config("F4"))) == ["a"]

@@ -291,6 +291,44 @@ def test_f1_full_config_sampled_rows():
     err = check(cfg, t, out, rows=sample_rows(cfg["M"], 48))
     print(f"F1 full err {err:.3e}")
 
+
+# ------------------------------------------ row-wise chains (no contraction)
+
+_ROW_DIST = dict(a=("normal", 1.0), bias=("uniform", -0.1, 0.1), gamma=("uniform", 0.5, 1.5),
+                 beta=("uniform", -0.1, 0.1), residual=("normal", 1.0))
+
+
+@pytest.mark.parametrize("M,N,ops,in_dtype,out_dtype", [
+    (37, 1024, [("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)], "bf16", "bf16"),  # 128-column groups
+    (5, 8192, [("groupnorm", 32, 1e-5), ("swish",), ("residual_add",)], "bf16", "bf16"),  # F3 rows
+    (9, 2048, [("groupnorm", 1, 1e-5)], "f32", "f32"),                                    # one group per row
+    (9, 2048, [("groupnorm", 256, 1e-5), ("relu",)], "bf16", "f32"),                      # 8-column groups
+    (33, 16384, [("row_softmax",)], "bf16", "bf16"),                                      # widest row
+    (3, 8, [("row_softmax",)], "f32", "f32"),                                             # narrowest row
+    (70, 3000, [("bias",), ("gelu_tanh",), ("scale", 0.5), ("row_logsumexp",)], "bf16", "f32"),
+    (16, 4104, [("bias",), ("tanh",), ("residual_add",), ("hardtanh", -0.5, 0.5)], "f32", "bf16"),
+    (2, 1024, [], "bf16", "bf16"),                                                        # a copy
+])
+def test_rowwise_chains(M, N, ops, in_dtype, out_dtype):
+    _torch()
+    cfg = inputs.config("F3", M=M, N=N, ops=ops, in_dtype=in_dtype, out_dtype=out_dtype, dist=_ROW_DIST)
+    t = inputs.generate(cfg, seed=M + N)
+    op, out = run_gpu(cfg, t)
+    assert op.kernel_name() == "kf_rowwise"
+    tol = TOL["bf16"] if "bf16" in (in_dtype, out_dtype) else TOL["f32"]
+    err = check(cfg, t, out, tol=tol)
+    print(f"rowwise {M}x{N} {[o[0] for o in ops]} err {err:.3e}")
+
+
+@pytest.mark.parametrize("name", ["F3", "F4"])
+def test_rowwise_full_config_sampled_rows(name):
+    _torch()
+    cfg = inputs.config(name)
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out, rows=sample_rows(cfg["M"], 64))
+    print(f"{name} full err {err:.3e}")
+
 # ------------------------------------------------------------ conv (C4)
 
 @pytest.mark.parametrize("batch,H,ops", [
@@ -393,6 +431,9 @@ def test_c4_integer_bit_exact_tile_ranges():
     ("C3", dict(M=300, N=512, K=136, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
     ("C4", dict(batch=2, H=8)),
     ("C5", dict(M=300, N=1040, K=208)),
+    ("F1", dict(M=300, N=520, K=136)),
+    ("F3", dict(M=37, N=1024, ops=[("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)])),
+    ("F4", dict(M=9, N=2048)),
 ])
 def test_unfused_chain_parity(name, kw):
     """The one-kernel-per-op comparator must compute the same chain.  Its
@@ -456,6 +497,8 @@ def test_epilogue_operand_paths(name, kw, res_f32):
     ("C5", dict(M=300, N=528, K=160)),                                     # fp8, bias, hardtanh, softmax
     ("C4", dict(batch=2, H=10)),                                           # conv, bias, ReLU, pool (pool first)
     ("F1", dict(M=300, N=520, K=136)),                                     # bias, swish, tanh, GELU(erf), hardtanh
+    ("F3", dict(M=37, N=2048)),                                            # rows: GroupNorm, swish, residual
+    ("F4", dict(M=37, N=4104)),                                            # rows: softmax
 ])
 def test_specialised_chain_matches_interpreted(name, kw):
     """The benchmarked op lists run an epilogue generated for that exact

@@ -360,6 +360,31 @@ def test_chain_f1_zero_weight_and_torch():
     assert -0.1068 < lo < -0.1066
     assert out.min() >= lo and out.max() < 0.8414
 
+
+def test_rowwise_chains_match_torch():
+    """No contraction: the op list over the rows of A.  GroupNorm + swish +
+    residual (the F3 chain) and softmax / logsumexp rows against torch's
+    CPU float64 modules, on a subset of rows as well."""
+    cfg, t = _small("F3", M=7, N=1024)
+    a = _t(oracle.decode_bf16(t["a"]))
+    r = _t(oracle.decode_bf16(t["residual"]))
+    out = oracle.run_chain(inputs.chain(cfg), t)
+    gn = F.group_norm(a, 32, _t(t["gamma"]), _t(t["beta"]), eps=1e-5)
+    assert np.allclose(out, (F.silu(gn) + r).numpy(), rtol=1e-12, atol=1e-12)
+    rows = np.array([5, 0, 3])
+    assert np.array_equal(oracle.run_chain(inputs.chain(cfg), t, rows=rows), out[rows])
+    cfg, t = _small("F4", M=5, N=2048)
+    a = _t(oracle.decode_bf16(t["a"]))
+    out = oracle.run_chain(inputs.chain(cfg), t)
+    assert np.allclose(out, torch.softmax(a, -1).numpy(), rtol=1e-12, atol=1e-15)
+    assert np.allclose(out.sum(-1), 1.0, atol=1e-13)
+    cfg = inputs.config("F4", M=5, N=2048, in_dtype="f32", out_dtype="f32",
+                        ops=[("bias",), ("relu",), ("row_logsumexp",)], dist=dict(a=("normal", 1.0), bias=("uniform", -0.1, 0.1)))
+    t = inputs.generate(cfg, seed=5)
+    out = oracle.run_chain(inputs.chain(cfg), t)
+    ref = torch.logsumexp(F.relu(_t(t["a"]) + _t(t["bias"])), -1).numpy()
+    assert np.allclose(out, ref, rtol=1e-13)
+
 def test_chain_c3_zero_weight_and_torch():
     cfg, t = _small("C3", M=6, N=512, K=96, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
     ch = inputs.chain(cfg)
