@@ -11,7 +11,9 @@ candidate kernel when its outputs are numerically equivalent to that reference.
 The operators in scope are the fusion patterns named in Appendix A ("Operator
 Fusion": matmul + activation, normalisation + activation, softmax; "Algorithmic
 Optimization": online softmax, reduced precision): a dense contraction (GEMM,
-or a 3x3 convolution) followed by an ordered list of epilogue ops.  The method
+a 3x3 convolution, or the 3x3x3 convolution of the Conv3d -> channel softmax ->
+max-pool operator of the Appendix C case study) followed by an ordered list of
+epilogue ops.  The method
 reaches the plain result of that reference, so this oracle is the plain
 definition of each step, applied in the listed order, in float64:
 
@@ -67,6 +69,8 @@ def _load():
         lib.kfo_gemm_rows.restype = None
         lib.kfo_conv2d_3x3.argtypes = [p, p, i64, i64, i64, i64, i64, p, i64, p]
         lib.kfo_conv2d_3x3.restype = None
+        lib.kfo_conv3d_3x3x3.argtypes = [p, p, i64, i64, i64, i64, i64, i64, p, i64, p]
+        lib.kfo_conv3d_3x3x3.restype = None
         lib.kfo_max_threads.argtypes = []
         lib.kfo_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -163,14 +167,31 @@ def conv2d_3x3(x: np.ndarray, w: np.ndarray, images=None) -> np.ndarray:
     return out
 
 
+def conv3d_3x3x3(x: np.ndarray, w: np.ndarray, images=None) -> np.ndarray:
+    """PyTorch Conv3d (cross-correlation) with a 3x3x3 kernel, stride 1, no
+    padding, no bias: x[Nb,Cin,D,H,W], w[Cout,Cin,3,3,3] ->
+    [n_sel,Cout,D-2,H-2,W-2]."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    Nb, Cin, D, H, W = x.shape
+    Cout = w.shape[0]
+    assert w.shape == (Cout, Cin, 3, 3, 3) and min(D, H, W) >= 3
+    images = np.arange(Nb, dtype=np.int64) if images is None else np.ascontiguousarray(images, dtype=np.int64)
+    out = np.empty((images.size, Cout, D - 2, H - 2, W - 2), dtype=np.float64)
+    if images.size:
+        _load().kfo_conv3d_3x3x3(x.ctypes.data, w.ctypes.data, Nb, Cin, D, H, W, Cout,
+                                 images.ctypes.data, images.size, out.ctypes.data)
+    return out
+
+
 # --------------------------------------------------------------------------
 # Epilogue ops (each the plain definition; float64 throughout)
 # --------------------------------------------------------------------------
 
 def _channel_shape(h: np.ndarray) -> tuple:
-    # Per-channel parameters broadcast along axis 1 of an NCHW tensor, and
-    # along the last axis (output features) of a 2-D GEMM output.
-    return (1, -1, 1, 1) if h.ndim == 4 else (1, -1)
+    # Per-channel parameters broadcast along axis 1 of an NCHW / NCDHW
+    # tensor, and along the last axis (output features) of a 2-D GEMM output.
+    return (1, -1) + (1,) * (h.ndim - 2) if h.ndim >= 4 else (1, -1)
 
 
 def op_bias(h, bias):
@@ -249,6 +270,23 @@ def op_maxpool2x2(h):
     return v.max(axis=(3, 5))
 
 
+def op_channel_softmax(h):
+    """Softmax over the channel axis (axis 1) at every position of an NCDHW
+    tensor, as torch.softmax(h, dim=1): e^(h - m) / sum_c e^(h - m), m the
+    maximum over the channels at that position."""
+    m = h.max(axis=1, keepdims=True)
+    e = np.exp(h - m)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def op_maxpool3d2(h):
+    """MaxPool3d(kernel 2, stride 2, no padding, floor mode) on NCDHW."""
+    n, c, D, H, W = h.shape
+    Do, Ho, Wo = D // 2, H // 2, W // 2
+    v = h[:, :, :2 * Do, :2 * Ho, :2 * Wo].reshape(n, c, Do, 2, Ho, 2, Wo, 2)
+    return v.max(axis=(3, 5, 7))
+
+
 def op_row_softmax(h):
     """Softmax over the last axis: e^(h - m) / sum e^(h - m), m the row max."""
     m = h.max(axis=-1, keepdims=True)
@@ -300,6 +338,10 @@ def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel) -> np.ndarray:
             h = op_residual_add(h, r)
         elif name == "maxpool2x2":
             h = op_maxpool2x2(h)
+        elif name == "channel_softmax":
+            h = op_channel_softmax(h)
+        elif name == "maxpool3d2":
+            h = op_maxpool3d2(h)
         elif name == "row_softmax":
             h = op_row_softmax(h)
         elif name == "row_logsumexp":
@@ -312,7 +354,8 @@ def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel) -> np.ndarray:
 def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
     """Evaluate one fused chain in float64.
 
-    chain:   {"contraction": "gemm" | "conv2d_3x3" | "rowwise", "in_dtype": "f32" | "bf16"
+    chain:   {"contraction": "gemm" | "conv2d_3x3" | "conv3d_3x3x3" | "rowwise",
+              "in_dtype": "f32" | "bf16"
               | "e4m3", "b_layout": "kn" | "nk", "scale_a": s_x, "scale_b": s_w,
               "ops": [(name, *params), ...]}
     tensors: raw storage: "a", "b" (in_dtype; no "b" for "rowwise", whose h is
@@ -338,6 +381,9 @@ def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
         sel = rows
     elif chain["contraction"] == "conv2d_3x3":
         h = conv2d_3x3(a, b, images)
+        sel = images
+    elif chain["contraction"] == "conv3d_3x3x3":
+        h = conv3d_3x3x3(a, b, images)
         sel = images
     else:
         raise ValueError(chain["contraction"])

@@ -17,6 +17,12 @@
  *                   out[n][co][oh][ow] = sum_{ci,kh,kw}
  *                       in[n][ci][oh+kh-1][ow+kw-1] * w[co][ci][kh][kw]
  *                   with in[...] = 0 outside [0,H) x [0,W).
+ *   kfo_conv3d_3x3x3 PyTorch Conv3d cross-correlation, 3x3x3 kernel, stride 1,
+ *                   no padding, NCDHW input / OIDHW weight (the conv of the
+ *                   paper's Conv3d -> softmax -> max-pool case study,
+ *                   Appendix C):
+ *                   out[n][co][od][oh][ow] = sum_{ci,kd,kh,kw}
+ *                       in[n][ci][od+kd][oh+kh][ow+kw] * w[co][ci][kd][kh][kw].
  *
  * Every sum runs over its index in ascending order in double precision; no
  * blocking, reordering or fusion is applied.  Rows (GEMM) or images (conv)
@@ -91,6 +97,47 @@ void kfo_conv2d_3x3(const double* in, const double* w, int64_t Nb,
             }
           }
           o[oh * W + ow] = s;
+        }
+      }
+    }
+  }
+}
+
+/* images[t] selects which batch entry to compute; out is nimg x Cout x Do x
+ * Ho x Wo with Do = D-2, Ho = H-2, Wo = W-2.  PyTorch Conv3d (the 3-D
+ * cross-correlation) with a 3x3x3 kernel, stride 1, no padding, dilation 1,
+ * groups 1, NCDHW input / OIDHW weight:
+ *   out[n][co][od][oh][ow] = sum_{ci,kd,kh,kw}
+ *       in[n][ci][od+kd][oh+kh][ow+kw] * w[co][ci][kd][kh][kw]
+ * Every input index stays inside the volume, so no padding value enters. */
+void kfo_conv3d_3x3x3(const double* in, const double* w, int64_t Nb,
+                      int64_t Cin, int64_t D, int64_t H, int64_t W,
+                      int64_t Cout, const int64_t* images, int64_t nimg,
+                      double* out) {
+  (void)Nb;
+  const int64_t Do = D - 2, Ho = H - 2, Wo = W - 2;
+  const int64_t vol = D * H * W, ovol = Do * Ho * Wo;
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int64_t t = 0; t < nimg; ++t) {
+    for (int64_t co = 0; co < Cout; ++co) {
+      const double* img = in + images[t] * Cin * vol;
+      double* o = out + (t * Cout + co) * ovol;
+      for (int64_t od = 0; od < Do; ++od) {
+        for (int64_t oh = 0; oh < Ho; ++oh) {
+          for (int64_t ow = 0; ow < Wo; ++ow) {
+            double s = 0.0;
+            for (int64_t ci = 0; ci < Cin; ++ci) {
+              for (int64_t kd = 0; kd < 3; ++kd) {
+                for (int64_t kh = 0; kh < 3; ++kh) {
+                  for (int64_t kw = 0; kw < 3; ++kw) {
+                    s += img[ci * vol + ((od + kd) * H + (oh + kh)) * W + (ow + kw)] *
+                         w[(((co * Cin + ci) * 3 + kd) * 3 + kh) * 3 + kw];
+                  }
+                }
+              }
+            }
+            o[(od * Ho + oh) * Wo + ow] = s;
+          }
         }
       }
     }

@@ -74,6 +74,17 @@ CONFIGS = {
         ops=[("bias",), ("swish",), ("tanh",), ("gelu_erf",), ("hardtanh", -1.0, 1.0)],
         dist=dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1)),
     ),
+    # the Conv3d -> channel softmax -> MaxPool3d -> MaxPool3d operator of the
+    # paper's case study (Appendix C), with the conv's bias; the paper gives
+    # no sizes, so these are chosen for one GPU: 16 volumes of 16 channels,
+    # each 34 x 66 x 66, and 64 output channels
+    "F2": dict(
+        workload="conv3d_bias_channelsoftmax_maxpool3d_x2_bf16",
+        contraction="conv3d_3x3x3", in_dtype="bf16", out_dtype="bf16",
+        batch=16, cin=16, D=34, H=66, W=66, cout=64,
+        ops=[("bias",), ("channel_softmax",), ("maxpool3d2",), ("maxpool3d2",)],
+        dist=dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1)),
+    ),
     # memory-bound reduction chains with no contraction (the paper's
     # reduction-dominated category, Table 2): C3's epilogue and C5's softmax
     # over stored [8192, 8192] bf16 activations
@@ -103,6 +114,16 @@ def default_seed(name: str) -> int:
     return BASE_SEED + int(name[1:]) + (100 if name.startswith("F") else 0)
 
 
+def conv3d_pooled_shape(cfg: dict) -> tuple:
+    """Output shape of a conv3d chain: [batch, cout, D', H', W'] after the
+    valid 3x3x3 conv and each MaxPool3d(2) (floor mode) of the op list."""
+    d, h, w = cfg["D"] - 2, cfg["H"] - 2, cfg["W"] - 2
+    for op in cfg["ops"]:
+        if op[0] == "maxpool3d2":
+            d, h, w = d // 2, h // 2, w // 2
+    return (cfg["batch"], cfg["cout"], d, h, w)
+
+
 def config(name: str, **overrides) -> dict:
     """A copy of workload `name` with shape fields overridden (M, N, K, batch,
     cin, H, W, cout, ops, b_layout, ...)."""
@@ -127,6 +148,9 @@ def flops(cfg: dict) -> int:
         return 0
     if cfg["contraction"] == "gemm":
         return 2 * cfg["M"] * cfg["N"] * cfg["K"]
+    if cfg["contraction"] == "conv3d_3x3x3":
+        outs = cfg["batch"] * (cfg["D"] - 2) * (cfg["H"] - 2) * (cfg["W"] - 2)
+        return 2 * outs * cfg["cout"] * cfg["cin"] * 27
     return 2 * cfg["batch"] * cfg["H"] * cfg["W"] * cfg["cout"] * cfg["cin"] * 9
 
 
@@ -220,6 +244,9 @@ def shapes(cfg: dict) -> dict:
         b = (K, N) if cfg.get("b_layout", "kn") == "kn" else (N, K)
         return dict(a=(M, K), b=b, bias=(N,), gamma=(N,), beta=(N,), residual=(M, N), fan_in=K)
     nb, ci, H, W, co = cfg["batch"], cfg["cin"], cfg["H"], cfg["W"], cfg["cout"]
+    if cfg["contraction"] == "conv3d_3x3x3":
+        D = cfg["D"]
+        return dict(a=(nb, ci, D, H, W), b=(co, ci, 3, 3, 3), bias=(co,), fan_in=ci * 27)
     return dict(a=(nb, ci, H, W), b=(co, ci, 3, 3), bias=(co,), gamma=(co,), beta=(co,),
                 residual=(nb, co, H // 2, W // 2), fan_in=ci * 9)
 

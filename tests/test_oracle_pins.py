@@ -450,3 +450,100 @@ def test_chain_c5_uniform_rows_sum_and_torch():
     # saturated rows (all logits >= 1 after the clamp) are uniform
     big = dict(t, bias=np.full_like(t["bias"], 1e6))
     assert np.allclose(oracle.run_chain(ch, big), 1.0 / 8192, rtol=1e-14)
+
+
+# ------------------------------------------------ Conv3d -> softmax -> pools
+
+def _brute_conv3d(x, w):
+    nb, ci, D, H, W = x.shape
+    co = w.shape[0]
+    out = np.zeros((nb, co, D - 2, H - 2, W - 2))
+    for n in range(nb):
+        for o in range(co):
+            for d in range(D - 2):
+                for i in range(H - 2):
+                    for j in range(W - 2):
+                        s = 0.0
+                        for c in range(ci):
+                            for kd in range(3):
+                                for kh in range(3):
+                                    for kw in range(3):
+                                        s += x[n, c, d + kd, i + kh, j + kw] * w[o, c, kd, kh, kw]
+                        out[n, o, d, i, j] = s
+    return out
+
+
+def test_conv3d_brute_force_tiny():
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((1, 2, 4, 5, 6))
+    w = rng.standard_normal((3, 2, 3, 3, 3))
+    assert np.allclose(oracle.conv3d_3x3x3(x, w), _brute_conv3d(x, w), atol=1e-13)
+
+
+def test_conv3d_matches_torch_scipy_and_image_selection():
+    from scipy.signal import correlate
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((3, 4, 6, 7, 9))
+    w = rng.standard_normal((5, 4, 3, 3, 3))
+    out = oracle.conv3d_3x3x3(x, w)
+    ref = F.conv3d(_t(x), _t(w)).numpy()
+    assert np.allclose(out, ref, atol=1e-12)
+    # the same cross-correlation from scipy's n-d routine, one (co, ci) pair at a time
+    sp = np.stack([np.stack([sum(correlate(x[n, c], w[o, c], mode="valid") for c in range(4))
+                             for o in range(5)]) for n in range(3)])
+    assert np.allclose(out, sp, atol=1e-12)
+    assert np.allclose(oracle.conv3d_3x3x3(x, w, images=[2, 0]), ref[[2, 0]], atol=1e-12)
+
+
+def test_conv3d_single_taps_shift_the_input():
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((2, 3, 5, 6, 7))
+    for (kd, kh, kw) in [(1, 1, 1), (0, 0, 0), (2, 0, 1)]:
+        w = np.zeros((3, 3, 3, 3, 3))
+        for c in range(3):
+            w[c, c, kd, kh, kw] = 1.0
+        # out[od, oh, ow] = in[od + kd, oh + kh, ow + kw]
+        exp = x[:, :, kd:kd + 3, kh:kh + 4, kw:kw + 5]
+        assert np.array_equal(oracle.conv3d_3x3x3(x, w), exp)
+
+
+def test_channel_softmax_and_maxpool3d_match_torch():
+    rng = np.random.default_rng(24)
+    h = rng.standard_normal((2, 6, 4, 6, 8)) * 3
+    s = oracle.op_channel_softmax(h)
+    assert np.allclose(s, torch.softmax(_t(h), dim=1).numpy(), rtol=1e-13, atol=0)
+    assert np.allclose(s.sum(axis=1), 1.0, atol=1e-14)
+    assert np.array_equal(oracle.op_maxpool3d2(h), F.max_pool3d(_t(h), 2).numpy())
+    g = rng.standard_normal((1, 2, 5, 7, 9))   # floor mode drops the last plane/row/col
+    assert np.array_equal(oracle.op_maxpool3d2(g), F.max_pool3d(_t(g), 2).numpy())
+    # two 2x pools are one max over aligned 4x4x4 blocks
+    two = oracle.op_maxpool3d2(oracle.op_maxpool3d2(h[:, :, :4, :4, :8]))
+    blocks = h[:, :, :4, :4, :8].reshape(2, 6, 1, 4, 1, 4, 2, 4).max(axis=(3, 5, 7))
+    assert np.array_equal(two, blocks)
+
+
+def test_chain_f2_uniform_bias_only_invariants_and_torch():
+    cfg, t = _small("F2", batch=2, cin=16, D=7, H=9, W=11, cout=64)
+    ch = inputs.chain(cfg)
+    assert inputs.conv3d_pooled_shape(cfg) == (2, 64, 1, 1, 2)
+    # W = 0, b = 0: uniform 1/64
+    z = dict(t, b=np.zeros_like(t["b"]), bias=np.zeros_like(t["bias"]))
+    out = oracle.run_chain(ch, z)
+    assert out.shape == (2, 64, 1, 1, 2)
+    assert np.all(out == GOLDEN["channel_softmax_uniform_64"]["value"])
+    # W = 0: every position holds softmax(bias), whatever the pooling
+    zb = dict(t, b=np.zeros_like(t["b"]))
+    bb = t["bias"].astype(np.float64)
+    sm = np.exp(bb - bb.max()) / np.exp(bb - bb.max()).sum()
+    assert np.allclose(oracle.run_chain(ch, zb), np.broadcast_to(sm[None, :, None, None, None], out.shape),
+                       rtol=1e-14, atol=0)
+    # invariants of max over positions of a per-position distribution:
+    # every channel-sum of a pooled cell is >= 1 and its largest entry >= 1/C
+    out = oracle.run_chain(ch, t)
+    assert np.all(out.sum(axis=1) >= 1.0 - 1e-12) and np.all(out.max(axis=1) >= 1.0 / 64 - 1e-15)
+    assert np.all(out.sum(axis=1) <= 64.0)
+    x = _t(oracle.decode_bf16(t["a"]))
+    w = _t(oracle.decode_bf16(t["b"]))
+    ref = F.max_pool3d(F.max_pool3d(torch.softmax(F.conv3d(x, w, _t(bb)), dim=1), 2), 2).numpy()
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-15)
+    assert np.allclose(oracle.run_chain(ch, t, images=[1]), ref[[1]], rtol=1e-12, atol=1e-15)
