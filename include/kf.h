@@ -16,8 +16,10 @@
  * Conventions
  *   - All tensors are device memory (hipMalloc'd or torch-allocated) owned
  *     by the caller; the library never frees or reallocates them.
- *   - Strides are in elements.  The innermost stride must be 1 and every
- *     base pointer 16-byte aligned (the kernels use 128-bit loads).
+ *   - Strides are in elements.  The innermost stride must be 1 (the
+ *     channels-last KF_CONV3D_3X3X3 input is the one exception, described
+ *     there) and every base pointer 16-byte aligned (the kernels use 128-bit
+ *     loads).
  *   - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *     Calls are asynchronous: launch errors are returned, device faults
  *     surface at the caller's next synchronisation on that stream.
@@ -61,7 +63,17 @@ typedef enum kf_contraction {
      reduction chains (softmax, logsumexp, GroupNorm with their element-wise
      neighbours).  No B input; K is ignored.  N <= 16384, N % 8 == 0;
      GROUPNORM needs (N / groups) % 8 == 0. */
-  KF_ROWWISE = 2
+  KF_ROWWISE = 2,
+  /* PyTorch Conv3d (3-D cross-correlation), 3x3x3 kernel, stride 1, no
+     padding (Conv3d's default), dilation 1, groups 1 -- the convolution of
+     the Conv3d -> softmax -> max-pool operator in the paper's case study
+     (Appendix C).  A = input [batch,cin,depth,height,width] stored
+     channels-last (torch.channels_last_3d: strides [D*H*W*cin, 1, H*W*cin,
+     W*cin, cin]), B = weight [cout,cin,3,3,3] contiguous (OIDHW); h is
+     [batch,cout,depth-2,height-2,width-2].  bf16 in and out; built for
+     cin = 16 and cout = 64 (the whole channel axis in one tile, so a channel
+     softmax is tile-local). */
+  KF_CONV3D_3X3X3 = 3
 } kf_contraction;
 
 typedef enum kf_dtype {
@@ -96,8 +108,16 @@ typedef enum kf_op_kind {
                               [batch,cout,H/2,W/2].                         */
   KF_OP_ROW_SOFTMAX = 13,  /* softmax over the last axis; GEMM or ROWWISE;
                               last op                                       */
-  KF_OP_ROW_LOGSUMEXP = 14 /* log sum exp over the last axis; GEMM or
+  KF_OP_ROW_LOGSUMEXP = 14,/* log sum exp over the last axis; GEMM or
                               ROWWISE; last op; output becomes fp32 [M]     */
+  KF_OP_CHANNEL_SOFTMAX = 15,/* softmax over the output channels at every
+                              position (torch.softmax(h, dim=1));
+                              CONV3D_3X3X3 only, at most once               */
+  KF_OP_MAXPOOL3D_2 = 16   /* MaxPool3d(2): kernel 2, stride 2, no padding,
+                              floor mode; CONV3D_3X3X3 only, after every
+                              other op.  The fused kernel takes zero or two
+                              of them (two in a row = one max over aligned
+                              4x4x4 blocks).                                */
 } kf_op_kind;
 
 typedef struct kf_op {
@@ -115,19 +135,23 @@ typedef struct kf_op_spec {
   int32_t out_dtype;       /* KF_F32 or KF_BF16 (ROW_LOGSUMEXP: KF_F32)      */
   int32_t b_layout;        /* kf_layout (GEMM)                              */
   int64_t M, N, K;         /* GEMM sizes                                    */
-  int64_t batch, cin, height, width, cout; /* CONV2D_3X3 sizes              */
+  int64_t batch, cin, height, width, cout; /* CONV2D_3X3 / CONV3D sizes     */
+  int64_t depth;           /* CONV3D_3X3X3 input depth                      */
   float scale_a, scale_b;  /* FP8_E4M3 per-tensor dequantisation scales     */
   int32_t residual_dtype;  /* KF_F32 or KF_BF16, for RESIDUAL_ADD           */
   int32_t n_ops;           /* 0..KF_MAX_OPS                                 */
   kf_op ops[KF_MAX_OPS];
 } kf_op_spec;
 
+#define KF_MAX_DIMS 5
+
 typedef struct kf_tensor {
   void* data;              /* device pointer, 16-byte aligned               */
   int32_t dtype;           /* kf_dtype                                      */
-  int32_t ndim;            /* 1..4                                          */
-  int64_t shape[4];
-  int64_t stride[4];       /* elements; stride[ndim-1] must be 1            */
+  int32_t ndim;            /* 1..KF_MAX_DIMS                                */
+  int64_t shape[KF_MAX_DIMS];
+  int64_t stride[KF_MAX_DIMS]; /* elements; stride[ndim-1] must be 1, except
+                              for the channels-last CONV3D input            */
 } kf_tensor;
 
 typedef struct kf_desc kf_desc;
@@ -176,9 +200,9 @@ int32_t kf_num_inputs(const kf_desc* desc);
 
 /* Expected dtype / shape of input slot `slot`, and of the single output. */
 kf_status kf_input_info(const kf_desc* desc, int32_t slot, int32_t* dtype,
-                        int32_t* ndim, int64_t shape[4]);
+                        int32_t* ndim, int64_t shape[KF_MAX_DIMS]);
 kf_status kf_output_info(const kf_desc* desc, int32_t* dtype, int32_t* ndim,
-                         int64_t shape[4]);
+                         int64_t shape[KF_MAX_DIMS]);
 
 /* Bytes of device workspace the descriptor owns (fused path). */
 size_t kf_workspace_bytes(const kf_desc* desc);

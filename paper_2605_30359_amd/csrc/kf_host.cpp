@@ -38,13 +38,14 @@ kf_status ok() {
   return KF_OK;
 }
 
-enum Variant { kVarGemmF32 = 0, kVarGemmBf16 = 1, kVarGemmFp8 = 2, kVarConvBf16 = 3, kVarRowwise = 4 };
+enum Variant { kVarGemmF32 = 0, kVarGemmBf16 = 1, kVarGemmFp8 = 2, kVarConvBf16 = 3, kVarRowwise = 4, kVarConv3d = 5 };
 
 struct Slot {
   int32_t dtype;
   int32_t ndim;
-  int64_t shape[4];
+  int64_t shape[KF_MAX_DIMS];
   const char* name;
+  bool channels_last;  // a 5-D [N, C, D, H, W] tensor stored as [N][D][H][W][C]
 };
 
 int64_t elem_size(int32_t dt) { return dt == KF_F32 ? 4 : dt == KF_BF16 ? 2 : 1; }
@@ -80,12 +81,12 @@ struct kf_desc {
 
 namespace {
 
-// The compile-time chain whose op kinds equal the spec's (GEMM chains 1-6 and 8,
-// the conv chain 7), else 0.
+// The compile-time chain whose op kinds equal the spec's and which belongs to
+// the spec's contraction (chain 1, no ops, to every one), else 0.
 int match_chain(const kf_op_spec* s) {
-  const bool conv = s->contraction == KF_CONV2D_3X3;
+  const int family = s->contraction == KF_CONV2D_3X3 ? 2 : s->contraction == KF_CONV3D_3X3X3 ? 3 : 1;
   for (int ch = 1; ch < kf::kNumChains; ++ch) {
-    if ((ch == 7) != conv || kf::kChainLen[ch] != s->n_ops) continue;
+    if ((kf::kChainFamily[ch] != 0 && kf::kChainFamily[ch] != family) || kf::kChainLen[ch] != s->n_ops) continue;
     bool same = true;
     for (int o = 0; o < s->n_ops; ++o) same = same && s->ops[o].kind == kf::kChainOps[ch][o];
     if (same) return ch;
@@ -95,7 +96,8 @@ int match_chain(const kf_op_spec* s) {
 
 kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   if (!s) return fail(KF_ERR_INVALID_ARG, "spec is NULL");
-  if (s->contraction != KF_GEMM && s->contraction != KF_CONV2D_3X3 && s->contraction != KF_ROWWISE)
+  if (s->contraction != KF_GEMM && s->contraction != KF_CONV2D_3X3 && s->contraction != KF_ROWWISE &&
+      s->contraction != KF_CONV3D_3X3X3)
     return fail(KF_ERR_INVALID_ARG, "unknown contraction %d", s->contraction);
   if (s->in_dtype != KF_F32 && s->in_dtype != KF_BF16 && s->in_dtype != KF_FP8_E4M3)
     return fail(KF_ERR_INVALID_ARG, "unknown in_dtype %d", s->in_dtype);
@@ -110,11 +112,11 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   d->epi_shape = kf::kEpiPlain;
   d->gn_group = 0;
   d->row_kind = 0;
-  int n_red = 0, n_pool = 0;
+  int n_red = 0, n_pool = 0, n_pool3 = 0, n_csm = 0;
   bool has_bias = false, has_gn = false, has_res = false;
   for (int i = 0; i < s->n_ops; ++i) {
     const kf_op& op = s->ops[i];
-    if (op.kind < KF_OP_BIAS || op.kind > KF_OP_ROW_LOGSUMEXP)
+    if (op.kind < KF_OP_BIAS || op.kind > KF_OP_MAXPOOL3D_2)
       return fail(KF_ERR_INVALID_ARG, "op %d: unknown kind %d", i, op.kind);
     d->prog.op[i] = kf::EpiOp{op.kind, op.groups, op.p0, op.p1};
     switch (op.kind) {
@@ -148,16 +150,31 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       case KF_OP_ROW_SOFTMAX:
       case KF_OP_ROW_LOGSUMEXP:
         if (i != s->n_ops - 1) return fail(KF_ERR_UNSUPPORTED, "op %d: a row softmax/logsumexp must be the last op", i);
-        if (s->contraction == KF_CONV2D_3X3) return fail(KF_ERR_UNSUPPORTED, "op %d: row ops need a GEMM or ROWWISE", i);
+        if (s->contraction != KF_GEMM && s->contraction != KF_ROWWISE)
+          return fail(KF_ERR_UNSUPPORTED, "op %d: row ops need a GEMM or ROWWISE", i);
         ++n_red;
         d->red_index = i;
         d->epi_shape = kf::kEpiRow;
         d->row_kind = op.kind;
         break;
+      case KF_OP_CHANNEL_SOFTMAX:
+        if (s->contraction != KF_CONV3D_3X3X3)
+          return fail(KF_ERR_UNSUPPORTED, "op %d: CHANNEL_SOFTMAX needs CONV3D_3X3X3", i);
+        if (n_pool3) return fail(KF_ERR_UNSUPPORTED, "op %d: CHANNEL_SOFTMAX must come before the pools", i);
+        ++n_csm;
+        break;
+      case KF_OP_MAXPOOL3D_2:
+        if (s->contraction != KF_CONV3D_3X3X3)
+          return fail(KF_ERR_UNSUPPORTED, "op %d: MAXPOOL3D_2 needs CONV3D_3X3X3", i);
+        ++n_pool3;
+        break;
       default:
         break;
     }
+    if (n_pool3 && op.kind != KF_OP_MAXPOOL3D_2)
+      return fail(KF_ERR_UNSUPPORTED, "op %d: the MAXPOOL3D_2 ops must be the last ops", i);
   }
+  if (n_csm > 1) return fail(KF_ERR_UNSUPPORTED, "at most one CHANNEL_SOFTMAX op");
   if (n_red > 1) return fail(KF_ERR_UNSUPPORTED, "at most one reduction op (GROUPNORM / ROW_*) per chain");
   if (n_pool > 1) return fail(KF_ERR_UNSUPPORTED, "at most one MAXPOOL2X2 op");
   if (d->row_kind == KF_OP_ROW_LOGSUMEXP && s->out_dtype != KF_F32)
@@ -170,8 +187,8 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     if (s->M > INT32_MAX || s->N > INT32_MAX || s->K > INT32_MAX) return fail(KF_ERR_UNSUPPORTED, "GEMM sizes must be < 2^31");
     if (s->b_layout != KF_LAYOUT_KN && s->b_layout != KF_LAYOUT_NK) return fail(KF_ERR_INVALID_ARG, "unknown b_layout %d", s->b_layout);
     const bool nk = s->b_layout == KF_LAYOUT_NK;
-    d->inputs.push_back(Slot{dt, 2, {s->M, s->K, 0, 0}, "A"});
-    d->inputs.push_back(Slot{dt, 2, {nk ? s->N : s->K, nk ? s->K : s->N, 0, 0}, "B"});
+    d->inputs.push_back(Slot{dt, 2, {s->M, s->K, 0, 0, 0}, "A", false});
+    d->inputs.push_back(Slot{dt, 2, {nk ? s->N : s->K, nk ? s->K : s->N, 0, 0, 0}, "B", false});
     if (dt == KF_F32) {
       d->variant = kVarGemmF32;
       if (d->epi_shape != kf::kEpiPlain)
@@ -202,17 +219,17 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     }
     for (int i = 0; i < s->n_ops; ++i) {
       const int k = s->ops[i].kind;
-      if (k == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "bias"});
+      if (k == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0, 0}, "bias", false});
       if (k == KF_OP_GROUPNORM) {
-        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "gamma"});
-        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "beta"});
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0, 0}, "gamma", false});
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0, 0}, "beta", false});
       }
-      if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0}, "residual"});
+      if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0, 0}, "residual", false});
     }
     if (d->row_kind == KF_OP_ROW_LOGSUMEXP)
-      d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0}, "out"};
+      d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0, 0}, "out", false};
     else
-      d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0}, "out"};
+      d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0, 0}, "out", false};
     if (d->row_kind) {
       d->tiles_n = (int)((s->N + kf::gemm_mfma_tile_n() - 1) / kf::gemm_mfma_tile_n());
       if (d->tiles_n > kf::row_finish_max_tiles())
@@ -233,20 +250,55 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     }
     d->variant = kVarRowwise;
     d->kernel_name = "kf_rowwise";
-    d->inputs.push_back(Slot{dt, 2, {s->M, s->N, 0, 0}, "A"});
+    d->inputs.push_back(Slot{dt, 2, {s->M, s->N, 0, 0, 0}, "A", false});
     for (int i = 0; i < s->n_ops; ++i) {
       const int k = s->ops[i].kind;
-      if (k == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "bias"});
+      if (k == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0, 0}, "bias", false});
       if (k == KF_OP_GROUPNORM) {
-        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "gamma"});
-        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0}, "beta"});
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0, 0}, "gamma", false});
+        d->inputs.push_back(Slot{KF_F32, 1, {s->N, 0, 0, 0, 0}, "beta", false});
       }
-      if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0}, "residual"});
+      if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0, 0}, "residual", false});
     }
     if (d->row_kind == KF_OP_ROW_LOGSUMEXP)
-      d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0}, "out"};
+      d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0, 0}, "out", false};
     else
-      d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0}, "out"};
+      d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0, 0}, "out", false};
+  } else if (s->contraction == KF_CONV3D_3X3X3) {
+    // 3x3x3 convolution, stride 1, no padding, channels-last input / OIDHW weight
+    if (dt != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 supports bf16 inputs only");
+    if (s->out_dtype != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 writes bf16 outputs only");
+    if (s->batch < 0 || s->cin < 1 || s->cout < 1 || s->depth < 3 || s->height < 3 || s->width < 3)
+      return fail(KF_ERR_SHAPE, "CONV3D_3X3X3 needs batch >= 0, cin, cout >= 1 and depth, height, width >= 3");
+    if (s->cin != kf::conv3d_cin() || s->cout != kf::conv3d_cout())
+      return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 kernel is built for cin=%d, cout=%d", kf::conv3d_cin(),
+                  kf::conv3d_cout());
+    if (s->depth * s->height * s->width * s->cin * 2 >= (int64_t(1) << 30))
+      return fail(KF_ERR_UNSUPPORTED, "one input volume must be smaller than 1 GiB");
+    if (n_pool3 != 0 && n_pool3 != 2)
+      return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 takes zero or two MAXPOOL3D_2 ops (got %d)", n_pool3);
+    for (int i = 0; i < s->n_ops; ++i) {
+      const int k = s->ops[i].kind;
+      if (!(k == KF_OP_BIAS || k == KF_OP_CHANNEL_SOFTMAX || k == KF_OP_MAXPOOL3D_2 || is_elementwise_kind(k)))
+        return fail(KF_ERR_UNSUPPORTED,
+                    "op %d: CONV3D_3X3X3 supports BIAS, element-wise ops, CHANNEL_SOFTMAX and MAXPOOL3D_2", i);
+    }
+    int64_t od = s->depth - 2, oh = s->height - 2, ow = s->width - 2;
+    // the unfused chain runs the conv alone over every position
+    if (s->batch * ((od + 3) / 4) * ((oh + 7) / 8) * ((ow + 15) / 16) > INT32_MAX)
+      return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 supports at most 2^31 - 1 tiles");
+    for (int i = 0; i < n_pool3; ++i) {
+      od /= 2;
+      oh /= 2;
+      ow /= 2;
+    }
+    d->variant = kVarConv3d;
+    d->kernel_name = "kf_conv3d_bf16_64x512";
+    d->inputs.push_back(Slot{dt, 5, {s->batch, s->cin, s->depth, s->height, s->width}, "A", true});
+    d->inputs.push_back(Slot{dt, 5, {s->cout, s->cin, 3, 3, 3}, "B", false});
+    for (int i = 0; i < s->n_ops; ++i)
+      if (s->ops[i].kind == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->cout, 0, 0, 0, 0}, "bias", false});
+    d->output = Slot{KF_BF16, 5, {s->batch, s->cout, od, oh, ow}, "out", false};
   } else {
     // 3x3 convolution, stride 1, zero padding 1, NCHW input / OIHW weight
     if (dt != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 supports bf16 inputs only");
@@ -268,14 +320,14 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     }
     d->variant = kVarConvBf16;
     d->kernel_name = "kf_conv3x3_bf16_256x128";
-    d->inputs.push_back(Slot{dt, 4, {s->batch, s->cin, s->height, s->width}, "A"});
-    d->inputs.push_back(Slot{dt, 4, {s->cout, s->cin, 3, 3}, "B"});
+    d->inputs.push_back(Slot{dt, 4, {s->batch, s->cin, s->height, s->width}, "A", false});
+    d->inputs.push_back(Slot{dt, 4, {s->cout, s->cin, 3, 3}, "B", false});
     for (int i = 0; i < s->n_ops; ++i)
-      if (s->ops[i].kind == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->cout, 0, 0, 0}, "bias"});
+      if (s->ops[i].kind == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->cout, 0, 0, 0, 0}, "bias", false});
     if (n_pool)
-      d->output = Slot{KF_BF16, 4, {s->batch, s->cout, s->height / 2, s->width / 2}, "out"};
+      d->output = Slot{KF_BF16, 4, {s->batch, s->cout, s->height / 2, s->width / 2}, "out", false};
     else
-      d->output = Slot{KF_BF16, 4, {s->batch, s->cout, s->height, s->width}, "out"};
+      d->output = Slot{KF_BF16, 4, {s->batch, s->cout, s->height, s->width}, "out", false};
   }
   return KF_OK;
 }
@@ -292,7 +344,18 @@ kf_status check_tensor(const kf_tensor* t, const Slot& s, bool is_output, bool v
   }
   if (numel == 0) return KF_OK;  // never dereferenced
   if (!t->data) return fail(KF_ERR_INVALID_ARG, "%s '%s': data is NULL", what, s.name);
-  if (t->stride[s.ndim - 1] != 1) return fail(KF_ERR_UNSUPPORTED, "%s '%s': innermost stride must be 1", what, s.name);
+  if (s.channels_last) {
+    // [N, C, D, H, W] with strides [D H W C, 1, H W C, W C, C]
+    const int64_t C = s.shape[1];
+    const int64_t expect[5] = {s.shape[2] * s.shape[3] * s.shape[4] * C, 1, s.shape[3] * s.shape[4] * C,
+                               s.shape[4] * C, C};
+    for (int i = 0; i < 5; ++i)
+      if (t->stride[i] != expect[i] && s.shape[i] != 1)
+        return fail(KF_ERR_UNSUPPORTED, "%s '%s': must be channels-last (torch.channels_last_3d) and dense", what,
+                    s.name);
+  } else if (t->stride[s.ndim - 1] != 1) {
+    return fail(KF_ERR_UNSUPPORTED, "%s '%s': innermost stride must be 1", what, s.name);
+  }
   const int64_t es = elem_size(s.dtype);
   const int64_t align = vec16 ? 16 : es;
   if (reinterpret_cast<uintptr_t>(t->data) % align)
@@ -301,10 +364,11 @@ kf_status check_tensor(const kf_tensor* t, const Slot& s, bool is_output, bool v
     if (t->stride[0] < s.shape[1]) return fail(KF_ERR_SHAPE, "%s '%s': row stride %lld < row length %lld", what, s.name, (long long)t->stride[0], (long long)s.shape[1]);
     if (vec16 && (t->stride[0] * es) % 16)
       return fail(KF_ERR_UNSUPPORTED, "%s '%s': row stride must be a multiple of 16 bytes", what, s.name);
-  } else if (s.ndim == 4) {
+  } else if (s.ndim >= 4 && !s.channels_last) {
     int64_t expect = 1;
-    for (int i = 3; i >= 0; --i) {
-      if (t->stride[i] != expect) return fail(KF_ERR_UNSUPPORTED, "%s '%s': 4-D tensors must be contiguous", what, s.name);
+    for (int i = s.ndim - 1; i >= 0; --i) {
+      if (t->stride[i] != expect && s.shape[i] != 1)
+        return fail(KF_ERR_UNSUPPORTED, "%s '%s': %d-D tensors must be contiguous", what, s.name, s.ndim);
       expect *= s.shape[i];
     }
   }
@@ -313,6 +377,43 @@ kf_status check_tensor(const kf_tensor* t, const Slot& s, bool is_output, bool v
 
 // Byte extents addressed through 32-bit buffer offsets must stay below 2^31.
 bool fits_31(int64_t bytes) { return bytes >= 0 && bytes < (int64_t(1) << 31); }
+
+// Kernel arguments of a CONV3D_3X3X3 plan; pools = 0 stores every conv
+// output position, pools = 2 the 4x4x4-block maxima.
+kf::Conv3dArgs conv3d_args(const kf_desc* d, const kf_tensor* inputs, void* out, int pools) {
+  const kf_op_spec& s = d->spec;
+  kf::Conv3dArgs a;
+  memset(&a, 0, sizeof(a));
+  a.x = inputs[0].data;
+  a.batch = (int32_t)s.batch;
+  a.D = (int32_t)s.depth;
+  a.H = (int32_t)s.height;
+  a.W = (int32_t)s.width;
+  a.prog = d->prog;
+  for (int i = 0; i < s.n_ops; ++i)
+    if (s.ops[i].kind == KF_OP_BIAS) a.bias = static_cast<const float*>(inputs[2].data);
+  a.out = out;
+  a.pools = pools;
+  const int64_t od = s.depth - 2, oh = s.height - 2, ow = s.width - 2;
+  a.Dp = (int32_t)(pools ? od / 4 : od);
+  a.Hp = (int32_t)(pools ? oh / 4 : oh);
+  a.Wp = (int32_t)(pools ? ow / 4 : ow);
+  // conv positions the output needs, in tiles of 4 x 8 x 16
+  const int64_t nd = pools ? 4 * (int64_t)a.Dp : od, nh = pools ? 4 * (int64_t)a.Hp : oh,
+                nw = pools ? 4 * (int64_t)a.Wp : ow;
+  a.tiles_d = (int32_t)((nd + 3) / 4);
+  a.tiles_h = (int32_t)((nh + 7) / 8);
+  a.tiles_w = (int32_t)((nw + 15) / 16);
+  a.tiles = (int32_t)(s.batch * a.tiles_d * a.tiles_h * a.tiles_w);
+  a.grid = d->num_cu;
+  return a;
+}
+
+int conv3d_pool_count(const kf_op_spec& s) {
+  int n = 0;
+  for (int i = 0; i < s.n_ops; ++i) n += s.ops[i].kind == KF_OP_MAXPOOL3D_2;
+  return n;
+}
 
 }  // namespace
 
@@ -371,8 +472,10 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
   d->device = dev;
   d->num_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
 
-  if (d->variant == kVarConvBf16) {
-    d->workspace_bytes = (size_t)9 * spec->cout * spec->cin * 2;  // repacked weights
+  if (d->variant == kVarConvBf16 || d->variant == kVarConv3d) {
+    // repacked weights
+    d->workspace_bytes =
+        d->variant == kVarConvBf16 ? (size_t)9 * spec->cout * spec->cin * 2 : kf::conv3d_packed_bytes();
     if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
       (void)hipGetLastError();
       delete d;
@@ -400,21 +503,21 @@ void kf_destroy(kf_desc* d) {
 
 int32_t kf_num_inputs(const kf_desc* d) { return d ? (int32_t)d->inputs.size() : -1; }
 
-kf_status kf_input_info(const kf_desc* d, int32_t slot, int32_t* dtype, int32_t* ndim, int64_t shape[4]) {
+kf_status kf_input_info(const kf_desc* d, int32_t slot, int32_t* dtype, int32_t* ndim, int64_t shape[KF_MAX_DIMS]) {
   if (!d || !dtype || !ndim || !shape) return fail(KF_ERR_INVALID_ARG, "NULL argument");
   if (slot < 0 || slot >= (int32_t)d->inputs.size()) return fail(KF_ERR_INVALID_ARG, "slot %d out of range", slot);
   const Slot& s = d->inputs[slot];
   *dtype = s.dtype;
   *ndim = s.ndim;
-  for (int i = 0; i < 4; ++i) shape[i] = s.shape[i];
+  for (int i = 0; i < KF_MAX_DIMS; ++i) shape[i] = s.shape[i];
   return ok();
 }
 
-kf_status kf_output_info(const kf_desc* d, int32_t* dtype, int32_t* ndim, int64_t shape[4]) {
+kf_status kf_output_info(const kf_desc* d, int32_t* dtype, int32_t* ndim, int64_t shape[KF_MAX_DIMS]) {
   if (!d || !dtype || !ndim || !shape) return fail(KF_ERR_INVALID_ARG, "NULL argument");
   *dtype = d->output.dtype;
   *ndim = d->output.ndim;
-  for (int i = 0; i < 4; ++i) shape[i] = d->output.shape[i];
+  for (int i = 0; i < KF_MAX_DIMS; ++i) shape[i] = d->output.shape[i];
   return ok();
 }
 
@@ -438,6 +541,16 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
 
   const kf_op_spec& s = d->spec;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (s.contraction == KF_CONV3D_3X3X3) {
+    const kf::Conv3dArgs a = conv3d_args(d, inputs, outputs[0].data, conv3d_pool_count(s));
+    if (a.tiles == 0) return ok();
+    hipError_t e = kf::launch_conv3d_pack(inputs[1].data, d->workspace, hs);
+    if (e == hipSuccess && ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
+    if (e == hipSuccess) e = kf::launch_conv3d_bf16(a, d->workspace, d->chain, hs);
+    if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
+    if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return ok();
+  }
   if (s.contraction == KF_ROWWISE) {
     if (s.M == 0) return ok();
     kf::RowArgs r;
@@ -575,6 +688,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   const bool gemm = s.contraction == KF_GEMM;
   const bool rowwise = s.contraction == KF_ROWWISE;
+  const bool conv3d = s.contraction == KF_CONV3D_3X3X3;
   const bool rows = gemm || rowwise;  // an [M, N] intermediate
   if ((rows && s.M == 0) || (!rows && s.batch == 0)) return ok();
   // the per-op kernels index [M, N] tensors as contiguous rows
@@ -583,7 +697,9 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
 
   // intermediates: bf16 (fp32 for an fp32 chain), full contraction size
   const bool ibf16 = rowwise ? s.in_dtype == KF_BF16 : d->variant != kVarGemmF32;
-  const int64_t n_full = rows ? s.M * s.N : s.batch * s.cout * s.height * s.width;
+  const int64_t n_full = rows     ? s.M * s.N
+                         : conv3d ? s.batch * s.cout * (s.depth - 2) * (s.height - 2) * (s.width - 2)
+                                  : s.batch * s.cout * s.height * s.width;
   const size_t need = (size_t)n_full * (ibf16 ? 2 : 4);
   if (d->ubuf_bytes < need) {
     for (void*& b : d->ubuf) {
@@ -630,6 +746,11 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     const bool nk = s.b_layout == KF_LAYOUT_NK;
     e = d->variant == kVarGemmF32 ? kf::launch_gemm_f32(a, nk, hs)
                                   : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk);
+  } else if (conv3d) {
+    // the convolution alone: every conv output position, NCDHW
+    const kf::Conv3dArgs a = conv3d_args(d, inputs, cur, 0);
+    e = kf::launch_conv3d_pack(inputs[1].data, d->workspace, hs);
+    if (e == hipSuccess && a.tiles) e = kf::launch_conv3d_bf16(a, d->workspace, 1, hs);
   } else {
     kf::ConvArgs c;
     memset(&c, 0, sizeof(c));
@@ -652,7 +773,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   // 2. one kernel per op, ping-ponging between the buffers; the last op
   //    writes the output
   int64_t n = n_full;
-  int64_t hh = s.height, ww = s.width;
+  int64_t dd = conv3d ? s.depth - 2 : 1, hh = conv3d ? s.height - 2 : s.height, ww = conv3d ? s.width - 2 : s.width;
   int which = 0;
   for (int i = 0; i < s.n_ops && e == hipSuccess; ++i) {
     const kf_op& op = s.ops[i];
@@ -662,7 +783,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     switch (op.kind) {
       case KF_OP_BIAS: {
         const float* bias = static_cast<const float*>(inputs[slot++].data);
-        const int64_t fdiv = rows ? 1 : hh * ww, fmod = rows ? s.N : s.cout;
+        const int64_t fdiv = rows ? 1 : dd * hh * ww, fmod = rows ? s.N : s.cout;
         e = kf::launch_unfused_elementwise(cur, cur_bf16, dst, dst_bf16, n, op.kind, 0.f, 0.f, bias, fdiv, fmod, hs);
         break;
       }
@@ -680,6 +801,16 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
       case KF_OP_ROW_SOFTMAX:
       case KF_OP_ROW_LOGSUMEXP:
         e = kf::launch_unfused_rowop(cur, cur_bf16, dst, dst_bf16, s.M, s.N, op.kind == KF_OP_ROW_SOFTMAX, hs);
+        break;
+      case KF_OP_CHANNEL_SOFTMAX:
+        e = kf::launch_unfused_channel_softmax(cur, cur_bf16, dst, dst_bf16, s.batch, (int)s.cout, dd * hh * ww, hs);
+        break;
+      case KF_OP_MAXPOOL3D_2:
+        e = kf::launch_unfused_maxpool3d(cur, cur_bf16, dst, dst_bf16, s.batch * s.cout, (int)dd, (int)hh, (int)ww, hs);
+        dd /= 2;
+        hh /= 2;
+        ww /= 2;
+        n = s.batch * s.cout * dd * hh * ww;
         break;
       case KF_OP_MAXPOOL2X2:
         e = kf::launch_unfused_maxpool(cur, cur_bf16, dst, dst_bf16, s.batch * s.cout, (int)hh, (int)ww, hs);

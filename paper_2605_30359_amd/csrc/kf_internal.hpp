@@ -29,8 +29,8 @@ enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
 // is interpreted at run time.  The paper turns each operator into its own
 // specialised kernel; these are the chains of the benchmarked operators and
 // the plain building blocks, and every other chain runs interpreted.
-constexpr int kNumChains = 10;
-constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1};
+constexpr int kNumChains = 11;
+constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1, 4};
 constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {},                                                                         // 0: interpreted
     {},                                                                         // 1: contraction only
@@ -42,7 +42,11 @@ constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {KF_OP_BIAS, KF_OP_RELU, KF_OP_MAXPOOL2X2},                                // 7: conv, ReLU, max-pool
     {KF_OP_BIAS, KF_OP_SWISH, KF_OP_TANH, KF_OP_GELU_ERF, KF_OP_HARDTANH},     // 8: GEMM + activation chain
     {KF_OP_ROW_SOFTMAX},                                                        // 9: softmax rows
+    {KF_OP_BIAS, KF_OP_CHANNEL_SOFTMAX, KF_OP_MAXPOOL3D_2, KF_OP_MAXPOOL3D_2},  // 10: conv3d, softmax, pools
 };
+// Which contraction a chain belongs to: 0 any, 1 GEMM / ROWWISE, 2 CONV2D_3X3,
+// 3 CONV3D_3X3X3.
+constexpr int kChainFamily[kNumChains] = {0, 0, 1, 1, 1, 1, 1, 2, 1, 1, 3};
 
 // Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).
 struct GemmArgs {
@@ -100,6 +104,20 @@ struct ConvArgs {
   int32_t pool_index;     // position of the pool op in prog
   int32_t tiles;          // number of output tiles (batch x H/2 row pairs)
   int32_t grid;           // workgroups of the persistent launch (at most tiles)
+};
+
+// Arguments of the implicit-GEMM 3x3x3 convolution kernel.
+struct Conv3dArgs {
+  const void* x;          // [batch][D][H][W][cin] (channels-last)
+  int32_t batch, D, H, W;
+  EpiProgram prog;
+  const float* bias;      // [cout] or null
+  void* out;              // [batch, cout, Dp, Hp, Wp] (NCDHW)
+  int32_t pools;          // 0, or 2 (two MaxPool3d(2) = max over 4x4x4 blocks)
+  int32_t Dp, Hp, Wp;     // output extents (after the pools)
+  int32_t tiles_d, tiles_h, tiles_w;  // output tiles of 4 x 8 x 16 conv positions
+  int32_t tiles;          // batch * tiles_d * tiles_h * tiles_w
+  int32_t grid;           // workgroups of the persistent launch
 };
 
 }  // namespace kf

@@ -42,6 +42,17 @@ int conv_bf16_cin();
 int conv_bf16_width();
 int conv_bf16_cout();
 
+// 3x3x3 conv (bf16, channels-last input, OIDHW weight) + fused bias,
+// element-wise ops, channel softmax and two 3-D max-pools:
+// launch_conv3d_pack repacks the weights into `packed_weights` (device
+// scratch of conv3d_packed_bytes()), launch_conv3d_bf16 runs the convolution
+// from it.  Supports cin == conv3d_cin(), cout == conv3d_cout().
+hipError_t launch_conv3d_pack(const void* w, void* packed_weights, hipStream_t stream);
+hipError_t launch_conv3d_bf16(const Conv3dArgs& args, const void* packed_weights, int chain, hipStream_t stream);
+int conv3d_cin();
+int conv3d_cout();
+size_t conv3d_packed_bytes();
+
 }  // namespace kf
 
 namespace kf {
@@ -59,5 +70,9 @@ hipError_t launch_unfused_rowop(const void* in, bool in_bf16, void* out, bool ou
                                 bool softmax, hipStream_t stream);
 hipError_t launch_unfused_maxpool(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t planes, int H,
                                   int W, hipStream_t stream);
+hipError_t launch_unfused_channel_softmax(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t batch,
+                                         int channels, int64_t spatial, hipStream_t stream);
+hipError_t launch_unfused_maxpool3d(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t planes, int D,
+                                    int H, int W, hipStream_t stream);
 
 }  // namespace kf

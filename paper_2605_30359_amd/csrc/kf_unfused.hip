@@ -147,6 +147,47 @@ __global__ __launch_bounds__(256) void kf_unfused_maxpool(const void* in, int in
   }
 }
 
+// Softmax over the channel axis of an NCDHW tensor, one thread per (image,
+// position): consecutive threads take consecutive positions, so every read
+// of one channel plane is coalesced.  Three passes over the channels (max,
+// sum of exponentials, normalised store), as torch.softmax(h, dim=1) does.
+__global__ __launch_bounds__(256) void kf_unfused_channel_softmax(const void* in, int in_bf16, void* out,
+                                                                  int out_bf16, int64_t batch, int C,
+                                                                  int64_t S) {
+  const int64_t n = batch * S;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t b = (i / S) * C * S + i % S;
+    float m = -INFINITY;
+    for (int c = 0; c < C; ++c) m = fmaxf(m, load_elem(in, b + c * S, in_bf16));
+    float sum = 0.0f;
+    for (int c = 0; c < C; ++c) sum += fexp(load_elem(in, b + c * S, in_bf16) - m);
+    const float inv = 1.0f / sum;
+    for (int c = 0; c < C; ++c) store_elem(out, b + c * S, fexp(load_elem(in, b + c * S, in_bf16) - m) * inv, out_bf16);
+  }
+}
+
+// MaxPool3d(2), stride 2, floor mode, over [planes][D][H][W].
+__global__ __launch_bounds__(256) void kf_unfused_maxpool3d(const void* in, int in_bf16, void* out, int out_bf16,
+                                                            int64_t planes, int D, int H, int W) {
+  const int Do = D / 2, Ho = H / 2, Wo = W / 2;
+  const int64_t per = (int64_t)Do * Ho * Wo;
+  const int64_t n = planes * per;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t pl = i / per;
+    const int r = (int)(i % per);
+    const int pd = r / (Ho * Wo), ph = (r / Wo) % Ho, pw = r % Wo;
+    float v = -INFINITY;
+#pragma unroll
+    for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int64_t b = ((pl * D + 2 * pd + dd) * H + 2 * ph + hh) * W + 2 * pw;
+        v = fmaxf(v, fmaxf(load_elem(in, b, in_bf16), load_elem(in, b + 1, in_bf16)));
+      }
+    store_elem(out, i, v, out_bf16);
+  }
+}
+
 static unsigned grid_for(int64_t n) {
   const int64_t g = (n + 255) / 256;
   return (unsigned)(g < 8192 ? (g > 0 ? g : 1) : 8192);
@@ -188,6 +229,20 @@ hipError_t launch_unfused_maxpool(const void* in, bool in_bf16, void* out, bool 
                                   int W, hipStream_t stream) {
   hipLaunchKernelGGL(kf_unfused_maxpool, dim3(grid_for(planes * (H / 2) * (W / 2))), dim3(256), 0, stream, in,
                      in_bf16 ? 1 : 0, out, out_bf16 ? 1 : 0, planes, H, W);
+  return hipGetLastError();
+}
+
+hipError_t launch_unfused_channel_softmax(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t batch,
+                                         int channels, int64_t spatial, hipStream_t stream) {
+  hipLaunchKernelGGL(kf_unfused_channel_softmax, dim3(grid_for(batch * spatial)), dim3(256), 0, stream, in,
+                     in_bf16 ? 1 : 0, out, out_bf16 ? 1 : 0, batch, channels, spatial);
+  return hipGetLastError();
+}
+
+hipError_t launch_unfused_maxpool3d(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t planes, int D,
+                                    int H, int W, hipStream_t stream) {
+  hipLaunchKernelGGL(kf_unfused_maxpool3d, dim3(grid_for(planes * (D / 2) * (H / 2) * (W / 2))), dim3(256), 0,
+                     stream, in, in_bf16 ? 1 : 0, out, out_bf16 ? 1 : 0, planes, D, H, W);
   return hipGetLastError();
 }
 

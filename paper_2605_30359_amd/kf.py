@@ -19,16 +19,19 @@ LIB_PATH = os.path.join(_PKG, "libkf.so")
 # ---------------------------------------------------------------- C mirror
 
 KF_OK, KF_ERR_INVALID_ARG, KF_ERR_SHAPE, KF_ERR_UNSUPPORTED, KF_ERR_NO_DEVICE, KF_ERR_OOM, KF_ERR_HIP = range(7)
-KF_GEMM, KF_CONV2D_3X3, KF_ROWWISE = 0, 1, 2
-CONTRACTIONS = {"gemm": KF_GEMM, "conv2d_3x3": KF_CONV2D_3X3, "rowwise": KF_ROWWISE}
+KF_GEMM, KF_CONV2D_3X3, KF_ROWWISE, KF_CONV3D_3X3X3 = 0, 1, 2, 3
+CONTRACTIONS = {"gemm": KF_GEMM, "conv2d_3x3": KF_CONV2D_3X3, "rowwise": KF_ROWWISE,
+                "conv3d_3x3x3": KF_CONV3D_3X3X3}
 KF_F32, KF_BF16, KF_FP8_E4M3 = 0, 1, 2
 KF_LAYOUT_KN, KF_LAYOUT_NK = 0, 1
 KF_MAX_OPS = 8
+KF_MAX_DIMS = 5
 
 OP_KINDS = {
     "bias": 1, "relu": 2, "gelu_tanh": 3, "gelu_erf": 4, "swish": 5, "sigmoid": 6,
     "tanh": 7, "hardtanh": 8, "scale": 9, "groupnorm": 10, "residual_add": 11,
-    "maxpool2x2": 12, "row_softmax": 13, "row_logsumexp": 14,
+    "maxpool2x2": 12, "row_softmax": 13, "row_logsumexp": 14, "channel_softmax": 15,
+    "maxpool3d2": 16,
 }
 DTYPES = {"f32": KF_F32, "bf16": KF_BF16, "e4m3": KF_FP8_E4M3}
 DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
@@ -48,7 +51,7 @@ class KfOpSpec(ctypes.Structure):
                 ("out_dtype", ctypes.c_int32), ("b_layout", ctypes.c_int32),
                 ("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
                 ("batch", ctypes.c_int64), ("cin", ctypes.c_int64), ("height", ctypes.c_int64),
-                ("width", ctypes.c_int64), ("cout", ctypes.c_int64),
+                ("width", ctypes.c_int64), ("cout", ctypes.c_int64), ("depth", ctypes.c_int64),
                 ("scale_a", ctypes.c_float), ("scale_b", ctypes.c_float),
                 ("residual_dtype", ctypes.c_int32), ("n_ops", ctypes.c_int32),
                 ("ops", KfOp * KF_MAX_OPS)]
@@ -56,7 +59,7 @@ class KfOpSpec(ctypes.Structure):
 
 class KfTensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
-                ("shape", ctypes.c_int64 * 4), ("stride", ctypes.c_int64 * 4)]
+                ("shape", ctypes.c_int64 * KF_MAX_DIMS), ("stride", ctypes.c_int64 * KF_MAX_DIMS)]
 
 
 class KFError(RuntimeError):
@@ -89,9 +92,9 @@ def lib():
         L.kf_destroy.restype = None
         L.kf_num_inputs.argtypes = [vp]
         L.kf_num_inputs.restype = i32
-        L.kf_input_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.c_int64 * 4]
+        L.kf_input_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.c_int64 * KF_MAX_DIMS]
         L.kf_input_info.restype = i32
-        L.kf_output_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.c_int64 * 4]
+        L.kf_output_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.c_int64 * KF_MAX_DIMS]
         L.kf_output_info.restype = i32
         L.kf_workspace_bytes.argtypes = [vp]
         L.kf_workspace_bytes.restype = ctypes.c_size_t
@@ -120,7 +123,7 @@ def _check(status: int):
 
 # ------------------------------------------------------------ spec building
 
-def make_spec(chain: dict, *, M=0, N=0, K=0, batch=0, cin=0, H=0, W=0, cout=0) -> KfOpSpec:
+def make_spec(chain: dict, *, M=0, N=0, K=0, batch=0, cin=0, D=0, H=0, W=0, cout=0) -> KfOpSpec:
     """Fill a kf_op_spec from a chain description (see paper_2605_30359_amd.inputs)."""
     s = KfOpSpec()
     s.contraction = CONTRACTIONS[chain["contraction"]]
@@ -129,6 +132,7 @@ def make_spec(chain: dict, *, M=0, N=0, K=0, batch=0, cin=0, H=0, W=0, cout=0) -
     s.b_layout = KF_LAYOUT_NK if chain.get("b_layout", "kn") == "nk" else KF_LAYOUT_KN
     s.M, s.N, s.K = M, N, K
     s.batch, s.cin, s.height, s.width, s.cout = batch, cin, H, W, cout
+    s.depth = D
     s.scale_a = float(chain.get("scale_a", 1.0))
     s.scale_b = float(chain.get("scale_b", 1.0))
     s.residual_dtype = DTYPES[chain.get("residual_dtype", "bf16")]
@@ -168,6 +172,8 @@ def sizes_of(cfg: dict) -> dict:
         return dict(M=cfg["M"], N=cfg["N"], K=cfg["K"])
     if cfg["contraction"] == "rowwise":
         return dict(M=cfg["M"], N=cfg["N"])
+    if cfg["contraction"] == "conv3d_3x3x3":
+        return dict(batch=cfg["batch"], cin=cfg["cin"], D=cfg["D"], H=cfg["H"], W=cfg["W"], cout=cfg["cout"])
     return dict(batch=cfg["batch"], cin=cfg["cin"], H=cfg["H"], W=cfg["W"], cout=cfg["cout"])
 
 
@@ -183,10 +189,15 @@ def torch_dtype(code: int):
     return {KF_F32: torch.float32, KF_BF16: torch.bfloat16, KF_FP8_E4M3: torch.float8_e4m3fn}[code]
 
 
-def device_tensor(arr: np.ndarray, dtype: str, device="cuda"):
+def device_tensor(arr: np.ndarray, dtype: str, device="cuda", channels_last=False):
     """Copy raw storage (float32 / bf16 bits as uint16 / e4m3 codes as uint8)
-    to the device as a tensor of the matching torch dtype."""
+    to the device as a tensor of the matching torch dtype.  channels_last: a
+    5-D [N, C, D, H, W] array is stored as [N][D][H][W][C] (the strides of
+    torch.channels_last_3d), transposed on the host."""
     torch = _torch()
+    if channels_last:
+        t = device_tensor(np.ascontiguousarray(np.moveaxis(arr, 1, -1)), dtype, device)
+        return t.permute(0, 4, 1, 2, 3)
     arr = np.ascontiguousarray(arr)
     if dtype == "f32":
         return torch.from_numpy(arr.astype(np.float32, copy=False)).to(device)
@@ -202,8 +213,8 @@ def to_kf_tensor(t) -> KfTensor:
     codes = {torch.float32: KF_F32, torch.bfloat16: KF_BF16, torch.float8_e4m3fn: KF_FP8_E4M3}
     if t.dtype not in codes:
         raise TypeError(f"unsupported tensor dtype {t.dtype}")
-    if t.dim() < 1 or t.dim() > 4:
-        raise ValueError("tensors must have 1..4 dimensions")
+    if t.dim() < 1 or t.dim() > KF_MAX_DIMS:
+        raise ValueError(f"tensors must have 1..{KF_MAX_DIMS} dimensions")
     k = KfTensor()
     k.data = t.data_ptr()
     k.dtype = codes[t.dtype]
@@ -245,12 +256,12 @@ class FusedOp:
         return lib().kf_num_inputs(self._h)
 
     def input_info(self, slot: int):
-        dt, nd, shp = ctypes.c_int32(), ctypes.c_int32(), (ctypes.c_int64 * 4)()
+        dt, nd, shp = ctypes.c_int32(), ctypes.c_int32(), (ctypes.c_int64 * KF_MAX_DIMS)()
         _check(lib().kf_input_info(self._h, slot, ctypes.byref(dt), ctypes.byref(nd), shp))
         return DTYPE_NAMES[dt.value], tuple(shp[i] for i in range(nd.value))
 
     def output_info(self):
-        dt, nd, shp = ctypes.c_int32(), ctypes.c_int32(), (ctypes.c_int64 * 4)()
+        dt, nd, shp = ctypes.c_int32(), ctypes.c_int32(), (ctypes.c_int64 * KF_MAX_DIMS)()
         _check(lib().kf_output_info(self._h, ctypes.byref(dt), ctypes.byref(nd), shp))
         return DTYPE_NAMES[dt.value], tuple(shp[i] for i in range(nd.value))
 
@@ -302,5 +313,6 @@ class FusedOp:
                 dt = self.chain.get("residual_dtype", "bf16")
             else:
                 dt = "f32"
-            out.append(device_tensor(tensors[name], dt, device))
+            cl = name == "a" and self.chain["contraction"] == "conv3d_3x3x3"
+            out.append(device_tensor(tensors[name], dt, device, channels_last=cl))
         return out

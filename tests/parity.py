@@ -4,8 +4,9 @@ compare with the fp64 oracle on the same seeded bits.
 Comparison metric (max over compared elements):
     err = max |g - o| / max(|o|, floor)
 with floor = 1 (absolute error below magnitude 1, relative above) except for
-softmax outputs, whose floor is the uniform probability 1/N (values near
-1/N are compared relative to that scale).  Any NaN / Inf in the GPU output
+softmax outputs, whose floor is the uniform probability 1/N (1/cout for a
+softmax over channels; values near it are compared relative to that
+scale).  Any NaN / Inf in the GPU output
 fails.  Tolerances per input dtype: fp32 1e-4, bf16 2e-2, fp8 6e-2, all with
 fp32 accumulation.
 """
@@ -20,8 +21,11 @@ TOL = {"f32": 1e-4, "bf16": 2e-2, "e4m3": 6e-2}
 
 
 def floor_for(cfg) -> float:
-    if cfg["ops"] and cfg["ops"][-1][0] == "row_softmax":
+    names = [o[0] for o in cfg["ops"]]
+    if names and names[-1] == "row_softmax":
         return 1.0 / cfg["N"]
+    if "channel_softmax" in names:
+        return 1.0 / cfg["cout"]
     return 1.0
 
 

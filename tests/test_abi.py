@@ -59,8 +59,8 @@ def test_status_strings():
 def test_ctypes_struct_layout_matches_header():
     # kf_op 16 B; kf_op_spec: 4 ints, 8 int64, 2 floats, 2 ints, 8 ops
     assert ctypes.sizeof(kf.KfOp) == 16
-    assert ctypes.sizeof(kf.KfOpSpec) == 16 + 64 + 8 + 8 + 8 * 16
-    assert ctypes.sizeof(kf.KfTensor) == 8 + 4 + 4 + 32 + 32
+    assert ctypes.sizeof(kf.KfOpSpec) == 16 + 72 + 8 + 8 + 8 * 16
+    assert ctypes.sizeof(kf.KfTensor) == 8 + 4 + 4 + 40 + 40
 
 
 def _create(spec):
@@ -222,3 +222,29 @@ def test_rowwise_input_slots():
     ch = inputs.chain(inputs.config("F3"))
     assert kf.input_names(ch) == ["a", "gamma", "beta", "residual"]
     assert kf.input_names(inputs.chain(inputs.config("F4"))) == ["a"]
+
+
+def test_conv3d_validation():
+    for kw, status in [(dict(cin=32), kf.KF_ERR_UNSUPPORTED), (dict(cout=32), kf.KF_ERR_UNSUPPORTED),
+                       (dict(D=2), kf.KF_ERR_SHAPE), (dict(W=2), kf.KF_ERR_SHAPE),
+                       (dict(out_dtype="f32"), kf.KF_ERR_UNSUPPORTED), (dict(in_dtype="f32"), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("bias",), ("channel_softmax",), ("maxpool3d2",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("maxpool3d2",), ("maxpool3d2",), ("channel_softmax",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("maxpool3d2",), ("relu",), ("maxpool3d2",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("channel_softmax",), ("channel_softmax",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("groupnorm", 2, 1e-5)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("row_softmax",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(ops=[("maxpool2x2",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(D=2000, H=2000, W=20), kf.KF_ERR_UNSUPPORTED)]:
+        st, h = _create(_spec("F2", **kw))
+        assert st == status, (kw, st, kf.last_error())
+        assert not h.value
+    # the conv3d ops on other contractions
+    for name, ops in [("C2", [("channel_softmax",)]), ("C4", [("maxpool3d2",), ("maxpool3d2",)]),
+                      ("F4", [("channel_softmax",)])]:
+        st, _ = _create(_spec(name, ops=ops))
+        assert st == kf.KF_ERR_UNSUPPORTED, (name, ops)
+    if not _gpu_present():
+        for kw in [{}, dict(ops=[]), dict(ops=[("bias",), ("channel_softmax",)])]:
+            st, _ = _create(_spec("F2", **kw))
+            assert st == kf.KF_ERR_NO_DEVICE, (kw, kf.last_error())

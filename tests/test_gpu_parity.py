@@ -423,6 +423,94 @@ def test_c4_integer_bit_exact_tile_ranges():
         ref = oracle.conv2d_3x3(x[n:n + 1].astype(np.float64), w.astype(np.float64))
         assert np.array_equal(got_bits[n:n + 1], inputs.f32_to_bf16_bits(ref.astype(np.float32))), f"image {n}"
 
+# ------------------------------------------- Conv3d, channel softmax, pools (F2)
+
+_F2_OPS = [("bias",), ("channel_softmax",), ("maxpool3d2",), ("maxpool3d2",)]
+
+
+@pytest.mark.parametrize("batch,D,H,W,ops", [
+    (2, 7, 11, 20, _F2_OPS),            # ragged: 5 x 9 x 18 conv positions, 1 x 2 x 4 pooled cells
+    (1, 6, 10, 18, _F2_OPS),            # one exact 4 x 8 x 16 tile
+    (3, 9, 19, 35, _F2_OPS),            # 7 x 17 x 33: partial tiles in every axis
+    (2, 7, 11, 20, []),                 # the conv alone, every position (ragged rows of 18)
+    (1, 10, 12, 34, [("bias",), ("channel_softmax",)]),  # softmax, no pools, rows of 32
+    (2, 7, 11, 20, [("bias",), ("sigmoid",), ("channel_softmax",), ("scale", 2.0), ("maxpool3d2",), ("maxpool3d2",)]),
+])
+def test_f2_small(batch, D, H, W, ops):
+    _torch()
+    cfg = inputs.config("F2", batch=batch, D=D, H=H, W=W, ops=ops)
+    t = inputs.generate(cfg, seed=batch + D + H + W)
+    _, out = run_gpu(cfg, t)
+    assert tuple(out.shape) == inputs.conv3d_pooled_shape(cfg)
+    err = check(cfg, t, out)
+    print(f"F2 {batch}x{D}x{H}x{W} ops={[o[0] for o in ops]} err {err:.3e}")
+
+
+def test_f2_degenerate_shapes():
+    """3x3x3 volumes (one conv position: no pooled cell) and an empty batch
+    produce empty outputs without a launch."""
+    _torch()
+    for batch, D in [(2, 3), (0, 8)]:
+        cfg = inputs.config("F2", batch=batch, D=D, H=8, W=8)
+        t = inputs.generate(cfg, seed=5)
+        _, out = run_gpu(cfg, t)
+        assert out.numel() == 0
+
+
+def test_f2_integer_bit_exact_many_tiles():
+    """Integer inputs in [-4, 4] and weights in [-2, 2], no ops: every fp32
+    partial sum is an exact integer (|sum| <= 432 * 8), so the stored conv
+    output equals the oracle's exact sum rounded to bf16, bit for bit; 512
+    tiles, two per workgroup, across image boundaries."""
+    torch = _torch()
+    batch, D, H, W = 8, 18, 34, 66
+    cfg = inputs.config("F2", batch=batch, D=D, H=H, W=W, ops=[])
+    rng = np.random.default_rng(45)
+    x = rng.integers(-4, 5, size=(batch, 16, D, H, W)).astype(np.float32)
+    w = rng.integers(-2, 3, size=(64, 16, 3, 3, 3)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
+    _, out = run_gpu(cfg, t)
+    ref = oracle.conv3d_3x3x3(x.astype(np.float64), w.astype(np.float64))
+    assert np.all(np.abs(ref) < 2 ** 24) and np.array_equal(ref, np.round(ref))
+    ref_bits = inputs.f32_to_bf16_bits(ref.astype(np.float32))
+    got_bits = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got_bits, ref_bits)
+
+
+def test_f2_zero_weights_uniform_bit_exact():
+    """W = 0, b = 0: every softmax is uniform, so every pooled cell is 1/64
+    exactly."""
+    torch = _torch()
+    cfg = inputs.config("F2", batch=2, D=10, H=18, W=34)
+    t = inputs.generate(cfg, seed=9)
+    z = dict(t, b=np.zeros_like(t["b"]), bias=np.zeros_like(t["bias"]))
+    _, out = run_gpu(cfg, z)
+    assert torch.all(out.float() == 1.0 / 64).item()
+
+
+def test_f2_full_config_sampled_images():
+    _torch()
+    cfg = inputs.config("F2")
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    assert np.all(np.isfinite(to_host_f64(out)))
+    err = check(cfg, t, out, images=np.array([0, 7, 15]))
+    print(f"F2 full err {err:.3e}")
+
+
+def test_f2_rejects_channels_first_input():
+    torch = _torch()
+    cfg = inputs.config("F2", batch=1, D=6, H=10, W=18)
+    t = inputs.generate(cfg, seed=1)
+    op = kf.FusedOp.from_config(cfg)
+    ins = op.device_inputs(t)
+    ins[0] = ins[0].contiguous()          # NCDHW instead of channels-last
+    with pytest.raises(kf.KFError) as e:
+        op(ins, op.empty_output("cuda"))
+    assert e.value.status == kf.KF_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+
+
 # ------------------------------------------------------------ unfused chain
 
 @pytest.mark.parametrize("name,kw", [
@@ -434,6 +522,7 @@ def test_c4_integer_bit_exact_tile_ranges():
     ("F1", dict(M=300, N=520, K=136)),
     ("F3", dict(M=37, N=1024, ops=[("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)])),
     ("F4", dict(M=9, N=2048)),
+    ("F2", dict(batch=2, D=7, H=11, W=20)),
 ])
 def test_unfused_chain_parity(name, kw):
     """The one-kernel-per-op comparator must compute the same chain.  Its
@@ -499,6 +588,7 @@ def test_epilogue_operand_paths(name, kw, res_f32):
     ("F1", dict(M=300, N=520, K=136)),                                     # bias, swish, tanh, GELU(erf), hardtanh
     ("F3", dict(M=37, N=2048)),                                            # rows: GroupNorm, swish, residual
     ("F4", dict(M=37, N=4104)),                                            # rows: softmax
+    ("F2", dict(batch=2, D=7, H=11, W=20)),                                # conv3d, bias, softmax, pools
 ])
 def test_specialised_chain_matches_interpreted(name, kw):
     """The benchmarked op lists run an epilogue generated for that exact
