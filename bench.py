@@ -84,6 +84,7 @@ KERNEL_FILES = {
     "kf_gemm_f32_8x8": ["kf_gemm_f32.hip"],
     "kf_conv3x3_bf16_256x128": ["kf_conv_bf16.hip"],
     "kf_rowwise": ["kf_rowwise.hip"],
+    "kf_conv3d_bf16_64x256": ["kf_conv3d_bf16.hip"],
 }
 
 
@@ -129,7 +130,9 @@ def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
     g_all = gpu_out.cpu()
     bf16_out = g_all.dtype == torch.bfloat16
     g_all = g_all.view(torch.int16).numpy().view(np.uint16) if bf16_out else g_all.numpy()
-    floor = 1.0 / cfg["N"] if cfg["ops"] and cfg["ops"][-1][0] == "row_softmax" else 1.0
+    names = [o[0] for o in cfg["ops"]]
+    floor = (1.0 / cfg["N"] if names and names[-1] == "row_softmax" else
+             1.0 / cfg["cout"] if "channel_softmax" in names else 1.0)
 
     perm = np.random.default_rng(0).permutation(units).astype(np.int64)
     pos, done, elapsed, err = 0, 0, 0.0, 0.0
@@ -170,7 +173,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="C2", help="C1..C5, F1, F3, F4 (default C2)")
+    ap.add_argument("--workload", default="C2", help="C1..C5, F1..F4 (default C2)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")

@@ -285,7 +285,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     }
     int64_t od = s->depth - 2, oh = s->height - 2, ow = s->width - 2;
     // the unfused chain runs the conv alone over every position
-    if (s->batch * ((od + 3) / 4) * ((oh + 7) / 8) * ((ow + 15) / 16) > INT32_MAX)
+    if (s->batch * ((od + 3) / 4) * ((oh + 3) / 4) * ((ow + 15) / 16) > INT32_MAX)
       return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 supports at most 2^31 - 1 tiles");
     for (int i = 0; i < n_pool3; ++i) {
       od /= 2;
@@ -293,7 +293,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       ow /= 2;
     }
     d->variant = kVarConv3d;
-    d->kernel_name = "kf_conv3d_bf16_64x512";
+    d->kernel_name = "kf_conv3d_bf16_64x256";
     d->inputs.push_back(Slot{dt, 5, {s->batch, s->cin, s->depth, s->height, s->width}, "A", true});
     d->inputs.push_back(Slot{dt, 5, {s->cout, s->cin, 3, 3, 3}, "B", false});
     for (int i = 0; i < s->n_ops; ++i)
@@ -398,14 +398,14 @@ kf::Conv3dArgs conv3d_args(const kf_desc* d, const kf_tensor* inputs, void* out,
   a.Dp = (int32_t)(pools ? od / 4 : od);
   a.Hp = (int32_t)(pools ? oh / 4 : oh);
   a.Wp = (int32_t)(pools ? ow / 4 : ow);
-  // conv positions the output needs, in tiles of 4 x 8 x 16
+  // conv positions the output needs, in tiles of 4 x 4 x 16
   const int64_t nd = pools ? 4 * (int64_t)a.Dp : od, nh = pools ? 4 * (int64_t)a.Hp : oh,
                 nw = pools ? 4 * (int64_t)a.Wp : ow;
   a.tiles_d = (int32_t)((nd + 3) / 4);
-  a.tiles_h = (int32_t)((nh + 7) / 8);
+  a.tiles_h = (int32_t)((nh + 3) / 4);
   a.tiles_w = (int32_t)((nw + 15) / 16);
   a.tiles = (int32_t)(s.batch * a.tiles_d * a.tiles_h * a.tiles_w);
-  a.grid = d->num_cu;
+  a.grid = 2 * d->num_cu;  // two workgroups per compute unit
   return a;
 }
 

@@ -115,7 +115,7 @@ struct Conv3dArgs {
   void* out;              // [batch, cout, Dp, Hp, Wp] (NCDHW)
   int32_t pools;          // 0, or 2 (two MaxPool3d(2) = max over 4x4x4 blocks)
   int32_t Dp, Hp, Wp;     // output extents (after the pools)
-  int32_t tiles_d, tiles_h, tiles_w;  // output tiles of 4 x 8 x 16 conv positions
+  int32_t tiles_d, tiles_h, tiles_w;  // output tiles of 4 x 4 x 16 conv positions
   int32_t tiles;          // batch * tiles_d * tiles_h * tiles_w
   int32_t grid;           // workgroups of the persistent launch
 };
