@@ -177,6 +177,7 @@ def main(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 5 times (for scaling HBM byte counters)")
     args = ap.parse_args(argv)
@@ -211,6 +212,17 @@ def main(argv=None):
     out = op.empty_output("cuda:0")
     stream = torch.cuda.current_stream()
     hip = _hip()
+
+    # the plan's launch candidates, timed on these inputs; the fastest is kept
+    # (every candidate computes the same bits)
+    tuning = None
+    if not args.no_autotune:
+        r = op.autotune(ins, out, reps=max(3, args.warmup // 2))
+        keys = ("raster_group", "xcd_remap", "wg_per_cu")
+        default = [c for c in r["candidates"] if (c["raster_group"], c["xcd_remap"], c["wg_per_cu"]) == (4, 1, 2)]
+        tuning = {"config": {k: r["best"][k] for k in keys}, "candidates": len(r["candidates"]),
+                  "best_ms": round(r["best"]["seconds"] * 1e3, 5),
+                  "default_ms": round(default[0]["seconds"] * 1e3, 5) if default else None}
 
     for _ in range(args.warmup):
         op(ins, out)
@@ -260,6 +272,11 @@ def main(argv=None):
         except kf.KFError as e:
             unfused = {"error": str(e)}
 
+    traffic = _traffic(kname, cfg["workload"])
+    diag = op.diagnose(kernel_ms * 1e-3, traffic or 0.0)
+    diagnosis = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in diag.items()
+                 if k in ("bound", "compute_frac", "memory_frac", "intensity", "ridge", "workgroups", "compute_units")}
+
     cpu, err = (None, None)
     if not args.no_cpu_baseline:
         cpu, err = _cpu_baseline(cfg, tensors, out, args.cpu_budget)
@@ -293,8 +310,10 @@ def main(argv=None):
             "frac": round(achieved / peak, 4),
             "kernel_us": round(kernel_ms * 1e3, 2),
             ("bytes_per_launch" if rowwise else "flops_per_launch"): work,
-            "traffic": _traffic(kname, cfg["workload"]),
+            "traffic": traffic,
         },
+        "diagnosis": diagnosis,
+        "tuning": tuning,
         "cpu_baseline": cpu,
         "parity_err_cpu_sample": err,
     }

@@ -210,6 +210,93 @@ size_t kf_workspace_bytes(const kf_desc* desc);
 /* Name of the main (contraction) kernel the plan launches. */
 const char* kf_kernel_name(const kf_desc* desc);
 
+/* ---- Diagnosis and tuning ------------------------------------------------
+   The deterministic core of the paper's diagnosis engine (Methodology,
+   Diagnosis and Experience-Guided Feedback): from runtime statistics and the
+   kernel's launch configuration a correct kernel is classified as
+   memory-bound, latency-bound or instruction-bound, and the launch fields of
+   the plan are then searched by timing, keeping the fastest -- the paper's
+   recommendations for such kernels are to autotune tile shapes and the
+   mapping of work to programs, and to keep accesses local to the caches
+   (Appendix B, latency-bound and memory-bound lists). */
+
+typedef enum kf_bound {
+  KF_BOUND_MEMORY = 0,      /* the HBM roof is the nearer one                 */
+  KF_BOUND_INSTRUCTION = 1, /* the arithmetic (matrix-core / vector) roof is
+                               the nearer one                                 */
+  KF_BOUND_LATENCY = 2      /* neither roof is approached, or the launch has
+                               fewer workgroups than compute units           */
+} kf_bound;
+
+typedef struct kf_diagnosis {
+  double flops;         /* algorithmic FLOPs of the main kernel (2 per MAC)  */
+  double bytes;         /* HBM bytes: the measured count if one was given,
+                           else the algorithmic bytes (each input read once,
+                           the output written once)                         */
+  double seconds;       /* the main kernel's duration                        */
+  double tflops;        /* flops / seconds / 1e12                            */
+  double gbps;          /* bytes / seconds / 1e9                             */
+  double peak_tflops;   /* dense peak of the kernel's arithmetic on MI355X   */
+  double peak_gbps;     /* HBM peak of MI355X (8000)                         */
+  double compute_frac;  /* tflops / peak_tflops                              */
+  double memory_frac;   /* gbps / peak_gbps                                  */
+  double intensity;     /* flops / bytes                                     */
+  double ridge;         /* peak FLOP/s / peak byte/s                         */
+  int64_t workgroups;   /* workgroups the main kernel launches               */
+  int32_t compute_units;
+  int32_t bound;        /* kf_bound                                          */
+} kf_diagnosis;
+
+/* The classification rule alone (no descriptor, no device): latency-bound if
+   workgroups < compute_units or both fractions are below 0.25, else
+   memory-bound if memory_frac >= compute_frac, else instruction-bound.
+   Fills every field of *out from the arguments; seconds must be > 0. */
+kf_status kf_classify(double flops, double bytes, double seconds, double peak_tflops, double peak_gbps,
+                      int64_t workgroups, int32_t compute_units, kf_diagnosis* out);
+
+/* Diagnose a planned op from a measured main-kernel duration (for instance
+   the event pair of kf_fused_op_timed) and, if hbm_bytes > 0, a measured HBM
+   byte count (e.g. the FETCH_SIZE + WRITE_SIZE counters of one launch);
+   hbm_bytes <= 0 uses the algorithmic bytes of the plan. */
+kf_status kf_diagnose(const kf_desc* desc, double kernel_seconds, double hbm_bytes, kf_diagnosis* out);
+
+typedef struct kf_tuning {
+  int32_t raster_group; /* GEMM: consecutive tiles walk this many tile rows
+                           column by column (1..64; default 4)               */
+  int32_t xcd_remap;    /* GEMM, CONV3D: 1 = the workgroups of one XCD take a
+                           contiguous range of tiles (default), 0 = the
+                           hardware's round-robin order                      */
+  int32_t wg_per_cu;    /* CONV3D: persistent workgroups per compute unit,
+                           1 or 2 (default 2)                                */
+  int32_t reserved;     /* 0                                                 */
+} kf_tuning;
+
+/* The plan's launch fields.  None of them changes a result bit: they reorder
+   independent tiles or resize a persistent grid.  kf_set_tuning validates
+   the values (KF_ERR_INVALID_ARG) and takes effect at the next call. */
+kf_status kf_get_tuning(const kf_desc* desc, kf_tuning* out);
+kf_status kf_set_tuning(kf_desc* desc, const kf_tuning* tuning);
+
+#define KF_MAX_TUNE_CANDIDATES 16
+
+typedef struct kf_tune_result {
+  int32_t n;            /* candidates timed                                  */
+  int32_t best;         /* index of the fastest                              */
+  kf_tuning config[KF_MAX_TUNE_CANDIDATES];
+  double seconds[KF_MAX_TUNE_CANDIDATES]; /* mean time of one kf_fused_op    */
+} kf_tune_result;
+
+/* Time every candidate launch configuration of the plan on the caller's
+   tensors -- one warm-up call, then `reps` (1..1000) calls between two HIP
+   events on `stream`, per candidate -- keep the fastest in the descriptor
+   and report all of them in *result.  Blocks until the stream is idle;
+   outputs[0] holds the result of the last call (the same bits for every
+   candidate).  Candidates: GEMM (bf16 / fp8) raster groups {1, 2, 4, 8, 16}
+   x XCD order {contiguous, hardware}; CONV3D workgroups per CU {2, 1} x XCD
+   order; every other plan has only its current configuration. */
+kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
+                      kf_tune_result* result);
+
 /* Static description of a status code. */
 const char* kf_status_string(kf_status status);
 

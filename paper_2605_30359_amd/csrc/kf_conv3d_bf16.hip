@@ -130,7 +130,8 @@ __global__ __launch_bounds__(NT3, 2) void kf_conv3d_bf16_64x256(Conv3dArgs p, co
   // round r of the persistent loop: the workgroups of XCD (b % 8) take
   // consecutive tiles
   const int G = p.grid;
-  const int slot = (G & 7) == 0 ? (int)(blockIdx.x & 7) * (G >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
+  const int slot =
+      (p.xcd_remap && (G & 7) == 0) ? (int)(blockIdx.x & 7) * (G >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
   auto tile_at = [&](int round) { return round * G + slot; };
   int t = tile_at(0);
   if (t >= p.tiles) return;

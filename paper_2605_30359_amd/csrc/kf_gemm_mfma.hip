@@ -12,6 +12,7 @@ hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, 
   GemmArgs p = args;
   p.tiles_m = (int)((p.M + BM - 1) / BM);
   p.tiles_n = (int)((p.N + BN - 1) / BN);
+  if (p.raster_group < 1) p.raster_group = 4;
   const dim3 grid(p.tiles_m * p.tiles_n), block(NT);
   if (fp8) {
     if (b_nk)

@@ -38,13 +38,14 @@ namespace {
 
 constexpr int BM = 256;
 
-__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int G, bool xcd_remap, int& tm,
+                                            int& tn) {
   const int nwg = tiles_m * tiles_n;
   int lid = bid;
   // Workgroups are dispatched round-robin over the 8 XCDs; renumber so that
   // each XCD receives a contiguous range of logical tiles.
-  if ((nwg & 7) == 0) lid = (bid & 7) * (nwg >> 3) + (bid >> 3);
-  constexpr int G = 4;
+  if (xcd_remap && (nwg & 7) == 0) lid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  // consecutive logical tiles walk a group of G tile rows column by column
   const int per_group = G * tiles_n;
   const int group = lid / per_group;
   const int first_m = group * G;
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   const int wn = wave >> 1;
 
   int tm, tn;
-  tile_coords(blockIdx.x, p.tiles_m, p.tiles_n, tm, tn);
+  tile_coords(blockIdx.x, p.tiles_m, p.tiles_n, p.raster_group, p.xcd_remap != 0, tm, tn);
   const int64_t m0 = (int64_t)tm * BM;
   const int64_t n0 = (int64_t)tn * BN;
   const int K = (int)p.K;

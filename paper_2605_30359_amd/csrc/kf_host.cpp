@@ -74,6 +74,7 @@ struct kf_desc {
   size_t workspace_bytes;
   int tiles_n;
   std::string kernel_name;
+  kf_tuning tuning;  // launch fields (see kf_set_tuning)
   // unfused comparator: two intermediate buffers, allocated on first use
   mutable void* ubuf[2];
   mutable size_t ubuf_bytes;
@@ -405,7 +406,8 @@ kf::Conv3dArgs conv3d_args(const kf_desc* d, const kf_tensor* inputs, void* out,
   a.tiles_h = (int32_t)((nh + 3) / 4);
   a.tiles_w = (int32_t)((nw + 15) / 16);
   a.tiles = (int32_t)(s.batch * a.tiles_d * a.tiles_h * a.tiles_w);
-  a.grid = 2 * d->num_cu;  // two workgroups per compute unit
+  a.grid = d->tuning.wg_per_cu * d->num_cu;  // persistent: wg_per_cu workgroups per compute unit
+  a.xcd_remap = d->tuning.xcd_remap;
   return a;
 }
 
@@ -415,9 +417,168 @@ int conv3d_pool_count(const kf_op_spec& s) {
   return n;
 }
 
+
+// Algorithmic work of the plan's main kernel: FLOPs (2 per multiply-add of
+// the contraction), bytes (each input read once, the output written once),
+// workgroups launched and the dense peak of its arithmetic.
+struct Work {
+  double flops, bytes, peak_tflops;
+  int64_t workgroups;
+};
+
+Work plan_work(const kf_desc* d) {
+  const kf_op_spec& s = d->spec;
+  Work w{0.0, 0.0, 157.3, 0};
+  auto numel = [](const Slot& sl) {
+    double n = 1.0;
+    for (int i = 0; i < sl.ndim; ++i) n *= (double)sl.shape[i];
+    return n;
+  };
+  for (const Slot& sl : d->inputs) w.bytes += numel(sl) * (double)elem_size(sl.dtype);
+  w.bytes += numel(d->output) * (double)elem_size(d->output.dtype);
+  switch (d->variant) {
+    case kVarGemmF32:
+      w.flops = 2.0 * s.M * s.N * s.K;
+      w.workgroups = ((s.M + 7) / 8) * ((s.N + 7) / 8);
+      break;
+    case kVarGemmBf16:
+    case kVarGemmFp8: {
+      w.flops = 2.0 * s.M * s.N * s.K;
+      w.peak_tflops = d->variant == kVarGemmFp8 ? 5033.2 : 2516.6;
+      const int64_t bm = kf::gemm_mfma_tile_m(), bn = kf::gemm_mfma_tile_n();
+      w.workgroups = ((s.M + bm - 1) / bm) * ((s.N + bn - 1) / bn);
+      break;
+    }
+    case kVarConvBf16:
+      w.flops = 2.0 * s.batch * s.height * s.width * s.cout * s.cin * 9;
+      w.peak_tflops = 2516.6;
+      w.workgroups = std::min<int64_t>(d->num_cu, s.batch * (s.height / 2));
+      break;
+    case kVarConv3d: {
+      w.flops = 2.0 * s.batch * (s.depth - 2) * (s.height - 2) * (s.width - 2) * s.cout * s.cin * 27;
+      w.peak_tflops = 2516.6;
+      int pools = 0;
+      for (int i = 0; i < s.n_ops; ++i) pools += s.ops[i].kind == KF_OP_MAXPOOL3D_2;
+      kf_tensor dummy[1];
+      memset(dummy, 0, sizeof(dummy));
+      const kf::Conv3dArgs a = conv3d_args(d, dummy, nullptr, pools);
+      w.workgroups = std::min<int64_t>(a.grid, a.tiles);
+      break;
+    }
+    case kVarRowwise:
+      w.workgroups = s.M;
+      break;
+  }
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
+
+kf_status kf_classify(double flops, double bytes, double seconds, double peak_tflops, double peak_gbps,
+                      int64_t workgroups, int32_t compute_units, kf_diagnosis* out) {
+  if (!out) return fail(KF_ERR_INVALID_ARG, "out is NULL");
+  if (!(seconds > 0.0) || !(peak_tflops > 0.0) || !(peak_gbps > 0.0) || flops < 0.0 || bytes < 0.0)
+    return fail(KF_ERR_INVALID_ARG, "seconds and peaks must be > 0, flops and bytes >= 0");
+  kf_diagnosis& g = *out;
+  g.flops = flops;
+  g.bytes = bytes;
+  g.seconds = seconds;
+  g.tflops = flops / seconds * 1e-12;
+  g.gbps = bytes / seconds * 1e-9;
+  g.peak_tflops = peak_tflops;
+  g.peak_gbps = peak_gbps;
+  g.compute_frac = g.tflops / peak_tflops;
+  g.memory_frac = g.gbps / peak_gbps;
+  g.intensity = bytes > 0.0 ? flops / bytes : 0.0;
+  g.ridge = peak_tflops * 1e12 / (peak_gbps * 1e9);
+  g.workgroups = workgroups;
+  g.compute_units = compute_units;
+  constexpr double kLatencyFrac = 0.25;
+  if (workgroups < compute_units || (g.compute_frac < kLatencyFrac && g.memory_frac < kLatencyFrac))
+    g.bound = KF_BOUND_LATENCY;
+  else
+    g.bound = g.memory_frac >= g.compute_frac ? KF_BOUND_MEMORY : KF_BOUND_INSTRUCTION;
+  return ok();
+}
+
+kf_status kf_diagnose(const kf_desc* d, double kernel_seconds, double hbm_bytes, kf_diagnosis* out) {
+  if (!d || !out) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  const Work w = plan_work(d);
+  return kf_classify(w.flops, hbm_bytes > 0.0 ? hbm_bytes : w.bytes, kernel_seconds, w.peak_tflops, 8000.0,
+                     w.workgroups, d->num_cu, out);
+}
+
+kf_status kf_get_tuning(const kf_desc* d, kf_tuning* out) {
+  if (!d || !out) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  *out = d->tuning;
+  return ok();
+}
+
+kf_status kf_set_tuning(kf_desc* d, const kf_tuning* t) {
+  if (!d || !t) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  if (t->raster_group < 1 || t->raster_group > 64) return fail(KF_ERR_INVALID_ARG, "raster_group must be in [1, 64]");
+  if (t->xcd_remap != 0 && t->xcd_remap != 1) return fail(KF_ERR_INVALID_ARG, "xcd_remap must be 0 or 1");
+  if (t->wg_per_cu != 1 && t->wg_per_cu != 2) return fail(KF_ERR_INVALID_ARG, "wg_per_cu must be 1 or 2");
+  d->tuning = *t;
+  d->tuning.reserved = 0;
+  return ok();
+}
+
+kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
+                      kf_tune_result* result) {
+  if (!d || !inputs || !outputs || !result) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  if (reps < 1 || reps > 1000) return fail(KF_ERR_INVALID_ARG, "reps must be in [1, 1000]");
+  std::vector<kf_tuning> cand;
+  const kf_tuning cur = d->tuning;
+  if (d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) {
+    for (int remap = 1; remap >= 0; --remap)
+      for (int g : {1, 2, 4, 8, 16}) cand.push_back(kf_tuning{g, remap, cur.wg_per_cu, 0});
+  } else if (d->variant == kVarConv3d) {
+    for (int remap = 1; remap >= 0; --remap)
+      for (int wg : {2, 1}) cand.push_back(kf_tuning{cur.raster_group, remap, wg, 0});
+  } else {
+    cand.push_back(cur);
+  }
+  memset(result, 0, sizeof(*result));
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    (void)hipGetLastError();
+    if (e0) (void)hipEventDestroy(e0);
+    return fail(KF_ERR_HIP, "hipEventCreate failed");
+  }
+  kf_status st = KF_OK;
+  int best = -1;
+  for (size_t c = 0; c < cand.size() && c < KF_MAX_TUNE_CANDIDATES && st == KF_OK; ++c) {
+    d->tuning = cand[c];
+    st = kf_fused_op(d, inputs, outputs, stream);  // warm-up (also validates the tensors)
+    if (st != KF_OK) break;
+    if (hipEventRecord(e0, hs) != hipSuccess) st = fail(KF_ERR_HIP, "hipEventRecord failed");
+    for (int r = 0; r < reps && st == KF_OK; ++r) st = kf_fused_op(d, inputs, outputs, stream);
+    if (st != KF_OK) break;
+    float ms = 0.0f;
+    if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+        hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+      st = fail(KF_ERR_HIP, "timing a candidate failed: %s", hipGetErrorString(hipGetLastError()));
+      break;
+    }
+    result->config[c] = cand[c];
+    result->seconds[c] = (double)ms * 1e-3 / reps;
+    result->n = (int32_t)c + 1;
+    if (best < 0 || result->seconds[c] < result->seconds[best]) best = (int)c;
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (st != KF_OK || best < 0) {
+    d->tuning = cur;
+    return st != KF_OK ? st : fail(KF_ERR_INVALID_ARG, "no candidate configuration");
+  }
+  result->best = best;
+  d->tuning = result->config[best];
+  return ok();
+}
 
 const char* kf_status_string(kf_status st) {
   switch (st) {
@@ -444,6 +605,7 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
   d->tiles_n = 0;
   d->ubuf[0] = d->ubuf[1] = nullptr;
   d->ubuf_bytes = 0;
+  d->tuning = kf_tuning{4, 1, 2, 0};
   kf_status st = validate_and_plan(spec, d);
   if (st != KF_OK) {
     delete d;
@@ -621,6 +783,8 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
     a.ldo = outputs[0].ndim == 2 ? outputs[0].stride[0] : 1;
     a.out_bf16 = outputs[0].dtype == KF_BF16;
     a.partials = d->workspace;
+    a.raster_group = d->tuning.raster_group;
+    a.xcd_remap = d->tuning.xcd_remap;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
     hipError_t e = hipSuccess;
     if (ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
@@ -743,6 +907,8 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     a.ldo = s.n_ops ? s.N : (outputs[0].ndim == 2 ? outputs[0].stride[0] : 1);
     a.out_bf16 = cur_bf16;
     a.red_index = 0;
+    a.raster_group = d->tuning.raster_group;
+    a.xcd_remap = d->tuning.xcd_remap;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
     e = d->variant == kVarGemmF32 ? kf::launch_gemm_f32(a, nk, hs)
                                   : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk);

@@ -69,6 +69,8 @@ struct GemmArgs {
   int32_t gn_group;       // GroupNorm group width in columns (0 = none)
   int32_t red_index;      // position of the reduction op in prog (n if none)
   float scale;            // dequantisation factor applied to the accumulator
+  int32_t raster_group;   // tile rows walked together (column by column) by consecutive tiles
+  int32_t xcd_remap;      // 1: each XCD takes a contiguous range of tiles
 };
 
 // Arguments of the row-wise kernel (no contraction: h = A).
@@ -118,6 +120,7 @@ struct Conv3dArgs {
   int32_t tiles_d, tiles_h, tiles_w;  // output tiles of 4 x 4 x 16 conv positions
   int32_t tiles;          // batch * tiles_d * tiles_h * tiles_w
   int32_t grid;           // workgroups of the persistent launch
+  int32_t xcd_remap;      // 1: the workgroups of one XCD take consecutive tiles
 };
 
 }  // namespace kf

@@ -38,7 +38,10 @@ DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
-            "kf_status_string", "kf_last_error")
+            "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
+            "kf_autotune")
+BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
+KF_MAX_TUNE_CANDIDATES = 16
 
 
 class KfOp(ctypes.Structure):
@@ -60,6 +63,30 @@ class KfOpSpec(ctypes.Structure):
 class KfTensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
                 ("shape", ctypes.c_int64 * KF_MAX_DIMS), ("stride", ctypes.c_int64 * KF_MAX_DIMS)]
+
+
+class KfDiagnosis(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("flops", "bytes", "seconds", "tflops", "gbps", "peak_tflops",
+                                               "peak_gbps", "compute_frac", "memory_frac", "intensity", "ridge")] + \
+               [("workgroups", ctypes.c_int64), ("compute_units", ctypes.c_int32), ("bound", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        d = {n: getattr(self, n) for n, _ in self._fields_}
+        d["bound"] = BOUNDS[self.bound]
+        return d
+
+
+class KfTuning(ctypes.Structure):
+    _fields_ = [("raster_group", ctypes.c_int32), ("xcd_remap", ctypes.c_int32), ("wg_per_cu", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        return {"raster_group": self.raster_group, "xcd_remap": self.xcd_remap, "wg_per_cu": self.wg_per_cu}
+
+
+class KfTuneResult(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("best", ctypes.c_int32), ("config", KfTuning * KF_MAX_TUNE_CANDIDATES),
+                ("seconds", ctypes.c_double * KF_MAX_TUNE_CANDIDATES)]
 
 
 class KFError(RuntimeError):
@@ -104,6 +131,18 @@ def lib():
         L.kf_status_string.restype = ctypes.c_char_p
         L.kf_last_error.argtypes = []
         L.kf_last_error.restype = ctypes.c_char_p
+        dbl = ctypes.c_double
+        L.kf_classify.argtypes = [dbl, dbl, dbl, dbl, dbl, ctypes.c_int64, i32, ctypes.POINTER(KfDiagnosis)]
+        L.kf_classify.restype = i32
+        L.kf_diagnose.argtypes = [vp, dbl, dbl, ctypes.POINTER(KfDiagnosis)]
+        L.kf_diagnose.restype = i32
+        L.kf_get_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
+        L.kf_get_tuning.restype = i32
+        L.kf_set_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
+        L.kf_set_tuning.restype = i32
+        L.kf_autotune.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp, i32,
+                                  ctypes.POINTER(KfTuneResult)]
+        L.kf_autotune.restype = i32
         _lib = L
     return _lib
 
@@ -119,6 +158,15 @@ def last_error() -> str:
 def _check(status: int):
     if status != KF_OK:
         raise KFError(status, last_error())
+
+
+def classify(flops: float, bytes_: float, seconds: float, peak_tflops: float, peak_gbps: float,
+             workgroups: int, compute_units: int) -> dict:
+    """kf_classify: the bound of a kernel from its work, time and launch."""
+    g = KfDiagnosis()
+    _check(lib().kf_classify(flops, bytes_, seconds, peak_tflops, peak_gbps, workgroups, compute_units,
+                             ctypes.byref(g)))
+    return g.as_dict()
 
 
 # ------------------------------------------------------------ spec building
@@ -302,6 +350,34 @@ class FusedOp:
 
     def unfused(self, inputs, out=None, stream=None):
         return self._call(lib().kf_unfused_op, inputs, out, stream)
+
+    def diagnose(self, kernel_seconds: float, hbm_bytes: float = 0.0) -> dict:
+        g = KfDiagnosis()
+        _check(lib().kf_diagnose(self._h, kernel_seconds, hbm_bytes or 0.0, ctypes.byref(g)))
+        return g.as_dict()
+
+    def tuning(self) -> dict:
+        t = KfTuning()
+        _check(lib().kf_get_tuning(self._h, ctypes.byref(t)))
+        return t.as_dict()
+
+    def set_tuning(self, raster_group: int, xcd_remap: int, wg_per_cu: int):
+        t = KfTuning(raster_group, xcd_remap, wg_per_cu, 0)
+        _check(lib().kf_set_tuning(self._h, ctypes.byref(t)))
+
+    def autotune(self, inputs, out, reps: int = 5, stream=None) -> dict:
+        """kf_autotune: time the plan's launch candidates, keep the fastest."""
+        torch = _torch()
+        arr = (KfTensor * max(1, len(inputs)))(*[to_kf_tensor(t) for t in inputs])
+        o = (KfTensor * 1)(to_kf_tensor(out))
+        if stream is None:
+            stream = torch.cuda.current_stream(out.device).cuda_stream
+        elif not isinstance(stream, int):
+            stream = stream.cuda_stream
+        r = KfTuneResult()
+        _check(lib().kf_autotune(self._h, arr, o, ctypes.c_void_p(stream), reps, ctypes.byref(r)))
+        cands = [dict(r.config[i].as_dict(), seconds=r.seconds[i]) for i in range(r.n)]
+        return {"best": cands[r.best], "candidates": cands}
 
     def device_inputs(self, tensors: dict, device="cuda") -> list:
         """Marshal raw generated storage into the slot order of this op."""

@@ -181,7 +181,8 @@ def test_struct_offsets_match_c_compiler(tmp_path):
     cc = shutil.which("gcc") or shutil.which("cc")
     if cc is None:
         pytest.skip("no C compiler")
-    structs = [("kf_op", kf.KfOp), ("kf_op_spec", kf.KfOpSpec), ("kf_tensor", kf.KfTensor)]
+    structs = [("kf_op", kf.KfOp), ("kf_op_spec", kf.KfOpSpec), ("kf_tensor", kf.KfTensor),
+               ("kf_diagnosis", kf.KfDiagnosis), ("kf_tuning", kf.KfTuning), ("kf_tune_result", kf.KfTuneResult)]
     lines, want = [], []
     for cname, py in structs:
         for f in py._fields_:
@@ -248,3 +249,28 @@ def test_conv3d_validation():
         for kw in [{}, dict(ops=[]), dict(ops=[("bias",), ("channel_softmax",)])]:
             st, _ = _create(_spec("F2", **kw))
             assert st == kf.KF_ERR_NO_DEVICE, (kw, kf.last_error())
+
+
+# ------------------------------------------------------------ diagnosis rule
+
+def test_classify_bounds():
+    """The three classes of the diagnosis rule on hand-computed cases
+    (MI355X bf16 peak 2516.6 TFLOP/s, HBM 8000 GB/s, 256 compute units)."""
+    P, B, CU = 2516.6, 8000.0, 256
+    # 4096^3 bf16 GEMM in 100 us: 1374 TFLOP/s = 54.6 % of peak, 0.67 GB/ms -> instruction-bound
+    g = kf.classify(2 * 4096 ** 3, 3 * 4096 * 4096 * 2, 100e-6, P, B, 256, CU)
+    assert g["bound"] == "instruction"
+    assert abs(g["tflops"] - 2 * 4096 ** 3 / 100e-6 / 1e12) < 1e-6 and abs(g["compute_frac"] - g["tflops"] / P) < 1e-12
+    assert abs(g["ridge"] - P * 1e12 / (B * 1e9)) < 1e-9
+    # 256 MiB streamed in 50 us (5369 GB/s, 67 %), no FLOPs -> memory-bound
+    g = kf.classify(0.0, 2 * 2 ** 27, 50e-6, P, B, 8192, CU)
+    assert g["bound"] == "memory" and abs(g["memory_frac"] - 2 ** 28 / 50e-6 / 1e9 / B) < 1e-12
+    # tiny fp32 op: 8.4 MFLOP and 0.6 MB in 6 us -> far below both roofs -> latency-bound
+    g = kf.classify(8388608, 624640, 6e-6, 157.3, B, 256, CU)
+    assert g["bound"] == "latency" and g["compute_frac"] < 0.25 and g["memory_frac"] < 0.25
+    # a launch with fewer workgroups than compute units is latency-bound whatever the rates
+    assert kf.classify(2 * 4096 ** 3, 1e8, 100e-6, P, B, 64, CU)["bound"] == "latency"
+    # ties between the roofs go to memory
+    assert kf.classify(P * 1e12 * 0.5, B * 1e9 * 0.5, 1.0, P, B, 1000, CU)["bound"] == "memory"
+    with pytest.raises(kf.KFError):
+        kf.classify(1.0, 1.0, 0.0, P, B, 1, CU)

@@ -606,3 +606,83 @@ def test_specialised_chain_matches_interpreted(name, kw):
         a, b = a.view(torch.int16), b.view(torch.int16)
     assert torch.equal(a, b), f"{name}: specialised and interpreted epilogues differ"
     check(cfg, t, out_spec)
+
+
+# ------------------------------------------------- launch tuning, diagnosis
+
+@pytest.mark.parametrize("name,kw", [
+    ("C3", dict(M=1024, N=1024, K=136, ops=[("groupnorm", 4, 1e-5), ("swish",), ("residual_add",)])),  # 16 tiles
+    ("C5", dict(M=1024, N=2048, K=128)),                                  # fp8, softmax rows across 8 column tiles
+    ("F2", dict(batch=3, D=9, H=19, W=35)),                               # conv3d, partial tiles
+])
+def test_tuning_candidates_bit_identical(name, kw):
+    """Every launch configuration the tuner may pick computes the same bits:
+    the fields only reorder independent tiles or resize a persistent grid."""
+    torch = _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=51)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    ref = op.empty_output("cuda")
+    op(ins, ref)
+    configs = ([(g, r, 2) for r in (1, 0) for g in (1, 2, 4, 8, 16)] if name != "F2" else
+               [(4, r, w) for r in (1, 0) for w in (2, 1)])
+    for g, r, w in configs:
+        op.set_tuning(g, r, w)
+        out = op.empty_output("cuda")
+        op(ins, out)
+        a, b = (ref, out) if ref.dtype != torch.bfloat16 else (ref.view(torch.int16), out.view(torch.int16))
+        assert torch.equal(a, b), (name, g, r, w)
+    check(cfg, t, ref)
+
+
+@pytest.mark.parametrize("name,kw,n", [
+    ("C2", dict(M=1024, N=2048, K=512), 10),
+    ("F2", dict(batch=2, D=10, H=18, W=34), 4),
+    ("F4", dict(M=256, N=2048), 1),
+])
+def test_autotune_keeps_the_fastest_candidate(name, kw, n):
+    _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=52)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    out = op.empty_output("cuda")
+    r = op.autotune(ins, out, reps=3)
+    assert len(r["candidates"]) == n
+    assert all(c["seconds"] > 0 for c in r["candidates"])
+    assert r["best"]["seconds"] == min(c["seconds"] for c in r["candidates"])
+    best = {k: r["best"][k] for k in ("raster_group", "xcd_remap", "wg_per_cu")}
+    assert op.tuning() == best
+    check(cfg, t, out)
+    out2 = op.empty_output("cuda")
+    op(ins, out2)
+    check(cfg, t, out2)
+    with pytest.raises(kf.KFError):
+        op.set_tuning(0, 1, 2)
+
+
+@pytest.mark.parametrize("name,bound", [("C1", "latency"), ("C2", "instruction"), ("F4", "memory")])
+def test_diagnosis_of_reference_workloads(name, bound):
+    """The diagnosis rule on measured times: the 32 x 512 fp32 linear layer is
+    latency-bound, the 4096^3 bf16 GEMM instruction-bound, and the softmax
+    over stored 8192 x 8192 bf16 rows memory-bound."""
+    torch = _torch()
+    cfg = inputs.config(name)
+    t = inputs.generate(cfg)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    out = op.empty_output("cuda")
+    for _ in range(3):
+        op(ins, out)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(10):
+        op(ins, out)
+    e.record()
+    torch.cuda.synchronize()
+    sec = s.elapsed_time(e) * 1e-3 / 10
+    g = op.diagnose(sec)
+    print(f"{name}: {g['bound']} compute {g['compute_frac']:.3f} memory {g['memory_frac']:.3f}")
+    assert g["bound"] == bound
+    assert g["flops"] == inputs.flops(cfg)
