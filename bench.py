@@ -18,8 +18,14 @@ already resident in device memory.  The default workload is the bf16 GEMM
   unfused      the same operation as the library's own one-kernel-per-op
                chain, timed the same way; speedup = unfused / fused time
   cpu_baseline the fp64 oracle timed on the host cores over a bounded sample
-               of rows of the same workload (every op in the chain is
-               row-local, so a row sample is the same computation per row)
+               of rows (or images) of the same workload (every op in the
+               chain is local to a row or an image, so a sample is the same
+               computation per unit)
+  tuning       the launch configuration kf_autotune kept before the timed
+               steps (every candidate computes the same bits), or the one
+               given with --tuning
+  diagnosis    kf_diagnose on the measured kernel time: compute and memory
+               fractions of the MI355X peaks and the bound
 """
 from __future__ import annotations
 
@@ -178,6 +184,9 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
+    ap.add_argument("--tuning", default=None, metavar="RG,XR,WG",
+                    help="use this launch configuration (raster group, XCD order, workgroups per CU) "
+                         "instead of autotuning")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 5 times (for scaling HBM byte counters)")
     args = ap.parse_args(argv)
@@ -216,7 +225,11 @@ def main(argv=None):
     # the plan's launch candidates, timed on these inputs; the fastest is kept
     # (every candidate computes the same bits)
     tuning = None
-    if not args.no_autotune:
+    if args.tuning:
+        rg, xr, wg = (int(v) for v in args.tuning.split(","))
+        op.set_tuning(rg, xr, wg)
+        tuning = {"config": op.tuning(), "candidates": 0, "best_ms": None, "default_ms": None}
+    elif not args.no_autotune:
         r = op.autotune(ins, out, reps=max(3, args.warmup // 2))
         keys = ("raster_group", "xcd_remap", "wg_per_cu")
         default = [c for c in r["candidates"] if (c["raster_group"], c["xcd_remap"], c["wg_per_cu"]) == (4, 1, 2)]
