@@ -380,19 +380,22 @@ kf_status check_tensor(const kf_tensor* t, const Slot& s, bool is_output, bool v
 bool fits_31(int64_t bytes) { return bytes >= 0 && bytes < (int64_t(1) << 31); }
 
 // Kernel arguments of a CONV3D_3X3X3 plan; pools = 0 stores every conv
-// output position, pools = 2 the 4x4x4-block maxima.
+// output position, pools = 2 the 4x4x4-block maxima.  inputs may be NULL
+// (the launch shape alone, for planning): then no tensor pointer is set.
 kf::Conv3dArgs conv3d_args(const kf_desc* d, const kf_tensor* inputs, void* out, int pools) {
   const kf_op_spec& s = d->spec;
   kf::Conv3dArgs a;
   memset(&a, 0, sizeof(a));
-  a.x = inputs[0].data;
   a.batch = (int32_t)s.batch;
   a.D = (int32_t)s.depth;
   a.H = (int32_t)s.height;
   a.W = (int32_t)s.width;
   a.prog = d->prog;
-  for (int i = 0; i < s.n_ops; ++i)
-    if (s.ops[i].kind == KF_OP_BIAS) a.bias = static_cast<const float*>(inputs[2].data);
+  if (inputs) {
+    a.x = inputs[0].data;
+    for (int i = 0; i < s.n_ops; ++i)
+      if (s.ops[i].kind == KF_OP_BIAS) a.bias = static_cast<const float*>(inputs[2].data);
+  }
   a.out = out;
   a.pools = pools;
   const int64_t od = s.depth - 2, oh = s.height - 2, ow = s.width - 2;
@@ -459,9 +462,7 @@ Work plan_work(const kf_desc* d) {
       w.peak_tflops = 2516.6;
       int pools = 0;
       for (int i = 0; i < s.n_ops; ++i) pools += s.ops[i].kind == KF_OP_MAXPOOL3D_2;
-      kf_tensor dummy[1];
-      memset(dummy, 0, sizeof(dummy));
-      const kf::Conv3dArgs a = conv3d_args(d, dummy, nullptr, pools);
+      const kf::Conv3dArgs a = conv3d_args(d, nullptr, nullptr, pools);
       w.workgroups = std::min<int64_t>(a.grid, a.tiles);
       break;
     }
