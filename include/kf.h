@@ -291,8 +291,8 @@ typedef struct kf_tune_result {
    events on `stream`, per candidate -- keep the fastest in the descriptor
    and report all of them in *result.  Blocks until the stream is idle;
    outputs[0] holds the result of the last call (the same bits for every
-   candidate).  Candidates: GEMM (bf16 / fp8) raster groups {1, 2, 4, 8, 16}
-   x XCD order {contiguous, hardware}; CONV3D workgroups per CU {2, 1} x XCD
+   candidate).  Candidates: GEMM (bf16 / fp8) raster groups {1, 2, 4, 8, 16, 32,
+   64} x XCD order {contiguous, hardware}; CONV3D workgroups per CU {2, 1} x XCD
    order; every other plan has only its current configuration. */
 kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
                       kf_tune_result* result);

@@ -535,7 +535,7 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
   const kf_tuning cur = d->tuning;
   if (d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) {
     for (int remap = 1; remap >= 0; --remap)
-      for (int g : {1, 2, 4, 8, 16}) cand.push_back(kf_tuning{g, remap, cur.wg_per_cu, 0});
+      for (int g : {1, 2, 4, 8, 16, 32, 64}) cand.push_back(kf_tuning{g, remap, cur.wg_per_cu, 0});
   } else if (d->variant == kVarConv3d) {
     for (int remap = 1; remap >= 0; --remap)
       for (int wg : {2, 1}) cand.push_back(kf_tuning{cur.raster_group, remap, wg, 0});

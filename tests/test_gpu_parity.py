@@ -625,7 +625,7 @@ def test_tuning_candidates_bit_identical(name, kw):
     ins = op.device_inputs(t)
     ref = op.empty_output("cuda")
     op(ins, ref)
-    configs = ([(g, r, 2) for r in (1, 0) for g in (1, 2, 4, 8, 16)] if name != "F2" else
+    configs = ([(g, r, 2) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)] if name != "F2" else
                [(4, r, w) for r in (1, 0) for w in (2, 1)])
     for g, r, w in configs:
         op.set_tuning(g, r, w)
@@ -637,7 +637,7 @@ def test_tuning_candidates_bit_identical(name, kw):
 
 
 @pytest.mark.parametrize("name,kw,n", [
-    ("C2", dict(M=1024, N=2048, K=512), 10),
+    ("C2", dict(M=1024, N=2048, K=512), 14),
     ("F2", dict(batch=2, D=10, H=18, W=34), 4),
     ("F4", dict(M=256, N=2048), 1),
 ])
@@ -662,7 +662,8 @@ def test_autotune_keeps_the_fastest_candidate(name, kw, n):
         op.set_tuning(0, 1, 2)
 
 
-@pytest.mark.parametrize("name,bound", [("C1", "latency"), ("C2", "instruction"), ("F4", "memory")])
+@pytest.mark.parametrize("name,bound", [("C1", "latency"), ("C2", "instruction"), ("F4", "memory"),
+                                        ("F2", "instruction")])
 def test_diagnosis_of_reference_workloads(name, bound):
     """The diagnosis rule on measured times: the 32 x 512 fp32 linear layer is
     latency-bound, the 4096^3 bf16 GEMM instruction-bound, and the softmax
