@@ -89,11 +89,13 @@ __device__ __forceinline__ float f_sigmoid(float x) { return frcp(1.0f + fexp(-x
 __device__ __forceinline__ float f_swish(float x) { return x * f_sigmoid(x); }
 // tanh(x) = 2 sigmoid(2x) - 1
 __device__ __forceinline__ float f_tanh(float x) { return 2.0f * f_sigmoid(2.0f * x) - 1.0f; }
-// 0.5 x (1 + tanh(u)) = x sigmoid(2u), u = sqrt(2/pi) (x + 0.044715 x^3)
+// 0.5 x (1 + tanh(u)) = x sigmoid(2u) = x / (1 + 2^t), u = sqrt(2/pi) (x +
+// 0.044715 x^3), t = -2 u log2 e = x (a + b x^2) with the constants folded
 __device__ __forceinline__ float f_gelu_tanh(float x) {
-  constexpr float c2 = 2.0f * 0.7978845608028654f;  // 2 sqrt(2/pi)
-  const float u2 = c2 * x * fmaf(0.044715f * x, x, 1.0f);
-  return x * f_sigmoid(u2);
+  constexpr float a = -2.0f * 0.7978845608028654f * kLog2e;  // -2 sqrt(2/pi) log2 e
+  constexpr float b = a * 0.044715f;
+  const float t = x * fmaf(b, x * x, a);
+  return x * frcp(1.0f + __builtin_amdgcn_exp2f(t));
 }
 // exact GELU via the device library's erff
 __device__ __forceinline__ float f_gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.7071067811865476f)); }

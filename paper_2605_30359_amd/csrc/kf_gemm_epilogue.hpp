@@ -329,7 +329,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       Row v;
       get_row(acc, bi, v);
 #pragma unroll
-      for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+      for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
       apply_phase<CH>(p, c, bi, 0, nops, v);
       store_row(p, c, bi, v);
     });
@@ -371,7 +371,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
         Row v;
         get_row(acc, bi, v);
 #pragma unroll
-        for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+        for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
         apply_phase<CH>(p, c, bi, 0, r, v);
 #pragma unroll
         for (int bj = 0; bj < 4; ++bj)
@@ -463,7 +463,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     Row v;
     get_row(acc, bi, v);
 #pragma unroll
-    for (int g = 0; g < 16; ++g) v[g] *= p.scale;
+    for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
     apply_phase<CH>(p, c, bi, 0, r, v);
     // columns past N take no part in a row reduction (only the last column
     // tile can have any)
