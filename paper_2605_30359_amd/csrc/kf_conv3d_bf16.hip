@@ -256,6 +256,7 @@ __global__ __launch_bounds__(NT3, 2) void kf_conv3d_bf16_64x256(Conv3dArgs p, co
       fb[buf][1] = lds_load<u32x4>(hb + toff + kPbOff);
     };
     read_tap(IC<0>{});
+    __builtin_amdgcn_s_setprio(2);  // the K loop's MFMA issue goes first; the other workgroup's epilogue fills in
     static_for<0, 27>([&](auto T_c) {
       constexpr int tap = decltype(T_c)::value, buf = tap & 1;
       if constexpr (tap + 1 < 27) read_tap(IC<tap + 1>{});
@@ -270,6 +271,7 @@ __global__ __launch_bounds__(NT3, 2) void kf_conv3d_bf16_64x256(Conv3dArgs p, co
       __builtin_amdgcn_sched_barrier(0);
     });
 
+    __builtin_amdgcn_s_setprio(0);
     // ---- epilogue: x[cb][pb][v] = channel acc_channel(cb, v, kg) at
     // position (pb, r32).  With pooling, the halo buffer is free once every
     // wave has left the K loop, and the next tile's halo is requested now;
