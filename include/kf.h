@@ -283,17 +283,21 @@ typedef struct kf_tune_result {
   int32_t n;            /* candidates timed                                  */
   int32_t best;         /* index of the fastest                              */
   kf_tuning config[KF_MAX_TUNE_CANDIDATES];
-  double seconds[KF_MAX_TUNE_CANDIDATES]; /* mean time of one kf_fused_op    */
+  double seconds[KF_MAX_TUNE_CANDIDATES]; /* time of one kf_fused_op (median
+                                             round)                          */
 } kf_tune_result;
 
 /* Time every candidate launch configuration of the plan on the caller's
-   tensors -- one warm-up call, then `reps` (1..1000) calls between two HIP
-   events on `stream`, per candidate -- keep the fastest in the descriptor
-   and report all of them in *result.  Blocks until the stream is idle;
-   outputs[0] holds the result of the last call (the same bits for every
-   candidate).  Candidates: GEMM (bf16 / fp8) raster groups {1, 2, 4, 8, 16, 32,
-   64} x XCD order {contiguous, hardware}; CONV3D workgroups per CU {2, 1} x XCD
-   order; every other plan has only its current configuration. */
+   tensors -- in three interleaved rounds, each candidate once per round: one
+   warm-up call, then `reps` (1..1000) calls between two HIP events on
+   `stream` -- rank each by its median round (the clock drifts under power
+   management), keep the fastest in the descriptor and report all of them in
+   *result (seconds: the median round's mean time of one call).  Blocks
+   until the stream is idle; outputs[0] holds the result of the last call
+   (the same bits for every candidate).  Candidates: GEMM (bf16 / fp8) raster
+   groups {1, 2, 4, 8, 16, 32, 64} x XCD order {contiguous, hardware}; CONV3D
+   workgroups per CU {2, 1} x XCD order; every other plan has only its
+   current configuration. */
 kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
                       kf_tune_result* result);
 

@@ -7,6 +7,7 @@
 // ABI; every failure is a status code plus a thread-local message.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -543,6 +544,7 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
     cand.push_back(cur);
   }
   memset(result, 0, sizeof(*result));
+  const int n = (int)std::min<size_t>(cand.size(), KF_MAX_TUNE_CANDIDATES);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
@@ -550,32 +552,44 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
     if (e0) (void)hipEventDestroy(e0);
     return fail(KF_ERR_HIP, "hipEventCreate failed");
   }
+  // The GPU's clock drifts under power management over a few milliseconds,
+  // so the candidates are timed in kRounds interleaved rounds and each is
+  // ranked by its median round: no candidate is favoured by when it ran.
+  constexpr int kRounds = 3;
+  std::vector<double> t((size_t)n * kRounds, 0.0);
   kf_status st = KF_OK;
-  int best = -1;
-  for (size_t c = 0; c < cand.size() && c < KF_MAX_TUNE_CANDIDATES && st == KF_OK; ++c) {
-    d->tuning = cand[c];
-    st = kf_fused_op(d, inputs, outputs, stream);  // warm-up (also validates the tensors)
-    if (st != KF_OK) break;
-    if (hipEventRecord(e0, hs) != hipSuccess) st = fail(KF_ERR_HIP, "hipEventRecord failed");
-    for (int r = 0; r < reps && st == KF_OK; ++r) st = kf_fused_op(d, inputs, outputs, stream);
-    if (st != KF_OK) break;
-    float ms = 0.0f;
-    if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
-        hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
-      st = fail(KF_ERR_HIP, "timing a candidate failed: %s", hipGetErrorString(hipGetLastError()));
-      break;
+  for (int round = 0; round < kRounds && st == KF_OK; ++round) {
+    for (int c = 0; c < n && st == KF_OK; ++c) {
+      d->tuning = cand[c];
+      st = kf_fused_op(d, inputs, outputs, stream);  // warm-up (also validates the tensors)
+      if (st != KF_OK) break;
+      if (hipEventRecord(e0, hs) != hipSuccess) st = fail(KF_ERR_HIP, "hipEventRecord failed");
+      for (int r = 0; r < reps && st == KF_OK; ++r) st = kf_fused_op(d, inputs, outputs, stream);
+      if (st != KF_OK) break;
+      float ms = 0.0f;
+      if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+          hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+        st = fail(KF_ERR_HIP, "timing a candidate failed: %s", hipGetErrorString(hipGetLastError()));
+        break;
+      }
+      t[(size_t)c * kRounds + round] = (double)ms * 1e-3 / reps;
     }
-    result->config[c] = cand[c];
-    result->seconds[c] = (double)ms * 1e-3 / reps;
-    result->n = (int32_t)c + 1;
-    if (best < 0 || result->seconds[c] < result->seconds[best]) best = (int)c;
   }
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
-  if (st != KF_OK || best < 0) {
+  if (st != KF_OK || n == 0) {
     d->tuning = cur;
     return st != KF_OK ? st : fail(KF_ERR_INVALID_ARG, "no candidate configuration");
   }
+  int best = 0;
+  for (int c = 0; c < n; ++c) {
+    double* r = &t[(size_t)c * kRounds];
+    std::sort(r, r + kRounds);
+    result->config[c] = cand[c];
+    result->seconds[c] = r[kRounds / 2];
+    if (result->seconds[c] < result->seconds[best]) best = c;
+  }
+  result->n = n;
   result->best = best;
   d->tuning = result->config[best];
   return ok();
