@@ -54,7 +54,8 @@ constexpr int kRaw = CIN * 2 * WID * 2;  // two input rows as loaded: [ci][2 row
 constexpr int kRawDma = kRaw / 1024 / 4;  // DMA instructions per wave for two input rows
 constexpr int kSteps = 9 * (CIN / 32);  // 18 K-steps of 32 per tile
 static_assert(kSteps % kWS == 0 && kSteps % 2 == 0, "a tile's steps cycle whole weight stages and fragment buffers");
-static_assert(kRawDma <= kSteps - kWS, "the next tile's rows are requested before its first weight stage");
+// the next tile's rows go out on the even K-steps 0, 2, .., 2 (kRawDma - 1)
+static_assert(kSteps == 18 && kWS == 6 && kRawDma == 8, "the DMA wait counts below are derived for this schedule");
 
 #define LDS3 __attribute__((address_space(3)))
 
@@ -275,21 +276,24 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   }
 
   CAcc acc;
-  constexpr int kDma = 3;  // DMA instructions per K-step: 2 weight blocks, then 1 row block (or dummy)
   // K-step s of a tile on weight stage S = s % 6: every wave has read its
   // fragments of stage S (during step s-1) once it passes the barrier, so the
   // DMA of step s+6 goes into stage S; the barrier also publishes stage S+1
-  // (DMA issued during step s-5), read during this step.  A wave's loads
-  // complete in issue order, so that wait also covers the input rows it
-  // requested up to step s-6: the HBM latency of a row request is hidden
-  // behind five K-steps.  The wait allows the row DMA of step s-5 and the
-  // 3 DMA instructions of each of steps s-4 .. s-1 in flight.
-  constexpr int kStepWait = 1 + 4 * kDma;
+  // (DMA issued during step s-5), read during this step.  Each step issues
+  // its 2 weight DMA instructions, and the even steps one row DMA after them
+  // (rows 0..7 on steps 0..14, a dummy on step 16): an LDS DMA instruction
+  // costs its issue slot and an LDS write even out of range, so there is no
+  // dummy on the odd steps.  A wave's loads complete in issue order, so the
+  // wait for stage S+1 leaves in flight exactly what was issued after it: the
+  // row DMA of step s-5 if s-5 is even, and the 8 weight and 2 row DMAs of
+  // steps s-4 .. s-1 -- 10 or 11 instructions, by the parity of s (= that of
+  // S); it also covers the rows requested up to step s-6, whose HBM latency
+  // is thereby hidden behind five K-steps.
   // the next tile's rows: image n_next, first input row ih_next (rows_live: any)
   auto step = [&](auto S_c, auto BUF_c, int s, bool next_live, bool rows_live, int n_next, int ih_next) {
     constexpr int S = decltype(S_c)::value;
     constexpr int BUF = decltype(BUF_c)::value;
-    wait_vmcnt_lgkm0<kStepWait>();
+    wait_vmcnt_lgkm0<(S & 1) ? 11 : 10>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     const bool live = s + kWS < kSteps || next_live;
@@ -301,7 +305,7 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
                                                             0, 0);
       if constexpr (i < kReads) read_one(IC<(S + 1) % kWS>{}, IC<BUF ^ 1>{}, I_c, s + 1);
       if constexpr (i == 1 || i == 3) dma_one(S_c, IC<(i == 1 ? 0 : 1)>{}, s + kWS, live);
-      if constexpr (i == 5) raw_dma(s < kRawDma ? s : 0, n_next, ih_next, rows_live && s < kRawDma);
+      if constexpr (i == 5 && S % 2 == 0) raw_dma(s / 2 < kRawDma ? s / 2 : 0, n_next, ih_next, rows_live && s / 2 < kRawDma);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
@@ -319,12 +323,13 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   auto continues = [&](int t) { return t > t_begin && t % rows_per_img != 0; };
 
   // prologue: input rows 0-1 of the first tile, then the weight stages of
-  // steps 0-5 (each followed by a dummy, as in a K-step)
+  // steps 0-5, issued as K-steps -6 .. -1 would issue them (a dummy row DMA
+  // after the even ones), so that the wait counts hold from step 0 on
   for (int i = 0; i < kRawDma; ++i) raw_dma(i, t_begin / rows_per_img, 2 * (t_begin % rows_per_img) - 1, true);
   static_for<0, kWS>([&](auto S_c) {
     dma_one(S_c, IC<0>{}, decltype(S_c)::value, true);
     dma_one(S_c, IC<1>{}, decltype(S_c)::value, true);
-    raw_dma(0, 0, 0, false);
+    if constexpr (decltype(S_c)::value % 2 == 0) raw_dma(0, 0, 0, false);
   });
 
   for (int tile = t_begin; tile < t_end; ++tile) {
@@ -340,11 +345,13 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
     const int n_next = next_tile / rows_per_img;
     const int ih_next = 2 * (next_tile % rows_per_img) + (next_cont ? 1 : -1);
 
-    // This tile's new input rows and weight stage 0 have landed (the DMA of
-    // the last five K-steps may still be in flight; the row requests are all
-    // older); every wave is past its last read of the slots rewritten here
-    // and of the previous tile's output staging.
-    wait_vmcnt_lgkm0<1 + 5 * kDma>();
+    // This tile's new input rows and weight stages 0-2 have landed: only the
+    // 7 DMA instructions issued after the last row request (step 14) -- the
+    // weights of steps 15-17 and the dummy of step 16 -- and the previous
+    // tile's output stores may still be in flight.  Every wave is past its
+    // last read of the slots rewritten here and of the previous tile's output
+    // staging.
+    wait_vmcnt_lgkm0<7>();
     __syncthreads();
     rb = cont ? (rb + 2) & 3 : 0;
     if (cont) {
