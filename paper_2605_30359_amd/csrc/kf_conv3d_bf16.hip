@@ -55,7 +55,7 @@ constexpr int HDn = TD + 2, HHn = TH + 2, HWn = TW + 2;  // halo 6 x 6 x 18
 constexpr int kPos = CI3 * 2;          // 32 bytes per position
 constexpr int kHaloChunks = HDn * HHn * HWn * 2;        // 1296 chunks of 16 B
 constexpr int kHaloDma = (kHaloChunks + 63) / 64;       // 21 DMA instructions of 1 KiB
-constexpr int kHaloPerWave = (kHaloDma + NWAVE - 1) / NWAVE;  // 6 (the surplus ones land in sDummy)
+constexpr int kHaloPerWave = (kHaloDma + NWAVE - 1) / NWAVE;  // at most 6 (wave 0: 6, the others 5)
 constexpr int kHaloBytes = kHaloDma * 1024;             // 21504
 constexpr int kWBytes = 27 * CO3 * kPos;                // 55296
 constexpr int kWDma = kWBytes / 1024;                   // 54
@@ -174,11 +174,14 @@ __global__ __launch_bounds__(NT3, 2) void kf_conv3d_bf16_64x256(Conv3dArgs p, co
     const TileXY c = coords(tt);
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)c.n * img_elems, img_bytes);
     const uint32_t soff = (uint32_t)(((((int64_t)c.td * TD * H + c.th * TH) * W + c.tw * TW) * CI3) * 2);
+    // the waits before the K loop leave nothing of the halo in flight, so
+    // the waves issue only their real instructions (an out-of-range DMA
+    // instruction would still cost its issue and a 1 KiB LDS write)
 #pragma unroll
     for (int i = 0; i < kHaloPerWave; ++i) {
       const int j = wave + NWAVE * i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS3 void*)(j < kHaloDma ? buf + j * 1024 : sDummy), 16, hoff[i],
-                                                soff, 0, 0);
+      if (j < kHaloDma)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS3 void*)(buf + j * 1024), 16, hoff[i], soff, 0, 0);
     }
   };
 
