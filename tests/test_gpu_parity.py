@@ -303,6 +303,8 @@ _ROW_DIST = dict(a=("normal", 1.0), bias=("uniform", -0.1, 0.1), gamma=("uniform
     (5, 8192, [("groupnorm", 32, 1e-5), ("swish",), ("residual_add",)], "bf16", "bf16"),  # F3 rows
     (9, 2048, [("groupnorm", 1, 1e-5)], "f32", "f32"),                                    # one group per row
     (9, 2048, [("groupnorm", 256, 1e-5), ("relu",)], "bf16", "f32"),                      # 8-column groups
+    (11, 1536, [("groupnorm", 4, 1e-5), ("swish",)], "bf16", "bf16"),                     # 48-chunk groups (LDS tree)
+    (7, 8192, [("groupnorm", 8, 1e-5), ("residual_add",)], "bf16", "bf16"),               # 128-chunk groups (LDS tree)
     (33, 16384, [("row_softmax",)], "bf16", "bf16"),                                      # widest row
     (3, 8, [("row_softmax",)], "f32", "f32"),                                             # narrowest row
     (70, 3000, [("bias",), ("gelu_tanh",), ("scale", 0.5), ("row_logsumexp",)], "bf16", "f32"),
