@@ -84,13 +84,29 @@ __device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.row
 
 typedef f32x4 Row[16];  // one lane's 64 values of one row
 
+// One accumulator register read into a VGPR where it is used.  The "a"
+// operand keeps the value in its AGPR until this point; with plain element
+// reads the register allocator copies the whole 256-register accumulator into
+// VGPRs at the end of the K loop, which overflows them into scratch.
+__device__ __forceinline__ float acc_read(float a) {
+  float v;
+  asm("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
+  return v;
+}
+// A value computed in a VGPR written back into an accumulator register.
+__device__ __forceinline__ float acc_write(float v) {
+  float a;
+  asm("v_accvgpr_write_b32 %0, %1" : "=a"(a) : "v"(v));
+  return a;
+}
+
 template <int RB>
 __device__ __forceinline__ void get_row(const AccT<RB>& acc, int bi, Row& v) {
 #pragma unroll
   for (int g = 0; g < 16; ++g) {
     const f32x16& a = acc[bi][g >> 2];
     const int o = (g & 3) * 4;
-    v[g] = f32x4{a[o], a[o + 1], a[o + 2], a[o + 3]};
+    v[g] = f32x4{acc_read(a[o]), acc_read(a[o + 1]), acc_read(a[o + 2]), acc_read(a[o + 3])};
   }
 }
 template <int RB>
@@ -332,6 +348,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
       apply_phase<CH>(p, c, bi, 0, nops, v);
       store_row(p, c, bi, v);
+      __builtin_amdgcn_sched_barrier(0);
     });
     return;
   }
@@ -364,7 +381,9 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 #pragma unroll
         for (int bj = 0; bj < 4; ++bj) {
           const f32x16& a = acc[bi][bj];
-          auto s4 = [&](int o) { return (a[o] + a[o + 1]) + (a[o + 2] + a[o + 3]); };
+          auto s4 = [&](int o) {
+            return (acc_read(a[o]) + acc_read(a[o + 1])) + (acc_read(a[o + 2]) + acc_read(a[o + 3]));
+          };
           s[bi][bj] = (s4(0) + s4(4)) + (s4(8) + s4(12));
         }
       } else {
@@ -426,7 +445,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
         float a = 0.0f;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
-          const float d = acc[bi][bj][q] - mean[bi][bj];
+          const float d = acc_read(acc[bi][bj][q]) - mean[bi][bj];
           a += d * d;
         }
         ss[bi][bj] = a;
@@ -494,7 +513,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       for (int q = 0; q < 16; ++q)
 #pragma unroll
         for (int bj = 0; bj < 4; ++bj) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(acc[bi][bj][q], kLog2e, -ml));
+          const float e = __builtin_amdgcn_exp2f(fmaf(acc_read(acc[bi][bj][q]), kLog2e, -ml));
           if constexpr (decltype(KEEP_c)::value) acc[bi][bj][q] = e;
           s += e;
         }
