@@ -93,12 +93,6 @@ __device__ __forceinline__ float acc_read(float a) {
   asm("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
   return v;
 }
-// A value computed in a VGPR written back into an accumulator register.
-__device__ __forceinline__ float acc_write(float v) {
-  float a;
-  asm("v_accvgpr_write_b32 %0, %1" : "=a"(a) : "v"(v));
-  return a;
-}
 
 template <int RB>
 __device__ __forceinline__ void get_row(const AccT<RB>& acc, int bi, Row& v) {
@@ -348,7 +342,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
       apply_phase<CH>(p, c, bi, 0, nops, v);
       store_row(p, c, bi, v);
-      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_sched_barrier(0);  // one row block's values at a time
     });
     return;
   }
