@@ -412,8 +412,8 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
         float v[32];  // v[r * 16 + i] = acc[2 r + bc][bj][i]: output row r
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          v[i] = acc[bc][bj][i];
-          v[16 + i] = acc[bc + 2][bj][i];
+          v[i] = acc_read(acc[bc][bj][i]);
+          v[16 + i] = acc_read(acc[bc + 2][bj][i]);
         }
         constexpr bool kPoolFirst = chain_pools_first(CH);
         if constexpr (!kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias_v[bj], v);

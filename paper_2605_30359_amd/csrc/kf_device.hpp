@@ -219,6 +219,19 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// ------------------------------------------------------ accumulator registers
+
+// One MFMA accumulator register read into a VGPR where it is used.  The "a"
+// operand keeps the value in its AGPR until this point; with plain element
+// reads of a large accumulator array the register allocator copies the whole
+// array into VGPRs where the K loop ends, which can overflow them into
+// scratch.
+__device__ __forceinline__ float acc_read(float a) {
+  float v;
+  asm("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
+  return v;
+}
+
 // ---------------------------------------------------------- cross-lane ops
 
 __device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }

@@ -84,16 +84,6 @@ __device__ __forceinline__ int row_local(const EpiCtx& c, int bi) { return c.row
 
 typedef f32x4 Row[16];  // one lane's 64 values of one row
 
-// One accumulator register read into a VGPR where it is used.  The "a"
-// operand keeps the value in its AGPR until this point; with plain element
-// reads the register allocator copies the whole 256-register accumulator into
-// VGPRs at the end of the K loop, which overflows them into scratch.
-__device__ __forceinline__ float acc_read(float a) {
-  float v;
-  asm("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
-  return v;
-}
-
 template <int RB>
 __device__ __forceinline__ void get_row(const AccT<RB>& acc, int bi, Row& v) {
 #pragma unroll
