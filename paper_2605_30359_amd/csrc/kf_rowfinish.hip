@@ -14,16 +14,28 @@
 
 namespace kf {
 
+// One row per group of L = 2^lanes_log2 lanes (the tile count rounded up to
+// a power of two, at most 64): lane i of a group takes tiles i, i + L, ... of
+// its row, so one load instruction of a wave covers 64 consecutive pairs, and
+// the max and the sum are combined across the group by xor exchanges (every
+// lane of the wave takes part in them, rows past M with nothing loaded).
 __global__ __launch_bounds__(256) void kf_row_logsumexp_finish(const float2* __restrict__ part, int tiles,
-                                                                int64_t M, float* __restrict__ out) {
-  const int64_t m = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (m >= M) return;
+                                                                int lanes_log2, int64_t M, float* __restrict__ out) {
+  const int L = 1 << lanes_log2;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t m = gid >> lanes_log2;
+  const int i = (int)(gid & (L - 1));
+  const bool live = m < M;
   const float2* pr = part + m * tiles;
   float mu = -INFINITY;
-  for (int t = 0; t < tiles; ++t) mu = fmaxf(mu, pr[t].x);
+  if (live)
+    for (int t = i; t < tiles; t += L) mu = fmaxf(mu, pr[t].x);
+  for (int d = 1; d < L; d <<= 1) mu = fmaxf(mu, __shfl_xor(mu, d, 64));
   float s = 0.0f;
-  for (int t = 0; t < tiles; ++t) s += pr[t].y * expf(pr[t].x - mu);
-  out[m] = mu + logf(s);
+  if (live)
+    for (int t = i; t < tiles; t += L) s += pr[t].y * expf(pr[t].x - mu);
+  for (int d = 1; d < L; d <<= 1) s += __shfl_xor(s, d, 64);
+  if (live && i == 0) out[m] = mu + logf(s);
 }
 
 constexpr int kMaxFinishTiles = 1024;
@@ -97,8 +109,11 @@ hipError_t launch_row_finish(bool softmax, const void* partials, int tiles, int6
     hipLaunchKernelGGL(kf_row_softmax_rescale, dim3((unsigned)M), dim3(256), 0, stream,
                        reinterpret_cast<const float2*>(partials), tiles, N, out, ldo, out_bf16 ? 1 : 0);
   } else {
-    hipLaunchKernelGGL(kf_row_logsumexp_finish, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<const float2*>(partials), tiles, M, reinterpret_cast<float*>(out));
+    int lanes_log2 = 0;
+    while ((1 << lanes_log2) < tiles && lanes_log2 < 6) ++lanes_log2;
+    const int64_t threads = M << lanes_log2;
+    hipLaunchKernelGGL(kf_row_logsumexp_finish, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
+                       reinterpret_cast<const float2*>(partials), tiles, lanes_log2, M, reinterpret_cast<float*>(out));
   }
   return hipGetLastError();
 }

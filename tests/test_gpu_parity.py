@@ -81,7 +81,8 @@ def test_bf16_contraction_bit_exact_nk_ragged():
     assert np.array_equal(out.cpu().numpy().astype(np.float64), a.astype(np.float64) @ b.astype(np.float64).T)
 
 
-@pytest.mark.parametrize("M,N,K", [(300, 520, 136), (256, 256, 64), (1, 8, 8), (513, 776, 1000)])
+@pytest.mark.parametrize("M,N,K", [(300, 520, 136), (256, 256, 64), (1, 8, 8), (513, 776, 1000),
+                                   (5, 16648, 40)])  # 66 column tiles: the row finish loops over them
 def test_c2_ragged(M, N, K):
     _torch()
     cfg = inputs.config("C2", M=M, N=N, K=K)
