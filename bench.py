@@ -204,7 +204,8 @@ def main(argv=None):
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the fused kernels need no cross-GPU exchange; see DESIGN.md for how the path shards)",
+              "(sharded along rows or the batch, each GPU would run this same single-GPU kernel on its "
+              "share with no cross-GPU exchange)",
               file=sys.stderr)
         return 2
 

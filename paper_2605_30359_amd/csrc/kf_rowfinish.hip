@@ -45,58 +45,69 @@ constexpr int kMaxFinishTiles = 1024;
 // passes of 4 chunks per thread (16 KiB per workgroup for bf16), all four
 // loads issued before any store, so that each thread keeps several reads in
 // flight: the kernel only moves data, and its speed is the number of bytes
-// in flight per CU.
+// in flight per CU.  The first pass's loads do not depend on the factors and
+// go out before the partials are read, so the two memory latencies overlap.
+// mu and S are combined by every wave over the tiles in lane order (lane i
+// takes tiles i, i + 64, ...), then across the wave by xor exchanges.
+template <typename V, int U>
+__device__ __forceinline__ void load_pass(const V* row, int64_t chunks, int64_t c0, int tid, V (&w)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t c = c0 + u * 256 + tid;
+    if (c < chunks) w[u] = row[c];
+  }
+}
+
 __global__ __launch_bounds__(256) void kf_row_softmax_rescale(const float2* __restrict__ part, int tiles,
                                                                int64_t N, void* out, int64_t ldo,
                                                                int out_bf16) {
-  __shared__ float2 ps[kMaxFinishTiles];
   __shared__ float fac[kMaxFinishTiles];
+  constexpr int U = 4;
   const int64_t m = blockIdx.x;
   const int tid = threadIdx.x;
-  for (int t = tid; t < tiles; t += 256) ps[t] = part[m * tiles + t];
-  __syncthreads();
+  const int lane = tid & 63;
+  const bool bf = out_bf16 != 0;
+  u32x4* rowb = reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out) + m * ldo);
+  f32x4* rowf = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(out) + m * ldo);
+  // N % 8 == 0 for bf16 outputs, N % 4 == 0 for fp32 outputs of the matrix-core GEMMs
+  const int64_t chunks = bf ? N / 8 : N / 4;
+  const int shift = bf ? 5 : 6;  // chunk -> 256-column tile
+  u32x4 w[U];
+  f32x4 v[U];
+  if (bf)
+    load_pass(rowb, chunks, 0, tid, w);
+  else
+    load_pass(rowf, chunks, 0, tid, v);
+
+  const float2* pr = part + m * tiles;
   float mu = -INFINITY;
-  for (int t = 0; t < tiles; ++t) mu = fmaxf(mu, ps[t].x);
+  for (int t = lane; t < tiles; t += 64) mu = fmaxf(mu, pr[t].x);
+  for (int d = 1; d < 64; d <<= 1) mu = fmaxf(mu, __shfl_xor(mu, d, 64));
   float s = 0.0f;
-  for (int t = 0; t < tiles; ++t) s += ps[t].y * expf(ps[t].x - mu);
+  for (int t = lane; t < tiles; t += 64) s += pr[t].y * expf(pr[t].x - mu);
+  for (int d = 1; d < 64; d <<= 1) s += __shfl_xor(s, d, 64);
   const float inv = 1.0f / s;
-  for (int t = tid; t < tiles; t += 256) fac[t] = expf(ps[t].x - mu) * inv;
+  for (int t = tid; t < tiles; t += 256) fac[t] = expf(pr[t].x - mu) * inv;
   __syncthreads();
-  constexpr int U = 4;
-  if (out_bf16) {
-    uint16_t* row = reinterpret_cast<uint16_t*>(out) + m * ldo;
-    const int64_t chunks = N / 8;  // N % 8 == 0 for bf16 outputs
-    for (int64_t c0 = 0; c0 < chunks; c0 += 256 * U) {
-      u32x4 w[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t c = c0 + u * 256 + tid;
-        if (c < chunks) w[u] = *reinterpret_cast<const u32x4*>(row + c * 8);
-      }
+
+  for (int64_t c0 = 0; c0 < chunks; c0 += 256 * U) {
+    if (bf) {
+      if (c0 > 0) load_pass(rowb, chunks, c0, tid, w);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t c = c0 + u * 256 + tid;
         if (c >= chunks) continue;
-        const float f = fac[(c * 8) >> 8];
+        const float f = fac[c >> shift];
 #pragma unroll
         for (int e = 0; e < 4; ++e) w[u][e] = pack_bf16x2(bf16_lo(w[u][e]) * f, bf16_hi(w[u][e]) * f);
-        *reinterpret_cast<u32x4*>(row + c * 8) = w[u];
+        rowb[c] = w[u];
       }
-    }
-  } else {
-    float* row = reinterpret_cast<float*>(out) + m * ldo;
-    const int64_t chunks = N / 4;  // N % 4 == 0 for fp32 outputs of the matrix-core GEMMs
-    for (int64_t c0 = 0; c0 < chunks; c0 += 256 * U) {
-      f32x4 v[U];
+    } else {
+      if (c0 > 0) load_pass(rowf, chunks, c0, tid, v);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t c = c0 + u * 256 + tid;
-        if (c < chunks) v[u] = *reinterpret_cast<const f32x4*>(row + c * 4);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t c = c0 + u * 256 + tid;
-        if (c < chunks) *reinterpret_cast<f32x4*>(row + c * 4) = v[u] * fac[(c * 4) >> 8];
+        if (c < chunks) rowf[c] = v[u] * fac[c >> shift];
       }
     }
   }

@@ -215,7 +215,7 @@ def _draw(rng, spec, shape, k_fan_in):
     if kind == "normal":
         return (rng.standard_normal(shape, dtype=np.float32) * np.float32(np.sqrt(spec[1])))
     if kind == "normal_invk":
-        return rng.standard_normal(shape, dtype=np.float32) * np.float32(1.0 / np.sqrt(k_fan_in))
+        return rng.standard_normal(shape, dtype=np.float32) * np.float32(1.0 / np.sqrt(max(k_fan_in, 1)))  # K = 0: an empty draw
     if kind == "uniform":
         return rng.uniform(spec[1], spec[2], size=shape).astype(np.float32)
     raise ValueError(kind)

@@ -177,6 +177,28 @@ def test_empty_m_is_a_no_op():
     assert out.numel() == 0
 
 
+@pytest.mark.parametrize("name,kw", [
+    ("C1", dict(M=33, N=72, K=0)),
+    ("C2", dict(M=70, N=296, K=0)),
+    ("C3", dict(M=40, N=512, K=0, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
+    ("C5", dict(M=33, N=272, K=0)),
+])
+def test_empty_contraction_k0(name, kw):
+    """K = 0: every pre-activation is exactly zero (an empty sum), so the
+    output is the epilogue applied to zeros -- e.g. C2's rows are all
+    LSE_j(0.5 gelu(b_j)), C3's GroupNorm sees zero variance."""
+    _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=3)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    g = to_host_f64(out)
+    assert np.all(np.isfinite(g))
+    if name == "C2":
+        assert np.ptp(g) == 0.0  # every row computes the same bits
+    print(f"{name} K=0 err {err:.3e}")
+
+
 def test_repeat_runs_bitwise_identical():
     torch = _torch()
     cfg = inputs.config("C3", M=512, N=512, K=256, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
