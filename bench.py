@@ -15,6 +15,8 @@ already resident in device memory.  The default workload is the bf16 GEMM
                MFMA peak of its input dtype; `traffic` is the HBM bytes per
                launch from the committed rocprofv3 counter summary, or null if
                the kernel source changed since those counters were taken
+               (`traffic_launch_config` names the launch configuration they
+               were counted with)
   unfused      the same operation as the library's own one-kernel-per-op
                chain, timed the same way; speedup = unfused / fused time
   cpu_baseline the fp64 oracle timed on the host cores over a bounded sample
@@ -94,8 +96,9 @@ KERNEL_FILES = {
 }
 
 
-def _traffic(kernel: str, workload: str):
-    """HBM bytes per launch from the committed counter summary, if it was
+def _traffic_record(kernel: str, workload: str):
+    """The committed counter summary of a kernel on a workload (HBM bytes per
+    launch and the launch configuration they were counted with), if it was
     taken on the current kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
@@ -106,7 +109,7 @@ def _traffic(kernel: str, workload: str):
         return None
     if not rec or rec.get("source_digest") != _source_digest(KERNEL_FILES.get(kernel, [])):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec
 
 
 def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
@@ -286,7 +289,8 @@ def main(argv=None):
         except kf.KFError as e:
             unfused = {"error": str(e)}
 
-    traffic = _traffic(kname, cfg["workload"])
+    trec = _traffic_record(kname, cfg["workload"])
+    traffic = trec.get("hbm_bytes_per_launch") if trec else None
     diag = op.diagnose(kernel_ms * 1e-3, traffic or 0.0)
     diagnosis = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in diag.items()
                  if k in ("bound", "compute_frac", "memory_frac", "intensity", "ridge", "workgroups", "compute_units")}
@@ -325,6 +329,9 @@ def main(argv=None):
             "kernel_us": round(kernel_ms * 1e3, 2),
             ("bytes_per_launch" if rowwise else "flops_per_launch"): work,
             "traffic": traffic,
+            # the launch configuration the counters were taken with (the
+            # raster order changes how often operand panels are re-fetched)
+            "traffic_launch_config": trec.get("launch_config") if trec else None,
         },
         "diagnosis": diagnosis,
         "tuning": tuning,
