@@ -199,6 +199,32 @@ def test_empty_contraction_k0(name, kw):
     print(f"{name} K=0 err {err:.3e}")
 
 
+@pytest.mark.parametrize("M,out_dtype,ops", [
+    ((1 << 21) + 37, "bf16", [("bias",), ("relu",)]),
+    ((1 << 20) + 37, "f32", [("bias",), ("relu",)]),
+    ((1 << 21) + 37, "bf16", [("bias",), ("hardtanh", -1.0, 1.0), ("row_softmax",)]),
+])
+def test_output_beyond_2gib(M, out_dtype, ops):
+    """An output of more than 2^31 bytes (8193+ tile rows of 520 columns):
+    tile bases are 64-bit, only offsets inside a tile are 32-bit, and the
+    row finishing kernel addresses rows with 64-bit offsets.  Sampled rows,
+    taken from the device output before the copy to the host."""
+    torch = _torch()
+    cfg = inputs.config("C2", M=M, N=520, K=40, out_dtype=out_dtype, ops=ops)
+    t = inputs.generate(cfg, seed=11)
+    _, out = run_gpu(cfg, t)
+    es = 2 if out_dtype == "bf16" else 4
+    assert out.numel() * es > (1 << 31)
+    rows = sample_rows(M, 40, seed=3)
+    sub = out[torch.as_tensor(rows, device=out.device)]
+    chain = inputs.chain_for(cfg, t)
+    ref = oracle.run_chain(chain, t, rows=rows)
+    from parity import floor_for
+    err = parity_error(to_host_f64(sub), ref, floor_for(cfg))
+    assert err <= TOL[cfg["in_dtype"]], f"parity error {err:.3e}"
+    print(f"M={M} {out_dtype} {[o[0] for o in ops]} err {err:.3e}")
+
+
 def test_repeat_runs_bitwise_identical():
     torch = _torch()
     cfg = inputs.config("C3", M=512, N=512, K=256, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
