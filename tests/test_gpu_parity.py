@@ -687,6 +687,35 @@ def test_tuning_candidates_bit_identical(name, kw):
     check(cfg, t, ref)
 
 
+@pytest.mark.parametrize("name", ["C2", "C3", "C5", "F1", "F2"])
+def test_full_size_tuned_launch_bit_identical(name):
+    """At the full workload size, the launch configuration the bench keeps
+    (by autotuning, as the bench does) and every other candidate compute the
+    same bits as the default configuration, whose output is compared with the
+    oracle on sampled rows (or images) here and in the full-size tests."""
+    torch = _torch()
+    cfg = inputs.config(name)
+    t = inputs.generate(cfg)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    ref = op.empty_output("cuda")
+    op(ins, ref)
+    bits = (lambda x: x.view(torch.int16)) if ref.dtype == torch.bfloat16 else (lambda x: x)
+    out = op.empty_output("cuda")
+    r = op.autotune(ins, out, reps=1)
+    assert torch.equal(bits(ref), bits(out)), (name, r["best"])
+    for c in r["candidates"]:
+        op.set_tuning(c["raster_group"], c["xcd_remap"], c["wg_per_cu"])
+        out.zero_()
+        op(ins, out)
+        assert torch.equal(bits(ref), bits(out)), (name, c)
+    if cfg["contraction"] == "conv3d_3x3x3":
+        check(cfg, t, ref, images=np.array([0, cfg["batch"] - 1]))
+    else:
+        check(cfg, t, ref, rows=sample_rows(cfg["M"], 8, seed=4))
+    print(f"{name}: {len(r['candidates'])} candidates bit-identical at full size, kept {r['best']}")
+
+
 @pytest.mark.parametrize("name,kw,n", [
     ("C2", dict(M=1024, N=2048, K=512), 14),
     ("F2", dict(batch=2, D=10, H=18, W=34), 4),
