@@ -32,6 +32,18 @@ __global__ __launch_bounds__(NT) void kf_gemm_f32_8x8(GemmArgs p) {
   const bool b_nk = p.ldb < 0;  // sign flags the NK layout; |ldb| is the stride
   const int64_t ldb = b_nk ? -p.ldb : p.ldb;
   const int r = lane >> 3, c = lane & 7;  // this lane's output (m0 + r, n0 + c)
+  const int64_t m = m0 + r, n = n0 + c;
+  const bool out_ok = m < p.M && n < p.N;
+  // the epilogue's tensor operands of this lane's output, requested now so
+  // that their latency overlaps the operand loads instead of following them
+  float bias_v = 0.0f, res_v = 0.0f;
+  if (wave == 0 && out_ok) {
+    if (p.bias) bias_v = p.bias[n];
+    if (p.residual)
+      res_v = p.residual_bf16
+                  ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(p.residual)[m * p.ldr + n] << 16)
+                  : reinterpret_cast<const float*>(p.residual)[m * p.ldr + n];
+  }
 
   float acc = 0.0f;
   for (int64_t k0 = 0; k0 < p.K; k0 += KC) {
@@ -74,19 +86,15 @@ __global__ __launch_bounds__(NT) void kf_gemm_f32_8x8(GemmArgs p) {
   __syncthreads();
   if (wave != 0) return;
 
-  const int64_t m = m0 + r, n = n0 + c;
-  if (m >= p.M || n >= p.N) return;
+  if (!out_ok) return;
   float x = ((part[lane] + part[64 + lane]) + part[128 + lane]) + part[192 + lane];
   x *= p.scale;
   for (int o = 0; o < p.prog.n; ++o) {
     const EpiOp op = p.prog.op[o];
     if (op.kind == KF_OP_BIAS) {
-      x += p.bias[n];
+      x += bias_v;
     } else if (op.kind == KF_OP_RESIDUAL_ADD) {
-      if (p.residual_bf16)
-        x += __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(p.residual)[m * p.ldr + n] << 16);
-      else
-        x += reinterpret_cast<const float*>(p.residual)[m * p.ldr + n];
+      x += res_v;
     } else {
       x = apply_elementwise(op.kind, op.p0, op.p1, x);
     }
