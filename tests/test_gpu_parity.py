@@ -225,6 +225,30 @@ def test_output_beyond_2gib(M, out_dtype, ops):
     print(f"M={M} {out_dtype} {[o[0] for o in ops]} err {err:.3e}")
 
 
+def test_binding_reuses_descriptors_only_for_the_same_tensors():
+    """The binding reuses the last call's tensor descriptors only when every
+    tensor has the same address, dtype, shape and strides: new input values
+    in a new buffer, and a new output buffer, are seen by the next call."""
+    torch = _torch()
+    cfg = inputs.config("C2", M=300, N=520, K=136)
+    t1 = inputs.generate(cfg, seed=61)
+    t2 = inputs.generate(cfg, seed=62)
+    op = kf.FusedOp(inputs.chain_for(cfg, t1), **kf.sizes_of(cfg))
+    ins1, ins2 = op.device_inputs(t1), op.device_inputs(t2)
+    o1, o2 = op.empty_output("cuda"), op.empty_output("cuda")
+    op(ins1, o1)
+    op(ins1, o1)  # same tensors: the descriptors are reused
+    op(ins2, o2)  # other buffers: new descriptors
+    op(ins1, o2)  # same inputs as the first call, other output
+    torch.cuda.synchronize()
+    check(cfg, t1, o1)
+    check(cfg, t1, o2)
+    op(ins2, o2)
+    torch.cuda.synchronize()
+    check(cfg, t2, o2)
+    assert not torch.equal(o1, o2)
+
+
 def test_repeat_runs_bitwise_identical():
     torch = _torch()
     cfg = inputs.config("C3", M=512, N=512, K=256, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])
