@@ -16,7 +16,8 @@ namespace kf {
 
 // One row per group of L = 2^lanes_log2 lanes (the tile count rounded up to
 // a power of two, at most 64): lane i of a group takes tiles i, i + L, ... of
-// its row, so one load instruction of a wave covers 64 consecutive pairs, and
+// its row, so one load instruction of a wave covers 64 consecutive pairs
+// when the tile count is a power of two (and nearly so otherwise), and
 // the max and the sum are combined across the group by xor exchanges (every
 // lane of the wave takes part in them, rows past M with nothing loaded).
 __global__ __launch_bounds__(256) void kf_row_logsumexp_finish(const float2* __restrict__ part, int tiles,
