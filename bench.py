@@ -1,22 +1,29 @@
 #!/usr/bin/env python3
 """Benchmark of the fused contraction + epilogue path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C5] [--also C3,C4]
 
 A step is one kf_fused_op call: the whole fused operation (contraction,
 fused epilogue, row finishing kernel) on one batch of seeded synthetic input
-already resident in device memory.  The default workload is the bf16 GEMM
-4096 x 4096 x 4096 + bias + GELU(tanh) + scale 0.5 + row logsumexp -> fp32
-[4096].  One JSON line is printed with:
+already resident in device memory.  The headline workload (default C5, the
+largest of the five: fp8 e4m3 GEMM 8192 x 8192 x 8192 with per-tensor scales
++ bias + hardtanh(-1, 1) + row softmax -> bf16 [8192, 8192]) fills the JSON
+line; each workload named by --also (default the large bf16 ones, C3 and C4)
+gets a block of the same fields under "also".  Per workload:
 
-  value        whole-step throughput in TFLOP/s (2*M*N*K / step time)
+  value        whole-step throughput in TFLOP/s (2*M*N*K / mean step time
+               over the K back-to-back steps)
+  steps_us     per-step HIP-event times: median, min, p90, mean -- warm
+               (back-to-back steps) and cold (a 512 MiB device write between
+               steps, outside the events, evicts the L2s and the 256 MB
+               Infinity Cache)
   roofline     the main contraction kernel alone, timed live with HIP events
-               recorded on its stream around each launch, against the dense
-               MFMA peak of its input dtype; `traffic` is the HBM bytes per
-               launch from the committed rocprofv3 counter summary, or null if
-               the kernel source changed since those counters were taken
-               (`traffic_launch_config` names the launch configuration they
-               were counted with)
+               recorded on its stream around each launch (achieved = the
+               algorithmic FLOPs per launch / the mean launch time; median,
+               min and p90 beside it), against the dense MFMA peak of its
+               input dtype; `traffic` is the HBM bytes per launch from the
+               committed rocprofv3 counter summary, or null if the kernel
+               source changed since those counters were taken
   unfused      the same operation as the library's own one-kernel-per-op
                chain, timed the same way; speedup = unfused / fused time
   cpu_baseline the fp64 oracle timed on the host cores over a bounded sample
@@ -45,6 +52,7 @@ sys.path.insert(0, ROOT)
 # Dense peaks of one MI355X (256 CUs at 2.4 GHz), TFLOP/s.
 PEAK_TFLOPS = {"bf16": 2516.6, "e4m3": 5033.2, "f32": 157.3}
 HBM_PEAK_GBS = 8000.0
+COLD_FLUSH_BYTES = 512 << 20
 
 
 def _hip():
@@ -54,6 +62,7 @@ def _hip():
     lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
     lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
     lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     return lib
 
 
@@ -72,6 +81,14 @@ def _elapsed_ms(hip, a, b) -> float:
     ms = ctypes.c_float()
     assert hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) == 0
     return float(ms.value)
+
+
+def _stats_us(ms_list) -> dict:
+    """median, min, p90 and mean of a list of durations in ms, in us."""
+    import numpy as np
+    v = np.sort(np.asarray(ms_list, dtype=np.float64)) * 1e3
+    return {"median": round(float(np.median(v)), 2), "min": round(float(v[0]), 2),
+            "p90": round(float(np.percentile(v, 90)), 2), "mean": round(float(v.mean()), 2), "n": int(v.size)}
 
 
 def _source_digest(kernel_files) -> str:
@@ -177,13 +194,175 @@ def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
     }, err
 
 
+def _timed_steps(hip, torch, run, steps, flush=None, kernel_events=True):
+    """`steps` calls of run(ev_before, ev_after) on the current stream, each
+    between two step events; `flush` (a device tensor) is overwritten before
+    every step, outside the events.  run() records ev_before / ev_after
+    around its main kernel when kernel_events is set.  Returns (total ms of
+    the loop, per-step ms, per-kernel ms)."""
+    stream = torch.cuda.current_stream()
+    kev = [(_event(hip), _event(hip)) for _ in range(steps)] if kernel_events else []
+    sev = [(_event(hip), _event(hip)) for _ in range(steps)]
+    start, end = _event(hip), _event(hip)
+    torch.cuda.synchronize()
+    s = ctypes.c_void_p(stream.cuda_stream)
+    hip.hipEventRecord(ctypes.c_void_p(start), s)
+    for i in range(steps):
+        if flush is not None:
+            flush.fill_(i & 0xFF)
+        hip.hipEventRecord(ctypes.c_void_p(sev[i][0]), s)
+        run(*(kev[i] if kernel_events else (None, None)))
+        hip.hipEventRecord(ctypes.c_void_p(sev[i][1]), s)
+    hip.hipEventRecord(ctypes.c_void_p(end), s)
+    torch.cuda.synchronize()
+    total = _elapsed_ms(hip, start, end)
+    step_ms = [_elapsed_ms(hip, a, b) for a, b in sev]
+    kern_ms = [_elapsed_ms(hip, a, b) for a, b in kev]
+    for a, b in kev + sev + [(start, end)]:
+        hip.hipEventDestroy(ctypes.c_void_p(a))
+        hip.hipEventDestroy(ctypes.c_void_p(b))
+    return total, step_ms, kern_ms
+
+
+def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
+    """Time one workload; returns the fields of its JSON block."""
+    import torch
+
+    from paper_2605_30359_amd import inputs, kf
+
+    print(f"[bench] {name}: generating inputs", file=sys.stderr, flush=True)
+    cfg = inputs.config(name)
+    tensors = inputs.generate(cfg)
+    chain = inputs.chain_for(cfg, tensors)
+    op = kf.FusedOp(chain, **kf.sizes_of(cfg))
+    ins = op.device_inputs(tensors, "cuda:0")
+    out = op.empty_output("cuda:0")
+
+    # the plan's launch candidates, timed on these inputs; the fastest is kept
+    # (every candidate computes the same bits)
+    tuning = None
+    if args.tuning:
+        rg, xr, wg = (int(v) for v in args.tuning.split(","))
+        op.set_tuning(rg, xr, wg)
+        tuning = {"config": op.tuning(), "candidates": 0, "best_ms": None, "default_ms": None}
+    elif not args.no_autotune:
+        r = op.autotune(ins, out, reps=max(3, args.warmup // 2))
+        keys = ("raster_group", "xcd_remap", "wg_per_cu")
+        default = [c for c in r["candidates"] if (c["raster_group"], c["xcd_remap"], c["wg_per_cu"]) == (4, 1, 2)]
+        tuning = {"config": {k: r["best"][k] for k in keys}, "candidates": len(r["candidates"]),
+                  "best_ms": round(r["best"]["seconds"] * 1e3, 5),
+                  "default_ms": round(default[0]["seconds"] * 1e3, 5) if default else None}
+
+    print(f"[bench] {name}: timing", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        op(ins, out)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    fused = lambda e0, e1: op.timed(ins, out, e0, e1)  # noqa: E731
+    total_ms, step_ms, kern_ms = _timed_steps(hip, torch, fused, K)
+    ms_per_step = total_ms / K
+    cold = None
+    if args.cold_steps > 0:
+        flush = torch.empty(COLD_FLUSH_BYTES, dtype=torch.uint8, device="cuda:0")
+        _, c_step, c_kern = _timed_steps(hip, torch, fused, args.cold_steps, flush=flush)
+        del flush
+        cold = {"step_us": _stats_us(c_step), "kernel_us": _stats_us(c_kern)}
+
+    # contraction chains are measured in FLOP/s against the MFMA (or fp32)
+    # peak; the row-wise chains, which have no contraction, in bytes per
+    # second against HBM bandwidth
+    rowwise = cfg["contraction"] == "rowwise"
+    dt = cfg["in_dtype"]
+    work = inputs.rowwise_bytes(cfg) if rowwise else inputs.flops(cfg)
+    peak = HBM_PEAK_GBS if rowwise else PEAK_TFLOPS[dt]
+    scale = 1e9 if rowwise else 1e12
+    kernel_ms = sum(kern_ms) / len(kern_ms)
+    value = work / (ms_per_step * 1e-3) / scale
+    achieved = work / (kernel_ms * 1e-3) / scale
+    kname = op.kernel_name()
+
+    unfused = None
+    if not args.no_unfused:
+        try:
+            u_out = op.empty_output("cuda:0")
+            for _ in range(max(2, args.warmup // 2)):
+                op.unfused(ins, u_out)
+            torch.cuda.synchronize()
+            u_total, u_step, _ = _timed_steps(hip, torch, lambda e0, e1: op.unfused(ins, u_out), K,
+                                              kernel_events=False)
+            u_ms = u_total / K
+            unfused = {"ms_per_step": round(u_ms, 5), "step_us": _stats_us(u_step),
+                       "speedup": round(u_ms / ms_per_step, 3)}
+            del u_out
+        except kf.KFError as e:
+            unfused = {"error": str(e)}
+
+    trec = _traffic_record(kname, cfg["workload"])
+    traffic = trec.get("hbm_bytes_per_launch") if trec else None
+    diag = op.diagnose(kernel_ms * 1e-3, traffic or 0.0)
+    diagnosis = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in diag.items()
+                 if k in ("bound", "compute_frac", "memory_frac", "intensity", "ridge", "workgroups", "compute_units")}
+
+    cpu, err = (None, None)
+    if cpu_budget > 0:
+        print(f"[bench] {name}: cpu baseline", file=sys.stderr, flush=True)
+        cpu, err = _cpu_baseline(cfg, tensors, out, cpu_budget)
+
+    sizes = kf.sizes_of(cfg)
+    block = {
+        "value": round(value, 2),
+        "unit": "GB/s" if rowwise else "TFLOP/s",
+        "ms_per_step": round(ms_per_step, 5),
+        "dtype": dt,
+        "config": dict({"workload": cfg["workload"], "ops": "+".join(o[0] for o in cfg["ops"]),
+                        "out_dtype": cfg["out_dtype"]}, **sizes),
+        ("pct_hbm_peak" if rowwise else "pct_mfma_peak"): round(100.0 * value / peak, 2),
+        "steps_us": {"warm": _stats_us(step_ms), "cold": cold["step_us"] if cold else None},
+        "speedup_vs_unfused": None if not unfused or "speedup" not in unfused else unfused["speedup"],
+        "unfused": unfused,
+        "roofline": {
+            "bound": "hbm" if rowwise else "mfma",
+            "kernel": kname,
+            "achieved": round(achieved, 2),
+            "peak": peak,
+            "unit": "GB/s" if rowwise else "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "kernel_us": round(kernel_ms * 1e3, 2),
+            "kernel_us_stats": _stats_us(kern_ms),
+            "kernel_us_cold": cold["kernel_us"] if cold else None,
+            ("bytes_per_launch" if rowwise else "flops_per_launch"): work,
+            "traffic": traffic,
+            # the launch configuration the counters were taken with (the
+            # raster order changes how often operand panels are re-fetched)
+            "traffic_launch_config": trec.get("launch_config") if trec else None,
+        },
+        "diagnosis": diagnosis,
+        "tuning": tuning,
+        "cpu_baseline": cpu,
+        "parity_err_cpu_sample": err,
+    }
+    op.close()
+    del ins, out, tensors
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    print(f"[bench] {name}: {block['value']} {block['unit']}, kernel {block['roofline']['kernel_us']} us",
+          file=sys.stderr, flush=True)
+    return block
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="C2", help="C1..C5, F1..F4 (default C2)")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--workload", default="C5", help="headline workload: C1..C5, F1..F4 (default C5)")
+    ap.add_argument("--also", default="C3,C4",
+                    help="comma-separated workloads timed after the headline, each reported under 'also' "
+                         "(default C3,C4; empty for none)")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="steps timed with a 512 MiB device write before each (0: no cold timing)")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
@@ -214,130 +393,32 @@ def main(argv=None):
 
     import torch
 
-    from paper_2605_30359_amd import inputs, kf
-
     torch.cuda.set_device(0)
-    cfg = inputs.config(args.workload)
-    tensors = inputs.generate(cfg)
-    chain = inputs.chain_for(cfg, tensors)
-    op = kf.FusedOp(chain, **kf.sizes_of(cfg))
-    ins = op.device_inputs(tensors, "cuda:0")
-    out = op.empty_output("cuda:0")
-    stream = torch.cuda.current_stream()
     hip = _hip()
+    budget = 0.0 if args.no_cpu_baseline else args.cpu_budget
+    head = run_workload(args.workload, args, hip, budget)
+    also = {}
+    for name in [w for w in args.also.split(",") if w and w != args.workload]:
+        also[name] = run_workload(name, args, hip, budget)
 
-    # the plan's launch candidates, timed on these inputs; the fastest is kept
-    # (every candidate computes the same bits)
-    tuning = None
-    if args.tuning:
-        rg, xr, wg = (int(v) for v in args.tuning.split(","))
-        op.set_tuning(rg, xr, wg)
-        tuning = {"config": op.tuning(), "candidates": 0, "best_ms": None, "default_ms": None}
-    elif not args.no_autotune:
-        r = op.autotune(ins, out, reps=max(3, args.warmup // 2))
-        keys = ("raster_group", "xcd_remap", "wg_per_cu")
-        default = [c for c in r["candidates"] if (c["raster_group"], c["xcd_remap"], c["wg_per_cu"]) == (4, 1, 2)]
-        tuning = {"config": {k: r["best"][k] for k in keys}, "candidates": len(r["candidates"]),
-                  "best_ms": round(r["best"]["seconds"] * 1e3, 5),
-                  "default_ms": round(default[0]["seconds"] * 1e3, 5) if default else None}
-
-    for _ in range(args.warmup):
-        op(ins, out)
-    torch.cuda.synchronize()
-
-    K = args.steps
-    evs = [(_event(hip), _event(hip)) for _ in range(K)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(K):
-        op.timed(ins, out, evs[i][0], evs[i][1])
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / K
-    kernel_ms = sum(_elapsed_ms(hip, a, b) for a, b in evs) / K
-    for a, b in evs:
-        hip.hipEventDestroy(ctypes.c_void_p(a))
-        hip.hipEventDestroy(ctypes.c_void_p(b))
-
-    # contraction chains are measured in FLOP/s against the MFMA (or fp32)
-    # peak; the row-wise chains, which have no contraction, in bytes per
-    # second against HBM bandwidth
-    rowwise = cfg["contraction"] == "rowwise"
-    dt = cfg["in_dtype"]
-    work = inputs.rowwise_bytes(cfg) if rowwise else inputs.flops(cfg)
-    peak = HBM_PEAK_GBS if rowwise else PEAK_TFLOPS[dt]
-    scale = 1e9 if rowwise else 1e12
-    value = work / (ms_per_step * 1e-3) / scale
-    achieved = work / (kernel_ms * 1e-3) / scale
-    kname = op.kernel_name()
-
-    unfused = None
-    if not args.no_unfused:
-        try:
-            u_out = op.empty_output("cuda:0")
-            for _ in range(max(2, args.warmup // 2)):
-                op.unfused(ins, u_out)
-            torch.cuda.synchronize()
-            start.record(stream)
-            for _ in range(K):
-                op.unfused(ins, u_out)
-            end.record(stream)
-            torch.cuda.synchronize()
-            u_ms = start.elapsed_time(end) / K
-            unfused = {"ms_per_step": u_ms, "speedup": u_ms / ms_per_step}
-        except kf.KFError as e:
-            unfused = {"error": str(e)}
-
-    trec = _traffic_record(kname, cfg["workload"])
-    traffic = trec.get("hbm_bytes_per_launch") if trec else None
-    diag = op.diagnose(kernel_ms * 1e-3, traffic or 0.0)
-    diagnosis = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in diag.items()
-                 if k in ("bound", "compute_frac", "memory_frac", "intensity", "ridge", "workgroups", "compute_units")}
-
-    cpu, err = (None, None)
-    if not args.no_cpu_baseline:
-        cpu, err = _cpu_baseline(cfg, tensors, out, args.cpu_budget)
-
-    sizes = kf.sizes_of(cfg)
+    rowwise = head["unit"] == "GB/s"
     line = {
         "metric": ("fused-op GB/s, % of HBM peak, speedup vs own unfused kernel chain" if rowwise else
                    "fused-op TFLOP/s, % of MFMA peak, speedup vs own unfused kernel chain"),
-        "value": round(value, 2),
-        "unit": "GB/s" if rowwise else "TFLOP/s",
+        "value": head["value"],
+        "unit": head["unit"],
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": dt,
+        "dtype": head["dtype"],
         "data": "synthetic",
-        "config": dict({"workload": cfg["workload"], "ops": "+".join(o[0] for o in cfg["ops"]),
-                        "out_dtype": cfg["out_dtype"]}, **sizes),
-        ("pct_hbm_peak" if rowwise else "pct_mfma_peak"): round(100.0 * value / peak, 2),
-        "speedup_vs_unfused": None if not unfused or "speedup" not in unfused else round(unfused["speedup"], 3),
-        "unfused": unfused,
-        "roofline": {
-            "bound": "hbm" if rowwise else "mfma",
-            "kernel": kname,
-            "achieved": round(achieved, 2),
-            "peak": peak,
-            "unit": "GB/s" if rowwise else "TFLOP/s",
-            "frac": round(achieved / peak, 4),
-            "kernel_us": round(kernel_ms * 1e3, 2),
-            ("bytes_per_launch" if rowwise else "flops_per_launch"): work,
-            "traffic": traffic,
-            # the launch configuration the counters were taken with (the
-            # raster order changes how often operand panels are re-fetched)
-            "traffic_launch_config": trec.get("launch_config") if trec else None,
-        },
-        "diagnosis": diagnosis,
-        "tuning": tuning,
-        "cpu_baseline": cpu,
-        "parity_err_cpu_sample": err,
     }
+    line.update({k: v for k, v in head.items() if k not in line and k != "unit"})
+    line["also"] = also
     print(json.dumps(line), flush=True)
     return 0
 
