@@ -304,10 +304,15 @@ def op_row_logsumexp(h):
 # Chains
 # --------------------------------------------------------------------------
 
-def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel) -> np.ndarray:
+def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel, store=None) -> np.ndarray:
     """The op list of `chain`, in order, on the float64 contraction result h
-    (rows / images `sel` of the full result, or all of it)."""
-    for op in chain["ops"]:
+    (rows / images `sel` of the full result, or all of it).  `store`, if
+    given, is applied to the result of every op but the last (the storage
+    rounding of an intermediate that is written to memory)."""
+    ops = chain["ops"]
+    for i, op in enumerate(ops):
+        if store is not None and i > 0:
+            h = store(h)
         name, params = op[0], op[1:]
         if name == "bias":
             h = op_bias(h, to_f64(tensors["bias"], "f32"))
@@ -351,6 +356,81 @@ def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel) -> np.ndarray:
     return h
 
 
+# --------------------------------------------------------------------------
+# Storage rounding of intermediates (the unfused chain)
+# --------------------------------------------------------------------------
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """float64 -> the nearest bfloat16 value (round half to even), as float64.
+
+    bfloat16 keeps 8 significant bits and binary32's exponent range: a finite
+    value in [2^E, 2^(E+1)) is a multiple of 2^(E-7), and below the normal
+    range (E < -126) of 2^-133.  Dividing by that quantum, rounding half to
+    even (np.rint) and multiplying back only rescales by powers of two, so
+    every step is exact in float64.  Magnitudes that round past the largest
+    finite value, (2 - 2^-7) 2^127, become infinite."""
+    x = np.asarray(x, dtype=np.float64)
+    ax = np.abs(x)
+    _, e = np.frexp(ax)                        # ax = m 2^e, m in [0.5, 1)
+    E = np.maximum(e - 1, -126)                # floor(log2 ax), clamped to the normal range
+    q = np.ldexp(np.rint(np.ldexp(ax, 7 - E)), E - 7)
+    q = np.where(q > (2.0 - 2.0 ** -7) * 2.0 ** 127, np.inf, q)
+    q = np.where(np.isnan(x), np.nan, q)
+    return np.copysign(q, x)
+
+
+def round_f32(x: np.ndarray) -> np.ndarray:
+    """float64 -> the nearest binary32 value (IEEE round half to even)."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def intermediate_dtype(chain: dict) -> str:
+    """Storage format of the unfused chain's intermediates: what an eager
+    chain of one operator per kernel stores in the operands' precision --
+    bfloat16 for bf16 and e4m3 contractions (and bf16 row-wise chains),
+    binary32 for fp32 ones."""
+    return "f32" if chain["in_dtype"] == "f32" else "bf16"
+
+
+def run_chain_unfused(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
+    """The chain as a one-operator-per-kernel evaluation computes it -- the
+    unfused form that operator fusion removes (Appendix A, "Operator
+    Fusion"): the contraction's result and the result of every op but the
+    last are written to memory, so each is rounded to the intermediate
+    storage format (``intermediate_dtype``) before the next op reads it.
+    Each op itself is the same plain float64 definition as in ``run_chain``,
+    applied to the stored values.  A chain with no ops writes the
+    contraction's result directly (no intermediate); a row-wise chain's first
+    op reads A itself.  The last op's result is returned unrounded, like
+    ``run_chain``'s."""
+    store = round_f32 if intermediate_dtype(chain) == "f32" else round_bf16
+    h, sel = _contraction(chain, tensors, rows, images)
+    if chain["ops"] and chain["contraction"] != "rowwise":
+        h = store(h)
+    return _apply_ops(chain, tensors, h, sel, store)
+
+
+def _contraction(chain: dict, tensors: dict, rows=None, images=None):
+    """The float64 contraction result of a chain (A itself for "rowwise"),
+    restricted to the selected rows / images, and the selection."""
+    dt = chain["in_dtype"]
+    a = to_f64(tensors["a"], dt)
+    if chain["contraction"] == "rowwise":
+        h = a if rows is None else a[np.asarray(rows, dtype=np.int64)]
+        return h, rows
+    b = to_f64(tensors["b"], dt)
+    if dt == "e4m3":
+        a = a * float(np.float32(chain["scale_a"]))
+        b = b * float(np.float32(chain["scale_b"]))
+    if chain["contraction"] == "gemm":
+        return gemm(a, b, chain.get("b_layout", "kn"), rows), rows
+    if chain["contraction"] == "conv2d_3x3":
+        return conv2d_3x3(a, b, images), images
+    if chain["contraction"] == "conv3d_3x3x3":
+        return conv3d_3x3x3(a, b, images), images
+    raise ValueError(chain["contraction"])
+
+
 def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
     """Evaluate one fused chain in float64.
 
@@ -365,26 +445,5 @@ def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
              (conv); every op in scope is local to a row (GEMM) or to one
              image (conv), so the selected slice is exact.
     """
-    dt = chain["in_dtype"]
-    a = to_f64(tensors["a"], dt)
-    if chain["contraction"] == "rowwise":
-        # no contraction: the ops run over the rows of A
-        h = a if rows is None else a[np.asarray(rows, dtype=np.int64)]
-        sel = rows
-        return _apply_ops(chain, tensors, h, sel)
-    b = to_f64(tensors["b"], dt)
-    if dt == "e4m3":
-        a = a * float(np.float32(chain["scale_a"]))
-        b = b * float(np.float32(chain["scale_b"]))
-    if chain["contraction"] == "gemm":
-        h = gemm(a, b, chain.get("b_layout", "kn"), rows)
-        sel = rows
-    elif chain["contraction"] == "conv2d_3x3":
-        h = conv2d_3x3(a, b, images)
-        sel = images
-    elif chain["contraction"] == "conv3d_3x3x3":
-        h = conv3d_3x3x3(a, b, images)
-        sel = images
-    else:
-        raise ValueError(chain["contraction"])
+    h, sel = _contraction(chain, tensors, rows, images)
     return _apply_ops(chain, tensors, h, sel)

@@ -547,3 +547,165 @@ def test_chain_f2_uniform_bias_only_invariants_and_torch():
     ref = F.max_pool3d(F.max_pool3d(torch.softmax(F.conv3d(x, w, _t(bb)), dim=1), 2), 2).numpy()
     assert np.allclose(out, ref, rtol=1e-12, atol=1e-15)
     assert np.allclose(oracle.run_chain(ch, t, images=[1]), ref[[1]], rtol=1e-12, atol=1e-15)
+
+
+# ----------------------------------------- the unfused chain (stored intermediates)
+
+def test_round_bf16_matches_torch_and_closed_forms():
+    """round_bf16 (float64 -> nearest bf16) against torch's float32 -> bf16
+    cast on float32 inputs (one rounding), and on float64 values that a
+    float32 step would turn into a tie: exactly halfway between 1 and its bf16
+    successor 1 + 2^-7 plus or minus 2^-40 must round away from the tie."""
+    rng = np.random.default_rng(3)
+    x = np.concatenate([rng.standard_normal(200000).astype(np.float32) * 7,
+                        (np.arange(2000, dtype=np.uint32) * 0x10000 + 0x3F808000).view(np.float32),
+                        np.array([0.0, -0.0, 1e-40, -3e-39, 3.3e38, -3.39e38, np.inf], np.float32)])
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    ours = oracle.round_bf16(x.astype(np.float64))
+    assert np.array_equal(ours, ref)
+    half = 1.0 + 2.0 ** -8
+    assert oracle.round_bf16(np.array([half]))[0] == 1.0                       # tie -> even
+    assert oracle.round_bf16(np.array([half + 2.0 ** -40]))[0] == 1.0 + 2.0 ** -7
+    assert oracle.round_bf16(np.array([half - 2.0 ** -40]))[0] == 1.0
+    assert oracle.round_bf16(np.array([-(half + 2.0 ** -40)]))[0] == -(1.0 + 2.0 ** -7)
+    big = (2.0 - 2.0 ** -7) * 2.0 ** 127                                         # largest finite bf16
+    # half a quantum (2^119) above it is the tie between it and 2^128: to even, overflow
+    assert np.array_equal(oracle.round_bf16(np.array([big + 2.0 ** 118, big + 2.0 ** 119])), [big, np.inf])
+
+
+def _bf16(x):
+    return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16)
+
+
+def _torch_eager_bf16(ch, t):
+    """The chain as an eager PyTorch module on the CPU runs it op by op with
+    bf16 activations stored between the ops: every op reads the stored bf16
+    tensor, is evaluated by torch's own float32 CPU kernel and its result is
+    stored in bf16 (fp32 parameters -- bias, gamma, beta -- enter in
+    float32).  The last op's result is returned in float32 (row logsumexp)
+    or bf16."""
+    bf = torch.bfloat16
+    dt = ch["in_dtype"]
+    if ch["contraction"] == "rowwise":
+        h = _bf16(t["a"])
+    elif dt == "e4m3":
+        a = torch.from_numpy(t["a"]).view(torch.float8_e4m3fn).float() * float(np.float32(ch["scale_a"]))
+        b = torch.from_numpy(t["b"]).view(torch.float8_e4m3fn).float() * float(np.float32(ch["scale_b"]))
+        h = (a.double() @ b.double()).to(torch.float32).to(bf)
+    elif ch["contraction"] == "gemm":
+        h = torch.matmul(_bf16(t["a"]), _bf16(t["b"]))
+    elif ch["contraction"] == "conv2d_3x3":
+        h = F.conv2d(_bf16(t["a"]), _bf16(t["b"]), padding=1)
+    else:
+        h = F.conv3d(_bf16(t["a"]), _bf16(t["b"]))
+    for name, *p in ch["ops"]:
+        x = h.float()
+        if name == "bias":
+            y = x + torch.from_numpy(t["bias"]).reshape((1, -1) + (1,) * (h.dim() - 2))
+        elif name == "relu":
+            y = F.relu(x)
+        elif name == "gelu_tanh":
+            y = F.gelu(x, approximate="tanh")
+        elif name == "gelu_erf":
+            y = F.gelu(x)
+        elif name == "swish":
+            y = F.silu(x)
+        elif name == "sigmoid":
+            y = torch.sigmoid(x)
+        elif name == "tanh":
+            y = torch.tanh(x)
+        elif name == "hardtanh":
+            y = F.hardtanh(x, p[0], p[1])
+        elif name == "scale":
+            y = x * p[0]
+        elif name == "groupnorm":
+            y = F.group_norm(x, p[0], torch.from_numpy(t["gamma"]), torch.from_numpy(t["beta"]), eps=p[1])
+        elif name == "residual_add":
+            y = x + _bf16(t["residual"]).float()
+        elif name == "maxpool2x2":
+            y = F.max_pool2d(x, 2)
+        elif name == "maxpool3d2":
+            y = F.max_pool3d(x, 2)
+        elif name == "channel_softmax":
+            y = torch.softmax(x, 1)
+        elif name == "row_softmax":
+            y = torch.softmax(x, -1)
+        elif name == "row_logsumexp":
+            y = torch.logsumexp(x, -1)
+        else:
+            raise ValueError(name)
+        h = y if name == "row_logsumexp" else y.to(bf)
+    return h
+
+
+_UNFUSED_CASES = [
+    ("C2", dict(M=48, N=520, K=136)),
+    ("C3", dict(M=40, N=512, K=96, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
+    ("C4", dict(batch=1, H=8, W=12)),
+    ("C5", dict(M=24, N=1024, K=128)),
+    ("F1", dict(M=40, N=264, K=72)),
+    ("F2", dict(batch=1, D=6, H=10, W=14)),
+    ("F3", dict(M=24, N=1024, ops=[("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)])),
+    ("F4", dict(M=16, N=2048)),
+]
+
+
+_ROUND_BF16 = oracle.round_bf16  # for the comparison itself, untouched by the planted mistake below
+
+
+def _unfused_vs_torch(name, kw):
+    cfg, t = _small(name, **kw)
+    ch = inputs.chain_for(cfg, t)
+    ours = oracle.run_chain_unfused(ch, t)
+    ref = _torch_eager_bf16(ch, t)
+    if ref.dtype == torch.float32:         # row logsumexp: fp32 output
+        return float(np.max(np.abs(ours - ref.double().numpy()))), None
+    ref = ref.double().numpy()
+    same = float(np.mean(_ROUND_BF16(ours) == ref))
+    return None, same
+
+
+@pytest.mark.parametrize("name,kw", _UNFUSED_CASES)
+def test_unfused_oracle_matches_torch_eager_bf16(name, kw):
+    """run_chain_unfused rounds the contraction's result and every op's
+    result but the last to bf16, as a one-operator-per-kernel chain stores
+    them.  Against torch's CPU eager composition with bf16 activations (an
+    independent implementation of every op, computing in float32), the final
+    bf16 outputs agree bit for bit except where a float32 evaluation lands
+    within a few float32 ulps of a bf16 rounding boundary (rare), and the
+    float32 logsumexp agrees to float32 accuracy.  A missing or misplaced
+    rounding step breaks both (see the planted-mistake test below)."""
+    diff, same = _unfused_vs_torch(name, kw)
+    if diff is not None:
+        assert diff < 2e-5, diff
+    else:
+        assert same >= 0.995, same
+
+
+@pytest.mark.parametrize("name,kw", [c for c in _UNFUSED_CASES if c[0] != "F4"])
+def test_unfused_oracle_pin_detects_a_missing_rounding(name, kw, monkeypatch):
+    """The pin above is discriminating: with the intermediate rounding planted
+    out of the oracle (intermediates kept in float64), the C2 logsumexp moves
+    by more than 2e-5 and the bf16 outputs of the other chains stop agreeing
+    with torch's in more than 0.5 % of the elements.  (F4's single op reads A
+    itself: it has no intermediate to round.)"""
+    monkeypatch.setattr(oracle, "round_bf16", lambda x: np.asarray(x, dtype=np.float64) if np.ndim(x) else x)
+    diff, same = _unfused_vs_torch(name, kw)
+    monkeypatch.undo()
+    if diff is not None:
+        assert diff > 2e-5, diff
+    else:
+        assert same < 0.995, same
+
+
+def test_unfused_oracle_equals_fused_without_ops_and_rounds_f32_chains():
+    """No op: nothing is stored between steps, so the unfused oracle is the
+    fused one exactly.  fp32 chains store float32 intermediates."""
+    cfg, t = _small("C2", M=8, N=64, K=32, ops=[], out_dtype="f32")
+    ch = inputs.chain(cfg)
+    assert np.array_equal(oracle.run_chain_unfused(ch, t), oracle.run_chain(ch, t))
+    cfg, t = _small("C1", M=8, N=64, K=256)
+    ch = inputs.chain(cfg)
+    h = oracle.gemm(t["a"].astype(np.float64), t["b"].astype(np.float64))
+    expect = np.maximum(oracle.round_f32(oracle.round_f32(h) + t["bias"].astype(np.float64)), 0.0)
+    assert np.array_equal(oracle.run_chain_unfused(ch, t), expect)
