@@ -56,6 +56,19 @@ __device__ __forceinline__ void buf_store4(uint32_t v, __amdgpu_buffer_rsrc_t r,
   __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
 }
 
+// Streaming (nontemporal) store: the written lines are not kept in the
+// caches -- for the outputs of the memory-bound kernels, which no later
+// kernel of the same op reads back.  On this GPU a 256 MiB read-and-write
+// stream of 16-byte lanes moved at ~4.7 TB/s with ordinary stores and
+// ~6.5 TB/s with nontemporal ones: ordinary writes fill the 256 MB
+// memory-side cache and evict the lines still to be read.  (The GEMM
+// epilogue's 8-byte stores were much slower with the bit, so the matrix-core
+// kernels store normally.)
+template <typename T>
+__device__ __forceinline__ void store_nt(T* p, T v) {
+  __builtin_nontemporal_store(v, p);
+}
+
 // ------------------------------------------------------------------- bf16
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -29,8 +29,8 @@ enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
 // is interpreted at run time.  The paper turns each operator into its own
 // specialised kernel; these are the chains of the benchmarked operators and
 // the plain building blocks, and every other chain runs interpreted.
-constexpr int kNumChains = 11;
-constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1, 4};
+constexpr int kNumChains = 13;
+constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1, 4, 1, 1};
 constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {},                                                                         // 0: interpreted
     {},                                                                         // 1: contraction only
@@ -43,10 +43,16 @@ constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {KF_OP_BIAS, KF_OP_SWISH, KF_OP_TANH, KF_OP_GELU_ERF, KF_OP_HARDTANH},     // 8: GEMM + activation chain
     {KF_OP_ROW_SOFTMAX},                                                        // 9: softmax rows
     {KF_OP_BIAS, KF_OP_CHANNEL_SOFTMAX, KF_OP_MAXPOOL3D_2, KF_OP_MAXPOOL3D_2},  // 10: conv3d, softmax, pools
+    {KF_OP_GROUPNORM},                                                          // 11: GroupNorm rows
+    {KF_OP_ROW_LOGSUMEXP},                                                      // 12: logsumexp rows
 };
 // Which contraction a chain belongs to: 0 any, 1 GEMM / ROWWISE, 2 CONV2D_3X3,
 // 3 CONV3D_3X3X3.
-constexpr int kChainFamily[kNumChains] = {0, 0, 1, 1, 1, 1, 1, 2, 1, 1, 3};
+constexpr int kChainFamily[kNumChains] = {0, 0, 1, 1, 1, 1, 1, 2, 1, 1, 3, 1, 1};
+// Chains of one row reduction (the unfused comparator's row-op kernels).
+constexpr int kChainRowSoftmax = 9;
+constexpr int kChainGroupNorm = 11;
+constexpr int kChainRowLogsumexp = 12;
 
 // Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).
 struct GemmArgs {

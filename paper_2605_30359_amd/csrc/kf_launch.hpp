@@ -8,6 +8,21 @@
 
 namespace kf {
 
+// Workgroups of `kernel` (block threads, no dynamic LDS) that the device holds
+// at once: compute units x resident workgroups per compute unit.  Streaming
+// kernels size a grid-stride launch by it, so that no partly filled last
+// round of workgroups trails the launch.  Callers cache it per kernel.
+template <typename Kernel>
+inline int resident_blocks(Kernel kernel, int block) {
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, block, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    return 1024;
+  }
+  return (cus > 0 ? cus : 1) * (per > 0 ? per : 1);
+}
+
 // bf16 or OCP fp8 e4m3 GEMM + epilogue on the matrix cores; `epi` is an
 // EpiShape, `chain` a compile-time chain id (0: the op list is interpreted).
 hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, hipStream_t stream, bool b_nk);

@@ -101,14 +101,14 @@ __global__ __launch_bounds__(256) void kf_row_softmax_rescale(const float2* __re
         const float f = fac[c >> shift];
 #pragma unroll
         for (int e = 0; e < 4; ++e) w[u][e] = pack_bf16x2(bf16_lo(w[u][e]) * f, bf16_hi(w[u][e]) * f);
-        rowb[c] = w[u];
+        store_nt(rowb + c, w[u]);
       }
     } else {
       if (c0 > 0) load_pass(rowf, chunks, c0, tid, v);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t c = c0 + u * 256 + tid;
-        if (c < chunks) rowf[c] = v[u] * fac[c >> shift];
+        if (c < chunks) store_nt(rowf + c, v[u] * fac[c >> shift]);
       }
     }
   }

@@ -18,6 +18,8 @@
 //            pairwise tree in LDS (any group width that is a multiple of 8
 //            columns); the mean and the biased variance take two such passes
 //            over the registers
+#include <algorithm>
+
 #include "kf_device.hpp"
 #include "kf_launch.hpp"
 
@@ -261,16 +263,172 @@ __global__ __launch_bounds__(RT) void kf_rowwise(RowArgs p) {
       u32x4 w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(v[j][2 * e], v[j][2 * e + 1]);
-      *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(p.out) + m * p.ldo + c * 8) = w;
+      store_nt(reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(p.out) + m * p.ldo + c * 8), w);
     } else {
       f32x4* f = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.out) + m * p.ldo + c * 8);
-      f[0] = f32x4{v[j][0], v[j][1], v[j][2], v[j][3]};
-      f[1] = f32x4{v[j][4], v[j][5], v[j][6], v[j][7]};
+      store_nt(f, f32x4{v[j][0], v[j][1], v[j][2], v[j][3]});
+      store_nt(f + 1, f32x4{v[j][4], v[j][5], v[j][6], v[j][7]});
+    }
+  }
+}
+
+
+// GroupNorm chains whose group is a power-of-two number of chunks up to 64
+// (group widths 8..512 columns), with element-wise ops, a bias and a
+// residual add around the GroupNorm but no whole-row reduction.  The groups
+// are independent, so the work is cut into column panels instead of rows:
+// each wave takes one group g for its whole life and walks rows, P = 64 / L
+// rows per step (lane = row-in-step * L + chunk-in-group).  gamma and beta
+// (and the bias) of the wave's 8 columns per lane are loaded once into
+// registers -- a row kernel re-reads them for every row, 64 KiB per row at
+// 8192 columns -- and the group statistics are sums over L lanes by xor
+// exchanges (no LDS, no barrier).  Each lane keeps kPanelUnroll steps of A
+// (and residual) chunks in flight.
+constexpr int kPanelUnroll = 4;
+
+template <int CH>
+__global__ __launch_bounds__(RT) void kf_rowwise_gn_panel(RowArgs p) {
+  const int lane = threadIdx.x & 63;
+  const int L = p.gn_group >> 3;  // chunks per group: a power of two, 1..64
+  const int P = 64 / L;           // rows per step
+  const int groups = (int)(p.N / p.gn_group);
+  const int g = blockIdx.x % groups;
+  const int waves = (int)(gridDim.x / groups) * (RT / 64);
+  const int wave = (int)(blockIdx.x / groups) * (RT / 64) + (threadIdx.x >> 6);
+  const int q = lane & (L - 1);
+  const int pr = lane / L;
+  const int64_t col = (int64_t)g * p.gn_group + q * 8;
+  const int nops = p.prog.n;
+  const OpTable ops = load_op_table(p.prog, lane);
+  const float inv_n = 1.0f / (float)p.gn_group;
+
+  float gam[8], bet[8], bia[8];
+  {
+    const f32x4* gp = reinterpret_cast<const f32x4*>(p.gamma + col);
+    const f32x4* bp = reinterpret_cast<const f32x4*>(p.beta + col);
+    const f32x4 g0 = gp[0], g1 = gp[1], b0 = bp[0], b1 = bp[1];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      gam[e] = g0[e];
+      gam[4 + e] = g1[e];
+      bet[e] = b0[e];
+      bet[4 + e] = b1[e];
+      bia[e] = bia[4 + e] = 0.0f;
+    }
+    if (p.bias) {
+      const f32x4* cp = reinterpret_cast<const f32x4*>(p.bias + col);
+      const f32x4 c0 = cp[0], c1 = cp[1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        bia[e] = c0[e];
+        bia[4 + e] = c1[e];
+      }
+    }
+  }
+
+  // sum over the L lanes of this lane's group (every lane gets the same bits)
+  auto group_sum = [&](float x) {
+    for (int d = 1; d < L; d <<= 1) x += shfl_xor(x, d);
+    return x;
+  };
+
+  const int64_t steps = (p.M + P - 1) / P;
+  for (int64_t s0 = wave; s0 < steps; s0 += (int64_t)waves * kPanelUnroll) {
+    Chunk v[kPanelUnroll], r[kPanelUnroll];
+    int64_t row[kPanelUnroll];
+    bool ok[kPanelUnroll];
+#pragma unroll
+    for (int u = 0; u < kPanelUnroll; ++u) {
+      row[u] = (s0 + (int64_t)u * waves) * P + pr;
+      ok[u] = s0 + (int64_t)u * waves < steps && row[u] < p.M;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[u][e] = r[u][e] = 0.0f;
+      if (ok[u]) {
+        load_chunk(p.a, p.in_bf16 != 0, row[u] * p.lda + col, v[u]);
+        if (p.residual) load_chunk(p.residual, p.residual_bf16 != 0, row[u] * p.ldr + col, r[u]);
+      }
+    }
+    auto run_op = [&](int kind, int o) {
+#pragma unroll
+      for (int u = 0; u < kPanelUnroll; ++u) {
+        if (kind == KF_OP_BIAS) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[u][e] += bia[e];
+        } else if (kind == KF_OP_RESIDUAL_ADD) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[u][e] += r[u][e];
+        } else if (kind == KF_OP_GROUPNORM) {
+          const float eps = op_p0(ops, o);
+          const float sum = ((v[u][0] + v[u][1]) + (v[u][2] + v[u][3])) + ((v[u][4] + v[u][5]) + (v[u][6] + v[u][7]));
+          const float mean = group_sum(sum) * inv_n;
+          float qd = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float d = v[u][e] - mean;
+            qd = fmaf(d, d, qd);
+          }
+          const float rs = rsqrtf(group_sum(qd) * inv_n + eps);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[u][e] = fmaf((v[u][e] - mean) * rs, gam[e], bet[e]);
+        } else {
+          apply_elementwise_array<8>(kind, op_p0(ops, o), op_p1(ops, o), v[u]);
+        }
+      }
+    };
+    if constexpr (CH == 0) {
+      for (int o = 0; o < nops; ++o) run_op(op_kind(ops, o), o);
+    } else {
+      static_for<0, kChainLen[CH]>([&](auto O_c) {
+        constexpr int o = decltype(O_c)::value;
+        run_op(kChainOps[CH][o], o);
+      });
+    }
+#pragma unroll
+    for (int u = 0; u < kPanelUnroll; ++u) {
+      if (!ok[u]) continue;
+      if (p.out_bf16) {
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(v[u][2 * e], v[u][2 * e + 1]);
+        store_nt(reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(p.out) + row[u] * p.ldo + col), w);
+      } else {
+        f32x4* f = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.out) + row[u] * p.ldo + col);
+        store_nt(f, f32x4{v[u][0], v[u][1], v[u][2], v[u][3]});
+        store_nt(f + 1, f32x4{v[u][4], v[u][5], v[u][6], v[u][7]});
+      }
     }
   }
 }
 
 namespace {
+
+// The column-panel form applies to a GroupNorm chain with no whole-row op
+// whose group is 1, 2, 4, ..., 64 chunks of 8 columns.
+bool panel_applies(const RowArgs& a) {
+  if (a.gn_group <= 0 || a.gn_group % 8 || a.gn_group > 512) return false;
+  const int L = a.gn_group / 8;
+  if (L & (L - 1)) return false;
+  for (int i = 0; i < a.prog.n; ++i) {
+    const int k = a.prog.op[i].kind;
+    if (k == KF_OP_ROW_SOFTMAX || k == KF_OP_ROW_LOGSUMEXP) return false;
+  }
+  return true;
+}
+
+template <int CH>
+hipError_t launch_panel(const RowArgs& args, hipStream_t stream) {
+  // as many workgroups as the device holds at once, whole sets of them per
+  // column group, and no more waves per group than it has row steps
+  static const int resident = resident_blocks(kf_rowwise_gn_panel<CH>, RT);
+  const int64_t groups = args.N / args.gn_group;
+  const int64_t P = 64 / (args.gn_group / 8);
+  const int64_t steps = (args.M + P - 1) / P;
+  int64_t per_group = std::max<int64_t>(1, resident / groups);
+  per_group = std::min<int64_t>(per_group, (steps + RT / 64 - 1) / (RT / 64));
+  const dim3 grid((unsigned)(groups * per_group)), block(RT);
+  hipLaunchKernelGGL((kf_rowwise_gn_panel<CH>), grid, block, 0, stream, args);
+  return hipGetLastError();
+}
 
 template <int CH>
 hipError_t launch_rowwise_chain(const RowArgs& args, hipStream_t stream) {
@@ -296,9 +454,18 @@ hipError_t launch_rowwise_chain(const RowArgs& args, hipStream_t stream) {
 // interpreted.
 hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream) {
   if (args.M <= 0) return hipSuccess;
+  if (panel_applies(args)) {
+    switch (chain) {
+      case 5: return launch_panel<5>(args, stream);
+      case kChainGroupNorm: return launch_panel<kChainGroupNorm>(args, stream);
+      default: return launch_panel<0>(args, stream);
+    }
+  }
   switch (chain) {
     case 5: return launch_rowwise_chain<5>(args, stream);
-    case 9: return launch_rowwise_chain<9>(args, stream);
+    case kChainRowSoftmax: return launch_rowwise_chain<kChainRowSoftmax>(args, stream);
+    case kChainGroupNorm: return launch_rowwise_chain<kChainGroupNorm>(args, stream);
+    case kChainRowLogsumexp: return launch_rowwise_chain<kChainRowLogsumexp>(args, stream);
     default: return launch_rowwise_chain<0>(args, stream);
   }
 }
