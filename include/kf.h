@@ -157,21 +157,35 @@ typedef struct kf_tensor {
 typedef struct kf_desc kf_desc;
 
 /* Validate `spec` and plan the operation: kernel variant, tile shape and a
-   device workspace for cross-tile row partials (owned by the descriptor).
+   device workspace (owned by the descriptor) for the repacked conv weights or
+   the cross-tile row partials.  The spec is the paper's problem statement of
+   an operator given as a PyTorch reference computation (Methodology,
+   Overview): the contraction, its shapes and dtypes, and the forward's op
+   sequence, parameters in module order.
    Validation happens on the host before any device call, so spec errors are
    reported (KF_ERR_INVALID_ARG / _SHAPE / _UNSUPPORTED) even with no GPU
-   present; a valid spec with no gfx950 device returns KF_ERR_NO_DEVICE.
-   On any error *out is set to NULL. */
+   present; a valid spec with no gfx950 device returns KF_ERR_NO_DEVICE, a
+   failed workspace allocation KF_ERR_OOM.  On any error *out is set to NULL.
+   The caller owns *out and frees it with kf_destroy. */
 kf_status kf_create(const kf_op_spec* spec, kf_desc** out);
 
-/* Run the fused operation on `stream`.
+/* Run the fused operation on `stream`: the contraction and the whole op list
+   in one kernel, intermediates kept in registers (the operator fusion and
+   online softmax of Appendix A), plus, for a row softmax / logsumexp over
+   more than one 256-column tile, a finishing kernel over the per-tile
+   partials (Appendix B, hierarchical reductions).
    inputs (in this order): A, B (no B for KF_ROWWISE), then one slot per
    tensor the ops need, in op order -- BIAS: bias; GROUPNORM: gamma, beta;
-   RESIDUAL_ADD: residual.
-   outputs: exactly one tensor (shape from kf_output_shape, dtype
-   spec.out_dtype).  The descriptor's workspace is reused by every call, so
-   at most one call per descriptor may be in flight at a time (use one
-   descriptor per stream). */
+   RESIDUAL_ADD: residual.  All are device pointers owned by the caller.
+   outputs: exactly one tensor (shape from kf_output_info, dtype
+   spec.out_dtype), written, never reallocated.
+   Returns KF_ERR_SHAPE / _UNSUPPORTED / _INVALID_ARG when a tensor does not
+   match the plan (nothing is launched), KF_ERR_HIP when a launch fails.  The
+   descriptor's workspace is reused by every call, so at most one call per
+   descriptor may be in flight at a time (use one descriptor per stream).
+   Conv plans repack B into the workspace on the first call and again only
+   when B's data pointer changes: after rewriting B's contents in place, call
+   kf_weights_changed first. */
 kf_status kf_fused_op(const kf_desc* desc, const kf_tensor* inputs,
                       kf_tensor* outputs, void* stream);
 
@@ -184,10 +198,17 @@ kf_status kf_fused_op_timed(const kf_desc* desc, const kf_tensor* inputs,
                             kf_tensor* outputs, void* stream, void* ev_before,
                             void* ev_after);
 
+/* Declare that the contents of the weight tensor B changed in place since
+   the last call: the next call of a conv plan repacks it.  (A different B
+   pointer is noticed without this.)  NULL is a no-op. */
+void kf_weights_changed(kf_desc* desc);
+
 /* The same operation as an unfused chain, one kernel per op, with every
    intermediate stored to device memory in bf16 (fp32 for fp32 chains) --
-   the comparator for the fused kernel.  Its intermediate buffers are
-   allocated on the first call and owned by the descriptor. */
+   the one-operator-per-kernel form that operator fusion removes (Appendix A,
+   "Operator Fusion"), the comparator for the fused kernel.  Its
+   intermediate buffers are allocated on the first call and owned by the
+   descriptor (KF_ERR_OOM if that fails); errors as for kf_fused_op. */
 kf_status kf_unfused_op(const kf_desc* desc, const kf_tensor* inputs,
                         kf_tensor* outputs, void* stream);
 

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -22,20 +23,20 @@
 
 namespace {
 
-thread_local std::string g_last_error;
+// The message of the last failing call on this thread: a fixed buffer, so
+// that reporting an error allocates nothing.
+thread_local char g_last_error[512];
 
 kf_status fail(kf_status st, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return st;
 }
 
 kf_status ok() {
-  g_last_error.clear();
+  g_last_error[0] = '\0';
   return KF_OK;
 }
 
@@ -47,6 +48,22 @@ struct Slot {
   int64_t shape[KF_MAX_DIMS];
   const char* name;
   bool channels_last;  // a 5-D [N, C, D, H, W] tensor stored as [N][D][H][W][C]
+};
+
+// The input slots of a plan: A, B and at most one bias, gamma, beta and
+// residual -- a fixed-capacity list, so that a plan can live on the stack.
+constexpr int kMaxSlots = 6;
+struct SlotList {
+  Slot s[kMaxSlots];
+  int n = 0;
+  void clear() { n = 0; }
+  void push_back(const Slot& x) {
+    if (n < kMaxSlots) s[n++] = x;
+  }
+  size_t size() const { return (size_t)n; }
+  const Slot& operator[](size_t i) const { return s[i]; }
+  const Slot* begin() const { return s; }
+  const Slot* end() const { return s + n; }
 };
 
 int64_t elem_size(int32_t dt) { return dt == KF_F32 ? 4 : dt == KF_BF16 ? 2 : 1; }
@@ -68,17 +85,20 @@ struct kf_desc {
   int gn_group;
   int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / 0
   int chain = 0;  // compile-time epilogue chain matching the op list (0: interpreted)
-  std::vector<Slot> inputs;
+  SlotList inputs;
   Slot output;
   int device;
   void* workspace;
   size_t workspace_bytes;
   int tiles_n;
-  std::string kernel_name;
+  const char* kernel_name = "";
   kf_tuning tuning;  // launch fields (see kf_set_tuning)
   // unfused comparator: two intermediate buffers, allocated on first use
   mutable void* ubuf[2];
   mutable size_t ubuf_bytes;
+  // conv plans: the weight tensor whose repacked copy the workspace holds
+  // (nullptr: none yet, or the caller declared the weights changed)
+  mutable const void* packed_from = nullptr;
 };
 
 namespace {
@@ -474,6 +494,66 @@ Work plan_work(const kf_desc* d) {
   return w;
 }
 
+void init_desc(kf_desc* d) {
+  d->workspace = nullptr;
+  d->workspace_bytes = 0;
+  d->tiles_n = 0;
+  d->ubuf[0] = d->ubuf[1] = nullptr;
+  d->ubuf_bytes = 0;
+  d->packed_from = nullptr;
+  d->tuning = kf_tuning{4, 1, 2, 0};
+}
+
+// The current device, checked to be a gfx950, and its compute units; the
+// properties are queried once per device and cached.
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_device_cus[kMaxDevices];  // 0 unknown, -1 not gfx950, else the CU count
+
+kf_status current_device(int* dev_out, int* cus_out) {
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count < 1) {
+    (void)hipGetLastError();
+    return fail(KF_ERR_NO_DEVICE, "no HIP device present");
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(KF_ERR_NO_DEVICE, "cannot query the current HIP device");
+  }
+  int cus = dev >= 0 && dev < kMaxDevices ? g_device_cus[dev].load(std::memory_order_relaxed) : 0;
+  if (cus == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(KF_ERR_NO_DEVICE, "cannot query the current HIP device");
+    }
+    cus = strncmp(prop.gcnArchName, "gfx950", 6) != 0 ? -1 : (prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1);
+    if (dev >= 0 && dev < kMaxDevices) g_device_cus[dev].store(cus, std::memory_order_relaxed);
+    if (cus < 0) return fail(KF_ERR_NO_DEVICE, "device %d is %s; this library is built for gfx950 only", dev, prop.gcnArchName);
+  }
+  if (cus < 0) return fail(KF_ERR_NO_DEVICE, "device %d is not a gfx950; this library is built for gfx950 only", dev);
+  *dev_out = dev;
+  *cus_out = cus;
+  return KF_OK;
+}
+
+// Device workspace a plan's kernels use: the repacked conv weights, or the
+// per-(row, column tile) (max, sum) partials of a GEMM's row softmax /
+// logsumexp.
+size_t plan_workspace_bytes(const kf_desc* d) {
+  const kf_op_spec& s = d->spec;
+  if (d->variant == kVarConvBf16) return (size_t)9 * s.cout * s.cin * 2;
+  if (d->variant == kVarConv3d) return kf::conv3d_packed_bytes();
+  if (d->row_kind && d->variant != kVarRowwise) return (size_t)std::max<int64_t>(s.M, 1) * d->tiles_n * sizeof(float) * 2;
+  return 0;
+}
+
+// Enqueue the fused operation of plan d with `ws` as its workspace.  The
+// conv weights are repacked into ws unless `ws_keeps_weights` and ws already
+// holds the repacked copy of this B tensor.
+kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_tensor* inputs, kf_tensor* outputs,
+                    void* stream, void* ev_before, void* ev_after);
+
 }  // namespace
 
 extern "C" {
@@ -608,19 +688,14 @@ const char* kf_status_string(kf_status st) {
   }
 }
 
-const char* kf_last_error(void) { return g_last_error.c_str(); }
+const char* kf_last_error(void) { return g_last_error; }
 
 kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
   if (!out) return fail(KF_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   kf_desc* d = new (std::nothrow) kf_desc();
   if (!d) return fail(KF_ERR_OOM, "host allocation failed");
-  d->workspace = nullptr;
-  d->workspace_bytes = 0;
-  d->tiles_n = 0;
-  d->ubuf[0] = d->ubuf[1] = nullptr;
-  d->ubuf_bytes = 0;
-  d->tuning = kf_tuning{4, 1, 2, 0};
+  init_desc(d);
   kf_status st = validate_and_plan(spec, d);
   if (st != KF_OK) {
     delete d;
@@ -629,42 +704,20 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out) {
   d->spec = *spec;
   d->chain = match_chain(spec);
 
-  int count = 0;
-  if (hipGetDeviceCount(&count) != hipSuccess || count < 1) {
-    (void)hipGetLastError();
+  int dev = 0, cus = 0;
+  st = current_device(&dev, &cus);
+  if (st != KF_OK) {
     delete d;
-    return fail(KF_ERR_NO_DEVICE, "no HIP device present");
-  }
-  int dev = 0;
-  hipDeviceProp_t prop;
-  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) {
-    (void)hipGetLastError();
-    delete d;
-    return fail(KF_ERR_NO_DEVICE, "cannot query the current HIP device");
-  }
-  if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
-    delete d;
-    return fail(KF_ERR_NO_DEVICE, "device %d is %s; this library is built for gfx950 only", dev, prop.gcnArchName);
+    return st;
   }
   d->device = dev;
-  d->num_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
+  d->num_cu = cus;
 
-  if (d->variant == kVarConvBf16 || d->variant == kVarConv3d) {
-    // repacked weights
-    d->workspace_bytes =
-        d->variant == kVarConvBf16 ? (size_t)9 * spec->cout * spec->cin * 2 : kf::conv3d_packed_bytes();
-    if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
-      (void)hipGetLastError();
-      delete d;
-      return fail(KF_ERR_OOM, "workspace of %zu bytes could not be allocated", d->workspace_bytes);
-    }
-  } else if (d->row_kind && d->variant != kVarRowwise) {
-    d->workspace_bytes = (size_t)std::max<int64_t>(spec->M, 1) * d->tiles_n * sizeof(float) * 2;
-    if (hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
-      (void)hipGetLastError();
-      delete d;
-      return fail(KF_ERR_OOM, "workspace of %zu bytes could not be allocated", d->workspace_bytes);
-    }
+  d->workspace_bytes = plan_workspace_bytes(d);
+  if (d->workspace_bytes && hipMalloc(&d->workspace, d->workspace_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    delete d;
+    return fail(KF_ERR_OOM, "workspace of %zu bytes could not be allocated", d->workspace_bytes);
   }
   *out = d;
   return ok();
@@ -700,7 +753,7 @@ kf_status kf_output_info(const kf_desc* d, int32_t* dtype, int32_t* ndim, int64_
 
 size_t kf_workspace_bytes(const kf_desc* d) { return d ? d->workspace_bytes : 0; }
 
-const char* kf_kernel_name(const kf_desc* d) { return d ? d->kernel_name.c_str() : ""; }
+const char* kf_kernel_name(const kf_desc* d) { return d ? d->kernel_name : ""; }
 
 kf_status kf_fused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
   return kf_fused_op_timed(d, inputs, outputs, stream, nullptr, nullptr);
@@ -709,6 +762,18 @@ kf_status kf_fused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outp
 kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream,
                             void* ev_before, void* ev_after) {
   if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  return run_fused(d, d->workspace, true, inputs, outputs, stream, ev_before, ev_after);
+}
+
+void kf_weights_changed(kf_desc* d) {
+  if (d) d->packed_from = nullptr;
+}
+}  // extern "C"
+
+namespace {
+
+kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_tensor* inputs, kf_tensor* outputs,
+                    void* stream, void* ev_before, void* ev_after) {
   for (size_t i = 0; i < d->inputs.size(); ++i) {
     kf_status st = check_tensor(&inputs[i], d->inputs[i], false, d->variant != kVarGemmF32);
     if (st != KF_OK) return st;
@@ -721,9 +786,14 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
   if (s.contraction == KF_CONV3D_3X3X3) {
     const kf::Conv3dArgs a = conv3d_args(d, inputs, outputs[0].data, conv3d_pool_count(s));
     if (a.tiles == 0) return ok();
-    hipError_t e = kf::launch_conv3d_pack(inputs[1].data, d->workspace, hs);
+    hipError_t e = hipSuccess;
+    if (!ws_keeps_weights || d->packed_from != inputs[1].data) {
+      d->packed_from = nullptr;
+      e = kf::launch_conv3d_pack(inputs[1].data, ws, hs);
+      if (e == hipSuccess && ws_keeps_weights) d->packed_from = inputs[1].data;
+    }
     if (e == hipSuccess && ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
-    if (e == hipSuccess) e = kf::launch_conv3d_bf16(a, d->workspace, d->chain, hs);
+    if (e == hipSuccess) e = kf::launch_conv3d_bf16(a, ws, d->chain, hs);
     if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
     if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
@@ -797,7 +867,7 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
     a.out = outputs[0].data;
     a.ldo = outputs[0].ndim == 2 ? outputs[0].stride[0] : 1;
     a.out_bf16 = outputs[0].dtype == KF_BF16;
-    a.partials = d->workspace;
+    a.partials = ws;
     a.raster_group = d->tuning.raster_group;
     a.xcd_remap = d->tuning.xcd_remap;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
@@ -817,7 +887,7 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
       e = kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, d->epi_shape, d->chain, hs, nk);
       if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
       if (e == hipSuccess && d->row_kind)
-        e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, d->workspace, d->tiles_n, s.M, s.N, a.out,
+        e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, ws, d->tiles_n, s.M, s.N, a.out,
                                   a.ldo, a.out_bf16 != 0, hs);
     }
     if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -846,13 +916,22 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
   }
   c.out = outputs[0].data;
   c.out_bf16 = 1;
-  hipError_t e = kf::launch_conv_pack(c, d->workspace, hs);
+  hipError_t e = hipSuccess;
+  if (!ws_keeps_weights || d->packed_from != inputs[1].data) {
+    d->packed_from = nullptr;
+    e = kf::launch_conv_pack(c, ws, hs);
+    if (e == hipSuccess && ws_keeps_weights) d->packed_from = inputs[1].data;
+  }
   if (e == hipSuccess && ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
-  if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, d->chain, hs);
+  if (e == hipSuccess) e = kf::launch_conv_bf16(c, ws, d->chain, hs);
   if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
   if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
+
+}  // namespace
+
+extern "C" {
 
 kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
   if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
@@ -930,7 +1009,11 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   } else if (conv3d) {
     // the convolution alone: every conv output position, NCDHW
     const kf::Conv3dArgs a = conv3d_args(d, inputs, cur, 0);
-    e = kf::launch_conv3d_pack(inputs[1].data, d->workspace, hs);
+    if (d->packed_from != inputs[1].data) {
+      d->packed_from = nullptr;
+      e = kf::launch_conv3d_pack(inputs[1].data, d->workspace, hs);
+      if (e == hipSuccess) d->packed_from = inputs[1].data;
+    }
     if (e == hipSuccess && a.tiles) e = kf::launch_conv3d_bf16(a, d->workspace, 1, hs);
   } else {
     kf::ConvArgs c;
@@ -946,7 +1029,11 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     c.grid = d->num_cu;
     c.out = cur;
     c.out_bf16 = 1;
-    e = kf::launch_conv_pack(c, d->workspace, hs);
+    if (d->packed_from != inputs[1].data) {
+      d->packed_from = nullptr;
+      e = kf::launch_conv_pack(c, d->workspace, hs);
+      if (e == hipSuccess) d->packed_from = inputs[1].data;
+    }
     if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, 0, hs);
   }
   if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));

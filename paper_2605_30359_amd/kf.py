@@ -39,7 +39,7 @@ DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
-            "kf_autotune")
+            "kf_autotune", "kf_weights_changed")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
 KF_MAX_TUNE_CANDIDATES = 16
 
@@ -115,6 +115,8 @@ def lib():
         L.kf_fused_op_timed.restype = i32
         L.kf_unfused_op.argtypes = [vp, ctypes.POINTER(KfTensor), ctypes.POINTER(KfTensor), vp]
         L.kf_unfused_op.restype = i32
+        L.kf_weights_changed.argtypes = [vp]
+        L.kf_weights_changed.restype = None
         L.kf_destroy.argtypes = [vp]
         L.kf_destroy.restype = None
         L.kf_num_inputs.argtypes = [vp]
@@ -360,6 +362,10 @@ class FusedOp:
     def unfused(self, inputs, out=None, stream=None):
         return self._call(lib().kf_unfused_op, inputs, out, stream)
 
+    def weights_changed(self):
+        """kf_weights_changed: B was rewritten in place; the next call repacks it."""
+        lib().kf_weights_changed(self._h)
+
     def diagnose(self, kernel_seconds: float, hbm_bytes: float = 0.0) -> dict:
         g = KfDiagnosis()
         _check(lib().kf_diagnose(self._h, kernel_seconds, hbm_bytes or 0.0, ctypes.byref(g)))
@@ -401,3 +407,4 @@ class FusedOp:
             cl = name == "a" and self.chain["contraction"] == "conv3d_3x3x3"
             out.append(device_tensor(tensors[name], dt, device, channels_last=cl))
         return out
+
