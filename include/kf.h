@@ -322,6 +322,24 @@ typedef struct kf_tune_result {
 kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
                       kf_tune_result* result);
 
+/* ---- An entry point that allocates nothing ------------------------------
+   For callers that cannot allocate device memory: code under HIP graph
+   capture, tight serving loops, harnesses that forbid allocation.  Plans
+   `spec` on the stack (no descriptor, no host or device allocation) and runs
+   the fused operation exactly as kf_create + kf_fused_op would, with the
+   library's static device scratch (4 MiB per GPU, held from the first call
+   on a device until the process ends) in place of a descriptor workspace.
+   Arguments, tensor rules and errors are those of kf_create and
+   kf_fused_op; an op whose workspace exceeds the scratch (e.g. a row softmax
+   with more than 512 K (row, 256-column tile) pairs) is rejected with
+   KF_ERR_UNSUPPORTED before any device call.  Every call on one GPU uses the
+   same scratch and nothing in it needs to start at zero (each call writes
+   what it reads); calls that overlap on one GPU -- on different streams or
+   host threads -- race on it and must be serialised by the caller.  Conv
+   weights are repacked on every call. */
+kf_status kf_fused_op_noalloc(const kf_op_spec* spec, const kf_tensor* inputs,
+                              kf_tensor* outputs, void* stream);
+
 /* Static description of a status code. */
 const char* kf_status_string(kf_status status);
 

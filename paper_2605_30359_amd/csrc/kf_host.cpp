@@ -768,6 +768,34 @@ kf_status kf_fused_op_timed(const kf_desc* d, const kf_tensor* inputs, kf_tensor
 void kf_weights_changed(kf_desc* d) {
   if (d) d->packed_from = nullptr;
 }
+
+kf_status kf_fused_op_noalloc(const kf_op_spec* spec, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
+  if (!spec || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  kf_desc d;  // the plan lives on the stack: it holds no heap memory
+  init_desc(&d);
+  kf_status st = validate_and_plan(spec, &d);
+  if (st != KF_OK) return st;
+  d.spec = *spec;
+  d.chain = match_chain(spec);
+  const size_t need = plan_workspace_bytes(&d);
+  if (need > kf::scratch_bytes())
+    return fail(KF_ERR_UNSUPPORTED,
+                "this op needs %zu bytes of device scratch; kf_fused_op_noalloc's static scratch holds %zu "
+                "(use kf_create / kf_fused_op)",
+                need, kf::scratch_bytes());
+  int dev = 0, cus = 0;
+  st = current_device(&dev, &cus);
+  if (st != KF_OK) return st;
+  d.device = dev;
+  d.num_cu = cus;
+  void* ws = nullptr;
+  if (need) {
+    const hipError_t e = kf::scratch_address(dev, &ws);
+    if (e != hipSuccess) return fail(KF_ERR_HIP, "static scratch lookup failed: %s", hipGetErrorString(e));
+  }
+  return run_fused(&d, ws, false, inputs, outputs, stream, nullptr, nullptr);
+}
+
 }  // extern "C"
 
 namespace {

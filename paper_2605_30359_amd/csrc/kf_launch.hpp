@@ -23,6 +23,12 @@ inline int resident_blocks(Kernel kernel, int block) {
   return (cus > 0 ? cus : 1) * (per > 0 ? per : 1);
 }
 
+// Device address of the static scratch array on `device` (the current
+// device), looked up on the first call per device; scratch_bytes() is its
+// size.
+hipError_t scratch_address(int device, void** out);
+size_t scratch_bytes();
+
 // bf16 or OCP fp8 e4m3 GEMM + epilogue on the matrix cores; `epi` is an
 // EpiShape, `chain` a compile-time chain id (0: the op list is interpreted).
 hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, hipStream_t stream, bool b_nk);

@@ -39,7 +39,7 @@ DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
-            "kf_autotune", "kf_weights_changed")
+            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
 KF_MAX_TUNE_CANDIDATES = 16
 
@@ -117,6 +117,9 @@ def lib():
         L.kf_unfused_op.restype = i32
         L.kf_weights_changed.argtypes = [vp]
         L.kf_weights_changed.restype = None
+        L.kf_fused_op_noalloc.argtypes = [ctypes.POINTER(KfOpSpec), ctypes.POINTER(KfTensor),
+                                          ctypes.POINTER(KfTensor), vp]
+        L.kf_fused_op_noalloc.restype = i32
         L.kf_destroy.argtypes = [vp]
         L.kf_destroy.restype = None
         L.kf_num_inputs.argtypes = [vp]
@@ -408,3 +411,30 @@ class FusedOp:
             out.append(device_tensor(tensors[name], dt, device, channels_last=cl))
         return out
 
+
+def fused_op_noalloc(chain: dict, inputs, out, stream=None, **sizes):
+    """kf_fused_op_noalloc: plan `chain` on the stack and run it with the
+    library's static device scratch -- no allocation anywhere, for callers
+    that cannot allocate.  `inputs` / `out` are device tensors in the slot
+    order of FusedOp.device_inputs; returns `out`."""
+    torch = _torch()
+    spec = make_spec(chain, **sizes)
+    arr = (KfTensor * max(1, len(inputs)))(*[to_kf_tensor(t) for t in inputs])
+    o = (KfTensor * 1)(to_kf_tensor(out))
+    if stream is None:
+        stream = torch.cuda.current_stream(out.device).cuda_stream
+    elif not isinstance(stream, int):
+        stream = stream.cuda_stream
+    _check(lib().kf_fused_op_noalloc(ctypes.byref(spec), arr, o, ctypes.c_void_p(stream)))
+    return out
+
+
+def fused_op_noalloc_status(chain: dict, **sizes) -> tuple:
+    """(status, message) of kf_fused_op_noalloc for `chain` with no tensors
+    bound (NULL-free empty descriptors): the host-side planning and scratch
+    size checks, which run before any device call."""
+    spec = make_spec(chain, **sizes)
+    arr = (KfTensor * 8)()
+    o = (KfTensor * 1)()
+    st = lib().kf_fused_op_noalloc(ctypes.byref(spec), arr, o, None)
+    return st, last_error()

@@ -274,3 +274,24 @@ def test_classify_bounds():
     assert kf.classify(P * 1e12 * 0.5, B * 1e9 * 0.5, 1.0, P, B, 1000, CU)["bound"] == "memory"
     with pytest.raises(kf.KFError):
         kf.classify(1.0, 1.0, 0.0, P, B, 1, CU)
+
+
+def test_noalloc_rejects_before_any_device_call():
+    """kf_fused_op_noalloc plans on the host first: a malformed spec, and an
+    op whose workspace exceeds the 4 MiB static scratch, are rejected before
+    any device call (so also here, with no GPU); a valid small spec then
+    needs a device."""
+    ch = inputs.chain(inputs.config("C5"))
+    ch.update(scale_a=1.0, scale_b=1.0)
+    # 16384 rows x 64 column tiles of (max, sum) partials = 8 MiB > 4 MiB
+    st, msg = kf.fused_op_noalloc_status(ch, M=16384, N=16384, K=64)
+    assert st == kf.KF_ERR_UNSUPPORTED and "static scratch holds 4194304" in msg, msg
+    bad = dict(ch, ops=[("row_softmax",), ("relu",)])
+    st, msg = kf.fused_op_noalloc_status(bad, M=64, N=64, K=64)
+    assert st == kf.KF_ERR_UNSUPPORTED and "last op" in msg, msg
+    # exactly at the limit: 8192 rows x 64 tiles = 4 MiB is accepted by the planner
+    st, msg = kf.fused_op_noalloc_status(ch, M=8192, N=16384, K=64)
+    if not _gpu_present():
+        assert st == kf.KF_ERR_NO_DEVICE, msg
+    else:
+        assert st in (kf.KF_ERR_INVALID_ARG, kf.KF_ERR_SHAPE), msg  # the empty tensors are refused
