@@ -66,6 +66,9 @@ struct SlotList {
   const Slot* end() const { return s + n; }
 };
 
+// Rows a one-workgroup-per-row launch (256 threads each) can cover.
+constexpr int64_t kMaxRowLaunch = int64_t(1) << 24;
+
 int64_t elem_size(int32_t dt) { return dt == KF_F32 ? 4 : dt == KF_BF16 ? 2 : 1; }
 
 bool is_elementwise_kind(int k) {
@@ -201,6 +204,12 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   if (n_pool > 1) return fail(KF_ERR_UNSUPPORTED, "at most one MAXPOOL2X2 op");
   if (d->row_kind == KF_OP_ROW_LOGSUMEXP && s->out_dtype != KF_F32)
     return fail(KF_ERR_UNSUPPORTED, "ROW_LOGSUMEXP output must be KF_F32");
+  // the row kernels (row softmax / logsumexp finish, the row-wise chains)
+  // launch one 256-thread workgroup per row, and a launch holds fewer than
+  // 2^32 work-items
+  if ((d->row_kind || s->contraction == KF_ROWWISE) && s->M >= kMaxRowLaunch)
+    return fail(KF_ERR_UNSUPPORTED, "row reductions support M < %lld rows (one workgroup per row)",
+                (long long)kMaxRowLaunch);
 
   const int32_t dt = s->in_dtype;
   d->inputs.clear();
@@ -980,6 +989,16 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   // the per-op kernels index [M, N] tensors as contiguous rows
   if (rowwise && inputs[0].stride[0] != s.N)
     return fail(KF_ERR_UNSUPPORTED, "the unfused ROWWISE chain needs A with row stride N");
+  if (rows && s.n_ops) {
+    for (int i = 0; i < s.n_ops; ++i)
+      if (s.ops[i].kind == KF_OP_GROUPNORM && s.M * s.ops[i].groups >= kMaxRowLaunch)
+        return fail(KF_ERR_UNSUPPORTED, "the unfused GroupNorm supports M * groups < %lld", (long long)kMaxRowLaunch);
+    for (size_t i = 0; i < d->inputs.size(); ++i)
+      if (strcmp(d->inputs[i].name, "residual") == 0 && inputs[i].stride[0] != s.N)
+        return fail(KF_ERR_UNSUPPORTED, "the unfused chain needs a residual with row stride N");
+    if (outputs[0].ndim == 2 && outputs[0].stride[0] != s.N)
+      return fail(KF_ERR_UNSUPPORTED, "the unfused chain needs an output with row stride N");
+  }
 
   // intermediates: bf16 (fp32 for an fp32 chain), full contraction size
   const bool ibf16 = rowwise ? s.in_dtype == KF_BF16 : d->variant != kVarGemmF32;
@@ -1032,6 +1051,13 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     a.raster_group = d->tuning.raster_group;
     a.xcd_remap = d->tuning.xcd_remap;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
+    if (d->variant != kVarGemmF32) {
+      const int64_t es = elem_size(s.in_dtype);
+      // as in the fused path: 32-bit buffer offsets over up to 256 rows / k past the tile
+      if (!fits_31(256 * a.lda * es) || !fits_31((nk ? 256 * a.ldb : (s.K + 256) * a.ldb) * es) ||
+          !fits_31(256 * a.ldo * 4))
+        return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
+    }
     e = d->variant == kVarGemmF32 ? kf::launch_gemm_f32(a, nk, hs)
                                   : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk);
   } else if (conv3d) {

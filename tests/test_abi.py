@@ -120,6 +120,22 @@ def test_row_op_must_be_last():
     assert st == kf.KF_ERR_UNSUPPORTED and "last" in kf.last_error()
 
 
+def test_row_reductions_reject_more_rows_than_one_launch_covers():
+    """Row softmax / logsumexp finishing kernels and the row-wise chains run
+    one 256-thread workgroup per row: 2^24 rows would exceed the 2^32
+    work-items of one launch, so the plan refuses them on the host."""
+    for name, ops in (("C2", None), ("C5", None), ("F4", None)):
+        cfg = inputs.config(name, M=1 << 24, K=64, **({"ops": ops} if ops else {}))
+        ch = inputs.chain(cfg)
+        ch.update(scale_a=1.0, scale_b=1.0)
+        st, _ = _create(kf.make_spec(ch, **kf.sizes_of(cfg)))
+        assert st == kf.KF_ERR_UNSUPPORTED and "M < 16777216" in kf.last_error(), (name, kf.last_error())
+    # a plain GEMM epilogue has no per-row launch
+    cfg = inputs.config("C2", M=1 << 24, K=64, out_dtype="bf16", ops=[("bias",), ("relu",)])
+    st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+    assert st != kf.KF_ERR_UNSUPPORTED, kf.last_error()
+
+
 def test_logsumexp_needs_f32_output():
     cfg = inputs.config("C2", out_dtype="bf16")
     st, _ = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))

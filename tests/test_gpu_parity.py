@@ -819,3 +819,25 @@ def test_diagnosis_of_reference_workloads(name, bound):
     print(f"{name}: {g['bound']} compute {g['compute_frac']:.3f} memory {g['memory_frac']:.3f}")
     assert g["bound"] == bound
     assert g["flops"] == inputs.flops(cfg)
+
+
+def test_unfused_rejects_padded_rows():
+    """The unfused chain's per-op kernels index [M, N] tensors densely: a
+    residual or output with a padded row stride is refused, not misread."""
+    torch = _torch()
+    cfg = inputs.config("C2", M=64, N=256, K=64, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("relu",)])
+    t = inputs.generate(cfg, seed=3)
+    op = kf.FusedOp.from_config(cfg)
+    ins = op.device_inputs(t)
+    wide = torch.empty((64, 264), dtype=torch.bfloat16, device="cuda")[:, :256]
+    with pytest.raises(kf.KFError) as e:
+        op.unfused(ins, wide)
+    assert e.value.status == kf.KF_ERR_UNSUPPORTED and "row stride" in str(e.value)
+    ins[2] = torch.empty((64, 264), dtype=torch.bfloat16, device="cuda")[:, :256].copy_(ins[2])
+    with pytest.raises(kf.KFError) as e:
+        op.unfused(ins, op.empty_output("cuda"))
+    assert e.value.status == kf.KF_ERR_UNSUPPORTED and "residual" in str(e.value)
+    out = op.empty_output("cuda")
+    op(ins, out)                          # the fused kernel takes any row stride
+    torch.cuda.synchronize()
+    check(cfg, t, out)
