@@ -14,9 +14,9 @@ gets a block of the same fields under "also".  Per workload:
   value        whole-step throughput in TFLOP/s (2*M*N*K / mean step time
                over the K back-to-back steps)
   steps_us     per-step HIP-event times: median, min, p90, mean -- warm
-               (back-to-back steps) and cold (a 512 MiB device write between
-               steps, outside the events, evicts the L2s and the 256 MB
-               Infinity Cache)
+               (back-to-back steps, a second loop of K steps) and cold (a
+               512 MiB device write between steps, outside the events,
+               evicts the L2s and the 256 MB Infinity Cache)
   roofline     the main contraction kernel alone, timed live with HIP events
                recorded on its stream around each launch (achieved = the
                algorithmic FLOPs per launch / the mean launch time; median,
@@ -194,15 +194,16 @@ def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
     }, err
 
 
-def _timed_steps(hip, torch, run, steps, flush=None, kernel_events=True):
-    """`steps` calls of run(ev_before, ev_after) on the current stream, each
-    between two step events; `flush` (a device tensor) is overwritten before
-    every step, outside the events.  run() records ev_before / ev_after
-    around its main kernel when kernel_events is set.  Returns (total ms of
-    the loop, per-step ms, per-kernel ms)."""
+def _timed_steps(hip, torch, run, steps, flush=None, kernel_events=True, step_events=True):
+    """`steps` calls of run(ev_before, ev_after) on the current stream,
+    bracketed by two events, each step between two step events if
+    step_events; `flush` (a device tensor) is overwritten before every step,
+    outside the events.  run() records ev_before / ev_after around its main
+    kernel when kernel_events is set.  Returns (total ms of the loop,
+    per-step ms, per-kernel ms)."""
     stream = torch.cuda.current_stream()
     kev = [(_event(hip), _event(hip)) for _ in range(steps)] if kernel_events else []
-    sev = [(_event(hip), _event(hip)) for _ in range(steps)]
+    sev = [(_event(hip), _event(hip)) for _ in range(steps)] if step_events else []
     start, end = _event(hip), _event(hip)
     torch.cuda.synchronize()
     s = ctypes.c_void_p(stream.cuda_stream)
@@ -210,9 +211,11 @@ def _timed_steps(hip, torch, run, steps, flush=None, kernel_events=True):
     for i in range(steps):
         if flush is not None:
             flush.fill_(i & 0xFF)
-        hip.hipEventRecord(ctypes.c_void_p(sev[i][0]), s)
+        if step_events:
+            hip.hipEventRecord(ctypes.c_void_p(sev[i][0]), s)
         run(*(kev[i] if kernel_events else (None, None)))
-        hip.hipEventRecord(ctypes.c_void_p(sev[i][1]), s)
+        if step_events:
+            hip.hipEventRecord(ctypes.c_void_p(sev[i][1]), s)
     hip.hipEventRecord(ctypes.c_void_p(end), s)
     torch.cuda.synchronize()
     total = _elapsed_ms(hip, start, end)
@@ -260,8 +263,13 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
 
     K = args.steps
     fused = lambda e0, e1: op.timed(ins, out, e0, e1)  # noqa: E731
-    total_ms, step_ms, kern_ms = _timed_steps(hip, torch, fused, K)
+    # the timed steps: the main kernel bracketed by its own events, nothing
+    # else recorded inside the loop (each event record costs the stream a few
+    # microseconds)
+    total_ms, _, kern_ms = _timed_steps(hip, torch, fused, K, step_events=False)
     ms_per_step = total_ms / K
+    # per-step statistics from a second warm loop with step events only
+    _, step_ms, _ = _timed_steps(hip, torch, lambda e0, e1: op(ins, out), K, kernel_events=False)
     cold = None
     if args.cold_steps > 0:
         flush = torch.empty(COLD_FLUSH_BYTES, dtype=torch.uint8, device="cuda:0")

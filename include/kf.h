@@ -79,8 +79,9 @@ typedef enum kf_contraction {
 typedef enum kf_dtype {
   KF_F32 = 0,
   KF_BF16 = 1,
-  KF_FP8_E4M3 = 2  /* OCP E4M3 (bias 7, max 448, no Inf); GEMM only, with
+  KF_FP8_E4M3 = 2, /* OCP E4M3 (bias 7, max 448, no Inf); GEMM only, with
                       per-tensor fp32 scales: A_real = dec(A) * scale_a. */
+  KF_I32 = 3       /* int32: the class targets of ROW_CROSS_ENTROPY only   */
 } kf_dtype;
 
 typedef enum kf_layout { KF_LAYOUT_KN = 0, KF_LAYOUT_NK = 1 } kf_layout;
@@ -113,11 +114,18 @@ typedef enum kf_op_kind {
   KF_OP_CHANNEL_SOFTMAX = 15,/* softmax over the output channels at every
                               position (torch.softmax(h, dim=1));
                               CONV3D_3X3X3 only, at most once               */
-  KF_OP_MAXPOOL3D_2 = 16   /* MaxPool3d(2): kernel 2, stride 2, no padding,
+  KF_OP_MAXPOOL3D_2 = 16,  /* MaxPool3d(2): kernel 2, stride 2, no padding,
                               floor mode; CONV3D_3X3X3 only, after every
                               other op.  The fused kernel takes zero or two
                               of them (two in a row = one max over aligned
                               4x4x4 blocks).                                */
+  KF_OP_ROW_CROSS_ENTROPY = 17 /* nn.CrossEntropyLoss(reduction='none') with
+                              class-index targets: loss_m = logsumexp_n h[m][n]
+                              - h[m][t_m] (the loss operators of the paper's
+                              reduction categories, Table 2); GEMM or ROWWISE;
+                              last op; input int32 targets [M] (KF_I32), each
+                              in [0, N) -- a target outside gives NaN; output
+                              fp32 [M]                                      */
 } kf_op_kind;
 
 typedef struct kf_op {
@@ -176,7 +184,8 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out);
    partials (Appendix B, hierarchical reductions).
    inputs (in this order): A, B (no B for KF_ROWWISE), then one slot per
    tensor the ops need, in op order -- BIAS: bias; GROUPNORM: gamma, beta;
-   RESIDUAL_ADD: residual.  All are device pointers owned by the caller.
+   RESIDUAL_ADD: residual; ROW_CROSS_ENTROPY: targets.  All are device
+   pointers owned by the caller.
    outputs: exactly one tensor (shape from kf_output_info, dtype
    spec.out_dtype), written, never reallocated.
    Returns KF_ERR_SHAPE / _UNSUPPORTED / _INVALID_ARG when a tensor does not

@@ -300,6 +300,18 @@ def op_row_logsumexp(h):
     return (m + np.log(np.exp(h - m).sum(axis=-1, keepdims=True)))[..., 0]
 
 
+def op_row_cross_entropy(h, targets):
+    """Cross-entropy of each row against its class index, as
+    nn.CrossEntropyLoss(reduction='none') defines it: the row's logsumexp
+    minus the row's entry at the target column.  A target outside [0, N)
+    gives NaN (the GPU path's documented answer for it)."""
+    t = np.asarray(targets, dtype=np.int64)
+    N = h.shape[-1]
+    ok = (t >= 0) & (t < N)
+    picked = np.take_along_axis(h, np.clip(t, 0, N - 1)[:, None], axis=-1)[:, 0]
+    return np.where(ok, op_row_logsumexp(h) - picked, np.nan)
+
+
 # --------------------------------------------------------------------------
 # Chains
 # --------------------------------------------------------------------------
@@ -351,6 +363,11 @@ def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel, store=None) -> np
             h = op_row_softmax(h)
         elif name == "row_logsumexp":
             h = op_row_logsumexp(h)
+        elif name == "row_cross_entropy":
+            t = np.asarray(tensors["targets"], dtype=np.int64)
+            if sel is not None:
+                t = t[np.asarray(sel, dtype=np.int64)]
+            h = op_row_cross_entropy(h, t)
         else:
             raise ValueError(f"unknown op {name!r}")
     return h
@@ -440,7 +457,8 @@ def run_chain(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
               "ops": [(name, *params), ...]}
     tensors: raw storage: "a", "b" (in_dtype; no "b" for "rowwise", whose h is
              A itself), "bias", "gamma", "beta" (f32),
-             "residual" (its own dtype given by chain["residual_dtype"]).
+             "residual" (its own dtype given by chain["residual_dtype"]),
+             "targets" (int class indices, one per row).
     rows / images: evaluate only these output rows (GEMM) or batch entries
              (conv); every op in scope is local to a row (GEMM) or to one
              image (conv), so the selected slice is exact.

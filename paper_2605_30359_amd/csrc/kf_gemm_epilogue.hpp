@@ -42,7 +42,7 @@ using AccT = f32x16[RB][4];
 // The row softmax / logsumexp op of a compile-time chain (0: none, or chain 0).
 constexpr int chain_row_op(int ch) {
   for (int o = 0; o < kChainLen[ch]; ++o)
-    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kChainOps[ch][o];
+    if (is_row_op(kChainOps[ch][o])) return kChainOps[ch][o];
   return 0;
 }
 
@@ -50,7 +50,7 @@ constexpr int chain_row_op(int ch) {
 constexpr int chain_epi(int ch) {
   for (int o = 0; o < kChainLen[ch]; ++o) {
     if (kChainOps[ch][o] == KF_OP_GROUPNORM) return kEpiGroupNorm;
-    if (kChainOps[ch][o] == KF_OP_ROW_SOFTMAX || kChainOps[ch][o] == KF_OP_ROW_LOGSUMEXP) return kEpiRow;
+    if (is_row_op(kChainOps[ch][o])) return kEpiRow;
   }
   return kEpiPlain;
 }
@@ -458,6 +458,8 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 
   // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
   // this 256-column tile goes to the partials buffer.
+  const int row_op = chain_row_op(CH) ? chain_row_op(CH) : op_kind(c.ops, r);
+  const bool ce = row_op == KF_OP_ROW_CROSS_ENTROPY;
   rd.template issue<0, kRes>();
   res_wait(c);
   float mx[RB];
@@ -468,6 +470,25 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
 #pragma unroll
     for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
     apply_phase<CH>(p, c, bi, 0, r, v);
+    if (ce) {
+      // cross-entropy: the one lane of the grid that holds h[m][t_m] leaves it
+      // for the finishing kernel.  This lane's columns are col_local(c, g) +
+      // q = wn * 128 + 32 (g / 4) + 8 (g % 4) + 4 (lane / 32) + q.
+      const int64_t m = c.m0 + row_local(c, bi);
+      if (m < p.M) {
+        const int64_t t = p.targets[m];
+        const int64_t d = t - c.n0 - c.wn * 128 - (c.lane >> 5) * 4;
+        if (t < N && d >= 0 && d < 128 && (d & 4) == 0) {
+          const int sel = (int)(((d >> 5) * 4 + ((d >> 3) & 3)) * 4 + (d & 3));
+          float h = 0.0f;
+#pragma unroll
+          for (int g = 0; g < 16; ++g)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) h = sel == g * 4 + q ? v[g][q] : h;
+          p.tlogit[m] = h;
+        }
+      }
+    }
     // columns past N take no part in a row reduction (only the last column
     // tile can have any)
     if (c.n0 + BN > N) {
@@ -486,7 +507,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
   });
   row_combine<true>(c, mx, true);
   // softmax keeps e^(h - max) in the accumulators for the store below
-  const bool softmax = chain_row_op(CH) ? chain_row_op(CH) == KF_OP_ROW_SOFTMAX : op_kind(c.ops, r) == KF_OP_ROW_SOFTMAX;
+  const bool softmax = row_op == KF_OP_ROW_SOFTMAX;
   float se[RB];
   auto exp_sums = [&](auto KEEP_c) {
     static_for<0, RB>([&](auto bi_c) {
@@ -518,7 +539,7 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
     }
   }
-  if (!softmax) return;  // logsumexp: the finishing kernel writes
+  if (!softmax) return;  // logsumexp, cross-entropy: the finishing kernel writes
   // softmax: store e^(h - tile max); the row-finishing kernel rescales it
   static_for<0, RB>([&](auto bi_c) {
     constexpr int bi = decltype(bi_c)::value;

@@ -411,6 +411,7 @@ inline void launch_shape(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 
     case 5: launch_chain<FP8, B_NK, 5>(p, grid, block, stream); return;
     case 6: launch_chain<FP8, B_NK, 6>(p, grid, block, stream); return;
     case 8: launch_chain<FP8, B_NK, 8>(p, grid, block, stream); return;
+    case 14: launch_chain<FP8, B_NK, 14>(p, grid, block, stream); return;
     default: break;
   }
   switch (epi) {

@@ -69,7 +69,7 @@ struct SlotList {
 // Rows a one-workgroup-per-row launch (256 threads each) can cover.
 constexpr int64_t kMaxRowLaunch = int64_t(1) << 24;
 
-int64_t elem_size(int32_t dt) { return dt == KF_F32 ? 4 : dt == KF_BF16 ? 2 : 1; }
+int64_t elem_size(int32_t dt) { return dt == KF_F32 || dt == KF_I32 ? 4 : dt == KF_BF16 ? 2 : 1; }
 
 bool is_elementwise_kind(int k) {
   return k == KF_OP_RELU || k == KF_OP_GELU_TANH || k == KF_OP_GELU_ERF || k == KF_OP_SWISH ||
@@ -86,7 +86,7 @@ struct kf_desc {
   int epi_shape;
   int red_index;
   int gn_group;
-  int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / 0
+  int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / KF_OP_ROW_CROSS_ENTROPY / 0
   int chain = 0;  // compile-time epilogue chain matching the op list (0: interpreted)
   SlotList inputs;
   Slot output;
@@ -141,7 +141,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   bool has_bias = false, has_gn = false, has_res = false;
   for (int i = 0; i < s->n_ops; ++i) {
     const kf_op& op = s->ops[i];
-    if (op.kind < KF_OP_BIAS || op.kind > KF_OP_MAXPOOL3D_2)
+    if (op.kind < KF_OP_BIAS || op.kind > KF_OP_ROW_CROSS_ENTROPY)
       return fail(KF_ERR_INVALID_ARG, "op %d: unknown kind %d", i, op.kind);
     d->prog.op[i] = kf::EpiOp{op.kind, op.groups, op.p0, op.p1};
     switch (op.kind) {
@@ -174,6 +174,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
         break;
       case KF_OP_ROW_SOFTMAX:
       case KF_OP_ROW_LOGSUMEXP:
+      case KF_OP_ROW_CROSS_ENTROPY:
         if (i != s->n_ops - 1) return fail(KF_ERR_UNSUPPORTED, "op %d: a row softmax/logsumexp must be the last op", i);
         if (s->contraction != KF_GEMM && s->contraction != KF_ROWWISE)
           return fail(KF_ERR_UNSUPPORTED, "op %d: row ops need a GEMM or ROWWISE", i);
@@ -202,8 +203,9 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
   if (n_csm > 1) return fail(KF_ERR_UNSUPPORTED, "at most one CHANNEL_SOFTMAX op");
   if (n_red > 1) return fail(KF_ERR_UNSUPPORTED, "at most one reduction op (GROUPNORM / ROW_*) per chain");
   if (n_pool > 1) return fail(KF_ERR_UNSUPPORTED, "at most one MAXPOOL2X2 op");
-  if (d->row_kind == KF_OP_ROW_LOGSUMEXP && s->out_dtype != KF_F32)
-    return fail(KF_ERR_UNSUPPORTED, "ROW_LOGSUMEXP output must be KF_F32");
+  const bool row_scalar = d->row_kind == KF_OP_ROW_LOGSUMEXP || d->row_kind == KF_OP_ROW_CROSS_ENTROPY;
+  if (row_scalar && s->out_dtype != KF_F32)
+    return fail(KF_ERR_UNSUPPORTED, "ROW_LOGSUMEXP / ROW_CROSS_ENTROPY output must be KF_F32");
   // the row kernels (row softmax / logsumexp finish, the row-wise chains)
   // launch one 256-thread workgroup per row, and a launch holds fewer than
   // 2^32 work-items
@@ -257,7 +259,9 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       }
       if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0, 0}, "residual", false});
     }
-    if (d->row_kind == KF_OP_ROW_LOGSUMEXP)
+    if (d->row_kind == KF_OP_ROW_CROSS_ENTROPY)
+      d->inputs.push_back(Slot{KF_I32, 1, {s->M, 0, 0, 0, 0}, "targets", false});
+    if (row_scalar)
       d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0, 0}, "out", false};
     else
       d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0, 0}, "out", false};
@@ -291,7 +295,9 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       }
       if (k == KF_OP_RESIDUAL_ADD) d->inputs.push_back(Slot{s->residual_dtype, 2, {s->M, s->N, 0, 0, 0}, "residual", false});
     }
-    if (d->row_kind == KF_OP_ROW_LOGSUMEXP)
+    if (d->row_kind == KF_OP_ROW_CROSS_ENTROPY)
+      d->inputs.push_back(Slot{KF_I32, 1, {s->M, 0, 0, 0, 0}, "targets", false});
+    if (row_scalar)
       d->output = Slot{KF_F32, 1, {s->M, 0, 0, 0, 0}, "out", false};
     else
       d->output = Slot{s->out_dtype, 2, {s->M, s->N, 0, 0, 0}, "out", false};
@@ -553,7 +559,11 @@ size_t plan_workspace_bytes(const kf_desc* d) {
   const kf_op_spec& s = d->spec;
   if (d->variant == kVarConvBf16) return (size_t)9 * s.cout * s.cin * 2;
   if (d->variant == kVarConv3d) return kf::conv3d_packed_bytes();
-  if (d->row_kind && d->variant != kVarRowwise) return (size_t)std::max<int64_t>(s.M, 1) * d->tiles_n * sizeof(float) * 2;
+  if (d->row_kind && d->variant != kVarRowwise) {
+    // per-(row, tile) (max, sum) pairs; cross-entropy adds h[m][t_m] per row
+    const size_t rows = (size_t)std::max<int64_t>(s.M, 1);
+    return rows * d->tiles_n * sizeof(float) * 2 + (d->row_kind == KF_OP_ROW_CROSS_ENTROPY ? rows * sizeof(float) : 0);
+  }
   return 0;
 }
 
@@ -860,6 +870,7 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
         r.residual_bf16 = inputs[slot].dtype == KF_BF16;
         ++slot;
       }
+      if (k == KF_OP_ROW_CROSS_ENTROPY) r.targets = static_cast<const int32_t*>(inputs[slot++].data);
     }
     r.out = outputs[0].data;
     r.ldo = outputs[0].ndim == 2 ? outputs[0].stride[0] : 1;
@@ -900,11 +911,14 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
         a.residual_bf16 = inputs[slot].dtype == KF_BF16;
         ++slot;
       }
+      if (k == KF_OP_ROW_CROSS_ENTROPY) a.targets = static_cast<const int32_t*>(inputs[slot++].data);
     }
     a.out = outputs[0].data;
     a.ldo = outputs[0].ndim == 2 ? outputs[0].stride[0] : 1;
     a.out_bf16 = outputs[0].dtype == KF_BF16;
     a.partials = ws;
+    if (a.targets)  // the target logits follow the (max, sum) partials
+      a.tlogit = reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + (size_t)std::max<int64_t>(s.M, 1) * d->tiles_n * 8);
     a.raster_group = d->tuning.raster_group;
     a.xcd_remap = d->tuning.xcd_remap;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
@@ -925,7 +939,7 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
       if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
       if (e == hipSuccess && d->row_kind)
         e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, ws, d->tiles_n, s.M, s.N, a.out,
-                                  a.ldo, a.out_bf16 != 0, hs);
+                                  a.ldo, a.out_bf16 != 0, hs, a.targets, a.tlogit);
     }
     if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
@@ -1122,7 +1136,11 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
       }
       case KF_OP_ROW_SOFTMAX:
       case KF_OP_ROW_LOGSUMEXP:
-        e = kf::launch_unfused_rowop(cur, cur_bf16, dst, dst_bf16, s.M, s.N, op.kind == KF_OP_ROW_SOFTMAX, hs);
+        e = kf::launch_unfused_rowop(cur, cur_bf16, dst, dst_bf16, s.M, s.N, op.kind, nullptr, hs);
+        break;
+      case KF_OP_ROW_CROSS_ENTROPY:
+        e = kf::launch_unfused_rowop(cur, cur_bf16, dst, dst_bf16, s.M, s.N, op.kind,
+                                     static_cast<const int32_t*>(inputs[slot++].data), hs);
         break;
       case KF_OP_CHANNEL_SOFTMAX:
         e = kf::launch_unfused_channel_softmax(cur, cur_bf16, dst, dst_bf16, s.batch, (int)s.cout, dd * hh * ww, hs);

@@ -19,6 +19,10 @@ struct EpiProgram {
   EpiOp op[KF_MAX_OPS];
 };
 
+// A row op: one whose reduction runs over a whole row (the last op).
+constexpr bool is_row_op(int kind) {
+  return kind == KF_OP_ROW_SOFTMAX || kind == KF_OP_ROW_LOGSUMEXP || kind == KF_OP_ROW_CROSS_ENTROPY;
+}
 // Compile-time shape of an epilogue: element-wise ops only, or element-wise
 // ops around one GroupNorm, or element-wise ops followed by a row softmax /
 // logsumexp.
@@ -29,8 +33,8 @@ enum EpiShape { kEpiPlain = 0, kEpiGroupNorm = 1, kEpiRow = 2 };
 // is interpreted at run time.  The paper turns each operator into its own
 // specialised kernel; these are the chains of the benchmarked operators and
 // the plain building blocks, and every other chain runs interpreted.
-constexpr int kNumChains = 13;
-constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1, 4, 1, 1};
+constexpr int kNumChains = 15;
+constexpr int kChainLen[kNumChains] = {0, 0, 1, 2, 4, 3, 3, 3, 5, 1, 4, 1, 1, 1, 2};
 constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {},                                                                         // 0: interpreted
     {},                                                                         // 1: contraction only
@@ -45,14 +49,17 @@ constexpr int kChainOps[kNumChains][KF_MAX_OPS] = {
     {KF_OP_BIAS, KF_OP_CHANNEL_SOFTMAX, KF_OP_MAXPOOL3D_2, KF_OP_MAXPOOL3D_2},  // 10: conv3d, softmax, pools
     {KF_OP_GROUPNORM},                                                          // 11: GroupNorm rows
     {KF_OP_ROW_LOGSUMEXP},                                                      // 12: logsumexp rows
+    {KF_OP_ROW_CROSS_ENTROPY},                                                  // 13: cross-entropy rows
+    {KF_OP_BIAS, KF_OP_ROW_CROSS_ENTROPY},                                      // 14: GEMM + bias, cross-entropy
 };
 // Which contraction a chain belongs to: 0 any, 1 GEMM / ROWWISE, 2 CONV2D_3X3,
 // 3 CONV3D_3X3X3.
-constexpr int kChainFamily[kNumChains] = {0, 0, 1, 1, 1, 1, 1, 2, 1, 1, 3, 1, 1};
+constexpr int kChainFamily[kNumChains] = {0, 0, 1, 1, 1, 1, 1, 2, 1, 1, 3, 1, 1, 1, 1};
 // Chains of one row reduction (the unfused comparator's row-op kernels).
 constexpr int kChainRowSoftmax = 9;
 constexpr int kChainGroupNorm = 11;
 constexpr int kChainRowLogsumexp = 12;
+constexpr int kChainRowCrossEntropy = 13;
 
 // Arguments of the GEMM-shaped kernels (passed by value as kernel arguments).
 struct GemmArgs {
@@ -70,7 +77,9 @@ struct GemmArgs {
   int32_t out_bf16;
   void* out;              // [M, ldo] (or [M] for a row logsumexp)
   int64_t ldo;
-  void* partials;         // float2 [M][tiles_n] for row softmax / logsumexp
+  void* partials;         // float2 [M][tiles_n] for row softmax / logsumexp / cross-entropy
+  const int32_t* targets; // [M] class targets (ROW_CROSS_ENTROPY) or null
+  float* tlogit;          // [M] h[m][target_m], written by the tile holding it
   int32_t tiles_m, tiles_n;
   int32_t gn_group;       // GroupNorm group width in columns (0 = none)
   int32_t red_index;      // position of the reduction op in prog (n if none)
@@ -92,9 +101,10 @@ struct RowArgs {
   int64_t ldr;
   int32_t residual_bf16;
   int32_t out_bf16;
-  void* out;              // [M, ldo] (or [M] for a row logsumexp)
+  void* out;              // [M, ldo] (or [M] for a row logsumexp / cross-entropy)
   int64_t ldo;
   int32_t gn_group;       // GroupNorm group width in columns (0 = none)
+  const int32_t* targets; // [M] class targets (ROW_CROSS_ENTROPY) or null
 };
 
 // Arguments of the implicit-GEMM 3x3 convolution kernels.

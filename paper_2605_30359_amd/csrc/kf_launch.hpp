@@ -43,9 +43,12 @@ int rowwise_max_cols();
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);
 
-// Row softmax rescale / logsumexp combine from per-tile partials.
+// Row softmax rescale / logsumexp combine from per-tile partials; with
+// `targets`, the cross-entropy logsumexp - tlogit[m] (NaN where a target is
+// outside [0, N)).
 hipError_t launch_row_finish(bool softmax, const void* partials, int tiles, int64_t M, int64_t N, void* out,
-                             int64_t ldo, bool out_bf16, hipStream_t stream);
+                             int64_t ldo, bool out_bf16, hipStream_t stream, const int32_t* targets = nullptr,
+                             const float* tlogit = nullptr);
 int row_finish_max_tiles();
 
 }  // namespace kf
@@ -87,8 +90,9 @@ hipError_t launch_unfused_residual(const void* in, bool in_bf16, const void* res
                                    bool out_bf16, int64_t n, hipStream_t stream);
 hipError_t launch_unfused_groupnorm(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t rows, int64_t N,
                                     int groups, float eps, const float* gamma, const float* beta, hipStream_t stream);
+// kind: KF_OP_ROW_SOFTMAX, _LOGSUMEXP or _CROSS_ENTROPY (with targets)
 hipError_t launch_unfused_rowop(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t rows, int64_t N,
-                                bool softmax, hipStream_t stream);
+                                int kind, const int32_t* targets, hipStream_t stream);
 hipError_t launch_unfused_maxpool(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t planes, int H,
                                   int W, hipStream_t stream);
 hipError_t launch_unfused_channel_softmax(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t batch,

@@ -6,6 +6,7 @@
 //     mu = max_t mu_t,     S = sum_t s_t e^(mu_t - mu),
 //     logsumexp = mu + ln S,
 //     softmax_j = e^(h_j - mu_t) * e^(mu_t - mu) / S   for column j in tile t,
+//     cross-entropy = logsumexp - h_target  (h_target left by the tile holding it),
 // which is the hierarchical, online form of softmax the paper's Appendix A
 // (algorithmic optimisation: online softmax) and Appendix B (hierarchical
 // reductions, normalise before exponentiating) recommend.
@@ -21,7 +22,9 @@ namespace kf {
 // the max and the sum are combined across the group by xor exchanges (every
 // lane of the wave takes part in them, rows past M with nothing loaded).
 __global__ __launch_bounds__(256) void kf_row_logsumexp_finish(const float2* __restrict__ part, int tiles,
-                                                                int lanes_log2, int64_t M, float* __restrict__ out) {
+                                                                int lanes_log2, int64_t M, float* __restrict__ out,
+                                                                const int32_t* __restrict__ targets,
+                                                                const float* __restrict__ tlogit, int64_t N) {
   const int L = 1 << lanes_log2;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t m = gid >> lanes_log2;
@@ -36,7 +39,14 @@ __global__ __launch_bounds__(256) void kf_row_logsumexp_finish(const float2* __r
   if (live)
     for (int t = i; t < tiles; t += L) s += pr[t].y * expf(pr[t].x - mu);
   for (int d = 1; d < L; d <<= 1) s += __shfl_xor(s, d, 64);
-  if (live && i == 0) out[m] = mu + logf(s);
+  if (live && i == 0) {
+    float r = mu + logf(s);
+    if (targets) {
+      const int32_t t = targets[m];
+      r = (t >= 0 && t < N) ? r - tlogit[m] : __builtin_nanf("");
+    }
+    out[m] = r;
+  }
 }
 
 constexpr int kMaxFinishTiles = 1024;
@@ -115,7 +125,8 @@ __global__ __launch_bounds__(256) void kf_row_softmax_rescale(const float2* __re
 }
 
 hipError_t launch_row_finish(bool softmax, const void* partials, int tiles, int64_t M, int64_t N, void* out,
-                             int64_t ldo, bool out_bf16, hipStream_t stream) {
+                             int64_t ldo, bool out_bf16, hipStream_t stream, const int32_t* targets,
+                             const float* tlogit) {
   if (M <= 0) return hipSuccess;
   if (softmax) {
     hipLaunchKernelGGL(kf_row_softmax_rescale, dim3((unsigned)M), dim3(256), 0, stream,
@@ -125,7 +136,8 @@ hipError_t launch_row_finish(bool softmax, const void* partials, int tiles, int6
     while ((1 << lanes_log2) < tiles && lanes_log2 < 6) ++lanes_log2;
     const int64_t threads = M << lanes_log2;
     hipLaunchKernelGGL(kf_row_logsumexp_finish, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<const float2*>(partials), tiles, lanes_log2, M, reinterpret_cast<float*>(out));
+                       reinterpret_cast<const float2*>(partials), tiles, lanes_log2, M, reinterpret_cast<float*>(out),
+                       targets, tlogit, N);
   }
   return hipGetLastError();
 }

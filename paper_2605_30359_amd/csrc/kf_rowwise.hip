@@ -198,8 +198,21 @@ __global__ __launch_bounds__(RT) void kf_rowwise(RowArgs p) {
           v[j][4 + e] = fmaf((v[j][4 + e] - mean[j]) * rs[j], g1[e], b1[e]);
         }
       }
-    } else if (kind == KF_OP_ROW_SOFTMAX || kind == KF_OP_ROW_LOGSUMEXP) {
+    } else if (is_row_op(kind)) {
       // the last op: max, then the sum of e^(h - max)
+      // cross-entropy: the thread holding column t (chunk t / 8, slot
+      // chunk / 256) keeps h[t] before the exponentials replace it
+      int32_t tgt = -1;
+      float ht = 0.0f;
+      if (kind == KF_OP_ROW_CROSS_ENTROPY) {
+        tgt = p.targets[m];
+#pragma unroll
+        for (int j = 0; j < S; ++j) {
+          const int c = j * RT + t;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ht = (tgt >= 0 && tgt < p.N && tgt == c * 8 + e) ? v[j][e] : ht;
+        }
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < S; ++j) {
@@ -224,6 +237,12 @@ __global__ __launch_bounds__(RT) void kf_rowwise(RowArgs p) {
       s = row_reduce<false>(s, red);
       if (kind == KF_OP_ROW_LOGSUMEXP) {
         if (t == 0) reinterpret_cast<float*>(p.out)[m] = mx + logf(s);
+        return true;
+      }
+      if (kind == KF_OP_ROW_CROSS_ENTROPY) {
+        const bool valid = tgt >= 0 && tgt < p.N;
+        if (valid ? ((tgt >> 3) % RT == t) : t == 0)
+          reinterpret_cast<float*>(p.out)[m] = valid ? (mx + logf(s)) - ht : __builtin_nanf("");
         return true;
       }
       const float inv = 1.0f / s;
@@ -410,7 +429,7 @@ bool panel_applies(const RowArgs& a) {
   if (L & (L - 1)) return false;
   for (int i = 0; i < a.prog.n; ++i) {
     const int k = a.prog.op[i].kind;
-    if (k == KF_OP_ROW_SOFTMAX || k == KF_OP_ROW_LOGSUMEXP) return false;
+    if (is_row_op(k)) return false;
   }
   return true;
 }
@@ -466,6 +485,7 @@ hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream) {
     case kChainRowSoftmax: return launch_rowwise_chain<kChainRowSoftmax>(args, stream);
     case kChainGroupNorm: return launch_rowwise_chain<kChainGroupNorm>(args, stream);
     case kChainRowLogsumexp: return launch_rowwise_chain<kChainRowLogsumexp>(args, stream);
+    case kChainRowCrossEntropy: return launch_rowwise_chain<kChainRowCrossEntropy>(args, stream);
     default: return launch_rowwise_chain<0>(args, stream);
   }
 }

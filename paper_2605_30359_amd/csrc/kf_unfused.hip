@@ -119,9 +119,10 @@ __global__ __launch_bounds__(256) void kf_unfused_groupnorm(const void* in, int 
   }
 }
 
-// Row softmax / logsumexp over N columns: one workgroup per row.
+// Row softmax / logsumexp / cross-entropy over N columns: one workgroup per row.
 __global__ __launch_bounds__(256) void kf_unfused_rowop(const void* in, int in_bf16, void* out, int out_bf16,
-                                                        int64_t N, int softmax) {
+                                                        int64_t N, int kind, const int32_t* targets) {
+  const bool softmax = kind == KF_OP_ROW_SOFTMAX;
   __shared__ float red[4];
   const int64_t row = blockIdx.x;
   const int64_t base = row * N;
@@ -132,7 +133,14 @@ __global__ __launch_bounds__(256) void kf_unfused_rowop(const void* in, int in_b
   for (int64_t j = threadIdx.x; j < N; j += 256) s += fexp(load_elem(in, base + j, in_bf16) - m);
   s = block_reduce<false>(s, red);
   if (!softmax) {
-    if (threadIdx.x == 0) reinterpret_cast<float*>(out)[row] = m + logf(s);
+    if (threadIdx.x == 0) {
+      float r = m + logf(s);
+      if (kind == KF_OP_ROW_CROSS_ENTROPY) {
+        const int32_t t = targets[row];
+        r = (t >= 0 && t < N) ? r - load_elem(in, base + t, in_bf16) : __builtin_nanf("");
+      }
+      reinterpret_cast<float*>(out)[row] = r;
+    }
     return;
   }
   const float inv = 1.0f / s;
@@ -494,8 +502,9 @@ hipError_t launch_unfused_groupnorm(const void* in, bool in_bf16, void* out, boo
 }
 
 hipError_t launch_unfused_rowop(const void* in, bool in_bf16, void* out, bool out_bf16, int64_t rows, int64_t N,
-                                bool softmax, hipStream_t stream) {
+                                int kind, const int32_t* targets, hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
+  const bool softmax = kind == KF_OP_ROW_SOFTMAX;
   if (N % 8 == 0 && N <= rowwise_max_cols() && aligned16(in) && (!softmax || aligned16(out))) {
     RowArgs r{};
     r.a = in;
@@ -504,14 +513,19 @@ hipError_t launch_unfused_rowop(const void* in, bool in_bf16, void* out, bool ou
     r.lda = N;
     r.in_bf16 = in_bf16;
     r.prog.n = 1;
-    r.prog.op[0] = EpiOp{softmax ? KF_OP_ROW_SOFTMAX : KF_OP_ROW_LOGSUMEXP, 0, 0.0f, 0.0f};
+    r.prog.op[0] = EpiOp{kind, 0, 0.0f, 0.0f};
     r.out = out;
     r.ldo = softmax ? N : 1;
     r.out_bf16 = softmax && out_bf16;
-    return launch_rowwise(r, softmax ? kChainRowSoftmax : kChainRowLogsumexp, stream);
+    r.targets = targets;
+    return launch_rowwise(r,
+                          softmax                           ? kChainRowSoftmax
+                          : kind == KF_OP_ROW_LOGSUMEXP     ? kChainRowLogsumexp
+                                                            : kChainRowCrossEntropy,
+                          stream);
   }
   hipLaunchKernelGGL(kf_unfused_rowop, dim3((unsigned)rows), dim3(256), 0, stream, in, in_bf16 ? 1 : 0, out,
-                     out_bf16 ? 1 : 0, N, softmax ? 1 : 0);
+                     out_bf16 ? 1 : 0, N, kind, targets);
   return hipGetLastError();
 }
 

@@ -104,6 +104,25 @@ CONFIGS = {
         ops=[("row_softmax",)],
         dist=dict(a=("normal", 1.0)),
     ),
+    # the loss operators of the reduction categories (Table 2): per-row
+    # cross-entropy against class-index targets, over stored bf16 logits
+    # [8192, 16384], and fused behind a GEMM + bias that produces the logits
+    # (x [4096, 4096] times W [4096, 16384]: a classifier head) so that the
+    # logits never reach memory
+    "F5": dict(
+        workload="rows_cross_entropy_bf16",
+        contraction="rowwise", in_dtype="bf16", out_dtype="f32",
+        M=8192, N=16384,
+        ops=[("row_cross_entropy",)],
+        dist=dict(a=("normal", 1.0), targets=("classes",)),
+    ),
+    "F6": dict(
+        workload="gemm_bias_cross_entropy_bf16",
+        contraction="gemm", in_dtype="bf16", out_dtype="f32", b_layout="kn",
+        M=4096, N=16384, K=4096,
+        ops=[("bias",), ("row_cross_entropy",)],
+        dist=dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1), targets=("classes",)),
+    ),
 }
 
 BASE_SEED = 260530359
@@ -218,6 +237,8 @@ def _draw(rng, spec, shape, k_fan_in):
         return rng.standard_normal(shape, dtype=np.float32) * np.float32(1.0 / np.sqrt(max(k_fan_in, 1)))  # K = 0: an empty draw
     if kind == "uniform":
         return rng.uniform(spec[1], spec[2], size=shape).astype(np.float32)
+    if kind == "classes":  # class indices, uniform over the N columns
+        return rng.integers(0, shape[1], size=shape[0]).astype(np.int32)
     raise ValueError(kind)
 
 
@@ -231,7 +252,9 @@ def rowwise_bytes(cfg: dict) -> int:
     b += 4 * N * (("bias" in names) + 2 * ("groupnorm" in names))
     if "residual_add" in names:
         b += M * N * es[cfg.get("residual_dtype", "bf16")]
-    b += 4 * M if names and names[-1] == "row_logsumexp" else M * N * es[cfg["out_dtype"]]
+    if "row_cross_entropy" in names:
+        b += 4 * M  # int32 targets
+    b += 4 * M if names and names[-1] in ("row_logsumexp", "row_cross_entropy") else M * N * es[cfg["out_dtype"]]
     return b
 
 
@@ -275,6 +298,8 @@ def generate(cfg: dict, seed: int | None = None) -> dict:
         out["beta"] = _draw(rng, dist["beta"], shp["beta"], shp["fan_in"])
     if "residual_add" in names:
         out["residual"] = f32_to_bf16_bits(_draw(rng, dist["residual"], shp["residual"], shp["fan_in"]))
+    if "row_cross_entropy" in names:
+        out["targets"] = _draw(rng, dist["targets"], (shp["residual"][0], shp["residual"][1]), shp["fan_in"])
     dt = cfg["in_dtype"]
     if raw_b is None:  # a row-wise chain: A only
         if dt not in ("f32", "bf16"):

@@ -22,7 +22,7 @@ KF_OK, KF_ERR_INVALID_ARG, KF_ERR_SHAPE, KF_ERR_UNSUPPORTED, KF_ERR_NO_DEVICE, K
 KF_GEMM, KF_CONV2D_3X3, KF_ROWWISE, KF_CONV3D_3X3X3 = 0, 1, 2, 3
 CONTRACTIONS = {"gemm": KF_GEMM, "conv2d_3x3": KF_CONV2D_3X3, "rowwise": KF_ROWWISE,
                 "conv3d_3x3x3": KF_CONV3D_3X3X3}
-KF_F32, KF_BF16, KF_FP8_E4M3 = 0, 1, 2
+KF_F32, KF_BF16, KF_FP8_E4M3, KF_I32 = 0, 1, 2, 3
 KF_LAYOUT_KN, KF_LAYOUT_NK = 0, 1
 KF_MAX_OPS = 8
 KF_MAX_DIMS = 5
@@ -31,9 +31,9 @@ OP_KINDS = {
     "bias": 1, "relu": 2, "gelu_tanh": 3, "gelu_erf": 4, "swish": 5, "sigmoid": 6,
     "tanh": 7, "hardtanh": 8, "scale": 9, "groupnorm": 10, "residual_add": 11,
     "maxpool2x2": 12, "row_softmax": 13, "row_logsumexp": 14, "channel_softmax": 15,
-    "maxpool3d2": 16,
+    "maxpool3d2": 16, "row_cross_entropy": 17,
 }
-DTYPES = {"f32": KF_F32, "bf16": KF_BF16, "e4m3": KF_FP8_E4M3}
+DTYPES = {"f32": KF_F32, "bf16": KF_BF16, "e4m3": KF_FP8_E4M3, "i32": KF_I32}
 DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
@@ -217,6 +217,8 @@ def input_names(chain: dict) -> list:
             names += ["gamma", "beta"]
         elif op[0] == "residual_add":
             names.append("residual")
+        elif op[0] == "row_cross_entropy":
+            names.append("targets")
     return names
 
 
@@ -239,7 +241,7 @@ def _torch():
 
 def torch_dtype(code: int):
     torch = _torch()
-    return {KF_F32: torch.float32, KF_BF16: torch.bfloat16, KF_FP8_E4M3: torch.float8_e4m3fn}[code]
+    return {KF_F32: torch.float32, KF_BF16: torch.bfloat16, KF_FP8_E4M3: torch.float8_e4m3fn, KF_I32: torch.int32}[code]
 
 
 def device_tensor(arr: np.ndarray, dtype: str, device="cuda", channels_last=False):
@@ -258,12 +260,14 @@ def device_tensor(arr: np.ndarray, dtype: str, device="cuda", channels_last=Fals
         return torch.from_numpy(arr.view(np.int16)).to(device).view(torch.bfloat16)
     if dtype == "e4m3":
         return torch.from_numpy(arr.view(np.uint8)).to(device).view(torch.float8_e4m3fn)
+    if dtype == "i32":
+        return torch.from_numpy(arr.astype(np.int32, copy=False)).to(device)
     raise ValueError(dtype)
 
 
 def to_kf_tensor(t) -> KfTensor:
     torch = _torch()
-    codes = {torch.float32: KF_F32, torch.bfloat16: KF_BF16, torch.float8_e4m3fn: KF_FP8_E4M3}
+    codes = {torch.float32: KF_F32, torch.bfloat16: KF_BF16, torch.float8_e4m3fn: KF_FP8_E4M3, torch.int32: KF_I32}
     if t.dtype not in codes:
         raise TypeError(f"unsupported tensor dtype {t.dtype}")
     if t.dim() < 1 or t.dim() > KF_MAX_DIMS:
@@ -405,6 +409,8 @@ class FusedOp:
                 dt = self.chain["in_dtype"]
             elif name == "residual":
                 dt = self.chain.get("residual_dtype", "bf16")
+            elif name == "targets":
+                dt = "i32"
             else:
                 dt = "f32"
             cl = name == "a" and self.chain["contraction"] == "conv3d_3x3x3"

@@ -598,6 +598,8 @@ def test_f2_rejects_channels_first_input():
     ("F3", dict(M=37, N=1024, ops=[("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)])),
     ("F4", dict(M=9, N=2048)),
     ("F2", dict(batch=2, D=7, H=11, W=20)),
+    ("F5", dict(M=37, N=2056)),
+    ("F6", dict(M=300, N=1040, K=136)),
 ])
 def test_unfused_chain_parity(name, kw):
     """The one-kernel-per-op comparator computes the same chain with every
@@ -692,6 +694,8 @@ def test_epilogue_operand_paths(name, kw, res_f32):
     ("F3", dict(M=37, N=2048)),                                            # rows: GroupNorm, swish, residual
     ("F4", dict(M=37, N=4104)),                                            # rows: softmax
     ("F2", dict(batch=2, D=7, H=11, W=20)),                                # conv3d, bias, softmax, pools
+    ("F5", dict(M=37, N=4104)),                                            # rows: cross-entropy
+    ("F6", dict(M=300, N=1040, K=136)),                                    # GEMM, bias, cross-entropy
 ])
 def test_specialised_chain_matches_interpreted(name, kw):
     """The benchmarked op lists run an epilogue generated for that exact
@@ -825,7 +829,8 @@ def test_unfused_rejects_padded_rows():
     """The unfused chain's per-op kernels index [M, N] tensors densely: a
     residual or output with a padded row stride is refused, not misread."""
     torch = _torch()
-    cfg = inputs.config("C2", M=64, N=256, K=64, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("relu",)])
+    cfg = inputs.config("C2", M=64, N=256, K=64, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("relu",)],
+                        dist=_ALL_DIST)
     t = inputs.generate(cfg, seed=3)
     op = kf.FusedOp.from_config(cfg)
     ins = op.device_inputs(t)
@@ -833,11 +838,71 @@ def test_unfused_rejects_padded_rows():
     with pytest.raises(kf.KFError) as e:
         op.unfused(ins, wide)
     assert e.value.status == kf.KF_ERR_UNSUPPORTED and "row stride" in str(e.value)
-    ins[2] = torch.empty((64, 264), dtype=torch.bfloat16, device="cuda")[:, :256].copy_(ins[2])
+    ins[3] = torch.empty((64, 264), dtype=torch.bfloat16, device="cuda")[:, :256].copy_(ins[3])
     with pytest.raises(kf.KFError) as e:
         op.unfused(ins, op.empty_output("cuda"))
     assert e.value.status == kf.KF_ERR_UNSUPPORTED and "residual" in str(e.value)
     out = op.empty_output("cuda")
     op(ins, out)                          # the fused kernel takes any row stride
     torch.cuda.synchronize()
+    check(cfg, t, out)
+
+
+# ------------------------------------------------------- cross-entropy rows
+
+@pytest.mark.parametrize("M,N", [(37, 1032), (64, 4104), (5, 16384), (1, 8)])
+def test_f5_rows_cross_entropy(M, N):
+    _torch()
+    cfg = inputs.config("F5", M=M, N=N)
+    t = inputs.generate(cfg, seed=M + N)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"F5 {M}x{N} err {err:.3e}")
+
+
+@pytest.mark.parametrize("M,N,K,layout", [(300, 1040, 136, "kn"), (77, 16384, 64, "kn"), (129, 776, 200, "nk"),
+                                          (1, 8, 8, "kn")])
+def test_f6_gemm_cross_entropy(M, N, K, layout):
+    """The target logit is left by whichever lane of whichever tile holds it:
+    ragged last column tiles, many tiles per row, both B layouts."""
+    _torch()
+    cfg = inputs.config("F6", M=M, N=N, K=K, b_layout=layout)
+    t = inputs.generate(cfg, seed=M + N + K)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"F6 {M}x{N}x{K} {layout} err {err:.3e}")
+
+
+@pytest.mark.parametrize("name", ["F5", "F6"])
+def test_cross_entropy_full_config_sampled_rows(name):
+    _torch()
+    cfg = inputs.config(name)
+    t = inputs.generate(cfg)
+    _, out = run_gpu(cfg, t)
+    g = to_host_f64(out)
+    assert np.all(np.isfinite(g)) and np.all(g >= -1e-3)   # a loss is >= 0 up to rounding
+    err = check(cfg, t, out, rows=sample_rows(cfg["M"], 24))
+    print(f"{name} full err {err:.3e}")
+
+
+@pytest.mark.parametrize("name,kw", [("F5", dict(M=6, N=1024)), ("F6", dict(M=6, N=1040, K=64))])
+def test_cross_entropy_every_target_column_and_out_of_range(name, kw):
+    """Targets on the first and last column, on every lane position of a
+    tile, and outside [0, N): the fused kernels give NaN for the latter,
+    like the oracle, and the exact loss elsewhere; so does the unfused chain."""
+    _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=8)
+    N = cfg["N"]
+    t["targets"] = np.array([0, N - 1, 255, 256, -3, N], dtype=np.int32)
+    for unfused in (False, True):
+        _, out = run_gpu(cfg, t, unfused=unfused)
+        g = to_host_f64(out)
+        assert np.all(np.isnan(g[4:])) and np.all(np.isfinite(g[:4]))
+        ref = (oracle.run_chain_unfused if unfused else oracle.run_chain)(inputs.chain_for(cfg, t), t)
+        assert parity_error(g[:4], ref[:4], 1.0) <= TOL["bf16"]
+    cfg = inputs.config(name, **dict(kw, M=64))
+    t = inputs.generate(cfg, seed=9)
+    t["targets"] = np.arange(64, dtype=np.int32) * 16 % N   # lanes of every position across tiles
+    _, out = run_gpu(cfg, t)
     check(cfg, t, out)

@@ -632,9 +632,11 @@ def _torch_eager_bf16(ch, t):
             y = torch.softmax(x, -1)
         elif name == "row_logsumexp":
             y = torch.logsumexp(x, -1)
+        elif name == "row_cross_entropy":
+            y = F.cross_entropy(x, torch.from_numpy(t["targets"].astype(np.int64)), reduction="none")
         else:
             raise ValueError(name)
-        h = y if name == "row_logsumexp" else y.to(bf)
+        h = y if name in ("row_logsumexp", "row_cross_entropy") else y.to(bf)
     return h
 
 
@@ -647,6 +649,7 @@ _UNFUSED_CASES = [
     ("F2", dict(batch=1, D=6, H=10, W=14)),
     ("F3", dict(M=24, N=1024, ops=[("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)])),
     ("F4", dict(M=16, N=2048)),
+    ("F6", dict(M=24, N=1040, K=136)),
 ]
 
 
@@ -709,3 +712,49 @@ def test_unfused_oracle_equals_fused_without_ops_and_rounds_f32_chains():
     h = oracle.gemm(t["a"].astype(np.float64), t["b"].astype(np.float64))
     expect = np.maximum(oracle.round_f32(oracle.round_f32(h) + t["bias"].astype(np.float64)), 0.0)
     assert np.array_equal(oracle.run_chain_unfused(ch, t), expect)
+
+
+# ------------------------------------------------------- cross-entropy rows
+
+def test_row_cross_entropy_matches_torch_and_closed_forms():
+    """The loss op against torch's CPU float64 cross_entropy(reduction=
+    'none'); all-equal logits give ln N exactly; a one-hot logit row with a
+    huge margin gives ~0 when the target is the hot column and ~margin when
+    it is not; targets outside [0, N) give NaN."""
+    rng = np.random.default_rng(4)
+    h = rng.standard_normal((37, 1000)) * 3
+    t = rng.integers(0, 1000, 37)
+    ref = F.cross_entropy(_t(h), torch.from_numpy(t), reduction="none").numpy()
+    assert np.allclose(oracle.op_row_cross_entropy(h, t), ref, rtol=1e-13, atol=1e-13)
+    z = np.zeros((3, 16384))
+    assert np.allclose(oracle.op_row_cross_entropy(z, [0, 5, 16383]), math.log(16384), rtol=0, atol=1e-13)
+    hot = np.zeros((2, 64))
+    hot[:, 7] = 50.0
+    out = oracle.op_row_cross_entropy(hot, [7, 3])
+    assert out[0] < 1e-19 and abs(out[1] - 50.0) < 1e-19 + 63 * math.exp(-50) * 2
+    bad = oracle.op_row_cross_entropy(h[:3], [-1, 1000, 5])
+    assert np.isnan(bad[0]) and np.isnan(bad[1]) and np.isfinite(bad[2])
+    assert np.all(oracle.op_row_cross_entropy(h, t) >= 0)
+
+
+def test_chain_cross_entropy_gemm_and_rows_match_torch():
+    """The fused classifier-head chain (GEMM + bias + cross-entropy) against
+    torch's float64 composition, W = 0 and b = 0 giving ln N per row, a row
+    subset equal to the same rows of the whole; the row-wise chain against
+    torch on stored bf16 logits."""
+    cfg, t = _small("F6", M=9, N=1024, K=64)
+    ch = inputs.chain(cfg)
+    out = oracle.run_chain(ch, t)
+    x = _t(oracle.decode_bf16(t["a"]))
+    w = _t(oracle.decode_bf16(t["b"]))
+    ref = F.cross_entropy(x @ w + _t(t["bias"]), torch.from_numpy(t["targets"].astype(np.int64)), reduction="none")
+    assert np.allclose(out, ref.numpy(), rtol=1e-12)
+    z = dict(t, b=np.zeros_like(t["b"]), bias=np.zeros_like(t["bias"]))
+    assert np.allclose(oracle.run_chain(ch, z), math.log(1024), rtol=0, atol=1e-13)
+    rows = np.array([8, 2, 5])
+    assert np.array_equal(oracle.run_chain(ch, t, rows=rows), out[rows])
+    assert t["targets"].dtype == np.int32 and t["targets"].min() >= 0 and t["targets"].max() < 1024
+    cfg, t = _small("F5", M=7, N=2048)
+    a = _t(oracle.decode_bf16(t["a"]))
+    ref = F.cross_entropy(a, torch.from_numpy(t["targets"].astype(np.int64)), reduction="none")
+    assert np.allclose(oracle.run_chain(inputs.chain(cfg), t), ref.numpy(), rtol=1e-13)
