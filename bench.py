@@ -245,13 +245,13 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
     # (every candidate computes the same bits)
     tuning = None
     if args.tuning:
-        rg, xr, wg = (int(v) for v in args.tuning.split(","))
-        op.set_tuning(rg, xr, wg)
+        op.set_tuning(*(int(v) for v in args.tuning.split(",")))
         tuning = {"config": op.tuning(), "candidates": 0, "best_ms": None, "default_ms": None}
     elif not args.no_autotune:
+        keys = ("raster_group", "xcd_remap", "wg_per_cu", "variant")
+        plan_default = op.tuning()
         r = op.autotune(ins, out, reps=max(3, args.warmup // 2))
-        keys = ("raster_group", "xcd_remap", "wg_per_cu")
-        default = [c for c in r["candidates"] if (c["raster_group"], c["xcd_remap"], c["wg_per_cu"]) == (4, 1, 2)]
+        default = [c for c in r["candidates"] if all(c[k] == plan_default[k] for k in keys)]
         tuning = {"config": {k: r["best"][k] for k in keys}, "candidates": len(r["candidates"]),
                   "best_ms": round(r["best"]["seconds"] * 1e3, 5),
                   "default_ms": round(default[0]["seconds"] * 1e3, 5) if default else None}
@@ -374,8 +374,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
-    ap.add_argument("--tuning", default=None, metavar="RG,XR,WG",
-                    help="use this launch configuration (raster group, XCD order, workgroups per CU) "
+    ap.add_argument("--tuning", default=None, metavar="RG,XR,WG[,V]",
+                    help="use this launch configuration (raster group, XCD order, workgroups per CU, kernel variant) "
                          "instead of autotuning")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 5 times (for scaling HBM byte counters)")

@@ -298,11 +298,14 @@ typedef struct kf_tuning {
                            hardware's round-robin order                      */
   int32_t wg_per_cu;    /* CONV3D: persistent workgroups per compute unit,
                            1 or 2 (default 2)                                */
-  int32_t reserved;     /* 0                                                 */
+  int32_t variant;      /* kernel shape.  CONV2D_3X3: 1 (default) = the tile
+                           on 8 waves (64 x 64 wave blocks, two per SIMD),
+                           0 = on 4 waves (128 x 64); others: 0           */
 } kf_tuning;
 
 /* The plan's launch fields.  None of them changes a result bit: they reorder
-   independent tiles or resize a persistent grid.  kf_set_tuning validates
+   independent tiles, resize a persistent grid, or split a tile differently
+   among waves with every output's sum over k taken in the same order.  kf_set_tuning validates
    the values (KF_ERR_INVALID_ARG) and takes effect at the next call. */
 kf_status kf_get_tuning(const kf_desc* desc, kf_tuning* out);
 kf_status kf_set_tuning(kf_desc* desc, const kf_tuning* tuning);
@@ -326,8 +329,8 @@ typedef struct kf_tune_result {
    until the stream is idle; outputs[0] holds the result of the last call
    (the same bits for every candidate).  Candidates: GEMM (bf16 / fp8) raster
    groups {1, 2, 4, 8, 16, 32, 64} x XCD order {contiguous, hardware}; CONV3D
-   workgroups per CU {2, 1} x XCD order; every other plan has only its
-   current configuration. */
+   workgroups per CU {2, 1} x XCD order; CONV2D_3X3 kernel variant {0, 1};
+   every other plan has only its current configuration. */
 kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
                       kf_tune_result* result);
 

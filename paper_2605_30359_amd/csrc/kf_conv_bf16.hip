@@ -483,6 +483,313 @@ __global__ __launch_bounds__(NT, 1) void kf_conv3x3_bf16_256x128(ConvArgs p, con
   wait_vmcnt_lgkm0<0>();
 }
 
+// ---------------------------------------------------------------------------
+// The same tile (two output rows x 128 columns x 128 channels) on 8 waves, 2 x
+// 4 in (channels, pixels): each wave owns 32 columns of both rows x 64
+// channels = 2 x 2 blocks of v_mfma_f32_32x32x16_bf16 (row block bi = output
+// row bi), so two waves share each SIMD.  The 4-wave kernel's K-step is held
+// back by its LDS reads: every CU reads 48 KiB of fragments per 512 clocks of
+// matrix-core issue, and one wave per SIMD draws only ~132 bytes/clock from
+// the LDS; two waves per SIMD draw ~256.  Here the CU reads 64 KiB per step
+// (smaller wave blocks reuse each fragment less), half of what the LDS then
+// supplies.  Halo ring, weight stream and the epilogue are the 4-wave
+// kernel's, with the DMA work spread over 8 waves: one weight DMA per wave and
+// step, the next tile's input rows by 4 DMAs per wave on steps 0, 2, 4 and 6;
+// the 18 K-steps of a tile are unrolled, so every wait count is a constant.
+namespace {
+
+constexpr int NT8 = 512;
+constexpr int kRawDma8 = kRaw / 1024 / 8;  // 4 row DMA instructions per wave per tile
+static_assert(kRawDma8 == 4, "the wait counts below assume 4 row DMAs per wave, on steps 0, 2, 4, 6");
+
+constexpr bool w8_row_step(int s) { return s >= 0 && s < 2 * kRawDma8 && s % 2 == 0; }
+
+// Vector-memory instructions a wave issues after the weight DMA of step s - 5
+// and before step s's wait: the weight DMAs of steps s-4 .. s-1 and the row
+// DMAs of steps s-5 .. s-1 (steps before 0 are the previous tile's, or the
+// prologue's, which issue weights only).
+constexpr int w8_wait(int s) {
+  int n = 4;
+  for (int t = s - 5; t < s; ++t) n += w8_row_step(t) ? 1 : 0;
+  return n;
+}
+
+typedef f32x16 CAcc8[2][2];
+
+}  // namespace
+
+template <int CH>
+__global__ __launch_bounds__(NT8, 1) void kf_conv3x3_bf16_w8(ConvArgs p, const uint16_t* __restrict__ wp) {
+  __shared__ __attribute__((aligned(1024))) unsigned char sHalo[kHalo];
+  __shared__ __attribute__((aligned(1024))) unsigned char sRaw[kRaw];
+  __shared__ __attribute__((aligned(1024))) unsigned char sW0[kWStage], sW1[kWStage], sW2[kWStage], sW3[kWStage],
+      sW4[kWStage], sW5[kWStage];
+  auto stW = [&](auto S_c) -> unsigned char* {
+    constexpr int S = decltype(S_c)::value;
+    return S == 0 ? sW0 : S == 1 ? sW1 : S == 2 ? sW2 : S == 3 ? sW3 : S == 4 ? sW4 : sW5;
+  };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 3;   // 32-column quarter of the tile
+  const int wn = wave >> 2;  // 64-channel half
+  const int H = (int)p.H;
+  const int rows_per_img = H / 2;
+  const int64_t img_elems = (int64_t)CIN * H * WID;
+
+  // ---- halo ring and raw rows: as in the 4-wave kernel; wave w's DMA i
+  // (0 .. 3) fetches channels 2 (4 w + i) and 2 (4 w + i) + 1
+  auto rsw = [](int c) { return ((c >> 3) << 1) & 15; };
+  auto raw_dma = [&](int i, int n_img, int ih0, bool live) {
+    const int c = 2 * (wave * kRawDma8 + i) + (lane >> 5);
+    const int ih = ih0 + ((lane >> 4) & 1);
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(reinterpret_cast<const uint16_t*>(p.x) + (live ? n_img : 0) * img_elems, (uint32_t)(img_elems * 2));
+    const int q = (lane & 15) ^ rsw(c);
+    const bool ok = live && ih >= 0 && ih < H;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS3 void*)(sRaw + (wave * kRawDma8 + i) * 1024), 16,
+                                              ok ? (uint32_t)(((c * H + ih) * WID + q * 8) * 2) : kOOB, 0, 0, 0);
+  };
+  // sRaw -> halo slots s0 (its row 0) and s1 (row 1), zero padding columns;
+  // the first 256 threads transpose one 8 x 8 block each (spreading the
+  // blocks over all 512 threads as half blocks measured slower)
+  auto halo_write = [&](int s0, int s1) {
+    if (tid < 256) {
+      const int cg = tid & 7, pg = (tid >> 3) & 15, r = tid >> 7;
+      const int slot = r ? s1 : s0;
+      u32x4 hv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = cg * 8 + j;
+        hv[j] = *reinterpret_cast<const u32x4*>(sRaw + c * 512 + r * 256 + ((pg ^ rsw(c)) << 4));
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint32_t sel = (k & 1) ? 0x07060302u : 0x05040100u;
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(hv[2 * e + 1][k >> 1], hv[2 * e][k >> 1], sel);
+        const int pix = slot * HALO_COLS + pg * 8 + k + 1;
+        *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = o;
+      }
+    } else if (tid < 256 + 32) {
+      const int u = tid - 256;
+      const int r = u >> 4, side = (u >> 3) & 1, cg = u & 7;
+      const int pix = (r ? s1 : s0) * HALO_COLS + (side ? HALO_COLS - 1 : 0);
+      *reinterpret_cast<u32x4*>(sHalo + halo_off(pix, cg)) = u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+
+  // ---- weight stream: wave w fills rows [16 w, 16 w + 16) of a stage with
+  // one DMA (chunk c of row co stored at c ^ ((co >> 2) & 3))
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp, (uint32_t)(9 * COUT * CIN * 2));
+  const int dma_lc = (lane & 3) ^ ((lane >> 4) & 3);
+  const uint32_t vw = (uint32_t)(((wave * 16 + (lane >> 2)) * CIN + dma_lc * 8) * 2);
+  auto dma_w = [&](auto S_c, int s, bool live) {
+    const int sw = s >= kSteps ? s - kSteps : s;
+    const int soff = ((sw >> 1) * COUT * CIN + (sw & 1) * 32) * 2;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS3 void*)(stW(S_c) + wave * 1024), 16, live ? vw : kOOB, soff,
+                                              0, 0);
+  };
+
+  // ---- fragment reads
+  const int r32 = lane & 31, kg = lane >> 5;
+  uint32_t rB[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int ch = kk * 2 + kg;
+    rB[kk] = (uint32_t)((wn * 64 + r32) * 64 + ((ch ^ ((r32 >> 2) & 3)) << 4));
+  }
+  int rb = 0;                      // ring slot of logical halo row 0
+  u32x4 fa[2][2][2], fb[2][2][2];  // [buffer][16-k half][block]
+  constexpr int kReads8 = 8;       // per step: 4 A (2 blocks x 2 halves), 4 B
+  auto read_one = [&](auto S_c, auto BUF_c, auto J_c, int s) {
+    constexpr int BUF = decltype(BUF_c)::value;
+    constexpr int J = decltype(J_c)::value;
+    constexpr int kk = J / 4, j = J % 4;
+    if constexpr (j < 2) {
+      const int tap = s >> 1, kh = tap / 3, kw = tap - kh * 3;
+      const int slot = (rb + j + kh) & 3;
+      const int pix = slot * HALO_COLS + wm * 32 + r32 + kw;
+      const int ch = (s & 1) * 4 + kk * 2 + kg;
+      fa[BUF][kk][j] = lds_load<u32x4>(sHalo + halo_off(pix, ch));
+    } else {
+      fb[BUF][kk][j - 2] = lds_load<u32x4>(stW(S_c) + rB[kk] + (j - 2) * 2048);
+    }
+  };
+
+  float bias_v[2] = {0.0f, 0.0f};
+  if (p.bias) {
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) bias_v[bj] = p.bias[wn * 64 + bj * 32 + (lane & 31)];
+  }
+
+  CAcc8 acc;
+  // K-step s (0 .. 17): wait for weight stage (s + 1) % 6 (its DMA went out
+  // in step s - 5) and pass the barrier, after which every wave has read its
+  // fragments of stage s % 6; then 8 MFMAs with the reads of step s + 1, the
+  // weight DMA of step s + 6 into stage s % 6 and, on steps 0 .. 6 (even),
+  // one DMA of the next tile's input rows.
+  auto step = [&](auto s_c, bool next_live, int n_next, int ih_next) {
+    constexpr int s = decltype(s_c)::value;
+    constexpr int S = s % kWS, BUF = s % 2;
+    wait_vmcnt_lgkm0<w8_wait(s)>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    const bool live = s + kWS < kSteps || next_live;
+    static_for<0, 8>([&](auto I_c) {
+      constexpr int i = decltype(I_c)::value;
+      constexpr int kk = i / 4, bi = (i / 2) % 2, bj = i % 2;
+      acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[BUF][kk][bi]),
+                                                            __builtin_bit_cast(bf16x8, fb[BUF][kk][bj]), acc[bi][bj], 0,
+                                                            0, 0);
+      if constexpr (s + 1 < kSteps) read_one(IC<(S + 1) % kWS>{}, IC<BUF ^ 1>{}, I_c, s + 1);
+      if constexpr (i == 1) dma_w(IC<S>{}, s + kWS, live);
+      if constexpr (i == 5 && w8_row_step(s)) raw_dma(s / 2, n_next, ih_next, next_live);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  const int nops = p.prog.n;
+  const OpTable ops = load_op_table(p.prog, lane);
+  const int pidx = p.pool ? p.pool_index : nops;
+  const int64_t plane_out = p.pool ? (int64_t)(H / 2) * (WID / 2) : (int64_t)H * WID;
+  uint16_t* out = reinterpret_cast<uint16_t*>(p.out);
+
+  const int t_begin = (int)((int64_t)blockIdx.x * p.tiles / gridDim.x);
+  const int t_end = (int)((int64_t)(blockIdx.x + 1) * p.tiles / gridDim.x);
+  auto continues = [&](int t) { return t > t_begin && t % rows_per_img != 0; };
+
+  // prologue: input rows 0-1 of the first tile, then the weight stages of
+  // steps 0-5, issued as K-steps -6 .. -1 would issue them (weights only)
+  for (int i = 0; i < kRawDma8; ++i) raw_dma(i, t_begin / rows_per_img, 2 * (t_begin % rows_per_img) - 1, true);
+  static_for<0, kWS>([&](auto S_c) { dma_w(S_c, decltype(S_c)::value, true); });
+
+  for (int tile = t_begin; tile < t_end; ++tile) {
+    const int n_img = tile / rows_per_img;
+    const int ph = tile % rows_per_img;
+    const int oh0 = 2 * ph;
+    const bool cont = continues(tile);
+    const int next_tile = tile + 1;
+    const bool next_live = next_tile < t_end;
+    const bool next_cont = next_live && continues(next_tile);
+    const int n_next = next_tile / rows_per_img;
+    const int ih_next = 2 * (next_tile % rows_per_img) + (next_cont ? 1 : -1);
+
+    // This tile's input rows (requested in steps 0-6 of the previous tile,
+    // or in the prologue) and weight stage 0 (step 12, or the prologue) have
+    // landed once at most 5 vector-memory instructions are in flight: after
+    // stage 0 come only the weights of steps 13-17 (prologue: of steps 1-5)
+    // and the previous tile's output stores.
+    wait_vmcnt_lgkm0<5>();
+    __syncthreads();
+    rb = cont ? (rb + 2) & 3 : 0;
+    if (cont) {
+      halo_write((rb + 2) & 3, (rb + 3) & 3);
+    } else {
+      // start of the range or of an image: rows 0-1 are in sRaw; rows 2-3
+      // are requested now and waited for
+      halo_write(0, 1);
+      __syncthreads();
+      for (int i = 0; i < kRawDma8; ++i) raw_dma(i, n_img, oh0 + 1, true);
+      wait_vmcnt_lgkm0<0>();
+      __syncthreads();
+      halo_write(2, 3);
+    }
+    __syncthreads();
+    static_for<0, kReads8>([&](auto J_c) { read_one(IC<0>{}, IC<0>{}, J_c, 0); });
+
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.0f;
+
+    static_for<0, kSteps>([&](auto s_c) { step(s_c, next_live, n_next, ih_next); });
+
+    // ---- epilogue: as in the 4-wave kernel, per channel block bj, the two
+    // output rows in this lane's row blocks 0 and 1
+    // outputs are staged in the ring slots of this tile's input rows 0 and 1
+    // (last read in step 11)
+    unsigned char* const slot_a = sHalo + rb * kSlot;
+    unsigned char* const slot_b = sHalo + ((rb + 1) & 3) * kSlot;
+    auto stage_row = [&](int row) { return row < 64 ? slot_a + row * 256 : slot_b + (row - 64) * 256; };
+    const __amdgpu_buffer_rsrc_t ro =
+        make_rsrc(out + (int64_t)n_img * COUT * plane_out, (uint32_t)(COUT * plane_out * 2));
+    static_for<0, 2>([&](auto bj_c) {
+      constexpr int bj = decltype(bj_c)::value;
+      const int co = wn * 64 + bj * 32 + (lane & 31);
+      float v[32];  // v[r * 16 + i] = acc[r][bj][i]: output row r
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        v[i] = acc_read(acc[0][bj][i]);
+        v[16 + i] = acc_read(acc[1][bj][i]);
+      }
+      constexpr bool kPoolFirst = chain_pools_first(CH);
+      if constexpr (!kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias_v[bj], v);
+      if (p.pool) {
+        float pv[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2) {
+            const int i = q * 4 + h2 * 2;
+            pv[q * 2 + h2] = fmaxf(fmaxf(v[i], v[i + 1]), fmaxf(v[16 + i], v[16 + i + 1]));
+          }
+        if constexpr (kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias_v[bj], pv);
+        conv_apply_phase<CH>(ops, pidx + 1, nops, bias_v[bj], pv);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int pw = wm * 16 + q * 4 + (lane >> 5) * 2;
+          const int ch = pw >> 3;
+          *reinterpret_cast<uint32_t*>(slot_a + co * 128 + ((ch ^ (co & 7)) << 4) + (pw & 7) * 2) =
+              pack_bf16x2(pv[q * 2], pv[q * 2 + 1]);
+        }
+      } else {
+        const int col = wn * 32 + (lane & 31);  // channel within block bj
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int ow = wm * 32 + q * 8 + (lane >> 5) * 4;
+            const float* x = &v[r * 16 + q * 4];
+            *reinterpret_cast<u32x2*>(stage_row(col * 2 + r) + (((ow >> 3) ^ (co & 15)) << 4) + (ow & 7) * 2) =
+                u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+          }
+        // channel block bj: 64 channels x 2 rows x 16 chunks
+        __syncthreads();
+        const uint32_t row_off = (uint32_t)(oh0 * WID * 2);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int idx = tid + NT8 * k;
+          const int row = idx >> 4, ch = idx & 15;
+          const int col2 = row >> 1, r = row & 1;
+          const int co2 = (col2 >> 5) * 64 + bj * 32 + (col2 & 31);
+          const u32x4 w = *reinterpret_cast<const u32x4*>(stage_row(row) + ((ch ^ (co2 & 15)) << 4));
+          buf_store16(w, ro, (uint32_t)(co2 * plane_out * 2) + row_off + (uint32_t)(r * WID * 2) + ch * 16);
+        }
+        __syncthreads();
+      }
+    });
+    if (p.pool) {
+      // 128 channels x 8 chunks
+      __syncthreads();
+      const uint32_t row_off = (uint32_t)(ph * (WID / 2) * 2);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int idx = tid + NT8 * k;
+        const int co = idx >> 3, ch = idx & 7;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(slot_a + co * 128 + ((ch ^ (co & 7)) << 4));
+        buf_store16(w, ro, (uint32_t)(co * plane_out * 2) + row_off + ch * 16);
+      }
+    }
+  }
+  // nothing may land in LDS after the workgroup ends
+  wait_vmcnt_lgkm0<0>();
+}
+
 hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStream_t stream) {
   const int64_t pairs = args.cout * args.cin;
   const unsigned blocks = (unsigned)((pairs + 255) / 256 < 1024 ? (pairs + 255) / 256 : 1024);
@@ -496,10 +803,16 @@ hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, in
   if (args.tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)(args.grid < args.tiles ? args.grid : args.tiles));
   const uint16_t* wp = reinterpret_cast<const uint16_t*>(packed_weights);
-  if (chain == 7)
+  if (args.variant == 1) {
+    if (chain == 7)
+      hipLaunchKernelGGL(kf_conv3x3_bf16_w8<7>, grid, dim3(NT8), 0, stream, args, wp);
+    else
+      hipLaunchKernelGGL(kf_conv3x3_bf16_w8<0>, grid, dim3(NT8), 0, stream, args, wp);
+  } else if (chain == 7) {
     hipLaunchKernelGGL(kf_conv3x3_bf16_256x128<7>, grid, dim3(NT), 0, stream, args, wp);
-  else
+  } else {
     hipLaunchKernelGGL(kf_conv3x3_bf16_256x128<0>, grid, dim3(NT), 0, stream, args, wp);
+  }
   return hipGetLastError();
 }
 

@@ -357,6 +357,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     }
     d->variant = kVarConvBf16;
     d->kernel_name = "kf_conv3x3_bf16_256x128";
+    d->tuning.variant = 1;  // the 8-wave tile: faster at the C4 shape (the tuner may pick either)
     d->inputs.push_back(Slot{dt, 4, {s->batch, s->cin, s->height, s->width}, "A", false});
     d->inputs.push_back(Slot{dt, 4, {s->cout, s->cin, 3, 3}, "B", false});
     for (int i = 0; i < s->n_ops; ++i)
@@ -622,8 +623,10 @@ kf_status kf_set_tuning(kf_desc* d, const kf_tuning* t) {
   if (t->raster_group < 1 || t->raster_group > 64) return fail(KF_ERR_INVALID_ARG, "raster_group must be in [1, 64]");
   if (t->xcd_remap != 0 && t->xcd_remap != 1) return fail(KF_ERR_INVALID_ARG, "xcd_remap must be 0 or 1");
   if (t->wg_per_cu != 1 && t->wg_per_cu != 2) return fail(KF_ERR_INVALID_ARG, "wg_per_cu must be 1 or 2");
+  const int max_variant = d->variant == kVarConvBf16 ? 1 : 0;
+  if (t->variant < 0 || t->variant > max_variant)
+    return fail(KF_ERR_INVALID_ARG, "variant must be in [0, %d] for this plan", max_variant);
   d->tuning = *t;
-  d->tuning.reserved = 0;
   return ok();
 }
 
@@ -639,6 +642,8 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
   } else if (d->variant == kVarConv3d) {
     for (int remap = 1; remap >= 0; --remap)
       for (int wg : {2, 1}) cand.push_back(kf_tuning{cur.raster_group, remap, wg, 0});
+  } else if (d->variant == kVarConvBf16) {
+    for (int v : {0, 1}) cand.push_back(kf_tuning{cur.raster_group, cur.xcd_remap, cur.wg_per_cu, v});
   } else {
     cand.push_back(cur);
   }
@@ -957,6 +962,7 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
   c.cout = s.cout;
   c.tiles = (int32_t)(s.batch * (s.height / 2));
   c.grid = d->num_cu;
+  c.variant = d->tuning.variant;
   c.prog = d->prog;
   for (int i = 0; i < s.n_ops; ++i) {
     if (s.ops[i].kind == KF_OP_BIAS) c.bias = static_cast<const float*>(inputs[2].data);
@@ -1095,6 +1101,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     c.cout = s.cout;
     c.tiles = (int32_t)(s.batch * (s.height / 2));
     c.grid = d->num_cu;
+    c.variant = d->tuning.variant;
     c.out = cur;
     c.out_bf16 = 1;
     if (d->packed_from != inputs[1].data) {

@@ -78,10 +78,11 @@ class KfDiagnosis(ctypes.Structure):
 
 class KfTuning(ctypes.Structure):
     _fields_ = [("raster_group", ctypes.c_int32), ("xcd_remap", ctypes.c_int32), ("wg_per_cu", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("variant", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
-        return {"raster_group": self.raster_group, "xcd_remap": self.xcd_remap, "wg_per_cu": self.wg_per_cu}
+        return {"raster_group": self.raster_group, "xcd_remap": self.xcd_remap, "wg_per_cu": self.wg_per_cu,
+                "variant": self.variant}
 
 
 class KfTuneResult(ctypes.Structure):
@@ -383,8 +384,8 @@ class FusedOp:
         _check(lib().kf_get_tuning(self._h, ctypes.byref(t)))
         return t.as_dict()
 
-    def set_tuning(self, raster_group: int, xcd_remap: int, wg_per_cu: int):
-        t = KfTuning(raster_group, xcd_remap, wg_per_cu, 0)
+    def set_tuning(self, raster_group: int, xcd_remap: int, wg_per_cu: int, variant: int = 0):
+        t = KfTuning(raster_group, xcd_remap, wg_per_cu, variant)
         _check(lib().kf_set_tuning(self._h, ctypes.byref(t)))
 
     def autotune(self, inputs, out, reps: int = 5, stream=None) -> dict:

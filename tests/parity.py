@@ -46,12 +46,17 @@ def parity_error(gpu: np.ndarray, ref: np.ndarray, floor: float) -> float:
     return float(np.max(np.abs(gpu - ref) / np.maximum(np.abs(ref), floor)))
 
 
-def run_gpu(cfg, tensors, chain=None, unfused=False):
-    """Plan the op, copy inputs to the device, run, return (op, out tensor)."""
+def run_gpu(cfg, tensors, chain=None, unfused=False, tuning=None):
+    """Plan the op (with launch configuration `tuning`, a (raster group, XCD
+    order, workgroups per CU, variant) tuple, if given), copy inputs to the
+    device, run, return (op, out tensor)."""
     import torch
     chain = chain if chain is not None else inputs.chain_for(cfg, tensors)
     op = kf.FusedOp(chain, **kf.sizes_of(cfg))
-    print(f"[gpu] {cfg.get('name')} {kf.sizes_of(cfg)} ops={[o[0] for o in chain['ops']]} unfused={unfused}", flush=True)
+    if tuning is not None:
+        op.set_tuning(*tuning)
+    print(f"[gpu] {cfg.get('name')} {kf.sizes_of(cfg)} ops={[o[0] for o in chain['ops']]} unfused={unfused} "
+          f"tuning={tuning}", flush=True)
     ins = op.device_inputs(tensors)
     out = op.empty_output("cuda")
     if unfused:

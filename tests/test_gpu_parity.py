@@ -412,11 +412,12 @@ def test_rowwise_full_config_sampled_rows(name):
     (3, 6, [("bias",), ("relu",)]),
     (1, 4, [("bias",), ("gelu_tanh",), ("maxpool2x2",), ("scale", -2.0), ("swish",)]),
 ])
-def test_c4_small(batch, H, ops):
+@pytest.mark.parametrize("variant", [0, 1])
+def test_c4_small(batch, H, ops, variant):
     _torch()
     cfg = inputs.config("C4", batch=batch, H=H, ops=ops)
     t = inputs.generate(cfg, seed=batch * 10 + H)
-    _, out = run_gpu(cfg, t)
+    _, out = run_gpu(cfg, t, tuning=(4, 1, 2, variant))
     err = check(cfg, t, out)
     print(f"C4 batch={batch} H={H} ops={[o[0] for o in ops]} err {err:.3e}")
 
@@ -456,11 +457,12 @@ def test_c4_zero_weights_and_centre_tap():
     check(cfg, t2, out)
 
 
-def test_c4_full_config_sampled_images():
+@pytest.mark.parametrize("variant", [0, 1])
+def test_c4_full_config_sampled_images(variant):
     _torch()
     cfg = inputs.config("C4")
     t = inputs.generate(cfg)
-    _, out = run_gpu(cfg, t)
+    _, out = run_gpu(cfg, t, tuning=(4, 1, 2, variant))
     err = check(cfg, t, out, images=np.array([0, 37, 63]))
     assert np.all(np.isfinite(to_host_f64(out)))
     print(f"C4 full err {err:.3e}")
@@ -471,20 +473,23 @@ def test_c4_full_config_sampled_images():
     (5, 120, [("bias",), ("relu",), ("maxpool2x2",)]),   # 300 row-pair tiles, 60 per image
     (3, 200, [("bias",), ("relu",)]),                    # unpooled
 ])
-def test_c4_tile_ranges(batch, H, ops):
+@pytest.mark.parametrize("variant", [0, 1])
+def test_c4_tile_ranges(batch, H, ops, variant):
     """More tiles than workgroups: each workgroup walks a contiguous range of
     row pairs, reusing two halo rows from one tile to the next and reloading
     all four at the start of an image; ranges here cross image boundaries."""
     _torch()
     cfg = inputs.config("C4", batch=batch, H=H, ops=ops)
     t = inputs.generate(cfg, seed=batch + H)
-    _, out = run_gpu(cfg, t)
+    _, out = run_gpu(cfg, t, tuning=(4, 1, 2, variant))
     err = check(cfg, t, out, images=np.arange(batch))
     print(f"C4 batch={batch} H={H} err {err:.3e}")
 
 
-def test_c4_integer_bit_exact_tile_ranges():
-    """The integer test of the contraction with several tiles per workgroup."""
+@pytest.mark.parametrize("variant", [0, 1])
+def test_c4_integer_bit_exact_tile_ranges(variant):
+    """The integer test of the contraction with several tiles per workgroup,
+    on the 4-wave and the 8-wave tile."""
     torch = _torch()
     batch, H = 3, 200
     cfg = inputs.config("C4", batch=batch, H=H, ops=[])
@@ -492,7 +497,7 @@ def test_c4_integer_bit_exact_tile_ranges():
     x = rng.integers(-4, 5, size=(batch, 64, H, 128)).astype(np.float32)
     w = rng.integers(-2, 3, size=(128, 64, 3, 3)).astype(np.float32)
     t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
-    _, out = run_gpu(cfg, t)
+    _, out = run_gpu(cfg, t, tuning=(4, 1, 2, variant))
     got_bits = out.view(torch.int16).cpu().numpy().view(np.uint16)
     for n in range(batch):
         ref = oracle.conv2d_3x3(x[n:n + 1].astype(np.float64), w.astype(np.float64))
@@ -721,10 +726,14 @@ def test_specialised_chain_matches_interpreted(name, kw):
     ("C3", dict(M=1024, N=1024, K=136, ops=[("groupnorm", 4, 1e-5), ("swish",), ("residual_add",)])),  # 16 tiles
     ("C5", dict(M=1024, N=2048, K=128)),                                  # fp8, softmax rows across 8 column tiles
     ("F2", dict(batch=3, D=9, H=19, W=35)),                               # conv3d, partial tiles
+    ("C4", dict(batch=3, H=10)),                                          # conv: 4- and 8-wave tiles
+    ("C4", dict(batch=2, H=8, ops=[("bias",), ("swish",)])),              # unpooled, interpreted epilogue
 ])
 def test_tuning_candidates_bit_identical(name, kw):
     """Every launch configuration the tuner may pick computes the same bits:
-    the fields only reorder independent tiles or resize a persistent grid."""
+    the fields only reorder independent tiles, resize a persistent grid, or
+    split the conv tile among 4 or 8 waves (each output's sum over k in the
+    same order)."""
     torch = _torch()
     cfg = inputs.config(name, **kw)
     t = inputs.generate(cfg, seed=51)
@@ -732,18 +741,19 @@ def test_tuning_candidates_bit_identical(name, kw):
     ins = op.device_inputs(t)
     ref = op.empty_output("cuda")
     op(ins, ref)
-    configs = ([(g, r, 2) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)] if name != "F2" else
-               [(4, r, w) for r in (1, 0) for w in (2, 1)])
-    for g, r, w in configs:
-        op.set_tuning(g, r, w)
+    configs = ([(4, r, w, 0) for r in (1, 0) for w in (2, 1)] if name == "F2" else
+               [(4, 1, 2, v) for v in (1, 0)] if name == "C4" else
+               [(g, r, 2, 0) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)])
+    for g, r, w, v in configs:
+        op.set_tuning(g, r, w, v)
         out = op.empty_output("cuda")
         op(ins, out)
         a, b = (ref, out) if ref.dtype != torch.bfloat16 else (ref.view(torch.int16), out.view(torch.int16))
-        assert torch.equal(a, b), (name, g, r, w)
+        assert torch.equal(a, b), (name, g, r, w, v)
     check(cfg, t, ref)
 
 
-@pytest.mark.parametrize("name", ["C2", "C3", "C5", "F1", "F2"])
+@pytest.mark.parametrize("name", ["C2", "C3", "C4", "C5", "F1", "F2"])
 def test_full_size_tuned_launch_bit_identical(name):
     """At the full workload size, the launch configuration the bench keeps
     (by autotuning, as the bench does) and every other candidate compute the
@@ -761,11 +771,11 @@ def test_full_size_tuned_launch_bit_identical(name):
     r = op.autotune(ins, out, reps=1)
     assert torch.equal(bits(ref), bits(out)), (name, r["best"])
     for c in r["candidates"]:
-        op.set_tuning(c["raster_group"], c["xcd_remap"], c["wg_per_cu"])
+        op.set_tuning(c["raster_group"], c["xcd_remap"], c["wg_per_cu"], c["variant"])
         out.zero_()
         op(ins, out)
         assert torch.equal(bits(ref), bits(out)), (name, c)
-    if cfg["contraction"] == "conv3d_3x3x3":
+    if cfg["contraction"] in ("conv3d_3x3x3", "conv2d_3x3"):
         check(cfg, t, ref, images=np.array([0, cfg["batch"] - 1]))
     else:
         check(cfg, t, ref, rows=sample_rows(cfg["M"], 8, seed=4))
@@ -776,6 +786,7 @@ def test_full_size_tuned_launch_bit_identical(name):
     ("C2", dict(M=1024, N=2048, K=512), 14),
     ("F2", dict(batch=2, D=10, H=18, W=34), 4),
     ("F4", dict(M=256, N=2048), 1),
+    ("C4", dict(batch=8, H=16), 2),
 ])
 def test_autotune_keeps_the_fastest_candidate(name, kw, n):
     _torch()
@@ -788,7 +799,7 @@ def test_autotune_keeps_the_fastest_candidate(name, kw, n):
     assert len(r["candidates"]) == n
     assert all(c["seconds"] > 0 for c in r["candidates"])
     assert r["best"]["seconds"] == min(c["seconds"] for c in r["candidates"])
-    best = {k: r["best"][k] for k in ("raster_group", "xcd_remap", "wg_per_cu")}
+    best = {k: r["best"][k] for k in ("raster_group", "xcd_remap", "wg_per_cu", "variant")}
     assert op.tuning() == best
     check(cfg, t, out)
     out2 = op.empty_output("cuda")
