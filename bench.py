@@ -33,8 +33,10 @@ gets a block of the same fields under "also".  Per workload:
   tuning       the launch configuration kf_autotune kept before the timed
                steps (every candidate computes the same bits), or the one
                given with --tuning
-  diagnosis    kf_diagnose on the measured kernel time: compute and memory
-               fractions of the MI355X peaks and the bound
+  diagnosis    kf_diagnose_counters on the measured kernel time and the
+               committed counters (HBM bytes, matrix-core busy fraction, LDS
+               bank conflicts) when they match the kernel source: compute and
+               memory fractions, the bound and the recommendations
 """
 from __future__ import annotations
 
@@ -308,9 +310,15 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
 
     trec = _traffic_record(kname, cfg["workload"])
     traffic = trec.get("hbm_bytes_per_launch") if trec else None
-    diag = op.diagnose(kernel_ms * 1e-3, traffic or 0.0)
+    # the diagnosis from the live kernel time and, when the committed counter
+    # summary matches the kernel source, its counted bytes, matrix-core busy
+    # fraction and LDS bank conflicts
+    diag = op.diagnose_counters(kernel_ms * 1e-3, float(traffic) if traffic else -1.0,
+                                float(trec.get("mfma_busy", -1.0)) if trec else -1.0,
+                                float(trec.get("lds_conflict", -1.0)) if trec else -1.0)
     diagnosis = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in diag.items()
-                 if k in ("bound", "compute_frac", "memory_frac", "intensity", "ridge", "workgroups", "compute_units")}
+                 if k in ("bound", "compute_frac", "memory_frac", "intensity", "ridge", "workgroups", "compute_units",
+                          "mfma_busy", "lds_conflict", "traffic_ratio", "hints")}
 
     cpu, err = (None, None)
     if cpu_budget > 0:

@@ -275,7 +275,33 @@ typedef struct kf_diagnosis {
   int64_t workgroups;   /* workgroups the main kernel launches               */
   int32_t compute_units;
   int32_t bound;        /* kf_bound                                          */
+  double mfma_busy;     /* counted matrix-core busy fraction (-1: not given) */
+  double lds_conflict;  /* counted LDS bank-conflict share of LDS-active
+                           cycles (-1: not given)                           */
+  double traffic_ratio; /* counted HBM bytes / algorithmic bytes (-1: no
+                           count given)                                     */
+  uint32_t hints;       /* kf_hint bits: what to change, by the rules of
+                           kf_diagnose_counters                             */
+  int32_t reserved;     /* 0                                                 */
 } kf_diagnosis;
+
+/* Recommendations a diagnosis can carry (bits of kf_diagnosis.hints): the
+   paper's expert advice per bottleneck class (Appendix B), keyed on
+   counted evidence. */
+typedef enum kf_hint {
+  KF_HINT_REUSE = 1,        /* HBM traffic well above the algorithmic bytes:
+                               improve operand reuse (tile order / raster,
+                               keep data resident in LDS or registers)       */
+  KF_HINT_PARALLELISM = 2,  /* fewer workgroups than compute units: split the
+                               work finer or process more per launch         */
+  KF_HINT_PIPELINE = 4,     /* latency-bound: deepen prefetch / pipelining,
+                               raise the bytes in flight                      */
+  KF_HINT_OVERLAP = 8,      /* instruction-bound with the matrix cores idle
+                               much of the time: overlap loads, barriers and
+                               the epilogue with the MFMA work               */
+  KF_HINT_LDS_LAYOUT = 16   /* LDS bank conflicts: change the LDS layout or
+                               swizzle                                       */
+} kf_hint;
 
 /* The classification rule alone (no descriptor, no device): latency-bound if
    workgroups < compute_units or both fractions are below 0.25, else
@@ -289,6 +315,29 @@ kf_status kf_classify(double flops, double bytes, double seconds, double peak_tf
    byte count (e.g. the FETCH_SIZE + WRITE_SIZE counters of one launch);
    hbm_bytes <= 0 uses the algorithmic bytes of the plan. */
 kf_status kf_diagnose(const kf_desc* desc, double kernel_seconds, double hbm_bytes, kf_diagnosis* out);
+
+/* Hardware counters of one launch of the plan's main kernel, as rocprofv3
+   reports them (each field < 0 when not measured, except kernel_seconds). */
+typedef struct kf_counters {
+  double kernel_seconds;   /* duration of the launch, > 0                    */
+  double hbm_bytes;        /* FETCH_SIZE + WRITE_SIZE, scaled to bytes by a
+                              plain-copy calibration                         */
+  double mfma_busy;        /* SQ_VALU_MFMA_BUSY_CYCLES / (SIMDs x per-XCD
+                              GRBM_GUI_ACTIVE): 0..1                         */
+  double lds_conflict;     /* SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE: 0..1 */
+} kf_counters;
+
+/* kf_diagnose from counters: the compute fraction is the counted
+   matrix-core busy fraction when it is given (for matrix-core kernels; the
+   achieved FLOP rate over the datasheet peak otherwise), the memory fraction
+   the counted bytes over the HBM peak; the bound then follows kf_classify's
+   rule, and the hints are set as: REUSE if counted bytes exceed 1.5x the
+   algorithmic bytes of a memory-bound or matrix-core kernel; PARALLELISM if
+   fewer workgroups than compute units; PIPELINE if latency-bound; OVERLAP
+   if instruction-bound with the matrix cores busy less than 75% of the
+   cycles; LDS_LAYOUT if more than 5% of the LDS-active cycles are bank
+   conflicts.  The thresholds are this library's, not the paper's. */
+kf_status kf_diagnose_counters(const kf_desc* desc, const kf_counters* counters, kf_diagnosis* out);
 
 typedef struct kf_tuning {
   int32_t raster_group; /* GEMM: consecutive tiles walk this many tile rows

@@ -574,6 +574,16 @@ size_t plan_workspace_bytes(const kf_desc* d) {
 kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_tensor* inputs, kf_tensor* outputs,
                     void* stream, void* ev_before, void* ev_after);
 
+// latency-bound if the launch has fewer workgroups than compute units or
+// reaches under 25% of both peaks, else the nearer roof (memory on a tie)
+void classify_bound(kf_diagnosis* g) {
+  constexpr double kLatencyFrac = 0.25;
+  if (g->workgroups < g->compute_units || (g->compute_frac < kLatencyFrac && g->memory_frac < kLatencyFrac))
+    g->bound = KF_BOUND_LATENCY;
+  else
+    g->bound = g->memory_frac >= g->compute_frac ? KF_BOUND_MEMORY : KF_BOUND_INSTRUCTION;
+}
+
 }  // namespace
 
 extern "C" {
@@ -597,11 +607,13 @@ kf_status kf_classify(double flops, double bytes, double seconds, double peak_tf
   g.ridge = peak_tflops * 1e12 / (peak_gbps * 1e9);
   g.workgroups = workgroups;
   g.compute_units = compute_units;
-  constexpr double kLatencyFrac = 0.25;
-  if (workgroups < compute_units || (g.compute_frac < kLatencyFrac && g.memory_frac < kLatencyFrac))
-    g.bound = KF_BOUND_LATENCY;
-  else
-    g.bound = g.memory_frac >= g.compute_frac ? KF_BOUND_MEMORY : KF_BOUND_INSTRUCTION;
+  g.mfma_busy = -1.0;
+  g.lds_conflict = -1.0;
+  g.traffic_ratio = -1.0;
+  g.hints = 0;
+  g.reserved = 0;
+  classify_bound(&g);
+  if (g.bound == KF_BOUND_LATENCY) g.hints |= workgroups < compute_units ? KF_HINT_PARALLELISM : KF_HINT_PIPELINE;
   return ok();
 }
 
@@ -610,6 +622,31 @@ kf_status kf_diagnose(const kf_desc* d, double kernel_seconds, double hbm_bytes,
   const Work w = plan_work(d);
   return kf_classify(w.flops, hbm_bytes > 0.0 ? hbm_bytes : w.bytes, kernel_seconds, w.peak_tflops, 8000.0,
                      w.workgroups, d->num_cu, out);
+}
+
+kf_status kf_diagnose_counters(const kf_desc* d, const kf_counters* c, kf_diagnosis* out) {
+  if (!d || !c || !out) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  const Work w = plan_work(d);
+  const bool mfma = d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8 || d->variant == kVarConvBf16 ||
+                    d->variant == kVarConv3d;
+  kf_status st = kf_classify(w.flops, c->hbm_bytes > 0.0 ? c->hbm_bytes : w.bytes, c->kernel_seconds, w.peak_tflops,
+                             8000.0, w.workgroups, d->num_cu, out);
+  if (st != KF_OK) return st;
+  kf_diagnosis& g = *out;
+  if (mfma && c->mfma_busy >= 0.0) {
+    g.mfma_busy = c->mfma_busy;
+    g.compute_frac = c->mfma_busy;  // the counted share of cycles the matrix cores worked
+  }
+  if (c->lds_conflict >= 0.0) g.lds_conflict = c->lds_conflict;
+  if (c->hbm_bytes > 0.0 && w.bytes > 0.0) g.traffic_ratio = c->hbm_bytes / w.bytes;
+  classify_bound(&g);
+  g.hints = 0;
+  if (g.workgroups < g.compute_units) g.hints |= KF_HINT_PARALLELISM;
+  if (g.bound == KF_BOUND_LATENCY) g.hints |= KF_HINT_PIPELINE;
+  if (g.traffic_ratio > 1.5 && (g.bound == KF_BOUND_MEMORY || mfma)) g.hints |= KF_HINT_REUSE;
+  if (g.bound == KF_BOUND_INSTRUCTION && g.mfma_busy >= 0.0 && g.mfma_busy < 0.75) g.hints |= KF_HINT_OVERLAP;
+  if (g.lds_conflict > 0.05) g.hints |= KF_HINT_LDS_LAYOUT;
+  return ok();
 }
 
 kf_status kf_get_tuning(const kf_desc* d, kf_tuning* out) {

@@ -39,8 +39,9 @@ DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
-            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc")
+            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc", "kf_diagnose_counters")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
+HINTS = {1: "reuse", 2: "parallelism", 4: "pipeline", 8: "overlap", 16: "lds_layout"}
 KF_MAX_TUNE_CANDIDATES = 16
 
 
@@ -68,12 +69,19 @@ class KfTensor(ctypes.Structure):
 class KfDiagnosis(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("flops", "bytes", "seconds", "tflops", "gbps", "peak_tflops",
                                                "peak_gbps", "compute_frac", "memory_frac", "intensity", "ridge")] + \
-               [("workgroups", ctypes.c_int64), ("compute_units", ctypes.c_int32), ("bound", ctypes.c_int32)]
+               [("workgroups", ctypes.c_int64), ("compute_units", ctypes.c_int32), ("bound", ctypes.c_int32),
+                ("mfma_busy", ctypes.c_double), ("lds_conflict", ctypes.c_double), ("traffic_ratio", ctypes.c_double),
+                ("hints", ctypes.c_uint32), ("reserved", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
-        d = {n: getattr(self, n) for n, _ in self._fields_}
+        d = {n: getattr(self, n) for n, _ in self._fields_ if n != "reserved"}
         d["bound"] = BOUNDS[self.bound]
+        d["hints"] = [name for bit, name in HINTS.items() if self.hints & bit]
         return d
+
+
+class KfCounters(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("kernel_seconds", "hbm_bytes", "mfma_busy", "lds_conflict")]
 
 
 class KfTuning(ctypes.Structure):
@@ -142,6 +150,8 @@ def lib():
         L.kf_classify.restype = i32
         L.kf_diagnose.argtypes = [vp, dbl, dbl, ctypes.POINTER(KfDiagnosis)]
         L.kf_diagnose.restype = i32
+        L.kf_diagnose_counters.argtypes = [vp, ctypes.POINTER(KfCounters), ctypes.POINTER(KfDiagnosis)]
+        L.kf_diagnose_counters.restype = i32
         L.kf_get_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
         L.kf_get_tuning.restype = i32
         L.kf_set_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
@@ -377,6 +387,14 @@ class FusedOp:
     def diagnose(self, kernel_seconds: float, hbm_bytes: float = 0.0) -> dict:
         g = KfDiagnosis()
         _check(lib().kf_diagnose(self._h, kernel_seconds, hbm_bytes or 0.0, ctypes.byref(g)))
+        return g.as_dict()
+
+    def diagnose_counters(self, kernel_seconds: float, hbm_bytes: float = -1.0, mfma_busy: float = -1.0,
+                          lds_conflict: float = -1.0) -> dict:
+        """kf_diagnose_counters: the diagnosis from a launch's counters."""
+        g = KfDiagnosis()
+        c = KfCounters(kernel_seconds, hbm_bytes, mfma_busy, lds_conflict)
+        _check(lib().kf_diagnose_counters(self._h, ctypes.byref(c), ctypes.byref(g)))
         return g.as_dict()
 
     def tuning(self) -> dict:

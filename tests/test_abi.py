@@ -198,7 +198,8 @@ def test_struct_offsets_match_c_compiler(tmp_path):
     if cc is None:
         pytest.skip("no C compiler")
     structs = [("kf_op", kf.KfOp), ("kf_op_spec", kf.KfOpSpec), ("kf_tensor", kf.KfTensor),
-               ("kf_diagnosis", kf.KfDiagnosis), ("kf_tuning", kf.KfTuning), ("kf_tune_result", kf.KfTuneResult)]
+               ("kf_diagnosis", kf.KfDiagnosis), ("kf_tuning", kf.KfTuning), ("kf_tune_result", kf.KfTuneResult),
+               ("kf_counters", kf.KfCounters)]
     lines, want = [], []
     for cname, py in structs:
         for f in py._fields_:
@@ -311,3 +312,15 @@ def test_noalloc_rejects_before_any_device_call():
         assert st == kf.KF_ERR_NO_DEVICE, msg
     else:
         assert st in (kf.KF_ERR_INVALID_ARG, kf.KF_ERR_SHAPE), msg  # the empty tensors are refused
+
+
+def test_classify_sets_latency_hints():
+    """Latency-bound launches carry a hint: too few workgroups -> more
+    parallelism, enough workgroups but far from both roofs -> pipelining."""
+    few = kf.classify(1e9, 1e6, 1e-3, 2516.6, 8000.0, 100, 256)
+    assert few["bound"] == "latency" and few["hints"] == ["parallelism"]
+    slow = kf.classify(1e9, 1e6, 1e-3, 2516.6, 8000.0, 1000, 256)
+    assert slow["bound"] == "latency" and slow["hints"] == ["pipeline"]
+    busy = kf.classify(2e12, 1e9, 1e-3, 2516.6, 8000.0, 1000, 256)
+    assert busy["bound"] == "instruction" and busy["hints"] == []
+    assert busy["mfma_busy"] == -1.0 and busy["traffic_ratio"] == -1.0

@@ -917,3 +917,24 @@ def test_cross_entropy_every_target_column_and_out_of_range(name, kw):
     t["targets"] = np.arange(64, dtype=np.int32) * 16 % N   # lanes of every position across tiles
     _, out = run_gpu(cfg, t)
     check(cfg, t, out)
+
+
+def test_diagnosis_from_counters():
+    """kf_diagnose_counters on counter values of the kind the committed
+    profiles hold: a bf16 GEMM whose matrix cores are busy half the time and
+    whose operand panels are fetched 4.5x is instruction-bound with the
+    overlap and reuse hints; the softmax rows moving their algorithmic bytes
+    are memory-bound with no hint; LDS bank conflicts set the layout hint; a
+    busy fraction above 0.75 drops the overlap hint."""
+    _torch()
+    c2 = kf.FusedOp.from_config(inputs.config("C2"))
+    g = c2.diagnose_counters(115e-6, 303.8e6, 0.51, 0.0)
+    assert g["bound"] == "instruction" and sorted(g["hints"]) == ["overlap", "reuse"]
+    assert g["compute_frac"] == 0.51 and abs(g["traffic_ratio"] - 303.8e6 / 67141632) < 1e-9
+    g = c2.diagnose_counters(115e-6, 70e6, 0.8, 0.12)
+    assert g["bound"] == "instruction" and g["hints"] == ["lds_layout"]
+    f4 = kf.FusedOp.from_config(inputs.config("F4"))
+    g = f4.diagnose_counters(40e-6, 268.6e6)
+    assert g["bound"] == "memory" and g["hints"] == [] and g["mfma_busy"] == -1.0
+    g = f4.diagnose_counters(400e-6, 268.6e6)
+    assert g["bound"] == "latency" and g["hints"] == ["pipeline"]
