@@ -790,7 +790,197 @@ __global__ __launch_bounds__(NT8, 1) void kf_conv3x3_bf16_w8(ConvArgs p, const u
   wait_vmcnt_lgkm0<0>();
 }
 
+// ---------------------------------------------------------------------------
+// The general 3x3 convolution: any batch, cin, cout, H, W (pooling: even H
+// and W).  The shapes outside the tiled kernels' family take this simpler
+// implicit GEMM.  Tile: 2 output rows x 32 columns x 128 output channels per
+// workgroup of 4 waves; wave w owns channels [32 w, 32 w + 32) of the tile
+// and both rows (two 32 x 32 MFMA blocks, so a 2x2 pooling window sits in
+// one lane's accumulators).  k = (ci chunk of 16, tap): per chunk the input
+// patch -- 4 rows x 34 columns x 16 channels, zero outside the image and past
+// cin -- is staged in LDS as [pixel][16 channels] (32 bytes per pixel, so an
+// A fragment is one 16-byte read), loaded into registers one chunk ahead;
+// the B fragments (weights repacked to [tap][cout][cin rounded up to 16],
+// zero-padded) come straight from global memory, where the whole weight set
+// stays in L2.
+namespace {
+
+constexpr int kGenCols = 32, kGenRows = 2, kGenCo = 128;
+constexpr int kGenPatchCols = kGenCols + 2, kGenPatchRows = kGenRows + 2;
+constexpr int kGenPatch = 16 * kGenPatchRows * kGenPatchCols;  // 2176 elements per chunk
+constexpr int kGenLoads = (kGenPatch + 255) / 256;              // 9 per thread
+
+}  // namespace
+
+__host__ __device__ int conv_gen_cin_pad(int cin) { return (cin + 15) / 16 * 16; }
+
+// wp[tap][co][ci] = w[co][ci][kh][kw] for ci < cin, 0 up to the padded cin
+__global__ __launch_bounds__(256) void kf_conv_pack_weights_gen(const uint16_t* __restrict__ w,
+                                                                uint16_t* __restrict__ wp, int cout, int cin,
+                                                                int cin16) {
+  const int64_t pairs = (int64_t)cout * cin16;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < pairs; e += (int64_t)gridDim.x * 256) {
+    const int co = (int)(e / cin16), ci = (int)(e % cin16);
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+      wp[tap * pairs + e] = ci < cin ? w[((int64_t)co * cin + ci) * 9 + tap] : (uint16_t)0;
+  }
+}
+
+template <int CH>
+__global__ __launch_bounds__(256) void kf_conv3x3_bf16_gen(ConvArgs p, const uint16_t* __restrict__ wp) {
+  __shared__ __attribute__((aligned(16))) uint16_t sP[kGenPatch];  // [row][col][16 ci]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int H = (int)p.H, W = (int)p.W, cin = (int)p.cin, cout = (int)p.cout;
+  const int cin16 = conv_gen_cin_pad(cin);
+  const int chunks = cin16 / 16;
+  const int tiles_co = (cout + kGenCo - 1) / kGenCo;
+  const int tiles_w = (W + kGenCols - 1) / kGenCols;
+  const int tiles_h = (H + kGenRows - 1) / kGenRows;
+  int b = blockIdx.x;
+  const int tc = b % tiles_co;
+  b /= tiles_co;
+  const int tw = b % tiles_w;
+  b /= tiles_w;
+  const int th = b % tiles_h;
+  const int n = b / tiles_h;
+  const int oh0 = th * kGenRows, ow0 = tw * kGenCols;
+  const int co0 = tc * kGenCo + wave * 32;
+  const bool wave_live = co0 < cout;  // waves past cout compute nothing (they still meet every barrier)
+  const uint16_t* x = reinterpret_cast<const uint16_t*>(p.x) + (int64_t)n * cin * H * W;
+
+  // this thread's patch elements: e = tid + 256 j -> (ci, row, col), ci fastest
+  uint16_t pre[kGenLoads];
+  auto load_chunk = [&](int c) {
+#pragma unroll
+    for (int j = 0; j < kGenLoads; ++j) {
+      const int e = tid + 256 * j;
+      const int ci = e & 15, pix = e >> 4;
+      const int row = pix / kGenPatchCols, col = pix % kGenPatchCols;
+      const int ih = oh0 - 1 + row, iw = ow0 - 1 + col, cc = c * 16 + ci;
+      pre[j] = (e < kGenPatch && cc < cin && ih >= 0 && ih < H && iw >= 0 && iw < W)
+                   ? x[((int64_t)cc * H + ih) * W + iw]
+                   : (uint16_t)0;
+    }
+  };
+  auto store_chunk = [&]() {
+#pragma unroll
+    for (int j = 0; j < kGenLoads; ++j) {
+      const int e = tid + 256 * j;
+      if (e < kGenPatch) sP[e] = pre[j];
+    }
+  };
+  // B fragments of a chunk: lane (co0 + lane % 32, channels 8 (lane / 32) .. + 7)
+  const int r32 = lane & 31, kg = lane >> 5;
+  const int co_l = co0 + r32;
+  const int64_t taps_stride = (int64_t)cout * cin16;
+  u32x4 fb[9];
+  auto load_b = [&](int c) {
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+      fb[tap] = co_l < cout ? *reinterpret_cast<const u32x4*>(wp + tap * taps_stride + (int64_t)co_l * cin16 + c * 16 +
+                                                             kg * 8)
+                            : u32x4{0u, 0u, 0u, 0u};
+  };
+
+  f32x16 acc[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[r][i] = 0.0f;
+
+  load_chunk(0);
+  store_chunk();
+  __syncthreads();
+  for (int c = 0; c < chunks; ++c) {
+    if (wave_live) load_b(c);
+    if (c + 1 < chunks) load_chunk(c + 1);
+    if (wave_live) {
+#pragma unroll
+      for (int tap = 0; tap < 9; ++tap) {
+        const int kh = tap / 3, kw = tap % 3;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int pix = (r + kh) * kGenPatchCols + r32 + kw;
+          const u32x4 a = *reinterpret_cast<const u32x4*>(sP + pix * 16 + kg * 8);
+          acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                           __builtin_bit_cast(bf16x8, fb[tap]), acc[r], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+    if (c + 1 < chunks) {
+      store_chunk();
+      __syncthreads();
+    }
+  }
+  if (!wave_live) return;
+
+  // epilogue: acc[r][i] = output row oh0 + r, column ow0 + (i / 4) * 8 +
+  // (lane / 32) * 4 + i % 4, channel co_l
+  if (co_l >= cout) return;
+  const int nops = p.prog.n;
+  const OpTable ops = load_op_table(p.prog, lane);
+  const int pidx = p.pool ? p.pool_index : nops;
+  const float bias = p.bias ? p.bias[co_l] : 0.0f;
+  uint16_t* out = reinterpret_cast<uint16_t*>(p.out);
+  float v[32];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    v[i] = acc[0][i];
+    v[16 + i] = acc[1][i];
+  }
+  constexpr bool kPoolFirst = chain_pools_first(CH);
+  if constexpr (!kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias, v);
+  if (p.pool) {
+    const int Ho = H / 2, Wo = W / 2;
+    const int ph = oh0 / 2;
+    float pv[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int i = q * 4 + h2 * 2;
+        pv[q * 2 + h2] = fmaxf(fmaxf(v[i], v[i + 1]), fmaxf(v[16 + i], v[16 + i + 1]));
+      }
+    if constexpr (kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias, pv);
+    conv_apply_phase<CH>(ops, pidx + 1, nops, bias, pv);
+    if (ph < Ho) {
+      uint16_t* orow = out + (((int64_t)n * cout + co_l) * Ho + ph) * Wo;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int pw = (ow0 + (q / 2) * 8 + kg * 4) / 2 + (q & 1);
+        if (pw < Wo) orow[pw] = (uint16_t)f32_to_bf16_rne(pv[q]);
+      }
+    }
+  } else {
+    conv_apply_phase<CH>(ops, pidx, nops, bias, v);  // (no pool: pidx == nops, nothing left)
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int oh = oh0 + r;
+      if (oh >= H) continue;
+      uint16_t* orow = out + (((int64_t)n * cout + co_l) * H + oh) * W;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int ow = ow0 + (i / 4) * 8 + kg * 4 + (i & 3);
+        if (ow < W) orow[ow] = (uint16_t)f32_to_bf16_rne(v[r * 16 + i]);
+      }
+    }
+  }
+}
+
 hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStream_t stream) {
+  if (args.variant == 2) {
+    const int cin16 = conv_gen_cin_pad((int)args.cin);
+    const int64_t pairs = args.cout * cin16;
+    const unsigned blocks = (unsigned)((pairs + 255) / 256 < 1024 ? (pairs + 255) / 256 : 1024);
+    hipLaunchKernelGGL(kf_conv_pack_weights_gen, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, stream,
+                       reinterpret_cast<const uint16_t*>(args.w), reinterpret_cast<uint16_t*>(packed_weights),
+                       (int)args.cout, (int)args.cin, cin16);
+    return hipGetLastError();
+  }
   const int64_t pairs = args.cout * args.cin;
   const unsigned blocks = (unsigned)((pairs + 255) / 256 < 1024 ? (pairs + 255) / 256 : 1024);
   hipLaunchKernelGGL(kf_conv_pack_weights, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, stream,
@@ -800,9 +990,18 @@ hipError_t launch_conv_pack(const ConvArgs& args, void* packed_weights, hipStrea
 }
 
 hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, int chain, hipStream_t stream) {
+  const uint16_t* wp = reinterpret_cast<const uint16_t*>(packed_weights);
+  if (args.variant == 2) {
+    const int64_t tiles = conv_gen_tiles(args.batch, args.H, args.W, args.cout);
+    if (tiles <= 0) return hipSuccess;
+    if (chain == 7)
+      hipLaunchKernelGGL(kf_conv3x3_bf16_gen<7>, dim3((unsigned)tiles), dim3(256), 0, stream, args, wp);
+    else
+      hipLaunchKernelGGL(kf_conv3x3_bf16_gen<0>, dim3((unsigned)tiles), dim3(256), 0, stream, args, wp);
+    return hipGetLastError();
+  }
   if (args.tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)(args.grid < args.tiles ? args.grid : args.tiles));
-  const uint16_t* wp = reinterpret_cast<const uint16_t*>(packed_weights);
   if (args.variant == 1) {
     if (chain == 7)
       hipLaunchKernelGGL(kf_conv3x3_bf16_w8<7>, grid, dim3(NT8), 0, stream, args, wp);
@@ -814,6 +1013,10 @@ hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, in
     hipLaunchKernelGGL(kf_conv3x3_bf16_256x128<0>, grid, dim3(NT), 0, stream, args, wp);
   }
   return hipGetLastError();
+}
+
+int64_t conv_gen_tiles(int64_t batch, int64_t H, int64_t W, int64_t cout) {
+  return batch * ((H + kGenRows - 1) / kGenRows) * ((W + kGenCols - 1) / kGenCols) * ((cout + kGenCo - 1) / kGenCo);
 }
 
 int conv_bf16_cin() { return CIN; }

@@ -88,6 +88,7 @@ struct kf_desc {
   int gn_group;
   int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / KF_OP_ROW_CROSS_ENTROPY / 0
   int chain = 0;  // compile-time epilogue chain matching the op list (0: interpreted)
+  bool conv_special = false;  // CONV2D_3X3 in the tiled kernels' shape family
   SlotList inputs;
   Slot output;
   int device;
@@ -342,22 +343,28 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     if (s->out_dtype != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 writes bf16 outputs only");
     if (s->batch < 0 || s->cin < 1 || s->height < 1 || s->width < 1 || s->cout < 1)
       return fail(KF_ERR_SHAPE, "CONV2D_3X3 needs batch >= 0 and positive cin, height, width, cout");
-    if (s->cin != kf::conv_bf16_cin() || s->width != kf::conv_bf16_width() || s->cout != kf::conv_bf16_cout())
-      return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 kernel is built for cin=%d, width=%d, cout=%d",
-                  kf::conv_bf16_cin(), kf::conv_bf16_width(), kf::conv_bf16_cout());
-    if (s->height % 2) return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 needs an even height (tiles are row pairs)");
-    if ((int64_t)std::max(s->cin, s->cout) * s->height * s->width * 2 >= (int64_t(1) << 31))
+    if (n_pool && (s->height % 2 || s->width % 2))
+      return fail(KF_ERR_UNSUPPORTED, "MAXPOOL2X2 needs an even height and width");
+    if ((int64_t)std::max(s->cin, s->cout) * s->height * s->width * 2 >= (int64_t(1) << 31) || s->cin > (1 << 20) ||
+        s->cout > (1 << 20))
       return fail(KF_ERR_UNSUPPORTED, "one input or output image must be smaller than 2 GiB");
-    if ((int64_t)s->batch * (s->height / 2) > INT32_MAX)
+    // the tiled kernels are built for the 64 -> 128 channel, 128-column family
+    // with even height; every other shape takes the general kernel
+    d->conv_special = s->cin == kf::conv_bf16_cin() && s->width == kf::conv_bf16_width() &&
+                      s->cout == kf::conv_bf16_cout() && s->height % 2 == 0;
+    if (d->conv_special && (int64_t)s->batch * (s->height / 2) > INT32_MAX)
       return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 supports at most 2^31 - 1 row-pair tiles");
+    if (!d->conv_special && kf::conv_gen_tiles(s->batch, s->height, s->width, s->cout) >= (int64_t(1) << 24))
+      return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 (general shapes) supports fewer than 2^24 tiles of 2 x 32 x 128");
     for (int i = 0; i < s->n_ops; ++i) {
       const int k = s->ops[i].kind;
       if (!(k == KF_OP_BIAS || k == KF_OP_MAXPOOL2X2 || is_elementwise_kind(k)))
         return fail(KF_ERR_UNSUPPORTED, "op %d: CONV2D_3X3 supports BIAS, element-wise ops and MAXPOOL2X2", i);
     }
     d->variant = kVarConvBf16;
-    d->kernel_name = "kf_conv3x3_bf16_256x128";
-    d->tuning.variant = 1;  // the 8-wave tile: faster at the C4 shape (the tuner may pick either)
+    d->kernel_name = d->conv_special ? "kf_conv3x3_bf16_256x128" : "kf_conv3x3_bf16_gen";
+    // the 8-wave tile is the faster at the C4 shape (the tuner may pick any)
+    d->tuning.variant = d->conv_special ? 1 : 2;
     d->inputs.push_back(Slot{dt, 4, {s->batch, s->cin, s->height, s->width}, "A", false});
     d->inputs.push_back(Slot{dt, 4, {s->cout, s->cin, 3, 3}, "B", false});
     for (int i = 0; i < s->n_ops; ++i)
@@ -492,7 +499,8 @@ Work plan_work(const kf_desc* d) {
     case kVarConvBf16:
       w.flops = 2.0 * s.batch * s.height * s.width * s.cout * s.cin * 9;
       w.peak_tflops = 2516.6;
-      w.workgroups = std::min<int64_t>(d->num_cu, s.batch * (s.height / 2));
+      w.workgroups = d->tuning.variant == 2 ? kf::conv_gen_tiles(s.batch, s.height, s.width, s.cout)
+                                            : std::min<int64_t>(d->num_cu, s.batch * (s.height / 2));
       break;
     case kVarConv3d: {
       w.flops = 2.0 * s.batch * (s.depth - 2) * (s.height - 2) * (s.width - 2) * s.cout * s.cin * 27;
@@ -558,7 +566,7 @@ kf_status current_device(int* dev_out, int* cus_out) {
 // logsumexp.
 size_t plan_workspace_bytes(const kf_desc* d) {
   const kf_op_spec& s = d->spec;
-  if (d->variant == kVarConvBf16) return (size_t)9 * s.cout * s.cin * 2;
+  if (d->variant == kVarConvBf16) return (size_t)9 * s.cout * kf::conv_gen_cin_pad((int)s.cin) * 2;
   if (d->variant == kVarConv3d) return kf::conv3d_packed_bytes();
   if (d->row_kind && d->variant != kVarRowwise) {
     // per-(row, tile) (max, sum) pairs; cross-entropy adds h[m][t_m] per row
@@ -660,9 +668,10 @@ kf_status kf_set_tuning(kf_desc* d, const kf_tuning* t) {
   if (t->raster_group < 1 || t->raster_group > 64) return fail(KF_ERR_INVALID_ARG, "raster_group must be in [1, 64]");
   if (t->xcd_remap != 0 && t->xcd_remap != 1) return fail(KF_ERR_INVALID_ARG, "xcd_remap must be 0 or 1");
   if (t->wg_per_cu != 1 && t->wg_per_cu != 2) return fail(KF_ERR_INVALID_ARG, "wg_per_cu must be 1 or 2");
-  const int max_variant = d->variant == kVarConvBf16 ? 1 : 0;
-  if (t->variant < 0 || t->variant > max_variant)
-    return fail(KF_ERR_INVALID_ARG, "variant must be in [0, %d] for this plan", max_variant);
+  const int min_variant = d->variant == kVarConvBf16 && !d->conv_special ? 2 : 0;
+  const int max_variant = d->variant == kVarConvBf16 ? 2 : 0;
+  if (t->variant < min_variant || t->variant > max_variant)
+    return fail(KF_ERR_INVALID_ARG, "variant must be in [%d, %d] for this plan", min_variant, max_variant);
   d->tuning = *t;
   return ok();
 }
@@ -679,7 +688,7 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
   } else if (d->variant == kVarConv3d) {
     for (int remap = 1; remap >= 0; --remap)
       for (int wg : {2, 1}) cand.push_back(kf_tuning{cur.raster_group, remap, wg, 0});
-  } else if (d->variant == kVarConvBf16) {
+  } else if (d->variant == kVarConvBf16 && d->conv_special) {
     for (int v : {0, 1}) cand.push_back(kf_tuning{cur.raster_group, cur.xcd_remap, cur.wg_per_cu, v});
   } else {
     cand.push_back(cur);

@@ -122,7 +122,7 @@ struct ConvArgs {
   int32_t pool_index;     // position of the pool op in prog
   int32_t tiles;          // number of output tiles (batch x H/2 row pairs)
   int32_t grid;           // workgroups of the persistent launch (at most tiles)
-  int32_t variant;        // 0: 4 waves (128 x 64 wave blocks), 1: 8 waves (64 x 64)
+  int32_t variant;        // 0: 4 waves (128 x 64 wave blocks), 1: 8 waves (64 x 64), 2: general shapes
 };
 
 // Arguments of the implicit-GEMM 3x3x3 convolution kernel.

@@ -65,6 +65,11 @@ hipError_t launch_conv_bf16(const ConvArgs& args, const void* packed_weights, in
 int conv_bf16_cin();
 int conv_bf16_width();
 int conv_bf16_cout();
+// The general conv (ConvArgs.variant 2): any shape; its packed weights hold
+// 9 * cout * conv_gen_cin_pad(cin) bf16 and it launches conv_gen_tiles(...)
+// workgroups.
+__host__ __device__ int conv_gen_cin_pad(int cin);
+int64_t conv_gen_tiles(int64_t batch, int64_t H, int64_t W, int64_t cout);
 
 // 3x3x3 conv (bf16, channels-last input, OIDHW weight) + fused bias,
 // element-wise ops, channel softmax and two 3-D max-pools:

@@ -75,11 +75,18 @@ def _spec(name, **kw):
 
 
 def test_conv_validation():
-    for kw, status in [(dict(cin=32), kf.KF_ERR_UNSUPPORTED), (dict(H=7), kf.KF_ERR_UNSUPPORTED),
+    """Any conv shape plans (the tiled kernels' family or the general
+    kernel); a 2x2 pool needs an even height and width; the op and dtype
+    rules hold for both."""
+    ok = kf.KF_ERR_NO_DEVICE if not _gpu_present() else kf.KF_OK
+    for kw, status in [(dict(cin=32), ok), (dict(cin=3, cout=40, W=50), ok), (dict(H=7, ops=[("bias",)]), ok),
+                       (dict(H=7), kf.KF_ERR_UNSUPPORTED), (dict(W=9), kf.KF_ERR_UNSUPPORTED),
                        (dict(ops=[("groupnorm", 2, 1e-5)]), kf.KF_ERR_UNSUPPORTED),
                        (dict(out_dtype="f32"), kf.KF_ERR_UNSUPPORTED), (dict(in_dtype="f32"), kf.KF_ERR_UNSUPPORTED)]:
-        st, _ = _create(_spec("C4", **kw))
+        st, h = _create(_spec("C4", **kw))
         assert st == status, (kw, st, kf.last_error())
+        if h.value:
+            kf.lib().kf_destroy(h)
 
 
 def test_create_null_arguments():

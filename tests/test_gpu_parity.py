@@ -412,7 +412,7 @@ def test_rowwise_full_config_sampled_rows(name):
     (3, 6, [("bias",), ("relu",)]),
     (1, 4, [("bias",), ("gelu_tanh",), ("maxpool2x2",), ("scale", -2.0), ("swish",)]),
 ])
-@pytest.mark.parametrize("variant", [0, 1])
+@pytest.mark.parametrize("variant", [0, 1, 2])
 def test_c4_small(batch, H, ops, variant):
     _torch()
     cfg = inputs.config("C4", batch=batch, H=H, ops=ops)
@@ -486,10 +486,10 @@ def test_c4_tile_ranges(batch, H, ops, variant):
     print(f"C4 batch={batch} H={H} err {err:.3e}")
 
 
-@pytest.mark.parametrize("variant", [0, 1])
+@pytest.mark.parametrize("variant", [0, 1, 2])
 def test_c4_integer_bit_exact_tile_ranges(variant):
     """The integer test of the contraction with several tiles per workgroup,
-    on the 4-wave and the 8-wave tile."""
+    on the 4-wave and the 8-wave tile and on the general kernel."""
     torch = _torch()
     batch, H = 3, 200
     cfg = inputs.config("C4", batch=batch, H=H, ops=[])
@@ -502,6 +502,56 @@ def test_c4_integer_bit_exact_tile_ranges(variant):
     for n in range(batch):
         ref = oracle.conv2d_3x3(x[n:n + 1].astype(np.float64), w.astype(np.float64))
         assert np.array_equal(got_bits[n:n + 1], inputs.f32_to_bf16_bits(ref.astype(np.float32))), f"image {n}"
+
+# ------------------------------------------------ conv, general shapes
+
+@pytest.mark.parametrize("batch,cin,H,W,cout,ops", [
+    (2, 3, 9, 50, 40, [("bias",), ("relu",)]),                       # odd height, ragged width, few channels
+    (1, 32, 8, 64, 96, [("bias",), ("relu",), ("maxpool2x2",)]),      # cout not a multiple of 128
+    (2, 16, 6, 34, 128, [("bias",), ("gelu_tanh",), ("maxpool2x2",)]),  # width not a multiple of 32
+    (1, 64, 5, 33, 160, [("bias",)]),                                 # two channel tiles, the last partial
+    (1, 130, 4, 20, 32, [("bias",), ("relu",), ("maxpool2x2",), ("scale", 0.5)]),  # cin not a multiple of 16
+    (3, 1, 1, 1, 1, []),                                              # one pixel, one channel
+])
+def test_conv_general_shapes(batch, cin, H, W, cout, ops):
+    """Shapes outside the tiled kernels' family run the general kernel."""
+    _torch()
+    cfg = inputs.config("C4", batch=batch, cin=cin, H=H, W=W, cout=cout, ops=ops)
+    t = inputs.generate(cfg, seed=batch + cin + H + W + cout)
+    op, out = run_gpu(cfg, t)
+    assert op.kernel_name() == "kf_conv3x3_bf16_gen"
+    err = check(cfg, t, out)
+    print(f"conv general {batch}x{cin}x{H}x{W} -> {cout} err {err:.3e}")
+
+
+def test_conv_general_integer_bit_exact():
+    """Integer inputs and weights: every partial sum is exact, so the general
+    kernel's output is the exact convolution rounded once to bf16."""
+    torch = _torch()
+    batch, cin, H, W, cout = 2, 48, 6, 40, 72
+    cfg = inputs.config("C4", batch=batch, cin=cin, H=H, W=W, cout=cout, ops=[])
+    rng = np.random.default_rng(44)
+    x = rng.integers(-4, 5, size=(batch, cin, H, W)).astype(np.float32)
+    w = rng.integers(-2, 3, size=(cout, cin, 3, 3)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
+    _, out = run_gpu(cfg, t)
+    ref = oracle.conv2d_3x3(x.astype(np.float64), w.astype(np.float64))
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, inputs.f32_to_bf16_bits(ref.astype(np.float32)))
+
+
+def test_conv_general_unfused_and_tuning():
+    """The unfused chain of a general-shape conv, and the tuning rule: a
+    general-shape plan runs only the general kernel (variant 2)."""
+    _torch()
+    cfg = inputs.config("C4", batch=2, cin=24, H=10, W=30, cout=64)
+    t = inputs.generate(cfg, seed=12)
+    op, out = run_gpu(cfg, t, unfused=True)
+    check(cfg, t, out, unfused=True)
+    assert op.tuning()["variant"] == 2
+    with pytest.raises(kf.KFError):
+        op.set_tuning(4, 1, 2, 1)
+
 
 # ------------------------------------------- Conv3d, channel softmax, pools (F2)
 
