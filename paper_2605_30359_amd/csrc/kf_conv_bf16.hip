@@ -793,11 +793,12 @@ __global__ __launch_bounds__(NT8, 1) void kf_conv3x3_bf16_w8(ConvArgs p, const u
 // ---------------------------------------------------------------------------
 // The general 3x3 convolution: any batch, cin, cout, H, W (pooling: even H
 // and W).  The shapes outside the tiled kernels' family take this simpler
-// implicit GEMM.  Tile: 2 output rows x 32 columns x 128 output channels per
+// implicit GEMM.  Tile: 4 output rows x 32 columns x 128 output channels per
 // workgroup of 4 waves; wave w owns channels [32 w, 32 w + 32) of the tile
-// and both rows (two 32 x 32 MFMA blocks, so a 2x2 pooling window sits in
-// one lane's accumulators).  k = (ci chunk of 16, tap): per chunk the input
-// patch -- 4 rows x 34 columns x 16 channels, zero outside the image and past
+// and all four rows (four 32 x 32 MFMA blocks, so each weight fragment
+// serves four, and a 2x2 pooling window sits in one lane's accumulators).
+// k = (ci chunk of 16, tap): per chunk the input
+// patch -- 6 rows x 34 columns x 16 channels, zero outside the image and past
 // cin -- is staged in LDS as [pixel][16 channels] (32 bytes per pixel, so an
 // A fragment is one 16-byte read), loaded into registers one chunk ahead;
 // the B fragments (weights repacked to [tap][cout][cin rounded up to 16],
@@ -805,10 +806,10 @@ __global__ __launch_bounds__(NT8, 1) void kf_conv3x3_bf16_w8(ConvArgs p, const u
 // stays in L2.
 namespace {
 
-constexpr int kGenCols = 32, kGenRows = 2, kGenCo = 128;
+constexpr int kGenCols = 32, kGenRows = 4, kGenCo = 128;
 constexpr int kGenPatchCols = kGenCols + 2, kGenPatchRows = kGenRows + 2;
-constexpr int kGenPatch = 16 * kGenPatchRows * kGenPatchCols;  // 2176 elements per chunk
-constexpr int kGenLoads = (kGenPatch + 255) / 256;              // 9 per thread
+constexpr int kGenPatch = 16 * kGenPatchRows * kGenPatchCols;  // 3264 elements per chunk
+constexpr int kGenLoads = (kGenPatch + 255) / 256;              // 13 per thread
 
 }  // namespace
 
@@ -885,9 +886,9 @@ __global__ __launch_bounds__(256) void kf_conv3x3_bf16_gen(ConvArgs p, const uin
                             : u32x4{0u, 0u, 0u, 0u};
   };
 
-  f32x16 acc[2];
+  f32x16 acc[kGenRows];
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
+  for (int r = 0; r < kGenRows; ++r)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[r][i] = 0.0f;
 
@@ -902,7 +903,7 @@ __global__ __launch_bounds__(256) void kf_conv3x3_bf16_gen(ConvArgs p, const uin
       for (int tap = 0; tap < 9; ++tap) {
         const int kh = tap / 3, kw = tap % 3;
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
+        for (int r = 0; r < kGenRows; ++r) {
           const int pix = (r + kh) * kGenPatchCols + r32 + kw;
           const u32x4 a = *reinterpret_cast<const u32x4*>(sP + pix * 16 + kg * 8);
           acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
@@ -926,46 +927,49 @@ __global__ __launch_bounds__(256) void kf_conv3x3_bf16_gen(ConvArgs p, const uin
   const int pidx = p.pool ? p.pool_index : nops;
   const float bias = p.bias ? p.bias[co_l] : 0.0f;
   uint16_t* out = reinterpret_cast<uint16_t*>(p.out);
-  float v[32];
+  // rows in pairs (0, 1) and (2, 3): a pair is one pooled row
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    v[i] = acc[0][i];
-    v[16 + i] = acc[1][i];
-  }
-  constexpr bool kPoolFirst = chain_pools_first(CH);
-  if constexpr (!kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias, v);
-  if (p.pool) {
-    const int Ho = H / 2, Wo = W / 2;
-    const int ph = oh0 / 2;
-    float pv[8];
+  for (int rp = 0; rp < kGenRows / 2; ++rp) {
+    float v[32];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const int i = q * 4 + h2 * 2;
-        pv[q * 2 + h2] = fmaxf(fmaxf(v[i], v[i + 1]), fmaxf(v[16 + i], v[16 + i + 1]));
-      }
-    if constexpr (kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias, pv);
-    conv_apply_phase<CH>(ops, pidx + 1, nops, bias, pv);
-    if (ph < Ho) {
-      uint16_t* orow = out + (((int64_t)n * cout + co_l) * Ho + ph) * Wo;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int pw = (ow0 + (q / 2) * 8 + kg * 4) / 2 + (q & 1);
-        if (pw < Wo) orow[pw] = (uint16_t)f32_to_bf16_rne(pv[q]);
-      }
+    for (int i = 0; i < 16; ++i) {
+      v[i] = acc[2 * rp][i];
+      v[16 + i] = acc[2 * rp + 1][i];
     }
-  } else {
-    conv_apply_phase<CH>(ops, pidx, nops, bias, v);  // (no pool: pidx == nops, nothing left)
+    constexpr bool kPoolFirst = chain_pools_first(CH);
+    if constexpr (!kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias, v);
+    if (p.pool) {
+      const int Ho = H / 2, Wo = W / 2;
+      const int ph = oh0 / 2 + rp;
+      float pv[8];
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int oh = oh0 + r;
-      if (oh >= H) continue;
-      uint16_t* orow = out + (((int64_t)n * cout + co_l) * H + oh) * W;
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int ow = ow0 + (i / 4) * 8 + kg * 4 + (i & 3);
-        if (ow < W) orow[ow] = (uint16_t)f32_to_bf16_rne(v[r * 16 + i]);
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int i = q * 4 + h2 * 2;
+          pv[q * 2 + h2] = fmaxf(fmaxf(v[i], v[i + 1]), fmaxf(v[16 + i], v[16 + i + 1]));
+        }
+      if constexpr (kPoolFirst) conv_apply_phase<CH>(ops, 0, pidx, bias, pv);
+      conv_apply_phase<CH>(ops, pidx + 1, nops, bias, pv);
+      if (ph < Ho) {
+        uint16_t* orow = out + (((int64_t)n * cout + co_l) * Ho + ph) * Wo;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int pw = (ow0 + (q / 2) * 8 + kg * 4) / 2 + (q & 1);
+          if (pw < Wo) orow[pw] = (uint16_t)f32_to_bf16_rne(pv[q]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int oh = oh0 + 2 * rp + r;
+        if (oh >= H) continue;
+        uint16_t* orow = out + (((int64_t)n * cout + co_l) * H + oh) * W;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int ow = ow0 + (i / 4) * 8 + kg * 4 + (i & 3);
+          if (ow < W) orow[ow] = (uint16_t)f32_to_bf16_rne(v[r * 16 + i]);
+        }
       }
     }
   }
