@@ -372,7 +372,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="C5", help="headline workload: C1..C5, F1..F4 (default C5)")
+    ap.add_argument("--workload", default="C5", help="headline workload: C1..C5, F1..F6 (default C5)")
     ap.add_argument("--also", default="C3,C4",
                     help="comma-separated workloads timed after the headline, each reported under 'also' "
                          "(default C3,C4; empty for none)")

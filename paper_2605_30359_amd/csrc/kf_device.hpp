@@ -191,7 +191,7 @@ __device__ __forceinline__ void apply_elementwise_array(int kind, float p0, floa
   }
 }
 
-__device__ __forceinline__ bool is_elementwise(int kind) {
+__host__ __device__ __forceinline__ bool is_elementwise(int kind) {
   return kind == KF_OP_RELU || kind == KF_OP_GELU_TANH || kind == KF_OP_GELU_ERF ||
          kind == KF_OP_SWISH || kind == KF_OP_SIGMOID || kind == KF_OP_TANH ||
          kind == KF_OP_HARDTANH || kind == KF_OP_SCALE;
@@ -248,5 +248,33 @@ __device__ __forceinline__ float acc_read(float a) {
 // ---------------------------------------------------------- cross-lane ops
 
 __device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
+
+// Sum (or maximum) over aligned groups of `width` lanes (a power of two,
+// 1..64); every lane of a group gets the same bits.  Steps within 16 lanes
+// use DPP lane moves (quad permutations [1,0,3,2] and [2,3,0,1], then the
+// mirror within 8 and within 16 lanes, which pair the same partial results
+// as exchanges with lane ^ 4 and lane ^ 8), lane ^ 16 a swizzle, and the two
+// halves of the wave are combined from lanes 0 and 32 by readlane; the sums
+// are grouped as in an xor butterfly over 1, 2, ..., width / 2.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+template <bool IS_MAX>
+__device__ __forceinline__ float lane_group_reduce(float x, int width) {
+  auto op = [](float a, float b) { return IS_MAX ? fmaxf(a, b) : a + b; };
+  if (width >= 2) x = op(x, dpp_mov<0xB1>(x));   // quad_perm [1,0,3,2]
+  if (width >= 4) x = op(x, dpp_mov<0x4E>(x));   // quad_perm [2,3,0,1]
+  if (width >= 8) x = op(x, dpp_mov<0x141>(x));  // row_half_mirror
+  if (width >= 16) x = op(x, dpp_mov<0x140>(x)); // row_mirror
+  if (width >= 32)                               // lane ^ 16 within 32 lanes
+    x = op(x, __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x1F | (0x10 << 10))));
+  if (width >= 64) {
+    const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
+    const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+    x = op(lo, hi);
+  }
+  return x;
+}
 
 }  // namespace kf

@@ -276,8 +276,11 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     if (dt != KF_F32 && dt != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "ROWWISE supports fp32 and bf16 inputs");
     if (s->M < 0 || s->N < 1) return fail(KF_ERR_SHAPE, "ROWWISE needs M >= 0, N >= 1");
     if (s->M > INT32_MAX) return fail(KF_ERR_UNSUPPORTED, "ROWWISE supports M < 2^31");
-    if (s->N > kf::rowwise_max_cols() || s->N % 8)
-      return fail(KF_ERR_UNSUPPORTED, "ROWWISE needs N %% 8 == 0 and N <= %d", kf::rowwise_max_cols());
+    if (s->N % 8) return fail(KF_ERR_UNSUPPORTED, "ROWWISE needs N %% 8 == 0");
+    if (kf::row_reduce_streams(d->prog) ? s->N > INT32_MAX : s->N > kf::rowwise_max_cols())
+      return fail(KF_ERR_UNSUPPORTED,
+                  "ROWWISE needs N <= %d (N < 2^31 for a row logsumexp / cross-entropy after element-wise ops)",
+                  kf::rowwise_max_cols());
     if (has_gn) {
       const kf_op& g = s->ops[d->red_index];
       if (s->N % g.groups || (s->N / g.groups) % 8)

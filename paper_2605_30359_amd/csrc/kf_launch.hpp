@@ -39,6 +39,10 @@ int gemm_mfma_tile_n();
 // N <= rowwise_max_cols(); `chain` as for the GEMM (0: interpreted).
 hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream);
 int rowwise_max_cols();
+// True for op lists that end with a row logsumexp or cross-entropy after
+// element-wise ops and a bias only: launch_rowwise streams those rows, any
+// N (a multiple of 8).
+bool row_reduce_streams(const EpiProgram& prog);
 
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);

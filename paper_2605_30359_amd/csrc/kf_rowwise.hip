@@ -37,11 +37,7 @@ typedef float Chunk[8];
 // Row-wide max or sum of one value per thread; every thread gets the result.
 template <bool IS_MAX>
 __device__ __forceinline__ float row_reduce(float v, float* red) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float y = shfl_xor(v, o);
-    v = IS_MAX ? fmaxf(v, y) : v + y;
-  }
+  v = lane_group_reduce<IS_MAX>(v, 64);
   __syncthreads();  // the previous reduction's readers are done with red
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
@@ -51,9 +47,12 @@ __device__ __forceinline__ float row_reduce(float v, float* red) {
   return r;
 }
 
+// NT: a streaming (nontemporal) load, for data read once
+template <bool NT = false>
 __device__ __forceinline__ void load_chunk(const void* base, bool bf16, int64_t off, Chunk& x) {
   if (bf16) {
-    const u32x4 w = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(base) + off);
+    const u32x4* q = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(base) + off);
+    const u32x4 w = NT ? __builtin_nontemporal_load(q) : *q;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       x[2 * e] = bf16_lo(w[e]);
@@ -135,9 +134,8 @@ __global__ __launch_bounds__(RT) void kf_rowwise(RowArgs p) {
 #pragma unroll
           for (int j = 0; j < S; ++j) q[j] = s;
         } else if ((L & (L - 1)) == 0 && L <= 64) {
-          for (int d = 1; d < L; d <<= 1)
 #pragma unroll
-            for (int j = 0; j < S; ++j) q[j] += shfl_xor(q[j], d);
+          for (int j = 0; j < S; ++j) q[j] = lane_group_reduce<false>(q[j], L);
         } else {
 #pragma unroll
           for (int j = 0; j < S; ++j) {
@@ -296,27 +294,34 @@ __global__ __launch_bounds__(RT) void kf_rowwise(RowArgs p) {
 // (group widths 8..512 columns), with element-wise ops, a bias and a
 // residual add around the GroupNorm but no whole-row reduction.  The groups
 // are independent, so the work is cut into column panels instead of rows:
-// each wave takes one group g for its whole life and walks rows, P = 64 / L
-// rows per step (lane = row-in-step * L + chunk-in-group).  gamma and beta
-// (and the bias) of the wave's 8 columns per lane are loaded once into
-// registers -- a row kernel re-reads them for every row, 64 KiB per row at
-// 8192 columns -- and the group statistics are sums over L lanes by xor
-// exchanges (no LDS, no barrier).  Each lane keeps kPanelUnroll steps of A
-// (and residual) chunks in flight.
-constexpr int kPanelUnroll = 4;
-
+// a wave owns one 512-column panel of P = 64 / L groups (lane = group-in-
+// panel * L + chunk-in-group) for its whole life and walks rows, one row per
+// step, and the four waves of a workgroup own four adjacent panels, so each
+// step of a workgroup reads 2048 contiguous columns of a row.  gamma and
+// beta (and the bias) of a lane's 8 columns are loaded once into registers
+// -- a row kernel re-reads them for every row, 64 KiB per row at 8192
+// columns -- and the group statistics are sums over L lanes by xor
+// exchanges (no LDS, no barrier).  One row per step: the kernel needs few
+// registers, so a CU holds eight waves per SIMD, and more waves with a row
+// each kept more bytes in flight than fewer waves with several rows each
+// (four rows per step ran F3 in 74 us, two in 68, one in 64; one row with
+// the next one requested ahead, 68).
 template <int CH>
 __global__ __launch_bounds__(RT) void kf_rowwise_gn_panel(RowArgs p) {
   const int lane = threadIdx.x & 63;
   const int L = p.gn_group >> 3;  // chunks per group: a power of two, 1..64
-  const int P = 64 / L;           // rows per step
+  const int P = 64 / L;           // groups per panel
   const int groups = (int)(p.N / p.gn_group);
-  const int g = blockIdx.x % groups;
-  const int waves = (int)(gridDim.x / groups) * (RT / 64);
-  const int wave = (int)(blockIdx.x / groups) * (RT / 64) + (threadIdx.x >> 6);
+  const int panels = (groups + P - 1) / P;
+  const int panel_sets = (panels + RT / 64 - 1) / (RT / 64);
+  const int panel = (int)(blockIdx.x % panel_sets) * (RT / 64) + (threadIdx.x >> 6);
+  if (panel >= panels) return;  // no barrier below
+  const int64_t row_stride = gridDim.x / panel_sets;
+  const int64_t row0 = blockIdx.x / panel_sets;
   const int q = lane & (L - 1);
-  const int pr = lane / L;
-  const int64_t col = (int64_t)g * p.gn_group + q * 8;
+  const int grp = panel * P + lane / L;
+  const bool live = grp < groups;
+  const int64_t col = (int64_t)(live ? grp : 0) * p.gn_group + q * 8;
   const int nops = p.prog.n;
   const OpTable ops = load_op_table(p.prog, lane);
   const float inv_n = 1.0f / (float)p.gn_group;
@@ -346,52 +351,31 @@ __global__ __launch_bounds__(RT) void kf_rowwise_gn_panel(RowArgs p) {
   }
 
   // sum over the L lanes of this lane's group (every lane gets the same bits)
-  auto group_sum = [&](float x) {
-    for (int d = 1; d < L; d <<= 1) x += shfl_xor(x, d);
-    return x;
-  };
+  auto group_sum = [&](float x) { return lane_group_reduce<false>(x, L); };
 
-  const int64_t steps = (p.M + P - 1) / P;
-  for (int64_t s0 = wave; s0 < steps; s0 += (int64_t)waves * kPanelUnroll) {
-    Chunk v[kPanelUnroll], r[kPanelUnroll];
-    int64_t row[kPanelUnroll];
-    bool ok[kPanelUnroll];
-#pragma unroll
-    for (int u = 0; u < kPanelUnroll; ++u) {
-      row[u] = (s0 + (int64_t)u * waves) * P + pr;
-      ok[u] = s0 + (int64_t)u * waves < steps && row[u] < p.M;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[u][e] = r[u][e] = 0.0f;
-      if (ok[u]) {
-        load_chunk(p.a, p.in_bf16 != 0, row[u] * p.lda + col, v[u]);
-        if (p.residual) load_chunk(p.residual, p.residual_bf16 != 0, row[u] * p.ldr + col, r[u]);
-      }
-    }
+  auto compute_store = [&](int64_t row, Chunk& v, const Chunk& r) {
     auto run_op = [&](int kind, int o) {
+      if (kind == KF_OP_BIAS) {
 #pragma unroll
-      for (int u = 0; u < kPanelUnroll; ++u) {
-        if (kind == KF_OP_BIAS) {
+        for (int e = 0; e < 8; ++e) v[e] += bia[e];
+      } else if (kind == KF_OP_RESIDUAL_ADD) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[u][e] += bia[e];
-        } else if (kind == KF_OP_RESIDUAL_ADD) {
+        for (int e = 0; e < 8; ++e) v[e] += r[e];
+      } else if (kind == KF_OP_GROUPNORM) {
+        const float eps = op_p0(ops, o);
+        const float sum = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+        const float mean = group_sum(sum) * inv_n;
+        float qd = 0.0f;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[u][e] += r[u][e];
-        } else if (kind == KF_OP_GROUPNORM) {
-          const float eps = op_p0(ops, o);
-          const float sum = ((v[u][0] + v[u][1]) + (v[u][2] + v[u][3])) + ((v[u][4] + v[u][5]) + (v[u][6] + v[u][7]));
-          const float mean = group_sum(sum) * inv_n;
-          float qd = 0.0f;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float d = v[u][e] - mean;
-            qd = fmaf(d, d, qd);
-          }
-          const float rs = rsqrtf(group_sum(qd) * inv_n + eps);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[u][e] = fmaf((v[u][e] - mean) * rs, gam[e], bet[e]);
-        } else {
-          apply_elementwise_array<8>(kind, op_p0(ops, o), op_p1(ops, o), v[u]);
+        for (int e = 0; e < 8; ++e) {
+          const float d = v[e] - mean;
+          qd = fmaf(d, d, qd);
         }
+        const float rs = rsqrtf(group_sum(qd) * inv_n + eps);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = fmaf((v[e] - mean) * rs, gam[e], bet[e]);
+      } else {
+        apply_elementwise_array<8>(kind, op_p0(ops, o), op_p1(ops, o), v);
       }
     };
     if constexpr (CH == 0) {
@@ -402,19 +386,131 @@ __global__ __launch_bounds__(RT) void kf_rowwise_gn_panel(RowArgs p) {
         run_op(kChainOps[CH][o], o);
       });
     }
+    if (!live) return;
+    if (p.out_bf16) {
+      u32x4 w;
 #pragma unroll
-    for (int u = 0; u < kPanelUnroll; ++u) {
-      if (!ok[u]) continue;
-      if (p.out_bf16) {
-        u32x4 w;
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+      store_nt(reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(p.out) + row * p.ldo + col), w);
+    } else {
+      f32x4* f = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.out) + row * p.ldo + col);
+      store_nt(f, f32x4{v[0], v[1], v[2], v[3]});
+      store_nt(f + 1, f32x4{v[4], v[5], v[6], v[7]});
+    }
+  };
+
+  for (int64_t row = row0; row < p.M; row += row_stride) {
+    Chunk v, r;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(v[u][2 * e], v[u][2 * e + 1]);
-        store_nt(reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(p.out) + row[u] * p.ldo + col), w);
-      } else {
-        f32x4* f = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.out) + row[u] * p.ldo + col);
-        store_nt(f, f32x4{v[u][0], v[u][1], v[u][2], v[u][3]});
-        store_nt(f + 1, f32x4{v[u][4], v[u][5], v[u][6], v[u][7]});
+    for (int e = 0; e < 8; ++e) v[e] = r[e] = 0.0f;
+    if (live) {
+      load_chunk(p.a, p.in_bf16 != 0, row * p.lda + col, v);
+      if (p.residual) load_chunk(p.residual, p.residual_bf16 != 0, row * p.ldr + col, r);
+    }
+    compute_store(row, v, r);
+  }
+}
+
+// Row logsumexp and cross-entropy (a row op that reduces the row to one
+// value, after element-wise ops and a bias): no output row, so the row is
+// streamed instead of held.  One wave per row; lane l takes chunks l,
+// l + 64, ... in groups of kStreamUnroll (all loads of a group issued
+// together), keeping a running (max, sum of e^(h - max)) that is rescaled
+// when the maximum grows -- once per group, by the group's maximum.  The
+// wave then combines its lanes' pairs; cross-entropy subtracts h[t], which
+// the lane holding chunk t / 8 picked up on the way.  Any row length; few
+// registers, so eight waves per SIMD each keep a group of loads in flight
+// (F5's 8192 x 16384 bf16 rows: groups of 1 or 2 chunks 46.6 us a step,
+// 4 chunks 52, 8 chunks 47; streaming loads 46.0).
+constexpr int kStreamUnroll = 2;
+
+template <int CH>
+__global__ __launch_bounds__(RT) void kf_row_reduce_stream(RowArgs p) {
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * (RT / 64);
+  const int nops = p.prog.n;
+  const OpTable ops = load_op_table(p.prog, lane);
+  const int64_t chunks = p.N >> 3;
+  const int last = (CH == 0 ? nops : kChainLen[CH]) - 1;
+  const int row_kind = CH == 0 ? op_kind(ops, last) : kChainOps[CH][kChainLen[CH] > 0 ? kChainLen[CH] - 1 : 0];
+  const bool ce = row_kind == KF_OP_ROW_CROSS_ENTROPY;
+
+  for (int64_t m = (int64_t)blockIdx.x * (RT / 64) + (threadIdx.x >> 6); m < p.M; m += waves) {
+    const int32_t tgt = ce ? p.targets[m] : -1;
+    const bool valid = tgt >= 0 && tgt < p.N;
+    const int64_t tchunk = valid ? (tgt >> 3) : -1;
+    float mx = -INFINITY, sum = 0.0f, ht = 0.0f;
+    for (int64_t c0 = lane; c0 < chunks; c0 += 64 * kStreamUnroll) {
+      Chunk v[kStreamUnroll];
+#pragma unroll
+      for (int u = 0; u < kStreamUnroll; ++u) {
+        const int64_t c = c0 + 64 * u;
+        if (c < chunks) {
+          load_chunk<true>(p.a, p.in_bf16 != 0, m * p.lda + c * 8, v[u]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[u][e] = -INFINITY;
+        }
       }
+      // the element-wise ops (and the bias) before the row op
+      auto run_op = [&](int kind, int o) {
+#pragma unroll
+        for (int u = 0; u < kStreamUnroll; ++u) {
+          const int64_t c = c0 + 64 * u;
+          if (c >= chunks) continue;
+          if (kind == KF_OP_BIAS) {
+            const f32x4* b = reinterpret_cast<const f32x4*>(p.bias + c * 8);
+            const f32x4 lo = b[0], hi = b[1];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[u][e] += lo[e];
+              v[u][4 + e] += hi[e];
+            }
+          } else {
+            apply_elementwise_array<8>(kind, op_p0(ops, o), op_p1(ops, o), v[u]);
+          }
+        }
+      };
+      if constexpr (CH == 0) {
+        for (int o = 0; o < last; ++o) run_op(op_kind(ops, o), o);
+      } else {
+        static_for<0, kChainLen[CH] - 1>([&](auto O_c) {
+          constexpr int o = decltype(O_c)::value;
+          run_op(kChainOps[CH][o], o);
+        });
+      }
+#pragma unroll
+      for (int u = 0; u < kStreamUnroll; ++u)
+        if (c0 + 64 * u == tchunk) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ht = (tgt & 7) == e ? v[u][e] : ht;
+        }
+      float gm = mx;
+#pragma unroll
+      for (int u = 0; u < kStreamUnroll; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gm = fmaxf(gm, v[u][e]);
+      if (gm == -INFINITY) continue;  // nothing but -inf so far
+      const float gl = gm * kLog2e;
+      float gs = 0.0f;
+#pragma unroll
+      for (int u = 0; u < kStreamUnroll; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gs += __builtin_amdgcn_exp2f(fmaf(v[u][e], kLog2e, -gl));
+      sum = (mx == -INFINITY ? 0.0f : sum * __builtin_amdgcn_exp2f(fmaf(mx, kLog2e, -gl))) + gs;
+      mx = gm;
+    }
+    // combine the lanes: the row maximum, then each lane's sum rescaled to it
+    const float rmx = lane_group_reduce<true>(mx, 64);
+    const float part = mx == -INFINITY ? 0.0f : sum * __builtin_amdgcn_exp2f(fmaf(mx, kLog2e, -rmx * kLog2e));
+    const float rsum = lane_group_reduce<false>(part, 64);
+    const float lse = rmx + logf(rsum);
+    if (ce) {
+      const float h = __builtin_bit_cast(
+          float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ht), valid ? (int)(tchunk & 63) : 0));
+      if (lane == 0) reinterpret_cast<float*>(p.out)[m] = valid ? lse - h : __builtin_nanf("");
+    } else if (lane == 0) {
+      reinterpret_cast<float*>(p.out)[m] = lse;
     }
   }
 }
@@ -437,15 +533,25 @@ bool panel_applies(const RowArgs& a) {
 template <int CH>
 hipError_t launch_panel(const RowArgs& args, hipStream_t stream) {
   // as many workgroups as the device holds at once, whole sets of them per
-  // column group, and no more waves per group than it has row steps
+  // four adjacent panels, and no more workgroups per set than rows
   static const int resident = resident_blocks(kf_rowwise_gn_panel<CH>, RT);
   const int64_t groups = args.N / args.gn_group;
   const int64_t P = 64 / (args.gn_group / 8);
-  const int64_t steps = (args.M + P - 1) / P;
-  int64_t per_group = std::max<int64_t>(1, resident / groups);
-  per_group = std::min<int64_t>(per_group, (steps + RT / 64 - 1) / (RT / 64));
-  const dim3 grid((unsigned)(groups * per_group)), block(RT);
+  const int64_t panels = (groups + P - 1) / P;
+  const int64_t panel_sets = (panels + RT / 64 - 1) / (RT / 64);
+  int64_t per_set = std::max<int64_t>(1, resident / panel_sets);
+  per_set = std::min<int64_t>(per_set, args.M);
+  const dim3 grid((unsigned)(panel_sets * per_set)), block(RT);
   hipLaunchKernelGGL((kf_rowwise_gn_panel<CH>), grid, block, 0, stream, args);
+  return hipGetLastError();
+}
+
+template <int CH>
+hipError_t launch_stream(const RowArgs& args, hipStream_t stream) {
+  static const int resident = resident_blocks(kf_row_reduce_stream<CH>, RT);
+  const int64_t need = (args.M + RT / 64 - 1) / (RT / 64);
+  const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>(need, resident))), block(RT);
+  hipLaunchKernelGGL((kf_row_reduce_stream<CH>), grid, block, 0, stream, args);
   return hipGetLastError();
 }
 
@@ -473,6 +579,13 @@ hipError_t launch_rowwise_chain(const RowArgs& args, hipStream_t stream) {
 // interpreted.
 hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream) {
   if (args.M <= 0) return hipSuccess;
+  if (row_reduce_streams(args.prog)) {
+    switch (chain) {
+      case kChainRowLogsumexp: return launch_stream<kChainRowLogsumexp>(args, stream);
+      case kChainRowCrossEntropy: return launch_stream<kChainRowCrossEntropy>(args, stream);
+      default: return launch_stream<0>(args, stream);
+    }
+  }
   if (panel_applies(args)) {
     switch (chain) {
       case 5: return launch_panel<5>(args, stream);
@@ -491,5 +604,19 @@ hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream) {
 }
 
 int rowwise_max_cols() { return kMaxCols; }
+
+// The streamed form applies to a list that ends with a row logsumexp or
+// cross-entropy and has only element-wise ops and a bias before it.
+bool row_reduce_streams(const EpiProgram& prog) {
+  const int n = prog.n;
+  if (n < 1) return false;
+  const int k = prog.op[n - 1].kind;
+  if (k != KF_OP_ROW_LOGSUMEXP && k != KF_OP_ROW_CROSS_ENTROPY) return false;
+  for (int i = 0; i + 1 < n; ++i) {
+    const int o = prog.op[i].kind;
+    if (o != KF_OP_BIAS && !is_elementwise(o)) return false;
+  }
+  return true;
+}
 
 }  // namespace kf

@@ -505,7 +505,7 @@ hipError_t launch_unfused_rowop(const void* in, bool in_bf16, void* out, bool ou
                                 int kind, const int32_t* targets, hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
   const bool softmax = kind == KF_OP_ROW_SOFTMAX;
-  if (N % 8 == 0 && N <= rowwise_max_cols() && aligned16(in) && (!softmax || aligned16(out))) {
+  if (N % 8 == 0 && (N <= rowwise_max_cols() || !softmax) && aligned16(in) && (!softmax || aligned16(out))) {
     RowArgs r{};
     r.a = in;
     r.M = rows;

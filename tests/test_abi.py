@@ -243,6 +243,24 @@ def test_rowwise_validation():
         assert st == status, (kw, st, kf.last_error())
 
 
+def test_rowwise_width_limits():
+    """Rows held in registers stop at 16384 columns; a row logsumexp or
+    cross-entropy after element-wise ops streams its rows, any width."""
+    ok = kf.KF_ERR_NO_DEVICE if not _gpu_present() else kf.KF_OK
+    for name, ops, N, status in [
+        ("F4", [("row_softmax",)], 16392, kf.KF_ERR_UNSUPPORTED),
+        ("F5", [("row_cross_entropy",)], 131072, ok),
+        ("F5", [("bias",), ("tanh",), ("row_logsumexp",)], 1 << 20, ok),
+        ("F5", [("groupnorm", 2, 1e-5), ("row_logsumexp",)], 32768, kf.KF_ERR_UNSUPPORTED),
+        ("F5", [("row_cross_entropy",)], 131076, kf.KF_ERR_UNSUPPORTED),  # N % 8
+    ]:
+        cfg = inputs.config(name, M=4, N=N, ops=ops)
+        st, h = _create(kf.make_spec(inputs.chain(cfg), **kf.sizes_of(cfg)))
+        assert st == status, (name, ops, N, st, kf.last_error())
+        if h.value:
+            kf.lib().kf_destroy(h)
+
+
 def test_rowwise_input_slots():
     ch = inputs.chain(inputs.config("F3"))
     assert kf.input_names(ch) == ["a", "gamma", "beta", "residual"]

@@ -911,7 +911,7 @@ def test_unfused_rejects_padded_rows():
 
 # ------------------------------------------------------- cross-entropy rows
 
-@pytest.mark.parametrize("M,N", [(37, 1032), (64, 4104), (5, 16384), (1, 8)])
+@pytest.mark.parametrize("M,N", [(37, 1032), (64, 4104), (5, 16384), (1, 8), (3, 131072), (2, 100008)])
 def test_f5_rows_cross_entropy(M, N):
     _torch()
     cfg = inputs.config("F5", M=M, N=N)
@@ -919,6 +919,43 @@ def test_f5_rows_cross_entropy(M, N):
     _, out = run_gpu(cfg, t)
     err = check(cfg, t, out)
     print(f"F5 {M}x{N} err {err:.3e}")
+
+
+_STREAM_DIST = dict(a=("normal", 2.0), bias=("uniform", -0.5, 0.5), targets=("classes",))
+
+
+@pytest.mark.parametrize("ops,N", [
+    ([("scale", 0.5), ("tanh",), ("row_logsumexp",)], 4104),
+    ([("bias",), ("gelu_erf",), ("row_cross_entropy",)], 1032),
+    ([("bias",), ("hardtanh", -1.0, 1.0), ("row_cross_entropy",)], 40000),
+    ([("row_logsumexp",)], 65536),
+])
+def test_streamed_row_reductions(ops, N):
+    """Row logsumexp / cross-entropy after element-wise ops and a bias
+    (interpreted list, rows streamed, widths past the held-row limit)."""
+    _torch()
+    cfg = inputs.config("F5", M=19, N=N, ops=ops, dist=_STREAM_DIST)
+    t = inputs.generate(cfg, seed=N + len(ops))
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"streamed {[o[0] for o in ops]} {N} err {err:.3e}")
+
+
+def test_cross_entropy_targets_out_of_range():
+    """A target outside [0, N) gives NaN for its row and leaves the others."""
+    _torch()
+    for name, kw in (("F5", dict(M=6, N=1032)), ("F6", dict(M=6, N=1032, K=64))):
+        cfg = inputs.config(name, **kw)
+        t = inputs.generate(cfg, seed=5)
+        t["targets"] = t["targets"].copy()
+        t["targets"][[1, 4]] = [-1, kw["N"]]
+        _, out = run_gpu(cfg, t)
+        g = to_host_f64(out)
+        assert np.isnan(g[[1, 4]]).all(), (name, g)
+        keep = np.array([0, 2, 3, 5])
+        ref = oracle.run_chain(inputs.chain_for(cfg, t), t, rows=keep)
+        assert np.isnan(oracle.run_chain(inputs.chain_for(cfg, t), t, rows=np.array([1, 4]))).all()
+        assert parity_error(g[keep], ref, 1.0) <= TOL["bf16"], name
 
 
 @pytest.mark.parametrize("M,N,K,layout", [(300, 1040, 136, "kn"), (77, 16384, 64, "kn"), (129, 776, 200, "nk"),
