@@ -110,7 +110,11 @@ KERNEL_FILES = {
                              "kf_gemm_mfma_fp8_kn.hip", "kf_gemm_mfma_fp8_nk.hip"],
     "kf_gemm_f32_8x8": ["kf_gemm_f32.hip"],
     "kf_conv3x3_bf16_256x128": ["kf_conv_bf16.hip"],
+    "kf_conv3x3_bf16_w8": ["kf_conv_bf16.hip"],
+    "kf_conv3x3_bf16_gen": ["kf_conv_bf16.hip"],
     "kf_rowwise": ["kf_rowwise.hip"],
+    "kf_rowwise_gn_panel": ["kf_rowwise.hip"],
+    "kf_row_reduce_stream": ["kf_rowwise.hip"],
     "kf_conv3d_bf16_64x256": ["kf_conv3d_bf16.hip"],
 }
 

@@ -237,7 +237,9 @@ kf_status kf_output_info(const kf_desc* desc, int32_t* dtype, int32_t* ndim,
 /* Bytes of device workspace the descriptor owns (fused path). */
 size_t kf_workspace_bytes(const kf_desc* desc);
 
-/* Name of the main (contraction) kernel the plan launches. */
+/* Name of the main kernel the plan launches (the contraction, or the row
+   kernel of a ROWWISE list) under its current launch configuration; a
+   static string. */
 const char* kf_kernel_name(const kf_desc* desc);
 
 /* ---- Diagnosis and tuning ------------------------------------------------
@@ -367,10 +369,16 @@ kf_status kf_set_tuning(kf_desc* desc, const kf_tuning* tuning);
 
 typedef struct kf_tune_result {
   int32_t n;            /* candidates timed                                  */
-  int32_t best;         /* index of the fastest                              */
+  int32_t best;         /* index of the one kept                             */
   kf_tuning config[KF_MAX_TUNE_CANDIDATES];
   double seconds[KF_MAX_TUNE_CANDIDATES]; /* time of one kf_fused_op (median
                                              round)                          */
+  double panel_bytes[KF_MAX_TUNE_CANDIDATES]; /* GEMM: operand bytes the
+                           candidate's tile order makes the eight L2s fetch
+                           (model: per XCD and round of concurrently
+                           resident tiles, one A panel per distinct tile row
+                           and one B panel per distinct tile column); -1
+                           for other plans                                   */
 } kf_tune_result;
 
 /* Time every candidate launch configuration of the plan on the caller's
@@ -383,7 +391,11 @@ typedef struct kf_tune_result {
    (the same bits for every candidate).  Candidates: GEMM (bf16 / fp8) raster
    groups {1, 2, 4, 8, 16, 32, 64} x XCD order {contiguous, hardware}; CONV3D
    workgroups per CU {2, 1} x XCD order; CONV2D_3X3 kernel variant {0, 1};
-   every other plan has only its current configuration. */
+   every other plan has only its current configuration.  Kept: the fastest,
+   except that among the GEMM candidates within 2% of the fastest time the
+   one with the fewest panel_bytes is kept (the timing cannot tell such
+   candidates apart; fewer L2 misses leave more HBM and fabric bandwidth to
+   the epilogue). */
 kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
                       kf_tune_result* result);
 

@@ -288,7 +288,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       d->gn_group = (int)(s->N / g.groups);
     }
     d->variant = kVarRowwise;
-    d->kernel_name = "kf_rowwise";
+    d->kernel_name = kf::rowwise_kernel(d->prog, d->gn_group);
     d->inputs.push_back(Slot{dt, 2, {s->M, s->N, 0, 0, 0}, "A", false});
     for (int i = 0; i < s->n_ops; ++i) {
       const int k = s->ops[i].kind;
@@ -358,7 +358,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     if (d->conv_special && (int64_t)s->batch * (s->height / 2) > INT32_MAX)
       return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 supports at most 2^31 - 1 row-pair tiles");
     if (!d->conv_special && kf::conv_gen_tiles(s->batch, s->height, s->width, s->cout) >= (int64_t(1) << 24))
-      return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 (general shapes) supports fewer than 2^24 tiles of 2 x 32 x 128");
+      return fail(KF_ERR_UNSUPPORTED, "CONV2D_3X3 (general shapes) supports fewer than 2^24 tiles of 4 x 32 x 128");
     for (int i = 0; i < s->n_ops; ++i) {
       const int k = s->ops[i].kind;
       if (!(k == KF_OP_BIAS || k == KF_OP_MAXPOOL2X2 || is_elementwise_kind(k)))
@@ -679,6 +679,53 @@ kf_status kf_set_tuning(kf_desc* d, const kf_tuning* t) {
   return ok();
 }
 
+namespace {
+
+// Operand bytes the eight L2s fetch for a GEMM plan under launch
+// configuration t (a model).  The grid has one workgroup per tile; workgroup
+// b goes to XCD b % 8 and the device holds resident_per_cu x CUs of them at
+// once, so consecutive ranges of that many workgroups run as rounds.  Within
+// a round an XCD's L2 fetches each A panel (BM rows x K) and B panel (K x BN)
+// that its tiles touch once; across rounds nothing is assumed to stay (a
+// panel is 2-8 MiB against a 4 MiB L2).
+double gemm_panel_bytes(const kf_desc* d, const kf_tuning& t) {
+  const kf_op_spec& s = d->spec;
+  const int64_t tm_n = (s.M + kf::gemm_mfma_tile_m() - 1) / kf::gemm_mfma_tile_m();
+  const int64_t tn_n = (s.N + kf::gemm_mfma_tile_n() - 1) / kf::gemm_mfma_tile_n();
+  const int64_t nwg = tm_n * tn_n;
+  if (nwg <= 0 || nwg > (int64_t(1) << 22)) return -1.0;
+  const double es = s.in_dtype == KF_FP8_E4M3 ? 1.0 : 2.0;
+  const double a_panel = (double)kf::gemm_mfma_tile_m() * (double)s.K * es;
+  const double b_panel = (double)kf::gemm_mfma_tile_n() * (double)s.K * es;
+  const int64_t round = std::max<int64_t>(8, (int64_t)d->num_cu);  // one 256x256 workgroup per CU
+  double bytes = 0.0;
+  std::vector<uint8_t> seen_m((size_t)tm_n * 8), seen_n((size_t)tn_n * 8);
+  for (int64_t r0 = 0; r0 < nwg; r0 += round) {
+    std::fill(seen_m.begin(), seen_m.end(), 0);
+    std::fill(seen_n.begin(), seen_n.end(), 0);
+    for (int64_t bid = r0; bid < std::min(nwg, r0 + round); ++bid) {
+      // the kernel's tile order (see tile_coords in the GEMM kernel)
+      int64_t lid = bid;
+      if (t.xcd_remap && (nwg & 7) == 0) lid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+      const int64_t per_group = (int64_t)t.raster_group * tn_n;
+      const int64_t group = lid / per_group;
+      const int64_t first_m = group * t.raster_group;
+      const int64_t gsize = std::min<int64_t>(tm_n - first_m, t.raster_group);
+      const int64_t rr = lid - group * per_group;
+      const int64_t tm = first_m + rr % gsize, tn = rr / gsize;
+      const int64_t x = bid & 7;
+      uint8_t& fm = seen_m[(size_t)(tm * 8 + x)];
+      uint8_t& fn = seen_n[(size_t)(tn * 8 + x)];
+      if (!fm) bytes += a_panel;
+      if (!fn) bytes += b_panel;
+      fm = fn = 1;
+    }
+  }
+  return bytes;
+}
+
+}  // namespace
+
 kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
                       kf_tune_result* result) {
   if (!d || !inputs || !outputs || !result) return fail(KF_ERR_INVALID_ARG, "NULL argument");
@@ -734,14 +781,22 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
     d->tuning = cur;
     return st != KF_OK ? st : fail(KF_ERR_INVALID_ARG, "no candidate configuration");
   }
+  const bool gemm = d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8;
   int best = 0;
   for (int c = 0; c < n; ++c) {
     double* r = &t[(size_t)c * kRounds];
     std::sort(r, r + kRounds);
     result->config[c] = cand[c];
     result->seconds[c] = r[kRounds / 2];
+    result->panel_bytes[c] = gemm ? gemm_panel_bytes(d, cand[c]) : -1.0;
     if (result->seconds[c] < result->seconds[best]) best = c;
   }
+  // within 2% of the fastest time, the fewest fetched operand panels
+  const double fastest = result->seconds[best];
+  for (int c = 0; c < n && gemm; ++c)
+    if (result->seconds[c] <= fastest * 1.02 && result->panel_bytes[c] >= 0.0 &&
+        result->panel_bytes[c] < result->panel_bytes[best])
+      best = c;
   result->n = n;
   result->best = best;
   d->tuning = result->config[best];
@@ -826,7 +881,14 @@ kf_status kf_output_info(const kf_desc* d, int32_t* dtype, int32_t* ndim, int64_
 
 size_t kf_workspace_bytes(const kf_desc* d) { return d ? d->workspace_bytes : 0; }
 
-const char* kf_kernel_name(const kf_desc* d) { return d ? d->kernel_name : ""; }
+const char* kf_kernel_name(const kf_desc* d) {
+  if (!d) return "";
+  if (d->variant == kVarConvBf16)  // the launch variant picks the kernel
+    return d->tuning.variant == 2 ? "kf_conv3x3_bf16_gen"
+           : d->tuning.variant == 1 ? "kf_conv3x3_bf16_w8"
+                                    : "kf_conv3x3_bf16_256x128";
+  return d->kernel_name;
+}
 
 kf_status kf_fused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
   return kf_fused_op_timed(d, inputs, outputs, stream, nullptr, nullptr);

@@ -43,6 +43,9 @@ int rowwise_max_cols();
 // element-wise ops and a bias only: launch_rowwise streams those rows, any
 // N (a multiple of 8).
 bool row_reduce_streams(const EpiProgram& prog);
+// The kernel launch_rowwise runs for an op list (GroupNorm group width
+// `gn_group` columns, 0 if none).
+const char* rowwise_kernel(const EpiProgram& prog, int gn_group);
 
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);

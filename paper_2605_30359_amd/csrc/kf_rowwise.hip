@@ -605,6 +605,13 @@ hipError_t launch_rowwise(const RowArgs& args, int chain, hipStream_t stream) {
 
 int rowwise_max_cols() { return kMaxCols; }
 
+const char* rowwise_kernel(const EpiProgram& prog, int gn_group) {
+  RowArgs a{};
+  a.prog = prog;
+  a.gn_group = gn_group;
+  return row_reduce_streams(prog) ? "kf_row_reduce_stream" : panel_applies(a) ? "kf_rowwise_gn_panel" : "kf_rowwise";
+}
+
 // The streamed form applies to a list that ends with a row logsumexp or
 // cross-entropy and has only element-wise ops and a bias before it.
 bool row_reduce_streams(const EpiProgram& prog) {

@@ -243,7 +243,7 @@ __device__ __forceinline__ void store8(void* p, int64_t c, const float (&x)[8]) 
 }
 
 enum VecMode { kVecOp = 0, kVecBiasCols = 1, kVecBiasPlane = 2, kVecResidual = 3 };
-constexpr int kVecUnroll = 4;  // chunks in flight per lane
+constexpr int kVecUnroll = 1;  // chunks per lane and iteration (1 ran faster than 2 or 4: more waves)
 
 // out = op(in) over `chunks` chunks: an element-wise op, + bias per column of
 // rows of fmod values (kVecBiasCols, fmod % 8 == 0), + bias per plane of

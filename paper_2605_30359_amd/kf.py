@@ -95,7 +95,8 @@ class KfTuning(ctypes.Structure):
 
 class KfTuneResult(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("best", ctypes.c_int32), ("config", KfTuning * KF_MAX_TUNE_CANDIDATES),
-                ("seconds", ctypes.c_double * KF_MAX_TUNE_CANDIDATES)]
+                ("seconds", ctypes.c_double * KF_MAX_TUNE_CANDIDATES),
+                ("panel_bytes", ctypes.c_double * KF_MAX_TUNE_CANDIDATES)]
 
 
 class KFError(RuntimeError):
@@ -417,7 +418,7 @@ class FusedOp:
             stream = stream.cuda_stream
         r = KfTuneResult()
         _check(lib().kf_autotune(self._h, arr, o, ctypes.c_void_p(stream), reps, ctypes.byref(r)))
-        cands = [dict(r.config[i].as_dict(), seconds=r.seconds[i]) for i in range(r.n)]
+        cands = [dict(r.config[i].as_dict(), seconds=r.seconds[i], panel_bytes=r.panel_bytes[i]) for i in range(r.n)]
         return {"best": cands[r.best], "candidates": cands}
 
     def device_inputs(self, tensors: dict, device="cuda") -> list:
