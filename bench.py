@@ -32,7 +32,8 @@ gets a block of the same fields under "also".  Per workload:
                computation per unit)
   tuning       the launch configuration kf_autotune kept before the timed
                steps (every candidate computes the same bits), or the one
-               given with --tuning
+               given with --tuning; for a GEMM also the modelled operand
+               bytes its tile order makes the L2s fetch
   diagnosis    kf_diagnose_counters on the measured kernel time and the
                committed counters (HBM bytes, matrix-core busy fraction, LDS
                bank conflicts) when they match the kernel source: compute and
@@ -247,8 +248,9 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
     ins = op.device_inputs(tensors, "cuda:0")
     out = op.empty_output("cuda:0")
 
-    # the plan's launch candidates, timed on these inputs; the fastest is kept
-    # (every candidate computes the same bits)
+    # the plan's launch candidates, timed on these inputs; the fastest is kept,
+    # or for a GEMM the fewest modelled L2 panel bytes within 2% of it (every
+    # candidate computes the same bits)
     tuning = None
     if args.tuning:
         op.set_tuning(*(int(v) for v in args.tuning.split(",")))
@@ -260,7 +262,8 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
         default = [c for c in r["candidates"] if all(c[k] == plan_default[k] for k in keys)]
         tuning = {"config": {k: r["best"][k] for k in keys}, "candidates": len(r["candidates"]),
                   "best_ms": round(r["best"]["seconds"] * 1e3, 5),
-                  "default_ms": round(default[0]["seconds"] * 1e3, 5) if default else None}
+                  "default_ms": round(default[0]["seconds"] * 1e3, 5) if default else None,
+                  "panel_bytes_model": r["best"]["panel_bytes"] if r["best"]["panel_bytes"] >= 0 else None}
 
     print(f"[bench] {name}: timing", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
