@@ -350,7 +350,7 @@ typedef struct kf_tuning {
   int32_t wg_per_cu;    /* CONV3D: persistent workgroups per compute unit,
                            1 or 2 (default 2)                                */
   int32_t variant;      /* kernel shape.  CONV2D_3X3 in the tiled family
-                           (cin 256, cout 128k, H 2k, W 128k): 1 (default)
+                           (cin 64, cout 128, W 128, even H): 1 (default)
                            = the tile on 8 waves (64 x 64 wave blocks, two
                            per SIMD), 0 = on 4 waves (128 x 64), 2 = the
                            general kernel; any other CONV2D_3X3 shape: 2
