@@ -109,6 +109,7 @@ def _source_digest(kernel_files) -> str:
 KERNEL_FILES = {
     "kf_gemm_mfma_256x256": ["kf_gemm_mfma.hpp", "kf_gemm_epilogue.hpp", "kf_gemm_mfma.hip", "kf_gemm_mfma_bf16_nk.hip",
                              "kf_gemm_mfma_fp8_kn.hip", "kf_gemm_mfma_fp8_nk.hip"],
+    "kf_gemm_mfma_pp128x256": ["kf_gemm_pp.hpp", "kf_gemm_epilogue.hpp", "kf_gemm_pp_bf16.hip", "kf_gemm_pp_fp8.hip"],
     "kf_gemm_f32_8x8": ["kf_gemm_f32.hip"],
     "kf_conv3x3_bf16_256x128": ["kf_conv_bf16.hip"],
     "kf_conv3x3_bf16_w8": ["kf_conv_bf16.hip"],

@@ -355,7 +355,11 @@ typedef struct kf_tuning {
                            per SIMD), 0 = on 4 waves (128 x 64), 2 = the
                            general kernel; any other CONV2D_3X3 shape: 2
                            only (4 rows x 32 columns x 128 channels per
-                           workgroup); other ops: 0                        */
+                           workgroup).  GEMM (bf16 / fp8): 0 (default) =
+                           256x256 tiles, one workgroup per CU; 1 = 128x256
+                           tiles, two persistent workgroups per CU (B in KN
+                           layout only; raster_group and xcd_remap unused).
+                           Other ops: 0                                      */
 } kf_tuning;
 
 /* The plan's launch fields.  None of them changes a result bit: they reorder
@@ -389,7 +393,8 @@ typedef struct kf_tune_result {
    *result (seconds: the median round's mean time of one call).  Blocks
    until the stream is idle; outputs[0] holds the result of the last call
    (the same bits for every candidate).  Candidates: GEMM (bf16 / fp8) raster
-   groups {1, 2, 4, 8, 16, 32, 64} x XCD order {contiguous, hardware}; CONV3D
+   groups {1, 2, 4, 8, 16, 32, 64} x XCD order {contiguous, hardware} of the
+   256x256 tile, and the 128x256 tile (variant 1) for B in KN layout; CONV3D
    workgroups per CU {2, 1} x XCD order; CONV2D_3X3 kernel variant {0, 1};
    every other plan has only its current configuration.  Kept: the fastest,
    except that among the GEMM candidates within 2% of the fastest time the

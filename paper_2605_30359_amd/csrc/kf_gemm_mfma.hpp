@@ -431,5 +431,9 @@ void launch_gemm_bf16_kn(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 
 void launch_gemm_bf16_nk(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
 void launch_gemm_fp8_kn(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
 void launch_gemm_fp8_nk(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+// the 128x256 two-workgroups-per-CU kernel (kf_gemm_pp.hpp, B in KN layout)
+void launch_gemm_pp_bf16(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+void launch_gemm_pp_fp8(const GemmArgs& p, int epi, int chain, dim3 grid, dim3 block, hipStream_t stream);
+int gemm_pp_tile_m();
 
 }  // namespace kf

@@ -476,6 +476,14 @@ struct Work {
   int64_t workgroups;
 };
 
+// Launch variant 1 of a GEMM plan: the 128x256 kernel, two persistent
+// workgroups per CU (0: the 256x256 kernel).
+int gemm_pp_workgroups(const kf_desc* d) {
+  if ((d->variant != kVarGemmBf16 && d->variant != kVarGemmFp8) || d->tuning.variant != 1) return 0;
+  const int64_t tiles = kf::gemm_pp_tiles(d->spec.M, d->spec.N);
+  return (int)std::max<int64_t>(1, std::min<int64_t>(tiles, 2 * (int64_t)d->num_cu));
+}
+
 Work plan_work(const kf_desc* d) {
   const kf_op_spec& s = d->spec;
   Work w{0.0, 0.0, 157.3, 0};
@@ -496,7 +504,7 @@ Work plan_work(const kf_desc* d) {
       w.flops = 2.0 * s.M * s.N * s.K;
       w.peak_tflops = d->variant == kVarGemmFp8 ? 5033.2 : 2516.6;
       const int64_t bm = kf::gemm_mfma_tile_m(), bn = kf::gemm_mfma_tile_n();
-      w.workgroups = ((s.M + bm - 1) / bm) * ((s.N + bn - 1) / bn);
+      w.workgroups = d->tuning.variant == 1 ? gemm_pp_workgroups(d) : ((s.M + bm - 1) / bm) * ((s.N + bn - 1) / bn);
       break;
     }
     case kVarConvBf16:
@@ -671,8 +679,9 @@ kf_status kf_set_tuning(kf_desc* d, const kf_tuning* t) {
   if (t->raster_group < 1 || t->raster_group > 64) return fail(KF_ERR_INVALID_ARG, "raster_group must be in [1, 64]");
   if (t->xcd_remap != 0 && t->xcd_remap != 1) return fail(KF_ERR_INVALID_ARG, "xcd_remap must be 0 or 1");
   if (t->wg_per_cu != 1 && t->wg_per_cu != 2) return fail(KF_ERR_INVALID_ARG, "wg_per_cu must be 1 or 2");
+  const bool gemm_kn = (d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) && d->spec.b_layout == KF_LAYOUT_KN;
   const int min_variant = d->variant == kVarConvBf16 && !d->conv_special ? 2 : 0;
-  const int max_variant = d->variant == kVarConvBf16 ? 2 : 0;
+  const int max_variant = d->variant == kVarConvBf16 ? 2 : gemm_kn ? 1 : 0;
   if (t->variant < min_variant || t->variant > max_variant)
     return fail(KF_ERR_INVALID_ARG, "variant must be in [%d, %d] for this plan", min_variant, max_variant);
   d->tuning = *t;
@@ -688,8 +697,11 @@ namespace {
 // a round an XCD's L2 fetches each A panel (BM rows x K) and B panel (K x BN)
 // that its tiles touch once; across rounds nothing is assumed to stay (a
 // panel is 2-8 MiB against a 4 MiB L2).
+double gemm_pp_panel_bytes(const kf_desc* d);
+
 double gemm_panel_bytes(const kf_desc* d, const kf_tuning& t) {
   const kf_op_spec& s = d->spec;
+  if (t.variant == 1) return gemm_pp_panel_bytes(d);
   const int64_t tm_n = (s.M + kf::gemm_mfma_tile_m() - 1) / kf::gemm_mfma_tile_m();
   const int64_t tn_n = (s.N + kf::gemm_mfma_tile_n() - 1) / kf::gemm_mfma_tile_n();
   const int64_t nwg = tm_n * tn_n;
@@ -724,6 +736,50 @@ double gemm_panel_bytes(const kf_desc* d, const kf_tuning& t) {
   return bytes;
 }
 
+// The same model for the 128x256 kernel: G = 2 x CUs persistent workgroups,
+// workgroup b on XCD b % 8 taking its i-th tile in round i, tiles ordered as
+// the kernel orders them (each XCD a contiguous eighth, 8-row rasters).
+double gemm_pp_panel_bytes(const kf_desc* d) {
+  const kf_op_spec& s = d->spec;
+  const int64_t tm_n = (s.M + 127) / 128;
+  const int64_t tn_n = (s.N + kf::gemm_mfma_tile_n() - 1) / kf::gemm_mfma_tile_n();
+  const int64_t T = tm_n * tn_n;
+  const int64_t G = gemm_pp_workgroups(d);
+  if (T <= 0 || T > (int64_t(1) << 22) || G <= 0) return -1.0;
+  const double es = s.in_dtype == KF_FP8_E4M3 ? 1.0 : 2.0;
+  const double a_panel = 128.0 * (double)s.K * es;
+  const double b_panel = (double)kf::gemm_mfma_tile_n() * (double)s.K * es;
+  double bytes = 0.0;
+  std::vector<uint8_t> seen_m((size_t)tm_n * 8), seen_n((size_t)tn_n * 8);
+  for (int64_t i = 0;; ++i) {
+    std::fill(seen_m.begin(), seen_m.end(), 0);
+    std::fill(seen_n.begin(), seen_n.end(), 0);
+    bool any = false;
+    for (int64_t b = 0; b < G; ++b) {
+      int64_t lid;
+      if ((T & 7) == 0 && (G & 7) == 0) {
+        const int64_t local = i * (G >> 3) + (b >> 3);
+        if (local >= (T >> 3)) continue;
+        lid = (b & 7) * (T >> 3) + local;
+      } else {
+        lid = b + i * G;
+        if (lid >= T) continue;
+      }
+      any = true;
+      const int64_t per_group = 8 * tn_n, group = lid / per_group, first_m = group * 8;
+      const int64_t gsize = std::min<int64_t>(tm_n - first_m, 8), rr = lid - group * per_group;
+      const int64_t tm = first_m + rr % gsize, tn = rr / gsize, x = b & 7;
+      uint8_t& fm = seen_m[(size_t)(tm * 8 + x)];
+      uint8_t& fn = seen_n[(size_t)(tn * 8 + x)];
+      if (!fm) bytes += a_panel;
+      if (!fn) bytes += b_panel;
+      fm = fn = 1;
+    }
+    if (!any) break;
+  }
+  return bytes;
+}
+
 }  // namespace
 
 kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int32_t reps,
@@ -735,6 +791,8 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
   if (d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) {
     for (int remap = 1; remap >= 0; --remap)
       for (int g : {1, 2, 4, 8, 16, 32, 64}) cand.push_back(kf_tuning{g, remap, cur.wg_per_cu, 0});
+    // the second tile shape (its tile order is fixed: raster and XCD fields unused)
+    if (d->spec.b_layout == KF_LAYOUT_KN) cand.push_back(kf_tuning{cur.raster_group, cur.xcd_remap, cur.wg_per_cu, 1});
   } else if (d->variant == kVarConv3d) {
     for (int remap = 1; remap >= 0; --remap)
       for (int wg : {2, 1}) cand.push_back(kf_tuning{cur.raster_group, remap, wg, 0});
@@ -883,6 +941,8 @@ size_t kf_workspace_bytes(const kf_desc* d) { return d ? d->workspace_bytes : 0;
 
 const char* kf_kernel_name(const kf_desc* d) {
   if (!d) return "";
+  if ((d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) && d->tuning.variant == 1)
+    return "kf_gemm_mfma_pp128x256";
   if (d->variant == kVarConvBf16)  // the launch variant picks the kernel
     return d->tuning.variant == 2 ? "kf_conv3x3_bf16_gen"
            : d->tuning.variant == 1 ? "kf_conv3x3_bf16_w8"
@@ -1051,7 +1111,7 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
           !fits_31(256 * a.ldo * 4) || (a.residual && !fits_31(256 * a.ldr * 4)))
         return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
       if (d->variant == kVarGemmFp8) a.scale = s.scale_a * s.scale_b;  // fl(s_a * s_b), applied to the fp32 accumulator
-      e = kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, d->epi_shape, d->chain, hs, nk);
+      e = kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, d->epi_shape, d->chain, hs, nk, gemm_pp_workgroups(d));
       if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
       if (e == hipSuccess && d->row_kind)
         e = kf::launch_row_finish(d->row_kind == KF_OP_ROW_SOFTMAX, ws, d->tiles_n, s.M, s.N, a.out,
@@ -1190,7 +1250,8 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
         return fail(KF_ERR_UNSUPPORTED, "operand extent too large for 32-bit buffer offsets");
     }
     e = d->variant == kVarGemmF32 ? kf::launch_gemm_f32(a, nk, hs)
-                                  : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk);
+                                  : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk,
+                                                         gemm_pp_workgroups(d));
   } else if (conv3d) {
     // the convolution alone: every conv output position, NCDHW
     const kf::Conv3dArgs a = conv3d_args(d, inputs, cur, 0);

@@ -31,7 +31,13 @@ size_t scratch_bytes();
 
 // bf16 or OCP fp8 e4m3 GEMM + epilogue on the matrix cores; `epi` is an
 // EpiShape, `chain` a compile-time chain id (0: the op list is interpreted).
-hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, hipStream_t stream, bool b_nk);
+// pp_workgroups == 0 runs the 256x256 tile kernel; > 0 the 128x256 kernel
+// with two workgroups per CU (B in KN layout only) as a persistent grid of
+// that many workgroups.
+hipError_t launch_gemm_mfma(const GemmArgs& args, bool fp8, int epi, int chain, hipStream_t stream, bool b_nk,
+                            int pp_workgroups);
+// Tiles of the 128x256 kernel for an M x N output.
+int64_t gemm_pp_tiles(int64_t M, int64_t N);
 int gemm_mfma_tile_m();
 int gemm_mfma_tile_n();
 

@@ -782,12 +782,17 @@ def test_specialised_chain_matches_interpreted(name, kw):
     ("F2", dict(batch=3, D=9, H=19, W=35)),                               # conv3d, partial tiles
     ("C4", dict(batch=3, H=10)),                                          # conv: 4- and 8-wave tiles
     ("C4", dict(batch=2, H=8, ops=[("bias",), ("swish",)])),              # unpooled, interpreted epilogue
+    ("C2", dict(M=300, N=1040, K=200)),                                   # ragged GEMM, logsumexp rows
+    ("F1", dict(M=520, N=776, K=136)),                                    # activation chain
+    ("F6", dict(M=260, N=1040, K=72)),                                    # cross-entropy rows
+    ("C3", dict(M=300, N=512, K=72, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
+    ("C2", dict(M=600, N=520, K=64, ops=[("bias",), ("sigmoid",), ("row_softmax",)], out_dtype="bf16")),  # interpreted
 ])
 def test_tuning_candidates_bit_identical(name, kw):
     """Every launch configuration the tuner may pick computes the same bits:
     the fields only reorder independent tiles, resize a persistent grid, or
-    split the conv tile among 4 or 8 waves (each output's sum over k in the
-    same order)."""
+    change the tile shape (GEMM 256x256 or 128x256, conv 4 or 8 waves) with
+    each output's sum over k in the same order."""
     torch = _torch()
     cfg = inputs.config(name, **kw)
     t = inputs.generate(cfg, seed=51)
@@ -797,7 +802,7 @@ def test_tuning_candidates_bit_identical(name, kw):
     op(ins, ref)
     configs = ([(4, r, w, 0) for r in (1, 0) for w in (2, 1)] if name == "F2" else
                [(4, 1, 2, v) for v in (1, 0)] if name == "C4" else
-               [(g, r, 2, 0) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)])
+               [(g, r, 2, 0) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)] + [(4, 1, 2, 1)])
     for g, r, w, v in configs:
         op.set_tuning(g, r, w, v)
         out = op.empty_output("cuda")
@@ -837,7 +842,7 @@ def test_full_size_tuned_launch_bit_identical(name):
 
 
 @pytest.mark.parametrize("name,kw,n", [
-    ("C2", dict(M=1024, N=2048, K=512), 14),
+    ("C2", dict(M=1024, N=2048, K=512), 15),
     ("F2", dict(batch=2, D=10, H=18, W=34), 4),
     ("F4", dict(M=256, N=2048), 1),
     ("C4", dict(batch=8, H=16), 2),
@@ -869,6 +874,26 @@ def test_autotune_keeps_the_fastest_candidate(name, kw, n):
     check(cfg, t, out2)
     with pytest.raises(kf.KFError):
         op.set_tuning(0, 1, 2)
+
+
+def test_autotune_picks_the_tile_shape():
+    """A short GEMM (256 x 8192 x 4096: 32 tiles of 256 x 256 for 256 CUs)
+    runs faster with 128 x 256 tiles (64 tiles, two workgroups per CU): the
+    tuner keeps that shape there, and the 256 x 256 tile at C2's size."""
+    _torch()
+    kept = {}
+    for tag, kw in (("short", dict(M=256, N=8192, K=4096)), ("C2", {})):
+        cfg = inputs.config("F6", **kw) if tag == "short" else inputs.config("C2")
+        t = inputs.generate(cfg, seed=9)
+        op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+        ins = op.device_inputs(t)
+        out = op.empty_output("cuda")
+        r = op.autotune(ins, out, reps=3)
+        kept[tag] = r["best"]["variant"]
+        times = {c["variant"]: c["seconds"] for c in r["candidates"] if c["variant"] == 1}
+        print(tag, r["best"], times)
+        check(cfg, t, out, rows=sample_rows(cfg["M"], 8, seed=2))
+    assert kept == {"short": 1, "C2": 0}, kept
 
 
 def test_panel_traffic_model():
