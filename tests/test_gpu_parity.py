@@ -69,6 +69,43 @@ def test_bf16_contraction_bit_exact_full_size():
     assert np.array_equal(g.astype(np.float64), ref)
 
 
+def test_bf16_contraction_bit_exact_c3_shape():
+    """The integer test at C3's shape (8192 x 2048 times 2048 x 8192, 1024
+    tiles: four per CU in the kept tile order and in both tile shapes),
+    every output checked."""
+    torch = _torch()
+    M, N, K = 8192, 8192, 2048
+    rng = np.random.default_rng(13)
+    a = rng.integers(-8, 9, size=(M, K)).astype(np.float32)
+    b = rng.integers(-8, 9, size=(K, N)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(a), "b": inputs.f32_to_bf16_bits(b)}
+    cfg = inputs.config("C3", out_dtype="f32", ops=[])
+    ref = a.astype(np.float64) @ b.astype(np.float64)
+    for tuning in ((2, 0, 2, 0), (4, 1, 2, 1)):
+        print(f"bit-exact 8192x8192x2048 tuning {tuning}", flush=True)
+        _, out = run_gpu(cfg, t, tuning=tuning)
+        assert np.array_equal(out.cpu().numpy().astype(np.float64), ref), tuning
+        del out
+
+
+def test_fp8_contraction_bit_exact_c5_shape():
+    """The integer test at C5's full 8192^3 (unit scales; 1024 sampled rows
+    against float64 products, exact since every partial sum is an integer
+    below 2^22)."""
+    _torch()
+    M = N = K = 8192
+    rng = np.random.default_rng(32)
+    a, qa = _int_e4m3(rng, (M, K))
+    b, qb = _int_e4m3(rng, (K, N))
+    t = {"a": qa, "b": qb, "scale_a": 1.0, "scale_b": 1.0}
+    cfg = inputs.config("C5", out_dtype="f32", ops=[])
+    print("fp8 bit-exact 8192^3", flush=True)
+    _, out = run_gpu(cfg, t)
+    rows = sample_rows(M, 1024, seed=5)
+    ref = a[rows].astype(np.float64) @ b.astype(np.float64)
+    assert np.array_equal(out.cpu().numpy()[rows].astype(np.float64), ref)
+
+
 def test_bf16_contraction_bit_exact_nk_ragged():
     torch = _torch()
     M, N, K = 300, 264, 200
@@ -131,7 +168,7 @@ def test_c3_full_config_sampled_rows():
     cfg = inputs.config("C3")
     t = inputs.generate(cfg)
     _, out = run_gpu(cfg, t)
-    rows = sample_rows(cfg["M"], 32)
+    rows = sample_rows(cfg["M"], 256)
     err = check(cfg, t, out, rows=rows)
     print(f"C3 full err {err:.3e}")
 
@@ -329,7 +366,7 @@ def test_c5_full_config_sampled_rows():
     cfg = inputs.config("C5")
     t = inputs.generate(cfg)
     _, out = run_gpu(cfg, t)
-    rows = sample_rows(cfg["M"], 16)
+    rows = sample_rows(cfg["M"], 128)
     err = check(cfg, t, out, rows=rows)
     g = to_host_f64(out)
     assert np.all(np.isfinite(g))
@@ -443,6 +480,24 @@ def test_c4_integer_bit_exact():
     assert np.array_equal(got_bits, ref_bits)
 
 
+def test_c4_integer_bit_exact_full_batch():
+    """The integer test at C4's full size (64 images of 64 x 128 x 128, 4096
+    row-pair tiles), eight images checked bit for bit."""
+    torch = _torch()
+    cfg = inputs.config("C4", ops=[])
+    rng = np.random.default_rng(43)
+    x = rng.integers(-4, 5, size=(64, 64, 128, 128)).astype(np.float32)
+    w = rng.integers(-2, 3, size=(128, 64, 3, 3)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
+    print("C4 integer bit-exact, full batch", flush=True)
+    _, out = run_gpu(cfg, t)
+    imgs = np.array([0, 9, 21, 32, 40, 51, 62, 63])
+    ref = oracle.conv2d_3x3(x[imgs].astype(np.float64), w.astype(np.float64))
+    ref_bits = inputs.f32_to_bf16_bits(ref.astype(np.float32))
+    got_bits = out.view(torch.int16).cpu().numpy().view(np.uint16)[imgs]
+    assert np.array_equal(got_bits, ref_bits)
+
+
 def test_c4_zero_weights_and_centre_tap():
     _torch()
     cfg = inputs.config("C4", batch=1, H=4)
@@ -466,7 +521,7 @@ def test_c4_full_config_sampled_images(variant):
     cfg = inputs.config("C4")
     t = inputs.generate(cfg)
     _, out = run_gpu(cfg, t, tuning=(4, 1, 2, variant))
-    err = check(cfg, t, out, images=np.array([0, 37, 63]))
+    err = check(cfg, t, out, images=np.array([0, 5, 19, 26, 37, 44, 58, 63]))
     assert np.all(np.isfinite(to_host_f64(out)))
     print(f"C4 full err {err:.3e}")
 
