@@ -118,6 +118,7 @@ KERNEL_FILES = {
     "kf_rowwise_gn_panel": ["kf_rowwise.hip"],
     "kf_row_reduce_stream": ["kf_rowwise.hip"],
     "kf_conv3d_bf16_64x256": ["kf_conv3d_bf16.hip"],
+    "kf_conv3d_bf16_gen": ["kf_conv3d_gen.hip"],
 }
 
 

@@ -61,18 +61,23 @@ typedef enum kf_contraction {
   /* No contraction: h = A, an [M,N] row-major tensor (fp32 or bf16, any row
      stride), and the op list runs over its rows -- the memory-bound
      reduction chains (softmax, logsumexp, GroupNorm with their element-wise
-     neighbours).  No B input; K is ignored.  N <= 16384, N % 8 == 0;
-     GROUPNORM needs (N / groups) % 8 == 0. */
+     neighbours).  No B input; K is ignored.  N % 8 == 0; N <= 16384, except
+     for a list that ends with ROW_LOGSUMEXP or ROW_CROSS_ENTROPY after only
+     BIAS and element-wise ops (rows streamed: N < 2^31); GROUPNORM needs
+     (N / groups) % 8 == 0. */
   KF_ROWWISE = 2,
   /* PyTorch Conv3d (3-D cross-correlation), 3x3x3 kernel, stride 1, no
      padding (Conv3d's default), dilation 1, groups 1 -- the convolution of
      the Conv3d -> softmax -> max-pool operator in the paper's case study
      (Appendix C).  A = input [batch,cin,depth,height,width] stored
      channels-last (torch.channels_last_3d: strides [D*H*W*cin, 1, H*W*cin,
-     W*cin, cin]), B = weight [cout,cin,3,3,3] contiguous (OIDHW); h is
-     [batch,cout,depth-2,height-2,width-2].  bf16 in and out; built for
-     cin = 16 and cout = 64 (the whole channel axis in one tile, so a channel
-     softmax is tile-local). */
+     W*cin, cin]) or, for lists of BIAS and element-wise ops only, contiguous
+     NCDHW; B = weight [cout,cin,3,3,3] contiguous (OIDHW); h is
+     [batch,cout,depth-2,height-2,width-2].  bf16 in and out.  cin = 16,
+     cout = 64 with a channels-last input runs the tiled kernel, which also
+     fuses CHANNEL_SOFTMAX and MAXPOOL3D_2 (the whole channel axis in one
+     tile, so the channel softmax is tile-local); any other cin, cout or
+     layout runs the general kernel, which takes BIAS and element-wise ops. */
   KF_CONV3D_3X3X3 = 3
 } kf_contraction;
 

@@ -48,6 +48,7 @@ struct Slot {
   int64_t shape[KF_MAX_DIMS];
   const char* name;
   bool channels_last;  // a 5-D [N, C, D, H, W] tensor stored as [N][D][H][W][C]
+  bool or_dense = false;  // channels_last slot that also takes a contiguous [N, C, D, H, W]
 };
 
 // The input slots of a plan: A, B and at most one bias, gamma, beta and
@@ -89,6 +90,7 @@ struct kf_desc {
   int row_kind;  // KF_OP_ROW_SOFTMAX / KF_OP_ROW_LOGSUMEXP / KF_OP_ROW_CROSS_ENTROPY / 0
   int chain = 0;  // compile-time epilogue chain matching the op list (0: interpreted)
   bool conv_special = false;  // CONV2D_3X3 in the tiled kernels' shape family
+  bool conv3d_tiled = false;  // CONV3D_3X3X3 in the tiled kernel's shape family (cin 16, cout 64)
   SlotList inputs;
   Slot output;
   int device;
@@ -103,6 +105,7 @@ struct kf_desc {
   // conv plans: the weight tensor whose repacked copy the workspace holds
   // (nullptr: none yet, or the caller declared the weights changed)
   mutable const void* packed_from = nullptr;
+  mutable int packed_kind = 0;  // conv3d: 1 = packed for the tiled kernel, 2 = for the general one
 };
 
 namespace {
@@ -311,11 +314,20 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     if (s->out_dtype != KF_BF16) return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 writes bf16 outputs only");
     if (s->batch < 0 || s->cin < 1 || s->cout < 1 || s->depth < 3 || s->height < 3 || s->width < 3)
       return fail(KF_ERR_SHAPE, "CONV3D_3X3X3 needs batch >= 0, cin, cout >= 1 and depth, height, width >= 3");
-    if (s->cin != kf::conv3d_cin() || s->cout != kf::conv3d_cout())
-      return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 kernel is built for cin=%d, cout=%d", kf::conv3d_cin(),
-                  kf::conv3d_cout());
-    if (s->depth * s->height * s->width * s->cin * 2 >= (int64_t(1) << 30))
+    // the tiled kernel: cin 16, cout 64, channels-last input, the whole op
+    // family; every other shape or layout: the general kernel, BIAS and
+    // element-wise ops
+    d->conv3d_tiled = s->cin == kf::conv3d_cin() && s->cout == kf::conv3d_cout();
+    if (!d->conv3d_tiled && (n_pool3 || n_csm))
+      return fail(KF_ERR_UNSUPPORTED,
+                  "CONV3D_3X3X3 fuses CHANNEL_SOFTMAX and MAXPOOL3D_2 for cin = %d, cout = %d (channels-last "
+                  "input); other shapes take BIAS and element-wise ops",
+                  kf::conv3d_cin(), kf::conv3d_cout());
+    if (d->conv3d_tiled && s->depth * s->height * s->width * s->cin * 2 >= (int64_t(1) << 30))
       return fail(KF_ERR_UNSUPPORTED, "one input volume must be smaller than 1 GiB");
+    if (s->cin > (int64_t(1) << 20) || s->cout > (int64_t(1) << 20) ||
+        kf::conv3d_gen_tiles(s->batch, s->depth, s->height, s->width, s->cout) > INT32_MAX)
+      return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 (general kernel) supports at most 2^31 - 1 tiles and 2^20 channels");
     if (n_pool3 != 0 && n_pool3 != 2)
       return fail(KF_ERR_UNSUPPORTED, "CONV3D_3X3X3 takes zero or two MAXPOOL3D_2 ops (got %d)", n_pool3);
     for (int i = 0; i < s->n_ops; ++i) {
@@ -334,8 +346,11 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
       ow /= 2;
     }
     d->variant = kVarConv3d;
-    d->kernel_name = "kf_conv3d_bf16_64x256";
-    d->inputs.push_back(Slot{dt, 5, {s->batch, s->cin, s->depth, s->height, s->width}, "A", true});
+    d->kernel_name = d->conv3d_tiled ? "kf_conv3d_bf16_64x256" : "kf_conv3d_bf16_gen";
+    // channels-last input; a contiguous NCDHW one too where the general
+    // kernel can run the list
+    d->inputs.push_back(Slot{dt, 5, {s->batch, s->cin, s->depth, s->height, s->width}, "A", true,
+                             !(n_pool3 || n_csm)});
     d->inputs.push_back(Slot{dt, 5, {s->cout, s->cin, 3, 3, 3}, "B", false});
     for (int i = 0; i < s->n_ops; ++i)
       if (s->ops[i].kind == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->cout, 0, 0, 0, 0}, "bias", false});
@@ -397,10 +412,16 @@ kf_status check_tensor(const kf_tensor* t, const Slot& s, bool is_output, bool v
     const int64_t C = s.shape[1];
     const int64_t expect[5] = {s.shape[2] * s.shape[3] * s.shape[4] * C, 1, s.shape[3] * s.shape[4] * C,
                                s.shape[4] * C, C};
-    for (int i = 0; i < 5; ++i)
-      if (t->stride[i] != expect[i] && s.shape[i] != 1)
-        return fail(KF_ERR_UNSUPPORTED, "%s '%s': must be channels-last (torch.channels_last_3d) and dense", what,
-                    s.name);
+    bool cl = true, dense = s.or_dense;
+    int64_t run = 1;
+    for (int i = 4; i >= 0; --i) {
+      if (t->stride[i] != expect[i] && s.shape[i] != 1) cl = false;
+      if (t->stride[i] != run && s.shape[i] != 1) dense = false;
+      run *= s.shape[i];
+    }
+    if (!cl && !dense)
+      return fail(KF_ERR_UNSUPPORTED, "%s '%s': must be channels-last (torch.channels_last_3d)%s and dense", what,
+                  s.name, s.or_dense ? " or contiguous NCDHW" : "");
   } else if (t->stride[s.ndim - 1] != 1) {
     return fail(KF_ERR_UNSUPPORTED, "%s '%s': innermost stride must be 1", what, s.name);
   }
@@ -467,6 +488,54 @@ int conv3d_pool_count(const kf_op_spec& s) {
   return n;
 }
 
+// The tiled conv3d kernel takes this call: a plan in its shape family with a
+// channels-last input (channel stride 1; a contiguous NCDHW input has a
+// channel stride of D H W >= 27).
+bool conv3d_uses_tiled(const kf_desc* d, const kf_tensor* inputs) {
+  return d->conv3d_tiled && inputs[0].stride[1] == 1;
+}
+
+// Kernel arguments of the general conv3d kernel (op list `prog`: the plan's,
+// or none for the unfused chain's convolution).
+kf::Conv3dGenArgs conv3d_gen_args(const kf_desc* d, const kf_tensor* inputs, void* out, const kf::EpiProgram& prog) {
+  const kf_op_spec& s = d->spec;
+  kf::Conv3dGenArgs g;
+  memset(&g, 0, sizeof(g));
+  const kf_tensor& x = inputs[0];
+  g.x = x.data;
+  g.sn = x.stride[0];
+  g.sc = x.stride[1];
+  g.sd = x.stride[2];
+  g.sh = x.stride[3];
+  g.sw = x.stride[4];
+  g.batch = (int32_t)s.batch;
+  g.cin = (int32_t)s.cin;
+  g.cout = (int32_t)s.cout;
+  g.D = (int32_t)s.depth;
+  g.H = (int32_t)s.height;
+  g.W = (int32_t)s.width;
+  g.prog = prog;
+  for (int i = 0; i < prog.n; ++i)
+    if (prog.op[i].kind == KF_OP_BIAS) g.bias = static_cast<const float*>(inputs[2].data);
+  g.out = out;
+  return g;
+}
+
+// Repack a conv3d plan's weights into ws for the kernel this call takes,
+// unless ws already holds them (keep: the descriptor's own workspace).
+hipError_t conv3d_pack(const kf_desc* d, void* ws, bool keep, bool tiled, const void* w, hipStream_t hs) {
+  const int want = tiled ? 1 : 2;
+  if (keep && d->packed_from == w && d->packed_kind == want) return hipSuccess;
+  d->packed_from = nullptr;
+  const hipError_t e = tiled ? kf::launch_conv3d_pack(w, ws, hs)
+                             : kf::launch_conv3d_gen_pack(w, ws, (int)d->spec.cout, (int)d->spec.cin, hs);
+  if (e == hipSuccess && keep) {
+    d->packed_from = w;
+    d->packed_kind = want;
+  }
+  return e;
+}
+
 
 // Algorithmic work of the plan's main kernel: FLOPs (2 per multiply-add of
 // the contraction), bytes (each input read once, the output written once),
@@ -519,7 +588,8 @@ Work plan_work(const kf_desc* d) {
       int pools = 0;
       for (int i = 0; i < s.n_ops; ++i) pools += s.ops[i].kind == KF_OP_MAXPOOL3D_2;
       const kf::Conv3dArgs a = conv3d_args(d, nullptr, nullptr, pools);
-      w.workgroups = std::min<int64_t>(a.grid, a.tiles);
+      w.workgroups = d->conv3d_tiled ? std::min<int64_t>(a.grid, a.tiles)
+                                     : kf::conv3d_gen_tiles(s.batch, s.depth, s.height, s.width, s.cout);
       break;
     }
     case kVarRowwise:
@@ -578,7 +648,13 @@ kf_status current_device(int* dev_out, int* cus_out) {
 size_t plan_workspace_bytes(const kf_desc* d) {
   const kf_op_spec& s = d->spec;
   if (d->variant == kVarConvBf16) return (size_t)9 * s.cout * kf::conv_gen_cin_pad((int)s.cin) * 2;
-  if (d->variant == kVarConv3d) return kf::conv3d_packed_bytes();
+  if (d->variant == kVarConv3d) {
+    const size_t gen = kf::conv3d_gen_packed_bytes(s.cout, s.cin);
+    if (!d->conv3d_tiled) return gen;
+    // the tiled kernel's packing, or the general one's for an NCDHW input
+    return d->inputs.size() && d->inputs[0].or_dense ? std::max(kf::conv3d_packed_bytes(), gen)
+                                                     : kf::conv3d_packed_bytes();
+  }
   if (d->row_kind && d->variant != kVarRowwise) {
     // per-(row, tile) (max, sum) pairs; cross-entropy adds h[m][t_m] per row
     const size_t rows = (size_t)std::max<int64_t>(s.M, 1);
@@ -1007,16 +1083,14 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
   const kf_op_spec& s = d->spec;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   if (s.contraction == KF_CONV3D_3X3X3) {
+    const bool tiled = conv3d_uses_tiled(d, inputs);
     const kf::Conv3dArgs a = conv3d_args(d, inputs, outputs[0].data, conv3d_pool_count(s));
-    if (a.tiles == 0) return ok();
-    hipError_t e = hipSuccess;
-    if (!ws_keeps_weights || d->packed_from != inputs[1].data) {
-      d->packed_from = nullptr;
-      e = kf::launch_conv3d_pack(inputs[1].data, ws, hs);
-      if (e == hipSuccess && ws_keeps_weights) d->packed_from = inputs[1].data;
-    }
+    if (tiled ? a.tiles == 0 : kf::conv3d_gen_tiles(s.batch, s.depth, s.height, s.width, s.cout) == 0) return ok();
+    hipError_t e = conv3d_pack(d, ws, ws_keeps_weights, tiled, inputs[1].data, hs);
     if (e == hipSuccess && ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
-    if (e == hipSuccess) e = kf::launch_conv3d_bf16(a, ws, d->chain, hs);
+    if (e == hipSuccess)
+      e = tiled ? kf::launch_conv3d_bf16(a, ws, d->chain, hs)
+                : kf::launch_conv3d_gen(conv3d_gen_args(d, inputs, outputs[0].data, d->prog), ws, hs);
     if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
     if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
@@ -1254,13 +1328,15 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
                                                          gemm_pp_workgroups(d));
   } else if (conv3d) {
     // the convolution alone: every conv output position, NCDHW
+    const bool tiled = conv3d_uses_tiled(d, inputs);
     const kf::Conv3dArgs a = conv3d_args(d, inputs, cur, 0);
-    if (d->packed_from != inputs[1].data) {
-      d->packed_from = nullptr;
-      e = kf::launch_conv3d_pack(inputs[1].data, d->workspace, hs);
-      if (e == hipSuccess) d->packed_from = inputs[1].data;
+    e = conv3d_pack(d, d->workspace, true, tiled, inputs[1].data, hs);
+    if (e == hipSuccess && tiled && a.tiles) e = kf::launch_conv3d_bf16(a, d->workspace, 1, hs);
+    if (e == hipSuccess && !tiled) {
+      kf::EpiProgram none;
+      memset(&none, 0, sizeof(none));
+      e = kf::launch_conv3d_gen(conv3d_gen_args(d, inputs, cur, none), d->workspace, hs);
     }
-    if (e == hipSuccess && a.tiles) e = kf::launch_conv3d_bf16(a, d->workspace, 1, hs);
   } else {
     kf::ConvArgs c;
     memset(&c, 0, sizeof(c));

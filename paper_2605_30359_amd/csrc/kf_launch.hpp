@@ -95,6 +95,24 @@ int conv3d_cin();
 int conv3d_cout();
 size_t conv3d_packed_bytes();
 
+// The general 3x3x3 conv (any batch, cin, cout, D, H, W >= 3) + bias and
+// element-wise ops, reading the input through its element strides (NCDHW or
+// channels-last), writing NCDHW; launch_conv3d_gen_pack repacks the OIDHW
+// weights into `packed` (conv3d_gen_packed_bytes()), launch_conv3d_gen runs
+// conv3d_gen_tiles(...) workgroups (fewer than 2^31).
+struct Conv3dGenArgs {
+  const void* x;                      // input [batch, cin, D, H, W] at these element strides
+  int64_t sn, sc, sd, sh, sw;
+  int32_t batch, cin, cout, D, H, W;
+  EpiProgram prog;                    // BIAS and element-wise ops
+  const float* bias;                  // [cout] or null
+  void* out;                          // [batch, cout, D - 2, H - 2, W - 2] contiguous
+};
+hipError_t launch_conv3d_gen_pack(const void* w, void* packed, int cout, int cin, hipStream_t stream);
+hipError_t launch_conv3d_gen(const Conv3dGenArgs& args, const void* packed, hipStream_t stream);
+int64_t conv3d_gen_tiles(int64_t batch, int64_t D, int64_t H, int64_t W, int64_t cout);
+size_t conv3d_gen_packed_bytes(int64_t cout, int64_t cin);
+
 }  // namespace kf
 
 namespace kf {

@@ -421,8 +421,9 @@ class FusedOp:
         cands = [dict(r.config[i].as_dict(), seconds=r.seconds[i], panel_bytes=r.panel_bytes[i]) for i in range(r.n)]
         return {"best": cands[r.best], "candidates": cands}
 
-    def device_inputs(self, tensors: dict, device="cuda") -> list:
-        """Marshal raw generated storage into the slot order of this op."""
+    def device_inputs(self, tensors: dict, device="cuda", conv3d_channels_last=True) -> list:
+        """Marshal raw generated storage into the slot order of this op (a
+        conv3d input channels-last unless conv3d_channels_last is False)."""
         out = []
         for name in input_names(self.chain):
             if name in ("a", "b"):
@@ -433,7 +434,7 @@ class FusedOp:
                 dt = "i32"
             else:
                 dt = "f32"
-            cl = name == "a" and self.chain["contraction"] == "conv3d_3x3x3"
+            cl = name == "a" and self.chain["contraction"] == "conv3d_3x3x3" and conv3d_channels_last
             out.append(device_tensor(tensors[name], dt, device, channels_last=cl))
         return out
 

@@ -268,7 +268,11 @@ def test_rowwise_input_slots():
 
 
 def test_conv3d_validation():
+    ok = kf.KF_ERR_NO_DEVICE if not _gpu_present() else kf.KF_OK
     for kw, status in [(dict(cin=32), kf.KF_ERR_UNSUPPORTED), (dict(cout=32), kf.KF_ERR_UNSUPPORTED),
+                       (dict(cin=32, ops=[("bias",), ("relu",)]), ok),      # the general kernel
+                       (dict(cin=3, cout=200, D=3, H=3, W=3, ops=[]), ok),
+                       (dict(cout=32, ops=[("bias",), ("channel_softmax",)]), kf.KF_ERR_UNSUPPORTED),
                        (dict(D=2), kf.KF_ERR_SHAPE), (dict(W=2), kf.KF_ERR_SHAPE),
                        (dict(out_dtype="f32"), kf.KF_ERR_UNSUPPORTED), (dict(in_dtype="f32"), kf.KF_ERR_UNSUPPORTED),
                        (dict(ops=[("bias",), ("channel_softmax",), ("maxpool3d2",)]), kf.KF_ERR_UNSUPPORTED),
@@ -281,7 +285,9 @@ def test_conv3d_validation():
                        (dict(D=2000, H=2000, W=20), kf.KF_ERR_UNSUPPORTED)]:
         st, h = _create(_spec("F2", **kw))
         assert st == status, (kw, st, kf.last_error())
-        assert not h.value
+        assert bool(h.value) == (st == kf.KF_OK)
+        if h.value:
+            kf.lib().kf_destroy(h)
     # the conv3d ops on other contractions
     for name, ops in [("C2", [("channel_softmax",)]), ("C4", [("maxpool3d2",), ("maxpool3d2",)]),
                       ("F4", [("channel_softmax",)])]:

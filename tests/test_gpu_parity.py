@@ -634,6 +634,71 @@ def test_f2_small(batch, D, H, W, ops):
     print(f"F2 {batch}x{D}x{H}x{W} ops={[o[0] for o in ops]} err {err:.3e}")
 
 
+_CONV3D_GEN_DIST = dict(a=("normal", 1.0), b=("normal_invk",), bias=("uniform", -0.1, 0.1))
+
+
+@pytest.mark.parametrize("batch,cin,cout,D,H,W,ops,cl", [
+    (2, 8, 32, 5, 9, 20, [("bias",)], True),                        # small channel counts, one partial tile
+    (1, 24, 96, 4, 12, 40, [("bias",), ("gelu_erf",)], False),      # NCDHW input, cin past one 16-chunk
+    (2, 40, 160, 3, 7, 35, [("bias",), ("relu",), ("scale", 0.5)], True),  # two channel tiles, ragged
+    (1, 16, 64, 6, 10, 18, [("bias",), ("tanh",)], False),          # the tiled family's shape, NCDHW input
+    (1, 3, 5, 3, 3, 3, [], False),                                  # one output position
+])
+def test_conv3d_general_shapes(batch, cin, cout, D, H, W, ops, cl):
+    """The general Conv3d kernel: any channel counts and extents, input
+    channels-last or contiguous NCDHW, bias and element-wise ops fused."""
+    _torch()
+    cfg = inputs.config("F2", batch=batch, cin=cin, cout=cout, D=D, H=H, W=W, ops=ops, dist=_CONV3D_GEN_DIST)
+    t = inputs.generate(cfg, seed=cin + cout + D)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    if (cin, cout) != (16, 64):
+        assert op.kernel_name() == "kf_conv3d_bf16_gen"
+    ins = op.device_inputs(t, conv3d_channels_last=cl)
+    out = op.empty_output("cuda")
+    op(ins, out)
+    err = check(cfg, t, out)
+    out2 = op.empty_output("cuda")
+    op.unfused(ins, out2)
+    check(cfg, t, out2, unfused=True)
+    print(f"conv3d general {batch}x{cin}->{cout} {D}x{H}x{W} cl={cl} err {err:.3e}")
+
+
+@pytest.mark.parametrize("cl", [True, False])
+def test_conv3d_general_integer_bit_exact(cl):
+    """Integer inputs and weights: every partial sum is an exact integer, so
+    the general kernel's output (no ops) is the exact sum rounded to bf16."""
+    torch = _torch()
+    batch, cin, cout, D, H, W = 2, 40, 136, 5, 11, 37
+    cfg = inputs.config("F2", batch=batch, cin=cin, cout=cout, D=D, H=H, W=W, ops=[])
+    rng = np.random.default_rng(45)
+    x = rng.integers(-4, 5, size=(batch, cin, D, H, W)).astype(np.float32)
+    w = rng.integers(-2, 3, size=(cout, cin, 3, 3, 3)).astype(np.float32)
+    t = {"a": inputs.f32_to_bf16_bits(x), "b": inputs.f32_to_bf16_bits(w)}
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t, conv3d_channels_last=cl)
+    out = op.empty_output("cuda")
+    op(ins, out)
+    ref = oracle.conv3d_3x3x3(x.astype(np.float64), w.astype(np.float64))
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, inputs.f32_to_bf16_bits(ref.astype(np.float32)))
+
+
+def test_conv3d_family_layouts():
+    """The tiled family's shape with the F2 chain needs a channels-last input
+    (refused for NCDHW); with bias and element-wise ops alone an NCDHW input
+    runs the general kernel and gives the oracle's result."""
+    _torch()
+    cfg = inputs.config("F2", batch=1, D=6, H=10, W=18)
+    t = inputs.generate(cfg, seed=5)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    with pytest.raises(kf.KFError) as e:
+        op(op.device_inputs(t, conv3d_channels_last=False), op.empty_output("cuda"))
+    assert e.value.status == kf.KF_ERR_UNSUPPORTED
+    out = op.empty_output("cuda")
+    op(op.device_inputs(t), out)
+    check(cfg, t, out)
+
+
 def test_f2_degenerate_shapes():
     """3x3x3 volumes (one conv position: no pooled cell) and an empty batch
     produce empty outputs without a launch."""
