@@ -15,8 +15,9 @@ gets a block of the same fields under "also".  Per workload:
                over the K back-to-back steps)
   steps_us     per-step HIP-event times: median, min, p90, mean -- warm
                (back-to-back steps, a second loop of K steps) and cold (a
-               512 MiB device write between steps, outside the events,
-               evicts the L2s and the 256 MB Infinity Cache)
+               read of a 512 MiB device buffer between steps, outside the
+               events, evicts the L2s and the 256 MB Infinity Cache and
+               leaves them clean)
   roofline     the main contraction kernel alone, timed live with HIP events
                recorded on its stream around each launch (achieved = the
                algorithmic FLOPs per launch / the mean launch time; median,
@@ -206,8 +207,10 @@ def _cpu_baseline(cfg, tensors, gpu_out, budget_s: float):
 def _timed_steps(hip, torch, run, steps, flush=None, kernel_events=True, step_events=True):
     """`steps` calls of run(ev_before, ev_after) on the current stream,
     bracketed by two events, each step between two step events if
-    step_events; `flush` (a device tensor) is overwritten before every step,
-    outside the events.  run() records ev_before / ev_after around its main
+    step_events; `flush` (a device tensor, written once beforehand) is read
+    whole before every step, outside the events: the caches then hold its
+    clean lines, and whatever the previous step left dirty in them is
+    written back before the step starts.  run() records ev_before / ev_after around its main
     kernel when kernel_events is set.  Returns (total ms of the loop,
     per-step ms, per-kernel ms)."""
     stream = torch.cuda.current_stream()
@@ -219,7 +222,7 @@ def _timed_steps(hip, torch, run, steps, flush=None, kernel_events=True, step_ev
     hip.hipEventRecord(ctypes.c_void_p(start), s)
     for i in range(steps):
         if flush is not None:
-            flush.fill_(i & 0xFF)
+            flush.view(torch.int32).sum()
         if step_events:
             hip.hipEventRecord(ctypes.c_void_p(sev[i][0]), s)
         run(*(kev[i] if kernel_events else (None, None)))
@@ -283,7 +286,7 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
     _, step_ms, _ = _timed_steps(hip, torch, lambda e0, e1: op(ins, out), K, kernel_events=False)
     cold = None
     if args.cold_steps > 0:
-        flush = torch.empty(COLD_FLUSH_BYTES, dtype=torch.uint8, device="cuda:0")
+        flush = torch.ones(COLD_FLUSH_BYTES, dtype=torch.uint8, device="cuda:0")
         _, c_step, c_kern = _timed_steps(hip, torch, fused, args.cold_steps, flush=flush)
         del flush
         cold = {"step_us": _stats_us(c_step), "kernel_us": _stats_us(c_kern)}
@@ -386,7 +389,7 @@ def main(argv=None):
                     help="comma-separated workloads timed after the headline, each reported under 'also' "
                          "(default C3,C4; empty for none)")
     ap.add_argument("--cold-steps", type=int, default=10,
-                    help="steps timed with a 512 MiB device write before each (0: no cold timing)")
+                    help="steps timed with a 512 MiB device read before each (0: no cold timing)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
