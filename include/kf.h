@@ -71,13 +71,17 @@ typedef enum kf_contraction {
      the Conv3d -> softmax -> max-pool operator in the paper's case study
      (Appendix C).  A = input [batch,cin,depth,height,width] stored
      channels-last (torch.channels_last_3d: strides [D*H*W*cin, 1, H*W*cin,
-     W*cin, cin]) or, for lists of BIAS and element-wise ops only, contiguous
-     NCDHW; B = weight [cout,cin,3,3,3] contiguous (OIDHW); h is
-     [batch,cout,depth-2,height-2,width-2].  bf16 in and out.  cin = 16,
-     cout = 64 with a channels-last input runs the tiled kernel, which also
-     fuses CHANNEL_SOFTMAX and MAXPOOL3D_2 (the whole channel axis in one
-     tile, so the channel softmax is tile-local); any other cin, cout or
-     layout runs the general kernel, which takes BIAS and element-wise ops. */
+     W*cin, cin]) or contiguous NCDHW; B = weight [cout,cin,3,3,3] contiguous
+     (OIDHW); h is [batch,cout,depth-2,height-2,width-2].  bf16 in and out.
+     cin = 16, cout = 64 with a channels-last input runs the tiled kernel,
+     which fuses the whole op list, CHANNEL_SOFTMAX and MAXPOOL3D_2 included
+     (the whole channel axis in one tile, so the channel softmax is
+     tile-local).  Any other cin, cout or layout runs the general kernel,
+     which fuses the leading BIAS and element-wise ops; a CHANNEL_SOFTMAX or
+     MAXPOOL3D_2 and every op after it then run partly fused: one kernel per
+     op over bf16 intermediates in two buffers the descriptor allocates on
+     the first such call (2 x batch x cout x (depth-2)(height-2)(width-2)
+     bf16; KF_ERR_OOM if that fails), which kf_fused_op_noalloc refuses. */
   KF_CONV3D_3X3X3 = 3
 } kf_contraction;
 
@@ -206,7 +210,8 @@ kf_status kf_fused_op(const kf_desc* desc, const kf_tensor* inputs,
 /* kf_fused_op, additionally recording `ev_before` and `ev_after` (hipEvent_t
    created by the caller, passed as void*) on `stream` immediately before and
    after the main contraction kernel, so that hipEventElapsedTime gives that
-   kernel's duration alone (finishing kernels fall outside the pair).  Either
+   kernel's duration alone (finishing kernels, and the per-op kernels of a
+   partly fused Conv3d chain, fall outside the pair).  Either
    event may be NULL. */
 kf_status kf_fused_op_timed(const kf_desc* desc, const kf_tensor* inputs,
                             kf_tensor* outputs, void* stream, void* ev_before,
@@ -419,7 +424,8 @@ kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs
    Arguments, tensor rules and errors are those of kf_create and
    kf_fused_op; an op whose workspace exceeds the scratch (e.g. a row softmax
    with more than 512 K (row, 256-column tile) pairs) is rejected with
-   KF_ERR_UNSUPPORTED before any device call.  Every call on one GPU uses the
+   KF_ERR_UNSUPPORTED before any device call, and so is a Conv3d chain that
+   runs partly fused (it needs intermediate buffers).  Every call on one GPU uses the
    same scratch and nothing in it needs to start at zero (each call writes
    what it reads); calls that overlap on one GPU -- on different streams or
    host threads -- race on it and must be serialised by the caller.  Conv

@@ -316,14 +316,14 @@ def op_row_cross_entropy(h, targets):
 # Chains
 # --------------------------------------------------------------------------
 
-def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel, store=None) -> np.ndarray:
+def _apply_ops(chain: dict, tensors: dict, h: np.ndarray, sel, store=None, first_store: int = 1) -> np.ndarray:
     """The op list of `chain`, in order, on the float64 contraction result h
     (rows / images `sel` of the full result, or all of it).  `store`, if
-    given, is applied to the result of every op but the last (the storage
-    rounding of an intermediate that is written to memory)."""
+    given, is applied to the input of every op from index `first_store` on
+    (the storage rounding of an intermediate that is written to memory)."""
     ops = chain["ops"]
     for i, op in enumerate(ops):
-        if store is not None and i > 0:
+        if store is not None and i >= first_store:
             h = store(h)
         name, params = op[0], op[1:]
         if name == "bias":
@@ -409,7 +409,7 @@ def intermediate_dtype(chain: dict) -> str:
     return "f32" if chain["in_dtype"] == "f32" else "bf16"
 
 
-def run_chain_unfused(chain: dict, tensors: dict, rows=None, images=None) -> np.ndarray:
+def run_chain_unfused(chain: dict, tensors: dict, rows=None, images=None, fused: int = 0) -> np.ndarray:
     """The chain as a one-operator-per-kernel evaluation computes it -- the
     unfused form that operator fusion removes (Appendix A, "Operator
     Fusion"): the contraction's result and the result of every op but the
@@ -419,12 +419,17 @@ def run_chain_unfused(chain: dict, tensors: dict, rows=None, images=None) -> np.
     applied to the stored values.  A chain with no ops writes the
     contraction's result directly (no intermediate); a row-wise chain's first
     op reads A itself.  The last op's result is returned unrounded, like
-    ``run_chain``'s."""
+    ``run_chain``'s.
+
+    fused > 0: the partly fused evaluation -- the contraction and its first
+    `fused` ops run as one kernel (nothing stored between them), the result
+    of op fused - 1 is stored, then one kernel per remaining op as above.
+    fused = len(ops) is ``run_chain``."""
     store = round_f32 if intermediate_dtype(chain) == "f32" else round_bf16
     h, sel = _contraction(chain, tensors, rows, images)
-    if chain["ops"] and chain["contraction"] != "rowwise":
+    if fused == 0 and chain["ops"] and chain["contraction"] != "rowwise":
         h = store(h)
-    return _apply_ops(chain, tensors, h, sel, store)
+    return _apply_ops(chain, tensors, h, sel, store, first_store=max(fused, 1))
 
 
 def _contraction(chain: dict, tensors: dict, rows=None, images=None):

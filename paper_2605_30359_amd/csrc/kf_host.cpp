@@ -91,6 +91,7 @@ struct kf_desc {
   int chain = 0;  // compile-time epilogue chain matching the op list (0: interpreted)
   bool conv_special = false;  // CONV2D_3X3 in the tiled kernels' shape family
   bool conv3d_tiled = false;  // CONV3D_3X3X3 in the tiled kernel's shape family (cin 16, cout 64)
+  int conv3d_split = 0;       // CONV3D_3X3X3: ops [0, split) are BIAS / element-wise (the general kernel fuses them)
   SlotList inputs;
   Slot output;
   int device;
@@ -318,11 +319,12 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     // family; every other shape or layout: the general kernel, BIAS and
     // element-wise ops
     d->conv3d_tiled = s->cin == kf::conv3d_cin() && s->cout == kf::conv3d_cout();
-    if (!d->conv3d_tiled && (n_pool3 || n_csm))
-      return fail(KF_ERR_UNSUPPORTED,
-                  "CONV3D_3X3X3 fuses CHANNEL_SOFTMAX and MAXPOOL3D_2 for cin = %d, cout = %d (channels-last "
-                  "input); other shapes take BIAS and element-wise ops",
-                  kf::conv3d_cin(), kf::conv3d_cout());
+    // the general kernel fuses the leading BIAS / element-wise ops; a channel
+    // softmax and the pools after them then run as one kernel each
+    d->conv3d_split = 0;
+    while (d->conv3d_split < s->n_ops && (s->ops[d->conv3d_split].kind == KF_OP_BIAS ||
+                                          is_elementwise_kind(s->ops[d->conv3d_split].kind)))
+      ++d->conv3d_split;
     if (d->conv3d_tiled && s->depth * s->height * s->width * s->cin * 2 >= (int64_t(1) << 30))
       return fail(KF_ERR_UNSUPPORTED, "one input volume must be smaller than 1 GiB");
     if (s->cin > (int64_t(1) << 20) || s->cout > (int64_t(1) << 20) ||
@@ -349,8 +351,7 @@ kf_status validate_and_plan(const kf_op_spec* s, kf_desc* d) {
     d->kernel_name = d->conv3d_tiled ? "kf_conv3d_bf16_64x256" : "kf_conv3d_bf16_gen";
     // channels-last input; a contiguous NCDHW one too where the general
     // kernel can run the list
-    d->inputs.push_back(Slot{dt, 5, {s->batch, s->cin, s->depth, s->height, s->width}, "A", true,
-                             !(n_pool3 || n_csm)});
+    d->inputs.push_back(Slot{dt, 5, {s->batch, s->cin, s->depth, s->height, s->width}, "A", true, true});
     d->inputs.push_back(Slot{dt, 5, {s->cout, s->cin, 3, 3, 3}, "B", false});
     for (int i = 0; i < s->n_ops; ++i)
       if (s->ops[i].kind == KF_OP_BIAS) d->inputs.push_back(Slot{KF_F32, 1, {s->cout, 0, 0, 0, 0}, "bias", false});
@@ -668,6 +669,8 @@ size_t plan_workspace_bytes(const kf_desc* d) {
 // holds the repacked copy of this B tensor.
 kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_tensor* inputs, kf_tensor* outputs,
                     void* stream, void* ev_before, void* ev_after);
+kf_status run_chain_split(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int prefix,
+                          void* ev_before, void* ev_after);
 
 // latency-bound if the launch has fewer workgroups than compute units or
 // reaches under 25% of both peaks, else the nearer roof (memory on a tie)
@@ -1084,6 +1087,15 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   if (s.contraction == KF_CONV3D_3X3X3) {
     const bool tiled = conv3d_uses_tiled(d, inputs);
+    if (!tiled && d->conv3d_split < s.n_ops) {
+      // the general kernel with the leading ops fused, then one kernel per
+      // remaining op through the descriptor's intermediate buffers
+      if (!ws_keeps_weights)
+        return fail(KF_ERR_UNSUPPORTED,
+                    "this Conv3d chain takes intermediate buffers outside the tiled kernel's family "
+                    "(use kf_create / kf_fused_op)");
+      return run_chain_split(d, inputs, outputs, stream, d->conv3d_split, ev_before, ev_after);
+    }
     const kf::Conv3dArgs a = conv3d_args(d, inputs, outputs[0].data, conv3d_pool_count(s));
     if (tiled ? a.tiles == 0 : kf::conv3d_gen_tiles(s.batch, s.depth, s.height, s.width, s.cout) == 0) return ok();
     hipError_t e = conv3d_pack(d, ws, ws_keeps_weights, tiled, inputs[1].data, hs);
@@ -1233,17 +1245,15 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
-  if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
-  const bool vec16 = d->variant != kVarGemmF32;
-  for (size_t i = 0; i < d->inputs.size(); ++i) {
-    kf_status st = check_tensor(&inputs[i], d->inputs[i], false, vec16);
-    if (st != KF_OK) return st;
-  }
-  kf_status st = check_tensor(&outputs[0], d->output, true, vec16);
-  if (st != KF_OK) return st;
+// Run plan d as its contraction with ops [0, prefix) fused (prefix > 0 only
+// for the general conv3d kernel: BIAS and element-wise ops), then one kernel
+// per remaining op, every intermediate stored in bf16 (fp32 for an fp32
+// chain) in the descriptor's two buffers, allocated on first use.  prefix 0
+// is the unfused comparator.  ev_before / ev_after bracket the contraction.
+kf_status run_chain_split(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream, int prefix,
+                          void* ev_before, void* ev_after) {
   const kf_op_spec& s = d->spec;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   const bool gemm = s.contraction == KF_GEMM;
@@ -1251,19 +1261,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   const bool conv3d = s.contraction == KF_CONV3D_3X3X3;
   const bool rows = gemm || rowwise;  // an [M, N] intermediate
   if ((rows && s.M == 0) || (!rows && s.batch == 0)) return ok();
-  // the per-op kernels index [M, N] tensors as contiguous rows
-  if (rowwise && inputs[0].stride[0] != s.N)
-    return fail(KF_ERR_UNSUPPORTED, "the unfused ROWWISE chain needs A with row stride N");
-  if (rows && s.n_ops) {
-    for (int i = 0; i < s.n_ops; ++i)
-      if (s.ops[i].kind == KF_OP_GROUPNORM && s.M * s.ops[i].groups >= kMaxRowLaunch)
-        return fail(KF_ERR_UNSUPPORTED, "the unfused GroupNorm supports M * groups < %lld", (long long)kMaxRowLaunch);
-    for (size_t i = 0; i < d->inputs.size(); ++i)
-      if (strcmp(d->inputs[i].name, "residual") == 0 && inputs[i].stride[0] != s.N)
-        return fail(KF_ERR_UNSUPPORTED, "the unfused chain needs a residual with row stride N");
-    if (outputs[0].ndim == 2 && outputs[0].stride[0] != s.N)
-      return fail(KF_ERR_UNSUPPORTED, "the unfused chain needs an output with row stride N");
-  }
+  const int n_rest = s.n_ops - prefix;
 
   // intermediates: bf16 (fp32 for an fp32 chain), full contraction size
   const bool ibf16 = rowwise ? s.in_dtype == KF_BF16 : d->variant != kVarGemmF32;
@@ -1271,7 +1269,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
                          : conv3d ? s.batch * s.cout * (s.depth - 2) * (s.height - 2) * (s.width - 2)
                                   : s.batch * s.cout * s.height * s.width;
   const size_t need = (size_t)n_full * (ibf16 ? 2 : 4);
-  if (d->ubuf_bytes < need) {
+  if (n_rest > 0 && d->ubuf_bytes < need) {
     for (void*& b : d->ubuf) {
       if (b) (void)hipFree(b);
       b = nullptr;
@@ -1288,10 +1286,12 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   //    straight into the output when there are no ops
   void* out = outputs[0].data;
   const bool out_bf16 = outputs[0].dtype == KF_BF16;
-  void* cur = s.n_ops ? d->ubuf[0] : out;
-  bool cur_bf16 = s.n_ops ? ibf16 : out_bf16;
+  void* cur = n_rest ? d->ubuf[0] : out;
+  bool cur_bf16 = n_rest ? ibf16 : out_bf16;
   hipError_t e = hipSuccess;
   size_t slot = 2;
+  for (int i = 0; i < prefix; ++i) slot += s.ops[i].kind == KF_OP_BIAS;  // tensors the fused prefix takes
+  if (ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);
   if (rowwise) {
     // no contraction: the first op reads A itself (an empty list copies it)
     slot = 1;
@@ -1327,15 +1327,17 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
                                   : kf::launch_gemm_mfma(a, d->variant == kVarGemmFp8, kf::kEpiPlain, 1, hs, nk,
                                                          gemm_pp_workgroups(d));
   } else if (conv3d) {
-    // the convolution alone: every conv output position, NCDHW
-    const bool tiled = conv3d_uses_tiled(d, inputs);
+    // the convolution (with the fused prefix): every conv output position, NCDHW
+    const bool tiled = prefix == 0 && conv3d_uses_tiled(d, inputs);
     const kf::Conv3dArgs a = conv3d_args(d, inputs, cur, 0);
-    e = conv3d_pack(d, d->workspace, true, tiled, inputs[1].data, hs);
+    if (e == hipSuccess) e = conv3d_pack(d, d->workspace, true, tiled, inputs[1].data, hs);
     if (e == hipSuccess && tiled && a.tiles) e = kf::launch_conv3d_bf16(a, d->workspace, 1, hs);
     if (e == hipSuccess && !tiled) {
-      kf::EpiProgram none;
-      memset(&none, 0, sizeof(none));
-      e = kf::launch_conv3d_gen(conv3d_gen_args(d, inputs, cur, none), d->workspace, hs);
+      kf::EpiProgram pre;
+      memset(&pre, 0, sizeof(pre));
+      pre.n = prefix;
+      for (int i = 0; i < prefix; ++i) pre.op[i] = d->prog.op[i];
+      e = kf::launch_conv3d_gen(conv3d_gen_args(d, inputs, cur, pre), d->workspace, hs);
     }
   } else {
     kf::ConvArgs c;
@@ -1359,6 +1361,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
     }
     if (e == hipSuccess) e = kf::launch_conv_bf16(c, d->workspace, 0, hs);
   }
+  if (e == hipSuccess && ev_after) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_after), hs);
   if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
 
   // 2. one kernel per op, ping-ponging between the buffers; the last op
@@ -1366,7 +1369,7 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   int64_t n = n_full;
   int64_t dd = conv3d ? s.depth - 2 : 1, hh = conv3d ? s.height - 2 : s.height, ww = conv3d ? s.width - 2 : s.width;
   int which = 0;
-  for (int i = 0; i < s.n_ops && e == hipSuccess; ++i) {
+  for (int i = prefix; i < s.n_ops && e == hipSuccess; ++i) {
     const kf_op& op = s.ops[i];
     const bool last = i == s.n_ops - 1;
     void* dst = last ? out : d->ubuf[which ^ 1];
@@ -1423,6 +1426,40 @@ kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* ou
   }
   if (e != hipSuccess) return fail(KF_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+kf_status kf_unfused_op(const kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
+  if (!d || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  const bool vec16 = d->variant != kVarGemmF32;
+  for (size_t i = 0; i < d->inputs.size(); ++i) {
+    kf_status st = check_tensor(&inputs[i], d->inputs[i], false, vec16);
+    if (st != KF_OK) return st;
+  }
+  kf_status st = check_tensor(&outputs[0], d->output, true, vec16);
+  if (st != KF_OK) return st;
+  const kf_op_spec& s = d->spec;
+  const bool rowwise = s.contraction == KF_ROWWISE;
+  const bool rows = s.contraction == KF_GEMM || rowwise;  // an [M, N] intermediate
+  if ((rows && s.M == 0) || (!rows && s.batch == 0)) return ok();
+  // the per-op kernels index [M, N] tensors as contiguous rows
+  if (rowwise && inputs[0].stride[0] != s.N)
+    return fail(KF_ERR_UNSUPPORTED, "the unfused ROWWISE chain needs A with row stride N");
+  if (rows && s.n_ops) {
+    for (int i = 0; i < s.n_ops; ++i)
+      if (s.ops[i].kind == KF_OP_GROUPNORM && s.M * s.ops[i].groups >= kMaxRowLaunch)
+        return fail(KF_ERR_UNSUPPORTED, "the unfused GroupNorm supports M * groups < %lld", (long long)kMaxRowLaunch);
+    for (size_t i = 0; i < d->inputs.size(); ++i)
+      if (strcmp(d->inputs[i].name, "residual") == 0 && inputs[i].stride[0] != s.N)
+        return fail(KF_ERR_UNSUPPORTED, "the unfused chain needs a residual with row stride N");
+    if (outputs[0].ndim == 2 && outputs[0].stride[0] != s.N)
+      return fail(KF_ERR_UNSUPPORTED, "the unfused chain needs an output with row stride N");
+  }
+
+  return run_chain_split(d, inputs, outputs, stream, 0, nullptr, nullptr);
 }
 
 }  // extern "C"

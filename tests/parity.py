@@ -75,13 +75,18 @@ def sample_rows(M: int, n: int, seed: int = 0) -> np.ndarray:
     return np.array(sorted(rows), dtype=np.int64)
 
 
-def check(cfg, tensors, gpu_out, rows=None, images=None, tol=None, chain=None, unfused=False):
+def check(cfg, tensors, gpu_out, rows=None, images=None, tol=None, chain=None, unfused=False, fused=None):
     """Compare a GPU output with the oracle: the fused chain's plain
     definition, or (unfused=True) the one-op-per-kernel evaluation that
-    stores every intermediate in the chain's intermediate format."""
+    stores every intermediate in the chain's intermediate format, or
+    (fused=p) the partly fused one: the contraction with its first p ops in
+    one kernel, then one kernel per op."""
     chain = chain if chain is not None else inputs.chain_for(cfg, tensors)
-    run = oracle.run_chain_unfused if unfused else oracle.run_chain
-    ref = run(chain, tensors, rows=rows, images=images)
+    if fused is not None:
+        ref = oracle.run_chain_unfused(chain, tensors, rows=rows, images=images, fused=fused)
+    else:
+        run = oracle.run_chain_unfused if unfused else oracle.run_chain
+        ref = run(chain, tensors, rows=rows, images=images)
     g = to_host_f64(gpu_out)
     if rows is not None:
         g = g[rows]

@@ -269,10 +269,11 @@ def test_rowwise_input_slots():
 
 def test_conv3d_validation():
     ok = kf.KF_ERR_NO_DEVICE if not _gpu_present() else kf.KF_OK
-    for kw, status in [(dict(cin=32), kf.KF_ERR_UNSUPPORTED), (dict(cout=32), kf.KF_ERR_UNSUPPORTED),
+    # outside the tiled kernel's shape family the whole op family runs, partly fused
+    for kw, status in [(dict(cin=32), ok), (dict(cout=32), ok),
                        (dict(cin=32, ops=[("bias",), ("relu",)]), ok),      # the general kernel
                        (dict(cin=3, cout=200, D=3, H=3, W=3, ops=[]), ok),
-                       (dict(cout=32, ops=[("bias",), ("channel_softmax",)]), kf.KF_ERR_UNSUPPORTED),
+                       (dict(cout=32, ops=[("bias",), ("channel_softmax",)]), ok),
                        (dict(D=2), kf.KF_ERR_SHAPE), (dict(W=2), kf.KF_ERR_SHAPE),
                        (dict(out_dtype="f32"), kf.KF_ERR_UNSUPPORTED), (dict(in_dtype="f32"), kf.KF_ERR_UNSUPPORTED),
                        (dict(ops=[("bias",), ("channel_softmax",), ("maxpool3d2",)]), kf.KF_ERR_UNSUPPORTED),

@@ -684,19 +684,61 @@ def test_conv3d_general_integer_bit_exact(cl):
 
 
 def test_conv3d_family_layouts():
-    """The tiled family's shape with the F2 chain needs a channels-last input
-    (refused for NCDHW); with bias and element-wise ops alone an NCDHW input
-    runs the general kernel and gives the oracle's result."""
-    _torch()
+    """The tiled family's shape with the F2 chain: a channels-last input runs
+    the tiled kernel, the whole chain fused; a contiguous NCDHW input runs
+    partly fused (the general kernel with the bias, then the channel softmax
+    and the pools one kernel each) and gives the partly fused oracle's
+    result."""
+    torch = _torch()
     cfg = inputs.config("F2", batch=1, D=6, H=10, W=18)
     t = inputs.generate(cfg, seed=5)
     op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
-    with pytest.raises(kf.KFError) as e:
-        op(op.device_inputs(t, conv3d_channels_last=False), op.empty_output("cuda"))
-    assert e.value.status == kf.KF_ERR_UNSUPPORTED
     out = op.empty_output("cuda")
     op(op.device_inputs(t), out)
     check(cfg, t, out)
+    ins = op.device_inputs(t, conv3d_channels_last=False)
+    assert ins[0].is_contiguous()
+    out2 = op.empty_output("cuda")
+    op(ins, out2)
+    torch.cuda.synchronize()
+    err = check(cfg, t, out2, fused=1)
+    # and back: the tiled kernel's packed weights are restored
+    out3 = op.empty_output("cuda")
+    op(op.device_inputs(t), out3)
+    assert torch.equal(out3.view(torch.int16), out.view(torch.int16))
+    print(f"F2 NCDHW partly fused err {err:.3e}")
+
+
+_F2_SPLIT = [("bias",), ("sigmoid",), ("channel_softmax",), ("scale", 2.0), ("maxpool3d2",), ("maxpool3d2",)]
+
+
+@pytest.mark.parametrize("batch,cin,cout,D,H,W,ops,cl,prefix", [
+    (2, 24, 96, 7, 11, 20, _F2_OPS, True, 1),          # general shape, channels-last
+    (1, 40, 160, 7, 9, 37, _F2_SPLIT, False, 2),       # two channel tiles, NCDHW, ragged pools
+    (2, 8, 32, 4, 6, 9, [("channel_softmax",)], True, 0),  # the softmax straight after the conv
+    (1, 16, 64, 6, 10, 18, _F2_SPLIT, False, 2),       # the tiled family's shape, NCDHW input
+])
+def test_conv3d_partly_fused_chains(batch, cin, cout, D, H, W, ops, cl, prefix):
+    """Outside the tiled kernel's family a Conv3d chain with a channel softmax
+    or pools runs partly fused: the general kernel with the leading bias and
+    element-wise ops, then one kernel per remaining op through bf16
+    intermediates.  Compared with the oracle of that evaluation, and the
+    unfused chain with the unfused oracle."""
+    torch = _torch()
+    cfg = inputs.config("F2", batch=batch, cin=cin, cout=cout, D=D, H=H, W=W, ops=ops, dist=_CONV3D_GEN_DIST)
+    t = inputs.generate(cfg, seed=cin + D)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t, conv3d_channels_last=cl)
+    print(f"[gpu] conv3d partly fused {batch}x{cin}->{cout} {D}x{H}x{W} cl={cl} prefix={prefix}", flush=True)
+    out = op.empty_output("cuda")
+    op(ins, out)
+    torch.cuda.synchronize()
+    assert tuple(out.shape) == inputs.conv3d_pooled_shape(cfg)
+    err = check(cfg, t, out, fused=prefix)
+    out2 = op.empty_output("cuda")
+    op.unfused(ins, out2)
+    check(cfg, t, out2, unfused=True)
+    print(f"conv3d partly fused err {err:.3e}")
 
 
 def test_f2_degenerate_shapes():
@@ -749,19 +791,6 @@ def test_f2_full_config_sampled_images():
     assert np.all(np.isfinite(to_host_f64(out)))
     err = check(cfg, t, out, images=np.array([0, 7, 15]))
     print(f"F2 full err {err:.3e}")
-
-
-def test_f2_rejects_channels_first_input():
-    torch = _torch()
-    cfg = inputs.config("F2", batch=1, D=6, H=10, W=18)
-    t = inputs.generate(cfg, seed=1)
-    op = kf.FusedOp.from_config(cfg)
-    ins = op.device_inputs(t)
-    ins[0] = ins[0].contiguous()          # NCDHW instead of channels-last
-    with pytest.raises(kf.KFError) as e:
-        op(ins, op.empty_output("cuda"))
-    assert e.value.status == kf.KF_ERR_UNSUPPORTED
-    torch.cuda.synchronize()
 
 
 # ------------------------------------------------------------ unfused chain

@@ -577,15 +577,38 @@ def _bf16(x):
     return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16)
 
 
-def _torch_eager_bf16(ch, t):
+def _torch_eager_bf16(ch, t, fused=0):
     """The chain as an eager PyTorch module on the CPU runs it op by op with
     bf16 activations stored between the ops: every op reads the stored bf16
     tensor, is evaluated by torch's own float32 CPU kernel and its result is
     stored in bf16 (fp32 parameters -- bias, gamma, beta -- enter in
     float32).  The last op's result is returned in float32 (row logsumexp)
-    or bf16."""
+    or bf16.  fused > 0 (conv3d only): the convolution runs in float32 on
+    the bf16 values and the first `fused` ops follow in float32 with nothing
+    stored until after them; every later op's input is the stored bf16."""
     bf = torch.bfloat16
     dt = ch["in_dtype"]
+    if fused:
+        assert ch["contraction"] == "conv3d_3x3x3"
+        h = F.conv3d(_bf16(t["a"]).float(), _bf16(t["b"]).float())
+        for k, (name, *p) in enumerate(ch["ops"]):
+            if k >= fused:
+                h = h.to(bf)
+            x = h.float()
+            if name == "bias":
+                y = x + torch.from_numpy(t["bias"]).reshape(1, -1, 1, 1, 1)
+            elif name == "sigmoid":
+                y = torch.sigmoid(x)
+            elif name == "scale":
+                y = x * p[0]
+            elif name == "maxpool3d2":
+                y = F.max_pool3d(x, 2)
+            elif name == "channel_softmax":
+                y = torch.softmax(x, 1)
+            else:
+                raise ValueError(name)
+            h = y
+        return h.to(bf)
     if ch["contraction"] == "rowwise":
         h = _bf16(t["a"])
     elif dt == "e4m3":
@@ -699,6 +722,33 @@ def test_unfused_oracle_pin_detects_a_missing_rounding(name, kw, monkeypatch):
         assert diff > 2e-5, diff
     else:
         assert same < 0.995, same
+
+
+_SPLIT_OPS = [("bias",), ("sigmoid",), ("scale", 2.0), ("channel_softmax",), ("maxpool3d2",), ("maxpool3d2",)]
+
+
+@pytest.mark.parametrize("fused", [1, 3])
+def test_partly_fused_oracle_matches_torch(fused):
+    """run_chain_unfused(fused=p): the conv and its first p ops as one kernel
+    (nothing stored between them), then one kernel per op.  Against torch's
+    CPU float32 conv + ops with the bf16 stores in the same places, the bf16
+    outputs agree except near rounding boundaries; the fully unfused oracle
+    (every intermediate stored) does not, so the pin tells the two apart."""
+    cfg, t = _small("F2", batch=1, D=6, H=10, W=14, ops=_SPLIT_OPS)
+    ch = inputs.chain_for(cfg, t)
+    ref = _torch_eager_bf16(ch, t, fused=fused).double().numpy()
+    same = float(np.mean(_ROUND_BF16(oracle.run_chain_unfused(ch, t, fused=fused)) == ref))
+    other = float(np.mean(_ROUND_BF16(oracle.run_chain_unfused(ch, t)) == ref))
+    assert same >= 0.995 and other < 0.995, (same, other)
+
+
+def test_partly_fused_oracle_end_points():
+    """fused = 0 is the unfused oracle; fused = the whole list is the fused
+    oracle, exactly."""
+    cfg, t = _small("F2", batch=1, D=5, H=7, W=9, ops=_SPLIT_OPS)
+    ch = inputs.chain_for(cfg, t)
+    assert np.array_equal(oracle.run_chain_unfused(ch, t, fused=0), oracle.run_chain_unfused(ch, t))
+    assert np.array_equal(oracle.run_chain_unfused(ch, t, fused=len(_SPLIT_OPS)), oracle.run_chain(ch, t))
 
 
 def test_unfused_oracle_equals_fused_without_ops_and_rounds_f32_chains():

@@ -56,3 +56,19 @@ def test_noalloc_full_size_softmax():
     cfg = inputs.config("C5")
     t, out = _noalloc(cfg, None)
     check(cfg, t, out, rows=sample_rows(cfg["M"], 4))
+
+
+def test_noalloc_refuses_partly_fused_conv3d():
+    """A Conv3d chain with a channel softmax outside the tiled kernel's
+    family (here an NCDHW input) needs intermediate buffers: the entry point
+    that allocates nothing refuses it before any launch."""
+    import torch
+    cfg = inputs.config("F2", batch=1, D=6, H=10, W=18)
+    t = inputs.generate(cfg, seed=3)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t, conv3d_channels_last=False)
+    out = op.empty_output("cuda")
+    with pytest.raises(kf.KFError) as e:
+        kf.fused_op_noalloc(inputs.chain_for(cfg, t), ins, out, **kf.sizes_of(cfg))
+    assert e.value.status == kf.KF_ERR_UNSUPPORTED and "intermediate" in str(e.value)
+    torch.cuda.synchronize()
