@@ -35,6 +35,11 @@ gets a block of the same fields under "also".  Per workload:
                steps (every candidate computes the same bits), or the one
                given with --tuning; for a GEMM also the modelled operand
                bytes its tile order makes the L2s fetch
+  probe        (bf16 / fp8 contractions) kf_probe_mfma: the matrix cores'
+               sustained rate with no memory traffic on this GPU in this
+               run, and the shader clock it ran at -- a measured ceiling
+               beside the datasheet peak (which assumes 2.4 GHz); the
+               roofline block carries achieved / that rate as frac_of_probe
   diagnosis    kf_diagnose_counters on the measured kernel time and the
                committed counters (HBM bytes, matrix-core busy fraction, LDS
                bank conflicts) when they match the kernel source: compute and
@@ -57,6 +62,23 @@ sys.path.insert(0, ROOT)
 PEAK_TFLOPS = {"bf16": 2516.6, "e4m3": 5033.2, "f32": 157.3}
 HBM_PEAK_GBS = 8000.0
 COLD_FLUSH_BYTES = 512 << 20
+# rounds of 8 MFMAs per SIMD for the matrix-core probe: about 30 ms each at
+# the clocks this GPU sustains under that load
+PROBE_ITERS = {"bf16": 200000, "e4m3": 100000}
+_probe_cache: dict = {}
+
+
+def _probe(dt: str):
+    """The matrix-core rate probe for dtype dt, once per process."""
+    from paper_2605_30359_amd import kf
+    if dt not in PROBE_ITERS:
+        return None
+    if dt not in _probe_cache:
+        r = kf.probe_mfma(dt, PROBE_ITERS[dt])
+        _probe_cache[dt] = {"dtype": dt, "tflops": round(r["tflops"], 1), "clock_ghz": round(r["clock_ghz"], 3),
+                            "frac_of_datasheet": round(r["tflops"] / PEAK_TFLOPS[dt], 4),
+                            "ms": round(r["seconds"] * 1e3, 3)}
+    return _probe_cache[dt]
 
 
 def _hip():
@@ -320,6 +342,8 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
         except kf.KFError as e:
             unfused = {"error": str(e)}
 
+    probe = None if (rowwise or args.no_probe) else _probe(dt)
+
     trec = _traffic_record(kname, cfg["workload"])
     traffic = trec.get("hbm_bytes_per_launch") if trec else None
     # the diagnosis from the live kernel time and, when the committed counter
@@ -356,6 +380,7 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
             "peak": peak,
             "unit": "GB/s" if rowwise else "TFLOP/s",
             "frac": round(achieved / peak, 4),
+            "frac_of_probe": round(achieved / probe["tflops"], 4) if probe else None,
             "kernel_us": round(kernel_ms * 1e3, 2),
             "kernel_us_stats": _stats_us(kern_ms),
             "kernel_us_cold": cold["kernel_us"] if cold else None,
@@ -365,6 +390,7 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
             # raster order changes how often operand panels are re-fetched)
             "traffic_launch_config": trec.get("launch_config") if trec else None,
         },
+        "probe": probe,
         "diagnosis": diagnosis,
         "tuning": tuning,
         "cpu_baseline": cpu,
@@ -394,6 +420,7 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
+    ap.add_argument("--no-probe", action="store_true", help="skip the matrix-core rate probe")
     ap.add_argument("--tuning", default=None, metavar="RG,XR,WG[,V]",
                     help="use this launch configuration (raster group, XCD order, workgroups per CU, kernel variant) "
                          "instead of autotuning")

@@ -433,6 +433,32 @@ kf_status kf_autotune(kf_desc* desc, const kf_tensor* inputs, kf_tensor* outputs
 kf_status kf_fused_op_noalloc(const kf_op_spec* spec, const kf_tensor* inputs,
                               kf_tensor* outputs, void* stream);
 
+/* A measured ceiling for the roofline beside the datasheet's: the matrix
+   cores' sustained rate with no memory traffic.  One workgroup of 4 waves
+   per compute unit, each SIMD issuing `iters` (1 .. 2^24) rounds of 8
+   independent 32x32 MFMAs of `in_dtype` from registers (KF_BF16:
+   v_mfma_f32_32x32x16_bf16; KF_FP8_E4M3: the 32x32x64 fp8 MFMA), after an
+   untimed launch a tenth as long.  The datasheet's dense peaks assume the
+   2.4 GHz peak engine clock; under sustained matrix-core load the clock is
+   set by power management, and the probe reports it: every workgroup reads
+   the shader-clock counter and the constant-rate counter at its start and
+   end.  The roofline evaluation the paper's diagnosis rests on
+   (Methodology, Diagnosis) compares a kernel with its hardware ceiling;
+   this is that ceiling as the chip sustains it.  Allocates and frees a
+   small device buffer and its own stream, and blocks until done.  Errors:
+   KF_ERR_NO_DEVICE without a GPU, KF_ERR_UNSUPPORTED for other dtypes,
+   KF_ERR_INVALID_ARG, KF_ERR_HIP. */
+typedef struct kf_mfma_probe {
+  double tflops;      /* FLOPs of the timed launch / its duration / 1e12     */
+  double seconds;     /* the timed launch's duration (HIP events)            */
+  double clock_ghz;   /* median over workgroups of shader-clock ticks per
+                         second of constant-rate time, / 1e9                 */
+  int32_t workgroups; /* launched (the device's compute units)               */
+  int32_t reserved;   /* 0                                                   */
+} kf_mfma_probe;
+
+kf_status kf_probe_mfma(int32_t in_dtype, int64_t iters, kf_mfma_probe* out);
+
 /* Static description of a status code. */
 const char* kf_status_string(kf_status status);
 

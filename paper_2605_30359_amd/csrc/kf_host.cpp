@@ -686,6 +686,65 @@ void classify_bound(kf_diagnosis* g) {
 
 extern "C" {
 
+kf_status kf_probe_mfma(int32_t in_dtype, int64_t iters, kf_mfma_probe* out) {
+  if (!out) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  memset(out, 0, sizeof(*out));
+  if (in_dtype != KF_BF16 && in_dtype != KF_FP8_E4M3)
+    return fail(KF_ERR_UNSUPPORTED, "the probe runs bf16 or fp8 e4m3 MFMAs");
+  if (iters < 1 || iters > (int64_t(1) << 24)) return fail(KF_ERR_INVALID_ARG, "iters must be in [1, 2^24]");
+  int dev = 0, cus = 0;
+  kf_status st = current_device(&dev, &cus);
+  if (st != KF_OK) return st;
+  int wall_khz = 0;
+  if (hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || wall_khz <= 0) {
+    (void)hipGetLastError();
+    return fail(KF_ERR_HIP, "cannot query the constant-rate counter's frequency");
+  }
+  const bool fp8 = in_dtype == KF_FP8_E4M3;
+  const int wgs = cus;
+  const size_t sink_bytes = (size_t)wgs * kf::probe_threads() * sizeof(float);
+  const size_t stamp_bytes = (size_t)wgs * 4 * sizeof(long long);
+  void* buf = nullptr;
+  hipStream_t hs = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  std::vector<long long> stamps((size_t)wgs * 4);
+  float ms = 0.0f;
+  hipError_t e = hipMalloc(&buf, sink_bytes + stamp_bytes);
+  if (e == hipSuccess) e = hipStreamCreate(&hs);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  float* sink = static_cast<float*>(buf);
+  long long* st_dev = reinterpret_cast<long long*>(static_cast<char*>(buf) + sink_bytes);
+  // an untimed launch of a tenth of the length first: clocks and power settle
+  if (e == hipSuccess) e = kf::launch_mfma_probe(fp8, std::max<int64_t>(1, iters / 10), wgs, sink, st_dev, hs);
+  if (e == hipSuccess) e = hipEventRecord(e0, hs);
+  if (e == hipSuccess) e = kf::launch_mfma_probe(fp8, iters, wgs, sink, st_dev, hs);
+  if (e == hipSuccess) e = hipEventRecord(e1, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (e == hipSuccess) e = hipMemcpy(stamps.data(), st_dev, stamp_bytes, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) (void)hipGetLastError();
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (hs) (void)hipStreamDestroy(hs);
+  if (buf) (void)hipFree(buf);
+  if (e != hipSuccess) return fail(KF_ERR_HIP, "probe failed: %s", hipGetErrorString(e));
+  // shader clock of each workgroup: its clock ticks over its real time
+  std::vector<double> ghz;
+  for (int w = 0; w < wgs; ++w) {
+    const long long dc = stamps[4 * w + 1] - stamps[4 * w], dw = stamps[4 * w + 3] - stamps[4 * w + 2];
+    if (dc > 0 && dw > 0) ghz.push_back((double)dc / ((double)dw / ((double)wall_khz * 1e3)) * 1e-9);
+  }
+  std::sort(ghz.begin(), ghz.end());
+  const double mfma_flops = fp8 ? 2.0 * 32 * 32 * 64 : 2.0 * 32 * 32 * 16;
+  const double flops = (double)wgs * (kf::probe_threads() / 64) * (double)iters * 8 * mfma_flops;
+  out->seconds = ms * 1e-3;
+  out->tflops = ms > 0.0f ? flops / (ms * 1e-3) * 1e-12 : 0.0;
+  out->clock_ghz = ghz.empty() ? 0.0 : ghz[ghz.size() / 2];
+  out->workgroups = wgs;
+  return ok();
+}
+
 kf_status kf_classify(double flops, double bytes, double seconds, double peak_tflops, double peak_gbps,
                       int64_t workgroups, int32_t compute_units, kf_diagnosis* out) {
   if (!out) return fail(KF_ERR_INVALID_ARG, "out is NULL");

@@ -53,6 +53,15 @@ bool row_reduce_streams(const EpiProgram& prog);
 // `gn_group` columns, 0 if none).
 const char* rowwise_kernel(const EpiProgram& prog, int gn_group);
 
+// The matrix-core rate probe: `workgroups` workgroups of probe_threads()
+// threads, each SIMD issuing `iters` rounds of 8 independent 32x32 MFMAs
+// (bf16 32x32x16 or fp8 32x32x64) from registers; sink takes one float per
+// thread, stamps 4 per workgroup (shader-clock counter at start and end,
+// constant-rate counter at start and end).
+hipError_t launch_mfma_probe(bool fp8, int64_t iters, int workgroups, float* sink, long long* stamps,
+                             hipStream_t stream);
+int probe_threads();
+
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);
 

@@ -39,7 +39,7 @@ DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
-            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc", "kf_diagnose_counters")
+            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc", "kf_diagnose_counters", "kf_probe_mfma")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
 HINTS = {1: "reuse", 2: "parallelism", 4: "pipeline", 8: "overlap", 16: "lds_layout"}
 KF_MAX_TUNE_CANDIDATES = 16
@@ -99,6 +99,11 @@ class KfTuneResult(ctypes.Structure):
                 ("panel_bytes", ctypes.c_double * KF_MAX_TUNE_CANDIDATES)]
 
 
+class KfMfmaProbe(ctypes.Structure):
+    _fields_ = [("tflops", ctypes.c_double), ("seconds", ctypes.c_double), ("clock_ghz", ctypes.c_double),
+                ("workgroups", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class KFError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{status_string(status)} -- {message}")
@@ -153,6 +158,8 @@ def lib():
         L.kf_diagnose.restype = i32
         L.kf_diagnose_counters.argtypes = [vp, ctypes.POINTER(KfCounters), ctypes.POINTER(KfDiagnosis)]
         L.kf_diagnose_counters.restype = i32
+        L.kf_probe_mfma.argtypes = [i32, ctypes.c_int64, ctypes.POINTER(KfMfmaProbe)]
+        L.kf_probe_mfma.restype = i32
         L.kf_get_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
         L.kf_get_tuning.restype = i32
         L.kf_set_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
@@ -465,3 +472,12 @@ def fused_op_noalloc_status(chain: dict, **sizes) -> tuple:
     o = (KfTensor * 1)()
     st = lib().kf_fused_op_noalloc(ctypes.byref(spec), arr, o, None)
     return st, last_error()
+
+
+def probe_mfma(in_dtype: str, iters: int) -> dict:
+    """kf_probe_mfma: the matrix cores' sustained rate for "bf16" or "e4m3"
+    MFMAs with no memory traffic, and the shader clock they ran at."""
+    r = KfMfmaProbe()
+    _check(lib().kf_probe_mfma(DTYPES[in_dtype], int(iters), ctypes.byref(r)))
+    return {"dtype": in_dtype, "tflops": r.tflops, "seconds": r.seconds, "clock_ghz": r.clock_ghz,
+            "workgroups": r.workgroups}

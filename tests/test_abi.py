@@ -206,7 +206,7 @@ def test_struct_offsets_match_c_compiler(tmp_path):
         pytest.skip("no C compiler")
     structs = [("kf_op", kf.KfOp), ("kf_op_spec", kf.KfOpSpec), ("kf_tensor", kf.KfTensor),
                ("kf_diagnosis", kf.KfDiagnosis), ("kf_tuning", kf.KfTuning), ("kf_tune_result", kf.KfTuneResult),
-               ("kf_counters", kf.KfCounters)]
+               ("kf_counters", kf.KfCounters), ("kf_mfma_probe", kf.KfMfmaProbe)]
     lines, want = [], []
     for cname, py in structs:
         for f in py._fields_:
@@ -223,6 +223,17 @@ def test_struct_offsets_match_c_compiler(tmp_path):
     assert got == want
 
 
+
+def test_probe_mfma_argument_checks():
+    """The matrix-core probe checks its arguments before touching a device."""
+    r = kf.KfMfmaProbe()
+    lib = kf.lib()
+    assert lib.kf_probe_mfma(kf.KF_BF16, 100, None) == kf.KF_ERR_INVALID_ARG
+    assert lib.kf_probe_mfma(kf.KF_F32, 100, ctypes.byref(r)) == kf.KF_ERR_UNSUPPORTED
+    assert lib.kf_probe_mfma(kf.KF_BF16, 0, ctypes.byref(r)) == kf.KF_ERR_INVALID_ARG
+    assert lib.kf_probe_mfma(kf.KF_FP8_E4M3, (1 << 24) + 1, ctypes.byref(r)) == kf.KF_ERR_INVALID_ARG
+    if not _gpu_present():
+        assert lib.kf_probe_mfma(kf.KF_BF16, 100, ctypes.byref(r)) == kf.KF_ERR_NO_DEVICE
 
 
 def test_rowwise_validation():

@@ -1231,3 +1231,17 @@ def test_diagnosis_from_counters():
     assert g["bound"] == "memory" and g["hints"] == [] and g["mfma_busy"] == -1.0
     g = f4.diagnose_counters(400e-6, 268.6e6)
     assert g["bound"] == "latency" and g["hints"] == ["pipeline"]
+
+
+@pytest.mark.parametrize("dt,peak", [("bf16", 2516.6), ("e4m3", 5033.2)])
+def test_mfma_probe(dt, peak):
+    """The matrix-core probe: one workgroup per compute unit; its rate is a
+    positive fraction of the datasheet peak, and it cannot exceed what the
+    matrix cores deliver at the clock it measured (the datasheet peak
+    scaled by clock / 2.4 GHz), so rate and clock check each other."""
+    torch = _torch()
+    r = kf.probe_mfma(dt, 20000)
+    print(f"[gpu] probe {dt}: {r}", flush=True)
+    assert r["workgroups"] == torch.cuda.get_device_properties(0).multi_processor_count
+    assert r["seconds"] > 0 and 0.5 < r["clock_ghz"] < 2.6
+    assert 0.2 * peak < r["tflops"] < 1.02 * peak * r["clock_ghz"] / 2.4
