@@ -459,6 +459,20 @@ typedef struct kf_mfma_probe {
 
 kf_status kf_probe_mfma(int32_t in_dtype, int64_t iters, kf_mfma_probe* out);
 
+/* The memory side's measured ceiling: a plain device copy of `bytes` (a
+   multiple of 16, at most 2^34) between two buffers this call allocates,
+   16-byte loads and streaming stores over a grid-stride launch, one untimed
+   copy then `reps` (1..1000) timed back to back.  A copy moves each byte
+   twice (read and write); gbps counts both.  Allocates and frees 2 x bytes
+   of device memory and its own stream, and blocks until done.  Errors:
+   KF_ERR_NO_DEVICE, KF_ERR_INVALID_ARG, KF_ERR_OOM, KF_ERR_HIP. */
+typedef struct kf_copy_probe {
+  double gbps;        /* 2 x bytes / seconds / 1e9                           */
+  double seconds;     /* one copy: the timed launches' total / reps          */
+} kf_copy_probe;
+
+kf_status kf_probe_copy(int64_t bytes, int32_t reps, kf_copy_probe* out);
+
 /* Static description of a status code. */
 const char* kf_status_string(kf_status status);
 

@@ -745,6 +745,50 @@ kf_status kf_probe_mfma(int32_t in_dtype, int64_t iters, kf_mfma_probe* out) {
   return ok();
 }
 
+kf_status kf_probe_copy(int64_t bytes, int32_t reps, kf_copy_probe* out) {
+  if (!out) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  memset(out, 0, sizeof(*out));
+  if (bytes < 16 || bytes % 16 || bytes > (int64_t(1) << 34))
+    return fail(KF_ERR_INVALID_ARG, "bytes must be a multiple of 16 in [16, 2^34]");
+  if (reps < 1 || reps > 1000) return fail(KF_ERR_INVALID_ARG, "reps must be in [1, 1000]");
+  int dev = 0, cus = 0;
+  kf_status st = current_device(&dev, &cus);
+  if (st != KF_OK) return st;
+  void* src = nullptr;
+  void* dst = nullptr;
+  hipStream_t hs = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  float ms = 0.0f;
+  const int64_t chunks = bytes / 16;
+  hipError_t e = hipMalloc(&src, (size_t)bytes);
+  if (e == hipSuccess) e = hipMalloc(&dst, (size_t)bytes);
+  if (e == hipSuccess) e = hipStreamCreate(&hs);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  // one untimed copy (also fills the source), then `reps` timed back to back
+  if (e == hipSuccess) e = hipMemsetAsync(src, 0x3c, (size_t)bytes, hs);
+  if (e == hipSuccess) e = kf::launch_copy_probe(src, dst, chunks, hs);
+  if (e == hipSuccess) e = hipEventRecord(e0, hs);
+  for (int i = 0; i < reps && e == hipSuccess; ++i) e = kf::launch_copy_probe(src, dst, chunks, hs);
+  if (e == hipSuccess) e = hipEventRecord(e1, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (e != hipSuccess) (void)hipGetLastError();
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (hs) (void)hipStreamDestroy(hs);
+  if (src) (void)hipFree(src);
+  if (dst) (void)hipFree(dst);
+  if (e != hipSuccess) {
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+      return fail(KF_ERR_OOM, "copy probe buffers of 2 x %lld bytes could not be allocated", (long long)bytes);
+    return fail(KF_ERR_HIP, "probe failed: %s", hipGetErrorString(e));
+  }
+  out->seconds = ms * 1e-3 / reps;
+  out->gbps = out->seconds > 0 ? 2.0 * (double)bytes / out->seconds * 1e-9 : 0.0;
+  return ok();
+}
+
 kf_status kf_classify(double flops, double bytes, double seconds, double peak_tflops, double peak_gbps,
                       int64_t workgroups, int32_t compute_units, kf_diagnosis* out) {
   if (!out) return fail(KF_ERR_INVALID_ARG, "out is NULL");

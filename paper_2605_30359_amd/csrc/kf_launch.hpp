@@ -61,6 +61,9 @@ const char* rowwise_kernel(const EpiProgram& prog, int gn_group);
 hipError_t launch_mfma_probe(bool fp8, int64_t iters, int workgroups, float* sink, long long* stamps,
                              hipStream_t stream);
 int probe_threads();
+// The copy probe: dst[i] = src[i] over `chunks` 16-byte chunks (streaming
+// stores), a resident-sized grid-stride launch.
+hipError_t launch_copy_probe(const void* src, void* dst, int64_t chunks, hipStream_t stream);
 
 // fp32 GEMM + element-wise epilogue.
 hipError_t launch_gemm_f32(const GemmArgs& args, bool b_nk, hipStream_t stream);

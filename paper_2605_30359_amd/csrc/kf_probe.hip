@@ -12,6 +12,7 @@
 // MFMAs see different data, as in a GEMM (the power drawn, and with it the
 // clock, depends on the operand bits changing).  Each workgroup stamps the
 // shader-clock counter and the constant-rate counter at its start and end.
+// Beside it, a plain device copy gives the memory side's measured ceiling.
 #include "kf_device.hpp"
 #include "kf_launch.hpp"
 
@@ -99,7 +100,40 @@ __global__ __launch_bounds__(kProbeThreads, 1) void kf_mfma_probe(int64_t iters,
   }
 }
 
+// A plain device copy of n 16-byte chunks: the memory side's measured
+// ceiling.  Spans of 256 x kCopyUnroll chunks per workgroup; each lane issues its kCopyUnroll loads (256 chunks apart, so
+// every load instruction of a wave reads 1 KiB of contiguous memory) before
+// its stores, which are streaming stores as in the library's memory-bound
+// kernels.
+constexpr int kCopyUnroll = 8;
+__global__ __launch_bounds__(256) void kf_copy_probe(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                     int64_t n) {
+  constexpr int64_t span = 256 * kCopyUnroll;
+  for (int64_t b0 = (int64_t)blockIdx.x * span; b0 < n; b0 += (int64_t)gridDim.x * span) {
+    u32x4 v[kCopyUnroll];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      const int64_t c = b0 + u * 256 + threadIdx.x;
+      if (c < n) v[u] = src[c];
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      const int64_t c = b0 + u * 256 + threadIdx.x;
+      if (c < n) store_nt(dst + c, v[u]);
+    }
+  }
+}
+
 int probe_threads() { return kProbeThreads; }
+
+hipError_t launch_copy_probe(const void* src, void* dst, int64_t chunks, hipStream_t stream) {
+  // one span per workgroup (at 2 x 512 MiB this measured 1-2% above a
+  // resident-sized grid that loops); the loop covers grids capped at 2^31
+  const int64_t need = (chunks + 256 * kCopyUnroll - 1) / (256 * kCopyUnroll);
+  hipLaunchKernelGGL(kf_copy_probe, dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>(need, INT32_MAX))),
+                     dim3(256), 0, stream, static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), chunks);
+  return hipGetLastError();
+}
 
 hipError_t launch_mfma_probe(bool fp8, int64_t iters, int workgroups, float* sink, long long* stamps,
                              hipStream_t stream) {

@@ -39,7 +39,8 @@ DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
 EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "kf_destroy", "kf_num_inputs",
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
-            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc", "kf_diagnose_counters", "kf_probe_mfma")
+            "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc", "kf_diagnose_counters", "kf_probe_mfma",
+            "kf_probe_copy")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
 HINTS = {1: "reuse", 2: "parallelism", 4: "pipeline", 8: "overlap", 16: "lds_layout"}
 KF_MAX_TUNE_CANDIDATES = 16
@@ -104,6 +105,10 @@ class KfMfmaProbe(ctypes.Structure):
                 ("workgroups", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class KfCopyProbe(ctypes.Structure):
+    _fields_ = [("gbps", ctypes.c_double), ("seconds", ctypes.c_double)]
+
+
 class KFError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{status_string(status)} -- {message}")
@@ -160,6 +165,8 @@ def lib():
         L.kf_diagnose_counters.restype = i32
         L.kf_probe_mfma.argtypes = [i32, ctypes.c_int64, ctypes.POINTER(KfMfmaProbe)]
         L.kf_probe_mfma.restype = i32
+        L.kf_probe_copy.argtypes = [ctypes.c_int64, i32, ctypes.POINTER(KfCopyProbe)]
+        L.kf_probe_copy.restype = i32
         L.kf_get_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
         L.kf_get_tuning.restype = i32
         L.kf_set_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
@@ -481,3 +488,11 @@ def probe_mfma(in_dtype: str, iters: int) -> dict:
     _check(lib().kf_probe_mfma(DTYPES[in_dtype], int(iters), ctypes.byref(r)))
     return {"dtype": in_dtype, "tflops": r.tflops, "seconds": r.seconds, "clock_ghz": r.clock_ghz,
             "workgroups": r.workgroups}
+
+
+def probe_copy(nbytes: int, reps: int) -> dict:
+    """kf_probe_copy: a plain device copy of nbytes, GB/s counting read and
+    write."""
+    r = KfCopyProbe()
+    _check(lib().kf_probe_copy(int(nbytes), int(reps), ctypes.byref(r)))
+    return {"gbps": r.gbps, "seconds": r.seconds, "bytes": int(nbytes)}

@@ -206,7 +206,8 @@ def test_struct_offsets_match_c_compiler(tmp_path):
         pytest.skip("no C compiler")
     structs = [("kf_op", kf.KfOp), ("kf_op_spec", kf.KfOpSpec), ("kf_tensor", kf.KfTensor),
                ("kf_diagnosis", kf.KfDiagnosis), ("kf_tuning", kf.KfTuning), ("kf_tune_result", kf.KfTuneResult),
-               ("kf_counters", kf.KfCounters), ("kf_mfma_probe", kf.KfMfmaProbe)]
+               ("kf_counters", kf.KfCounters), ("kf_mfma_probe", kf.KfMfmaProbe),
+               ("kf_copy_probe", kf.KfCopyProbe)]
     lines, want = [], []
     for cname, py in structs:
         for f in py._fields_:
@@ -224,8 +225,9 @@ def test_struct_offsets_match_c_compiler(tmp_path):
 
 
 
-def test_probe_mfma_argument_checks():
-    """The matrix-core probe checks its arguments before touching a device."""
+def test_probe_argument_checks():
+    """The matrix-core and copy probes check their arguments before touching
+    a device."""
     r = kf.KfMfmaProbe()
     lib = kf.lib()
     assert lib.kf_probe_mfma(kf.KF_BF16, 100, None) == kf.KF_ERR_INVALID_ARG
@@ -234,6 +236,13 @@ def test_probe_mfma_argument_checks():
     assert lib.kf_probe_mfma(kf.KF_FP8_E4M3, (1 << 24) + 1, ctypes.byref(r)) == kf.KF_ERR_INVALID_ARG
     if not _gpu_present():
         assert lib.kf_probe_mfma(kf.KF_BF16, 100, ctypes.byref(r)) == kf.KF_ERR_NO_DEVICE
+    c = kf.KfCopyProbe()
+    assert lib.kf_probe_copy(1 << 20, 1, None) == kf.KF_ERR_INVALID_ARG
+    assert lib.kf_probe_copy(1000, 1, ctypes.byref(c)) == kf.KF_ERR_INVALID_ARG      # not a multiple of 16
+    assert lib.kf_probe_copy(1 << 20, 0, ctypes.byref(c)) == kf.KF_ERR_INVALID_ARG
+    assert lib.kf_probe_copy((1 << 34) + 16, 1, ctypes.byref(c)) == kf.KF_ERR_INVALID_ARG
+    if not _gpu_present():
+        assert lib.kf_probe_copy(1 << 20, 1, ctypes.byref(c)) == kf.KF_ERR_NO_DEVICE
 
 
 def test_rowwise_validation():

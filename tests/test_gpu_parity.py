@@ -1245,3 +1245,13 @@ def test_mfma_probe(dt, peak):
     assert r["workgroups"] == torch.cuda.get_device_properties(0).multi_processor_count
     assert r["seconds"] > 0 and 0.5 < r["clock_ghz"] < 2.6
     assert 0.2 * peak < r["tflops"] < 1.02 * peak * r["clock_ghz"] / 2.4
+
+
+def test_copy_probe():
+    """The copy probe moves its bytes: 64 MiB copied at a rate between a
+    tenth of the datasheet HBM bandwidth and the datasheet itself (the
+    64 MiB buffers fit the 256 MB Infinity Cache, hence the loose bound)."""
+    _torch()
+    r = kf.probe_copy(64 << 20, 5)
+    print(f"[gpu] copy probe: {r}", flush=True)
+    assert r["seconds"] > 0 and 800 < r["gbps"] < 2 * 8000
