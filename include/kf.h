@@ -368,7 +368,11 @@ typedef struct kf_tuning {
                            workgroup).  GEMM (bf16 / fp8): 0 (default) =
                            256x256 tiles, one workgroup per CU; 1 = 128x256
                            tiles, two persistent workgroups per CU (B in KN
-                           layout only; raster_group and xcd_remap unused).
+                           layout only; raster_group and xcd_remap unused);
+                           2 = the 256x256 kernel storing a bf16 output
+                           through LDS, each store instruction writing two
+                           whole 512-byte tile rows (variant 0 stores
+                           8-byte pieces from registers; the same bits).
                            Other ops: 0                                      */
 } kf_tuning;
 
@@ -379,7 +383,7 @@ typedef struct kf_tuning {
 kf_status kf_get_tuning(const kf_desc* desc, kf_tuning* out);
 kf_status kf_set_tuning(kf_desc* desc, const kf_tuning* tuning);
 
-#define KF_MAX_TUNE_CANDIDATES 16
+#define KF_MAX_TUNE_CANDIDATES 32
 
 typedef struct kf_tune_result {
   int32_t n;            /* candidates timed                                  */
@@ -404,7 +408,8 @@ typedef struct kf_tune_result {
    until the stream is idle; outputs[0] holds the result of the last call
    (the same bits for every candidate).  Candidates: GEMM (bf16 / fp8) raster
    groups {1, 2, 4, 8, 16, 32, 64} x XCD order {contiguous, hardware} of the
-   256x256 tile, and the 128x256 tile (variant 1) for B in KN layout; CONV3D
+   256x256 tile with each store path (variants 0 and 2), and the 128x256
+   tile (variant 1) for B in KN layout; CONV3D
    workgroups per CU {2, 1} x XCD order; CONV2D_3X3 kernel variant {0, 1};
    every other plan has only its current configuration.  Kept: the fastest,
    except that among the GEMM candidates within 2% of the fastest time the

@@ -72,6 +72,11 @@ struct EpiCtx {
   bool res_lds;                  // the bf16 residual tile sits in LDS (see the kernel's residual staging)
   const unsigned char* res[4];   // LDS: this lane's residual row (lane & 31) of row block bi
   OpTable ops;                   // the op program, one op per lane
+  // LDS staging of a bf16 output row block bi in the residual's rows (res[bi]
+  // is this lane's row there): the first of the 16 rows (16 wn .. 16 wn + 15
+  // of the block, 512 bytes apart) that this wave stores from LDS, or null:
+  // the row block is stored from registers
+  const unsigned char* stg[4];
 };
 
 // run g (0..15) of a row = block bj = g / 4, group gi = g % 4: columns
@@ -231,11 +236,42 @@ __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, 
   }
 }
 
-// Store one row block (16 runs of 4 values per lane).
+// Store one row block (16 runs of 4 values per lane).  A bf16 row block
+// with LDS staging goes through LDS: each lane writes its 16 runs of 8 bytes
+// to its row there (the layout of the residual rows: 16-byte chunk q of row
+// m at q ^ (m & 15); a lane overwrites only the residual chunks it has read
+// itself), then, after a barrier, the two waves that share the 32 rows store
+// 16 rows each, 16 bytes per lane: every store instruction writes two whole
+// 512-byte tile rows, where the direct stores write 16-byte pieces of 32
+// rows.  Every wave of the workgroup must call it for the same row blocks.
 __device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, int bi, const Row& v) {
   const int64_t N = p.N;
   const int64_t rows = c.rows;
   const int64_t rl = row_local(c, bi);
+  if (p.out_bf16 && c.stg[bi] != nullptr) {
+    const int rr = c.lane & 31;
+    unsigned char* own = const_cast<unsigned char*>(c.res[bi]) + (c.lane >> 5) * 8;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      const int q = c.wn * 16 + (g >> 2) * 4 + (g & 3);
+      *reinterpret_cast<u32x2*>(own + ((q ^ (rr & 15)) << 4)) =
+          u32x2{pack_bf16x2(v[g][0], v[g][1]), pack_bf16x2(v[g][2], v[g][3])};
+    }
+    __syncthreads();
+    uint16_t* base = reinterpret_cast<uint16_t*>(p.out) + c.m0 * p.ldo + c.n0;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base, (uint32_t)(((rows - 1) * p.ldo + (N - c.n0)) * 2));
+    const unsigned char* half = c.stg[bi];
+    const int q = c.lane & 31;
+    const bool col_ok = c.n0 + q * 8 < N;
+    const int64_t row0 = c.row_base + bi * 32 + c.wn * 16;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int hr = 2 * i + (c.lane >> 5);  // row within the wave's 16
+      const u32x4 w = *reinterpret_cast<const u32x4*>(half + hr * 512 + ((q ^ ((c.wn * 16 + hr) & 15)) << 4));
+      buf_store16(w, r, col_ok ? (uint32_t)(((row0 + hr) * p.ldo + q * 8) * 2) : kOOB);
+    }
+    return;
+  }
   // Rows past M fall outside the descriptor's range.  Columns past N exist
   // only in the last column tile; in every other tile the 16 runs of a row
   // sit at fixed distances from the first, which become immediate offsets.

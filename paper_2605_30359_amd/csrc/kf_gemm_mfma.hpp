@@ -388,6 +388,14 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   const int rrow = (lane & 31) * 512;
   EpiCtx c{lane, wm, wn, wm * 128, rows_r, m0, n0, sRed, sCol, res_lds,
            {(wm ? sA2 : sA0) + rrow, (wm ? sB2 : sB0) + rrow, (wm ? sA3 : sA1) + rrow, (wm ? sB3 : sB1) + rrow}, ops};
+  // with stage_out, bf16 output row blocks are staged in the same 16 KiB
+  // regions; this wave stores rows 16 wn .. 16 wn + 15 of each
+  if (p.stage_out) {
+    c.stg[0] = (wm ? sA2 : sA0) + wn * 8192;
+    c.stg[1] = (wm ? sB2 : sB0) + wn * 8192;
+    c.stg[2] = (wm ? sA3 : sA1) + wn * 8192;
+    c.stg[3] = (wm ? sB3 : sB1) + wn * 8192;
+  }
   run_epilogue<EPI, CH, FP8, 4>(p, c, acc, rd);
 }
 

@@ -374,6 +374,7 @@ __global__ __launch_bounds__(NT, 2) void kf_gemm_mfma_pp128x256(GemmArgs p) {
     };
     EpiCtx c{le, wm, wn, wm * 64, rows_t, m0, n0, sRed, sCol, res_bf16,
              {resrow(wm * 2), resrow(wm * 2 + 1), nullptr, nullptr}, ops};
+    // (stores straight from registers: c.stg stays null)
     run_epilogue<EPI, CH, FP8, RB>(p, c, acc, rd);
   }
 }

@@ -861,11 +861,13 @@ kf_status kf_set_tuning(kf_desc* d, const kf_tuning* t) {
   if (t->raster_group < 1 || t->raster_group > 64) return fail(KF_ERR_INVALID_ARG, "raster_group must be in [1, 64]");
   if (t->xcd_remap != 0 && t->xcd_remap != 1) return fail(KF_ERR_INVALID_ARG, "xcd_remap must be 0 or 1");
   if (t->wg_per_cu != 1 && t->wg_per_cu != 2) return fail(KF_ERR_INVALID_ARG, "wg_per_cu must be 1 or 2");
-  const bool gemm_kn = (d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) && d->spec.b_layout == KF_LAYOUT_KN;
+  const bool gemm = d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8;
   const int min_variant = d->variant == kVarConvBf16 && !d->conv_special ? 2 : 0;
-  const int max_variant = d->variant == kVarConvBf16 ? 2 : gemm_kn ? 1 : 0;
+  const int max_variant = d->variant == kVarConvBf16 || gemm ? 2 : 0;
   if (t->variant < min_variant || t->variant > max_variant)
     return fail(KF_ERR_INVALID_ARG, "variant must be in [%d, %d] for this plan", min_variant, max_variant);
+  if (gemm && t->variant == 1 && d->spec.b_layout != KF_LAYOUT_KN)
+    return fail(KF_ERR_INVALID_ARG, "variant 1 (128x256 tiles) takes B in KN layout only");
   d->tuning = *t;
   return ok();
 }
@@ -971,8 +973,10 @@ kf_status kf_autotune(kf_desc* d, const kf_tensor* inputs, kf_tensor* outputs, v
   std::vector<kf_tuning> cand;
   const kf_tuning cur = d->tuning;
   if (d->variant == kVarGemmBf16 || d->variant == kVarGemmFp8) {
-    for (int remap = 1; remap >= 0; --remap)
-      for (int g : {1, 2, 4, 8, 16, 32, 64}) cand.push_back(kf_tuning{g, remap, cur.wg_per_cu, 0});
+    // both store paths of the 256x256 kernel over every tile order
+    for (int v : {0, 2})
+      for (int remap = 1; remap >= 0; --remap)
+        for (int g : {1, 2, 4, 8, 16, 32, 64}) cand.push_back(kf_tuning{g, remap, cur.wg_per_cu, v});
     // the second tile shape (its tile order is fixed: raster and XCD fields unused)
     if (d->spec.b_layout == KF_LAYOUT_KN) cand.push_back(kf_tuning{cur.raster_group, cur.xcd_remap, cur.wg_per_cu, 1});
   } else if (d->variant == kVarConv3d) {
@@ -1286,6 +1290,7 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
       a.tlogit = reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + (size_t)std::max<int64_t>(s.M, 1) * d->tiles_n * 8);
     a.raster_group = d->tuning.raster_group;
     a.xcd_remap = d->tuning.xcd_remap;
+    a.stage_out = d->tuning.variant == 2;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
     hipError_t e = hipSuccess;
     if (ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);

@@ -86,6 +86,7 @@ struct GemmArgs {
   float scale;            // dequantisation factor applied to the accumulator
   int32_t raster_group;   // tile rows walked together (column by column) by consecutive tiles
   int32_t xcd_remap;      // 1: each XCD takes a contiguous range of tiles
+  int32_t stage_out;      // 256x256 kernel: 1 = bf16 output row blocks go through LDS (coalesced stores)
 };
 
 // Arguments of the row-wise kernel (no contraction: h = A).

@@ -43,7 +43,7 @@ EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "k
             "kf_probe_copy")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
 HINTS = {1: "reuse", 2: "parallelism", 4: "pipeline", 8: "overlap", 16: "lds_layout"}
-KF_MAX_TUNE_CANDIDATES = 16
+KF_MAX_TUNE_CANDIDATES = 32
 
 
 class KfOp(ctypes.Structure):
