@@ -239,18 +239,20 @@ __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, 
 // Store one row block (16 runs of 4 values per lane).  A bf16 row block
 // with LDS staging goes through LDS: each lane writes its 16 runs of 8 bytes
 // to its row there (the layout of the residual rows: 16-byte chunk q of row
-// m at q ^ (m & 15); a lane overwrites only the residual chunks it has read
-// itself), then, after a barrier, the two waves that share the 32 rows store
-// 16 rows each, 16 bytes per lane: every store instruction writes two whole
-// 512-byte tile rows, where the direct stores write 16-byte pieces of 32
-// rows.  Every wave of the workgroup must call it for the same row blocks.
+// m at q ^ (m & 15), whose two 8-byte halves are swapped in rows 16-31, so
+// that the 32 rows of one write instruction meet 32 distinct 8-byte bank
+// slots; a lane overwrites only residual chunks its own wave has read),
+// then, after a barrier, the two waves that share the 32 rows store 16 rows
+// each, 16 bytes per lane: every store instruction writes two whole 512-byte
+// tile rows, where the direct stores write 16-byte pieces of 32 rows.
+// Every wave of the workgroup must call it for the same row blocks.
 __device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, int bi, const Row& v) {
   const int64_t N = p.N;
   const int64_t rows = c.rows;
   const int64_t rl = row_local(c, bi);
   if (p.out_bf16 && c.stg[bi] != nullptr) {
     const int rr = c.lane & 31;
-    unsigned char* own = const_cast<unsigned char*>(c.res[bi]) + (c.lane >> 5) * 8;
+    unsigned char* own = const_cast<unsigned char*>(c.res[bi]) + (((c.lane >> 5) ^ (rr >> 4)) * 8);
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
       const int q = c.wn * 16 + (g >> 2) * 4 + (g & 3);
@@ -267,7 +269,8 @@ __device__ __forceinline__ void store_row(const GemmArgs& p, const EpiCtx& c, in
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int hr = 2 * i + (c.lane >> 5);  // row within the wave's 16
-      const u32x4 w = *reinterpret_cast<const u32x4*>(half + hr * 512 + ((q ^ ((c.wn * 16 + hr) & 15)) << 4));
+      u32x4 w = *reinterpret_cast<const u32x4*>(half + hr * 512 + ((q ^ ((c.wn * 16 + hr) & 15)) << 4));
+      if (c.wn) w = u32x4{w[2], w[3], w[0], w[1]};  // rows 16-31: halves swapped in LDS
       buf_store16(w, r, col_ok ? (uint32_t)(((row0 + hr) * p.ldo + q * 8) * 2) : kOOB);
     }
     return;
