@@ -25,6 +25,9 @@ gets a block of the same fields under "also".  Per workload:
                input dtype; `traffic` is the HBM bytes per launch from the
                committed rocprofv3 counter summary, or null if the kernel
                source changed since those counters were taken
+  graph        the same step captured once in a HIP graph and replayed K
+               times (median, min, p90 per replay): the step without the
+               host's launch work
   unfused      the same operation as the library's own one-kernel-per-op
                chain, timed the same way; speedup = unfused / fused time
   cpu_baseline the fp64 oracle timed on the host cores over a bounded sample
@@ -320,6 +323,25 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
     ms_per_step = total_ms / K
     # per-step statistics from a second warm loop with step events only
     _, step_ms, _ = _timed_steps(hip, torch, lambda e0, e1: op(ins, out), K, kernel_events=False)
+    # the same step recorded once in a HIP graph and replayed: the launch work
+    # of the host (ctypes call, validation, kernel launches) leaves the loop
+    graph = None
+    if not args.no_graph:
+        try:
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                with torch.cuda.graph(g, stream=side):
+                    op(ins, out)
+            torch.cuda.current_stream().wait_stream(side)
+            g.replay()
+            torch.cuda.synchronize()
+            g_total, g_step, _ = _timed_steps(hip, torch, lambda e0, e1: g.replay(), K, kernel_events=False)
+            graph = {"ms_per_step": round(g_total / K, 5), "step_us": _stats_us(g_step)}
+            del g
+        except Exception as e:  # noqa: BLE001 -- reported, not fatal
+            graph = {"error": str(e)}
     cold = None
     if args.cold_steps > 0:
         flush = torch.ones(COLD_FLUSH_BYTES, dtype=torch.uint8, device="cuda:0")
@@ -386,6 +408,7 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
                         "out_dtype": cfg["out_dtype"]}, **sizes),
         ("pct_hbm_peak" if rowwise else "pct_mfma_peak"): round(100.0 * value / peak, 2),
         "steps_us": {"warm": _stats_us(step_ms), "cold": cold["step_us"] if cold else None},
+        "graph": graph,
         "speedup_vs_unfused": None if not unfused or "speedup" not in unfused else unfused["speedup"],
         "unfused": unfused,
         "roofline": {
@@ -440,7 +463,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
-    ap.add_argument("--no-probe", action="store_true", help="skip the matrix-core rate probe")
+    ap.add_argument("--no-probe", action="store_true", help="skip the measured-ceiling probe")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
     ap.add_argument("--tuning", default=None, metavar="RG,XR,WG[,V]",
                     help="use this launch configuration (raster group, XCD order, workgroups per CU, kernel variant) "
                          "instead of autotuning")

@@ -203,7 +203,10 @@ kf_status kf_create(const kf_op_spec* spec, kf_desc** out);
    descriptor may be in flight at a time (use one descriptor per stream).
    Conv plans repack B into the workspace on the first call and again only
    when B's data pointer changes: after rewriting B's contents in place, call
-   kf_weights_changed first. */
+   kf_weights_changed first.  After one call on the same tensors the call
+   enqueues kernels only (no allocation, memset or synchronisation), so it
+   can be recorded in a HIP graph and replayed (a Conv3d chain that runs
+   partly fused allocates its intermediates on that first call). */
 kf_status kf_fused_op(const kf_desc* desc, const kf_tensor* inputs,
                       kf_tensor* outputs, void* stream);
 
