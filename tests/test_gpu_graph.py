@@ -52,3 +52,46 @@ def test_graph_replay_matches_eager(name, kw):
         check(cfg, t, out, rows=sample_rows(cfg["M"], 6))
     else:
         check(cfg, t, out, images=np.array([0]))
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("C5", dict(M=1024, N=2048, K=512)),          # softmax partials in the static scratch
+    ("C4", dict(batch=2, H=16)),                  # conv weights repacked into the scratch on every call
+])
+def test_graph_replay_of_the_entry_point_that_allocates_nothing(name, kw):
+    """kf_fused_op_noalloc, the entry point for callers under HIP graph
+    capture, recorded once (after a first eager call has looked up the
+    scratch address) and replayed: every replay matches the eager result bit
+    for bit."""
+    import torch
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=62)
+    chain = inputs.chain_for(cfg, t)
+    sizes = kf.sizes_of(cfg)
+    op = kf.FusedOp(chain, **sizes)
+    ins = op.device_inputs(t)
+    ref = op.empty_output("cuda")
+    kf.fused_op_noalloc(chain, ins, ref, **sizes)
+    torch.cuda.synchronize()
+    bits = (lambda x: x.view(torch.int16)) if ref.dtype == torch.bfloat16 else (lambda x: x)
+    out = op.empty_output("cuda")
+    print(f"[gpu] graph noalloc {name} {kw}", flush=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            kf.fused_op_noalloc(chain, ins, out, stream=side, **sizes)
+    torch.cuda.current_stream().wait_stream(side)
+    for rep in range(3):
+        out.fill_(-1.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(bits(ref), bits(out)), (name, rep)
+        kf.fused_op_noalloc(chain, ins, ref, **sizes)   # eager work between replays
+        torch.cuda.synchronize()
+    if cfg["contraction"] == "gemm":
+        check(cfg, t, out, rows=sample_rows(cfg["M"], 6))
+    else:
+        check(cfg, t, out, images=np.array([0]))
