@@ -936,6 +936,10 @@ def test_specialised_chain_matches_interpreted(name, kw):
     ("F6", dict(M=260, N=1040, K=72)),                                    # cross-entropy rows
     ("C3", dict(M=300, N=512, K=72, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
     ("C2", dict(M=600, N=520, K=64, ops=[("bias",), ("sigmoid",), ("row_softmax",)], out_dtype="bf16")),  # interpreted
+    ("F1", dict(M=300, N=520, K=64, out_dtype="f32")),                    # fp32 tile: variant 2 stores from registers
+    ("C5", dict(M=520, N=1040, K=128, b_layout="nk")),                    # B in NK layout: variants 0 and 2 only
+    ("C3", dict(M=260, N=512, K=64, b_layout="nk",
+                ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),  # staged stores over the residual rows
 ])
 def test_tuning_candidates_bit_identical(name, kw):
     """Every launch configuration the tuner may pick computes the same bits:
@@ -950,9 +954,11 @@ def test_tuning_candidates_bit_identical(name, kw):
     ins = op.device_inputs(t)
     ref = op.empty_output("cuda")
     op(ins, ref)
+    kn = cfg.get("b_layout", "kn") == "kn"
     configs = ([(4, r, w, 0) for r in (1, 0) for w in (2, 1)] if name == "F2" else
                [(4, 1, 2, v) for v in (1, 0)] if name == "C4" else
-               [(g, r, 2, v) for v in (0, 2) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)] + [(4, 1, 2, 1)])
+               [(g, r, 2, v) for v in (0, 2) for r in (1, 0) for g in (1, 2, 4, 8, 16, 32, 64)] +
+               ([(4, 1, 2, 1)] if kn else []))
     for g, r, w, v in configs:
         op.set_tuning(g, r, w, v)
         out = op.empty_output("cuda")
