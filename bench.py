@@ -46,6 +46,10 @@ gets a block of the same fields under "also".  Per workload:
                copy (2 x 512 MiB, beyond the Infinity Cache); the roofline
                block carries achieved / that rate as frac_of_probe, and the
                cold kernel median's rate / that rate as frac_of_probe_cold
+  clock_stamps (GEMMs) the shader clock inside the kernel, from its
+               per-workgroup clock stamps (kf_set_clock_stamps) over 20
+               launches, the tile time, and the matrix cores' busy fraction
+               within a tile at that clock
   diagnosis    kf_diagnose_counters on the measured kernel time and the
                committed counters (HBM bytes, matrix-core busy fraction, LDS
                bank conflicts) when they match the kernel source: compute and
@@ -379,6 +383,18 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
             unfused = {"error": str(e)}
 
     probe = None if args.no_probe else _probe("hbm" if rowwise else dt)
+    # the shader clock inside the GEMM kernel, from its per-workgroup clock
+    # stamps, and the matrix cores' busy fraction within a tile at that clock
+    stamps = None
+    if kname == "kf_gemm_mfma_256x256" and not args.no_stamps:
+        tiles = -(-cfg["M"] // 256) * -(-cfg["N"] // 256)
+        stamps = op.clock_stamps(lambda: op(ins, out), tiles)
+        if "error" not in stamps:
+            per_cycle = 2048 if dt == "e4m3" else 1024   # FLOP per clock per SIMD of a 32x32 MFMA stream
+            mfma_cycles = 2.0 * 256 * 256 * cfg["K"] / 4 / per_cycle
+            stamps["mfma_busy_in_tile"] = round(
+                mfma_cycles / (stamps["tile_us_median"] * 1e-6 * stamps["clock_ghz_median"] * 1e9), 4)
+            stamps = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in stamps.items()}
     probe_rate = None if not probe else probe["gbps"] if rowwise else probe["tflops"]
 
     trec = _traffic_record(kname, cfg["workload"])
@@ -434,6 +450,7 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
             "traffic_launch_config": trec.get("launch_config") if trec else None,
         },
         "probe": probe,
+        "clock_stamps": stamps,
         "diagnosis": diagnosis,
         "tuning": tuning,
         "cpu_baseline": cpu,
@@ -465,6 +482,7 @@ def main(argv=None):
     ap.add_argument("--no-autotune", action="store_true", help="keep the default launch configuration")
     ap.add_argument("--no-probe", action="store_true", help="skip the measured-ceiling probe")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--no-stamps", action="store_true", help="skip the GEMM kernel's clock stamps")
     ap.add_argument("--tuning", default=None, metavar="RG,XR,WG[,V]",
                     help="use this launch configuration (raster group, XCD order, workgroups per CU, kernel variant) "
                          "instead of autotuning")

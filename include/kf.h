@@ -225,6 +225,24 @@ kf_status kf_fused_op_timed(const kf_desc* desc, const kf_tensor* inputs,
    pointer is noticed without this.)  NULL is a no-op. */
 void kf_weights_changed(kf_desc* desc);
 
+/* Clock stamps of the bf16 / fp8 GEMM kernel, for the diagnosis (which rests
+   on knowing what the kernel ran at, Methodology, Diagnosis): after this
+   call, every launch of the plan's 256x256 kernel (launch variants 0 and 2)
+   writes, for each workgroup b < `workgroups`, four int64 values to
+   stamps[4b .. 4b+3]: the shader-clock counter at the workgroup's start and
+   end, then the constant-rate counter (kf_wall_clock_hz) at its start and
+   end -- so (c1 - c0) / ((w1 - w0) / rate) is the shader
+   clock the tile ran at, and (w1 - w0) / rate its duration.  Workgroup b
+   computes one 256x256 output tile.  `stamps` is a device buffer of at least
+   4 x workgroups int64, 8-byte aligned, owned by the caller; NULL turns the
+   stamps off.  The 128x256 kernel (variant 1) records none.  Errors:
+   KF_ERR_UNSUPPORTED for other plans, KF_ERR_INVALID_ARG. */
+kf_status kf_set_clock_stamps(kf_desc* desc, void* stamps, int64_t workgroups);
+
+/* The frequency of the constant-rate counter of the current device in Hz
+   (the rate of the stamps' w values), or -1 without a device. */
+int64_t kf_wall_clock_hz(void);
+
 /* The same operation as an unfused chain, one kernel per op, with every
    intermediate stored to device memory in bf16 (fp32 for fp32 chains) --
    the one-operator-per-kernel form that operator fusion removes (Appendix A,

@@ -91,6 +91,9 @@ constexpr int kBStageNK = BN * 64;         // 16 KiB
 
 template <bool FP8, bool B_NK, int EPI, int CH>
 __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
+  // the shader-clock and constant-rate counters at the workgroup's start
+  // (stored with the end values when the caller asked for clock stamps)
+  const long long stamp_c0 = clock64(), stamp_w0 = wall_clock64();
   using C = ElemCfg<FP8>;
   constexpr int ES = C::ES;
   constexpr int kBS = B_NK ? kBStageNK : kBStageKN;
@@ -397,6 +400,16 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
     c.stg[3] = (wm ? sB3 : sB1) + wn * 8192;
   }
   run_epilogue<EPI, CH, FP8, 4>(p, c, acc, rd);
+  if (p.stamps != nullptr && blockIdx.x < p.stamp_cap) {
+    const long long stamp_c1 = clock64(), stamp_w1 = wall_clock64();
+    if (threadIdx.x == 0) {
+      long long* st = p.stamps + 4 * (int64_t)blockIdx.x;
+      st[0] = stamp_c0;
+      st[1] = stamp_c1;
+      st[2] = stamp_w0;
+      st[3] = stamp_w1;
+    }
+  }
 }
 
 // ------------------------------------------------------------ host launch

@@ -107,6 +107,9 @@ struct kf_desc {
   // (nullptr: none yet, or the caller declared the weights changed)
   mutable const void* packed_from = nullptr;
   mutable int packed_kind = 0;  // conv3d: 1 = packed for the tiled kernel, 2 = for the general one
+  // GEMM: the caller's buffer for per-workgroup clock stamps (or null)
+  long long* stamps = nullptr;
+  int64_t stamp_cap = 0;
 };
 
 namespace {
@@ -1150,6 +1153,26 @@ void kf_weights_changed(kf_desc* d) {
   if (d) d->packed_from = nullptr;
 }
 
+int64_t kf_wall_clock_hz(void) {
+  int dev = 0, khz = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return -1;
+  }
+  return (int64_t)khz * 1000;
+}
+
+kf_status kf_set_clock_stamps(kf_desc* d, void* stamps, int64_t workgroups) {
+  if (!d) return fail(KF_ERR_INVALID_ARG, "NULL argument");
+  if (d->variant != kVarGemmBf16 && d->variant != kVarGemmFp8)
+    return fail(KF_ERR_UNSUPPORTED, "clock stamps are recorded by the bf16 / fp8 GEMM kernel only");
+  if (stamps != nullptr && workgroups < 1) return fail(KF_ERR_INVALID_ARG, "workgroups must be >= 1");
+  if (reinterpret_cast<uintptr_t>(stamps) % 8) return fail(KF_ERR_INVALID_ARG, "stamps must be 8-byte aligned");
+  d->stamps = static_cast<long long*>(stamps);
+  d->stamp_cap = stamps ? workgroups : 0;
+  return ok();
+}
+
 kf_status kf_fused_op_noalloc(const kf_op_spec* spec, const kf_tensor* inputs, kf_tensor* outputs, void* stream) {
   if (!spec || !inputs || !outputs) return fail(KF_ERR_INVALID_ARG, "NULL argument");
   kf_desc d;  // the plan lives on the stack: it holds no heap memory
@@ -1291,6 +1314,8 @@ kf_status run_fused(const kf_desc* d, void* ws, bool ws_keeps_weights, const kf_
     a.raster_group = d->tuning.raster_group;
     a.xcd_remap = d->tuning.xcd_remap;
     a.stage_out = d->tuning.variant == 2;
+    a.stamps = d->stamps;
+    a.stamp_cap = d->stamp_cap;
     const bool nk = s.b_layout == KF_LAYOUT_NK;
     hipError_t e = hipSuccess;
     if (ev_before) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_before), hs);

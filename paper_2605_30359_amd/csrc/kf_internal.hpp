@@ -87,6 +87,8 @@ struct GemmArgs {
   int32_t raster_group;   // tile rows walked together (column by column) by consecutive tiles
   int32_t xcd_remap;      // 1: each XCD takes a contiguous range of tiles
   int32_t stage_out;      // 256x256 kernel: 1 = bf16 output row blocks go through LDS (coalesced stores)
+  long long* stamps;      // 256x256 kernel: 4 counters per workgroup (see kf_set_clock_stamps) or null
+  int64_t stamp_cap;      // workgroups stamps has room for
 };
 
 // Arguments of the row-wise kernel (no contraction: h = A).

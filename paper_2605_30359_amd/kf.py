@@ -40,7 +40,7 @@ EXPORTED = ("kf_create", "kf_fused_op", "kf_fused_op_timed", "kf_unfused_op", "k
             "kf_input_info", "kf_output_info", "kf_workspace_bytes", "kf_kernel_name",
             "kf_status_string", "kf_last_error", "kf_classify", "kf_diagnose", "kf_get_tuning", "kf_set_tuning",
             "kf_autotune", "kf_weights_changed", "kf_fused_op_noalloc", "kf_diagnose_counters", "kf_probe_mfma",
-            "kf_probe_copy")
+            "kf_probe_copy", "kf_set_clock_stamps", "kf_wall_clock_hz")
 BOUNDS = {0: "memory", 1: "instruction", 2: "latency"}
 HINTS = {1: "reuse", 2: "parallelism", 4: "pipeline", 8: "overlap", 16: "lds_layout"}
 KF_MAX_TUNE_CANDIDATES = 32
@@ -167,6 +167,10 @@ def lib():
         L.kf_probe_mfma.restype = i32
         L.kf_probe_copy.argtypes = [ctypes.c_int64, i32, ctypes.POINTER(KfCopyProbe)]
         L.kf_probe_copy.restype = i32
+        L.kf_set_clock_stamps.argtypes = [vp, vp, ctypes.c_int64]
+        L.kf_set_clock_stamps.restype = i32
+        L.kf_wall_clock_hz.argtypes = []
+        L.kf_wall_clock_hz.restype = ctypes.c_int64
         L.kf_get_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
         L.kf_get_tuning.restype = i32
         L.kf_set_tuning.argtypes = [vp, ctypes.POINTER(KfTuning)]
@@ -394,6 +398,41 @@ class FusedOp:
 
     def unfused(self, inputs, out=None, stream=None):
         return self._call(lib().kf_unfused_op, inputs, out, stream)
+
+    def set_clock_stamps(self, stamps=None):
+        """kf_set_clock_stamps with a device int64 tensor of 4 x workgroups
+        values (None: off)."""
+        if stamps is None:
+            _check(lib().kf_set_clock_stamps(self._h, None, 0))
+        else:
+            _check(lib().kf_set_clock_stamps(self._h, ctypes.c_void_p(stamps.data_ptr()), stamps.numel() // 4))
+        self._stamps = stamps
+
+    def clock_stamps(self, launch, workgroups: int, calls: int = 20) -> dict:
+        """Run launch() `calls` times with clock stamps on (a fresh device
+        buffer for `workgroups` workgroups), then turn them off; returns the
+        median shader clock (GHz) and tile time (us) over the workgroups of
+        the last call, from kf_set_clock_stamps' counters."""
+        torch = _torch()
+        import numpy as np
+        buf = torch.zeros(4 * workgroups, dtype=torch.int64, device="cuda")
+        self.set_clock_stamps(buf)
+        try:
+            for _ in range(calls):
+                launch()
+            torch.cuda.synchronize()
+        finally:
+            self.set_clock_stamps(None)
+        a = buf.view(workgroups, 4).cpu().numpy()
+        a = a[(a[:, 3] > a[:, 2]) & (a[:, 1] > a[:, 0])]
+        hz = float(lib().kf_wall_clock_hz())
+        if a.size == 0 or hz <= 0:
+            return {"error": "no stamps recorded"}
+        secs = (a[:, 3] - a[:, 2]) / hz
+        ghz = (a[:, 1] - a[:, 0]) / secs * 1e-9
+        return {"workgroups": int(a.shape[0]), "clock_ghz_median": float(np.median(ghz)),
+                "clock_ghz_min": float(ghz.min()), "clock_ghz_max": float(ghz.max()),
+                "tile_us_median": float(np.median(secs) * 1e6)}
 
     def weights_changed(self):
         """kf_weights_changed: B was rewritten in place; the next call repacks it."""

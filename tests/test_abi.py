@@ -245,6 +245,13 @@ def test_probe_argument_checks():
         assert lib.kf_probe_copy(1 << 20, 1, ctypes.byref(c)) == kf.KF_ERR_NO_DEVICE
 
 
+def test_clock_stamp_argument_checks():
+    lib = kf.lib()
+    assert lib.kf_set_clock_stamps(None, None, 0) == kf.KF_ERR_INVALID_ARG
+    if not _gpu_present():
+        assert lib.kf_wall_clock_hz() == -1
+
+
 def test_rowwise_validation():
     base = dict(M=64, N=1024)
     cases = [

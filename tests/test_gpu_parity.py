@@ -1283,3 +1283,44 @@ def test_copy_probe():
     r = kf.probe_copy(64 << 20, 5)
     print(f"[gpu] copy probe: {r}", flush=True)
     assert r["seconds"] > 0 and 800 < r["gbps"] < 2 * 8000
+
+
+@pytest.mark.parametrize("name,kw", [("C2", dict(M=520, N=776, K=256)), ("C5", dict(M=512, N=1024, K=512))])
+def test_gemm_clock_stamps(name, kw):
+    """kf_set_clock_stamps: every workgroup of the 256x256 kernel writes its
+    four counters, the shader clock they give is a clock the device can run
+    at, the tile times add up to no more than the launch, the output bits do
+    not change, and NULL turns the stamps off; other plans refuse them."""
+    torch = _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=63)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    ref = op.empty_output("cuda")
+    op(ins, ref)
+    tiles = -(-cfg["M"] // 256) * -(-cfg["N"] // 256)
+    buf = torch.zeros(4 * tiles + 4, dtype=torch.int64, device="cuda")
+    op.set_clock_stamps(buf)
+    out = op.empty_output("cuda")
+    op(ins, out)
+    torch.cuda.synchronize()
+    bits = (lambda x: x.view(torch.int16)) if ref.dtype == torch.bfloat16 else (lambda x: x)
+    assert torch.equal(bits(ref), bits(out))
+    a = buf.cpu().numpy().reshape(-1, 4)
+    assert np.all(a[:tiles, 1] > a[:tiles, 0]) and np.all(a[:tiles, 3] > a[:tiles, 2])
+    assert np.all(a[tiles:] == 0)           # room for one more workgroup than launched: untouched
+    hz = kf.lib().kf_wall_clock_hz()
+    ghz = (a[:tiles, 1] - a[:tiles, 0]) / ((a[:tiles, 3] - a[:tiles, 2]) / hz) * 1e-9
+    assert 0.3 < np.median(ghz) < 2.6, ghz
+    op.set_clock_stamps(None)
+    buf.zero_()
+    op(ins, out)
+    torch.cuda.synchronize()
+    assert int(buf.abs().sum().item()) == 0
+    st = op.clock_stamps(lambda: op(ins, out), tiles, calls=3)
+    print(f"[gpu] {name} stamps {st}", flush=True)
+    assert st["workgroups"] == tiles and 0.3 < st["clock_ghz_median"] < 2.6
+    rows = kf.FusedOp.from_config(inputs.config("F4", M=64, N=2048))
+    with pytest.raises(kf.KFError) as e:
+        rows.set_clock_stamps(buf)
+    assert e.value.status == kf.KF_ERR_UNSUPPORTED
