@@ -891,6 +891,47 @@ def test_epilogue_operand_paths(name, kw, res_f32):
     print(f"{name} {kw['ops']} err {err:.3e}")
 
 
+@pytest.mark.parametrize("name,kw", [
+    # K-step counts that are multiples of four (the pipeline's four stages
+    # end aligned): nk = 4 fills every stage once, nk = 12 loops
+    ("C3", dict(M=300, N=512, K=128, ops=[("groupnorm", 2, 1e-5), ("swish",), ("residual_add",)])),
+    ("C3", dict(M=300, N=1024, K=384, ops=[("groupnorm", 8, 1e-5), ("swish",), ("residual_add",)])),
+    # interpreted plain epilogue, ragged N (a last column tile of 8 columns)
+    ("C2", dict(M=300, N=520, K=256, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("relu",)])),
+    # residual before the GroupNorm statistics
+    ("C3", dict(M=260, N=512, K=256, ops=[("bias",), ("residual_add",), ("groupnorm", 2, 1e-5), ("swish",)])),
+    # residual feeding a row softmax
+    ("C2", dict(M=77, N=520, K=128, out_dtype="bf16", ops=[("bias",), ("residual_add",), ("row_softmax",)])),
+    # fp8 (64 k per K-step): nk = 4
+    ("C5", dict(M=300, N=528, K=256, ops=[("bias",), ("residual_add",), ("hardtanh", -1.0, 1.0)])),
+    # B in NK layout
+    ("C3", dict(M=100, N=256, K=128, b_layout="nk", ops=[("bias",), ("groupnorm", 1, 1e-5), ("residual_add",)])),
+])
+def test_residual_aligned_k_steps(name, kw):
+    """A bf16 residual with a K-step count that is a multiple of four (no
+    partial pipeline round at the end) gives the oracle's result on ragged
+    tiles, and the same bits under both store paths of the 256x256 tile and
+    with the 128x256 tile."""
+    torch = _torch()
+    cfg = inputs.config(name, dist=_ALL_DIST, residual_dtype="bf16", **kw)
+    t = inputs.generate(cfg, seed=33)
+    op = kf.FusedOp(inputs.chain_for(cfg, t), **kf.sizes_of(cfg))
+    ins = op.device_inputs(t)
+    ref = op.empty_output("cuda")
+    op.set_tuning(4, 1, 2, 0)
+    op(ins, ref)
+    torch.cuda.synchronize()
+    err = check(cfg, t, ref)
+    print(f"{name} {kw['ops']} K={kw['K']} err {err:.3e}")
+    variants = (2, 1) if cfg.get("b_layout", "kn") == "kn" else (2,)
+    for v in variants:
+        op.set_tuning(4, 1, 2, v)
+        out = op.empty_output("cuda")
+        op(ins, out)
+        torch.cuda.synchronize()
+        assert torch.equal(ref.view(torch.int16), out.view(torch.int16)), (name, v)
+
+
 # ------------------------------------- specialised vs interpreted epilogues
 
 @pytest.mark.parametrize("name,kw", [
