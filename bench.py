@@ -48,8 +48,9 @@ gets a block of the same fields under "also".  Per workload:
                cold kernel median's rate / that rate as frac_of_probe_cold
   clock_stamps (GEMMs) the shader clock inside the kernel, from its
                per-workgroup clock stamps (kf_set_clock_stamps) over 20
-               launches, the tile time, and the matrix cores' busy fraction
-               within a tile at that clock
+               launches, the tile time, the shares of prologue, K loop and
+               epilogue in a tile's cycles, and the matrix cores' busy
+               fraction within a tile and within its K loop at that clock
   diagnosis    kf_diagnose_counters on the measured kernel time and the
                committed counters (HBM bytes, matrix-core busy fraction, LDS
                bank conflicts) when they match the kernel source: compute and
@@ -384,16 +385,15 @@ def run_workload(name: str, args, hip, cpu_budget: float) -> dict:
 
     probe = None if args.no_probe else _probe("hbm" if rowwise else dt)
     # the shader clock inside the GEMM kernel, from its per-workgroup clock
-    # stamps, and the matrix cores' busy fraction within a tile at that clock
+    # stamps; the shares of prologue, K loop and epilogue in a tile's cycles;
+    # and the matrix cores' busy fraction within a tile and its K loop
     stamps = None
     if kname == "kf_gemm_mfma_256x256" and not args.no_stamps:
         tiles = -(-cfg["M"] // 256) * -(-cfg["N"] // 256)
-        stamps = op.clock_stamps(lambda: op(ins, out), tiles)
+        per_cycle = 2048 if dt == "e4m3" else 1024   # FLOP per clock per SIMD of a 32x32 MFMA stream
+        mfma_cycles = 2.0 * 256 * 256 * cfg["K"] / 4 / per_cycle
+        stamps = op.clock_stamps(lambda: op(ins, out), tiles, mfma_cycles=mfma_cycles)
         if "error" not in stamps:
-            per_cycle = 2048 if dt == "e4m3" else 1024   # FLOP per clock per SIMD of a 32x32 MFMA stream
-            mfma_cycles = 2.0 * 256 * 256 * cfg["K"] / 4 / per_cycle
-            stamps["mfma_busy_in_tile"] = round(
-                mfma_cycles / (stamps["tile_us_median"] * 1e-6 * stamps["clock_ghz_median"] * 1e9), 4)
             stamps = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in stamps.items()}
     probe_rate = None if not probe else probe["gbps"] if rowwise else probe["tflops"]
 

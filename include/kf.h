@@ -226,15 +226,19 @@ kf_status kf_fused_op_timed(const kf_desc* desc, const kf_tensor* inputs,
 void kf_weights_changed(kf_desc* desc);
 
 /* Clock stamps of the bf16 / fp8 GEMM kernel, for the diagnosis (which rests
-   on knowing what the kernel ran at, Methodology, Diagnosis): after this
-   call, every launch of the plan's 256x256 kernel (launch variants 0 and 2)
-   writes, for each workgroup b < `workgroups`, four int64 values to
-   stamps[4b .. 4b+3]: the shader-clock counter at the workgroup's start and
-   end, then the constant-rate counter (kf_wall_clock_hz) at its start and
-   end -- so (c1 - c0) / ((w1 - w0) / rate) is the shader
-   clock the tile ran at, and (w1 - w0) / rate its duration.  Workgroup b
-   computes one 256x256 output tile.  `stamps` is a device buffer of at least
-   4 x workgroups int64, 8-byte aligned, owned by the caller; NULL turns the
+   on knowing what the kernel ran at and where its time goes, Methodology,
+   Diagnosis): after this call, every launch of the plan's 256x256 kernel
+   (launch variants 0 and 2) writes, for each workgroup b < `workgroups`, six
+   int64 values to stamps[6b .. 6b+5]: c0, c1 = the shader-clock counter at
+   the workgroup's start and end; w0, w1 = the constant-rate counter
+   (kf_wall_clock_hz) at its start and end; cp, ck = the shader-clock counter
+   when the first operand stage has landed (end of the prologue) and when
+   the K loop has ended (its last stage drained, before the epilogue).  So
+   (c1 - c0) / ((w1 - w0) / rate) is the shader clock the tile ran at,
+   (w1 - w0) / rate its duration, and cp - c0, ck - cp, c1 - ck the shader
+   cycles of prologue, K loop and epilogue.  Workgroup b computes one
+   256x256 output tile.  `stamps` is a device buffer of at least
+   6 x workgroups int64, 8-byte aligned, owned by the caller; NULL turns the
    stamps off.  The 128x256 kernel (variant 1) records none.  Errors:
    KF_ERR_UNSUPPORTED for other plans, KF_ERR_INVALID_ARG. */
 kf_status kf_set_clock_stamps(kf_desc* desc, void* stamps, int64_t workgroups);

@@ -92,7 +92,8 @@ constexpr int kBStageNK = BN * 64;         // 16 KiB
 template <bool FP8, bool B_NK, int EPI, int CH>
 __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   // the shader-clock and constant-rate counters at the workgroup's start
-  // (stored with the end values when the caller asked for clock stamps)
+  // (stored with the end values, and the shader clock at the end of the
+  // prologue and of the K loop, when the caller asked for clock stamps)
   const long long stamp_c0 = clock64(), stamp_w0 = wall_clock64();
   using C = ElemCfg<FP8>;
   constexpr int ES = C::ES;
@@ -356,6 +357,7 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   dma(IC<3>{}, 3);
   wait_vmcnt_lgkm0<3 * kDma>();  // stage 0 has landed
   __builtin_amdgcn_s_barrier();
+  const long long stamp_cp = clock64();  // end of the prologue
   read_frags(IC<0>{}, IC<0>{});
 
   int t = 0;
@@ -372,6 +374,7 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   // the epilogue reuses the stage memory
   wait_vmcnt_lgkm0<0>();
   __syncthreads();
+  const long long stamp_ck = clock64();  // end of the K loop
 
   const bool res_lds = res_bf16;
   ResDma<4> rd;
@@ -403,11 +406,13 @@ __global__ __launch_bounds__(NT, 1) void kf_gemm_mfma_256x256(GemmArgs p) {
   if (p.stamps != nullptr && blockIdx.x < p.stamp_cap) {
     const long long stamp_c1 = clock64(), stamp_w1 = wall_clock64();
     if (threadIdx.x == 0) {
-      long long* st = p.stamps + 4 * (int64_t)blockIdx.x;
+      long long* st = p.stamps + 6 * (int64_t)blockIdx.x;
       st[0] = stamp_c0;
       st[1] = stamp_c1;
       st[2] = stamp_w0;
       st[3] = stamp_w1;
+      st[4] = stamp_cp;
+      st[5] = stamp_ck;
     }
   }
 }

@@ -400,22 +400,25 @@ class FusedOp:
         return self._call(lib().kf_unfused_op, inputs, out, stream)
 
     def set_clock_stamps(self, stamps=None):
-        """kf_set_clock_stamps with a device int64 tensor of 4 x workgroups
+        """kf_set_clock_stamps with a device int64 tensor of 6 x workgroups
         values (None: off)."""
         if stamps is None:
             _check(lib().kf_set_clock_stamps(self._h, None, 0))
         else:
-            _check(lib().kf_set_clock_stamps(self._h, ctypes.c_void_p(stamps.data_ptr()), stamps.numel() // 4))
+            _check(lib().kf_set_clock_stamps(self._h, ctypes.c_void_p(stamps.data_ptr()), stamps.numel() // 6))
         self._stamps = stamps
 
-    def clock_stamps(self, launch, workgroups: int, calls: int = 20) -> dict:
+    def clock_stamps(self, launch, workgroups: int, calls: int = 20, mfma_cycles: float = 0.0) -> dict:
         """Run launch() `calls` times with clock stamps on (a fresh device
-        buffer for `workgroups` workgroups), then turn them off; returns the
-        median shader clock (GHz) and tile time (us) over the workgroups of
-        the last call, from kf_set_clock_stamps' counters."""
+        buffer for `workgroups` workgroups), then turn them off; returns, over
+        the workgroups of the last call, the median shader clock (GHz) and
+        tile time (us), and the median shares of prologue, K loop and
+        epilogue in a tile's shader cycles, from kf_set_clock_stamps'
+        counters.  With mfma_cycles (the matrix-core issue cycles of one tile)
+        also the matrix cores' busy share of the tile and of its K loop."""
         torch = _torch()
         import numpy as np
-        buf = torch.zeros(4 * workgroups, dtype=torch.int64, device="cuda")
+        buf = torch.zeros(6 * workgroups, dtype=torch.int64, device="cuda")
         self.set_clock_stamps(buf)
         try:
             for _ in range(calls):
@@ -423,16 +426,26 @@ class FusedOp:
             torch.cuda.synchronize()
         finally:
             self.set_clock_stamps(None)
-        a = buf.view(workgroups, 4).cpu().numpy()
+        a = buf.view(workgroups, 6).cpu().numpy()
         a = a[(a[:, 3] > a[:, 2]) & (a[:, 1] > a[:, 0])]
         hz = float(lib().kf_wall_clock_hz())
         if a.size == 0 or hz <= 0:
             return {"error": "no stamps recorded"}
         secs = (a[:, 3] - a[:, 2]) / hz
         ghz = (a[:, 1] - a[:, 0]) / secs * 1e-9
-        return {"workgroups": int(a.shape[0]), "clock_ghz_median": float(np.median(ghz)),
-                "clock_ghz_min": float(ghz.min()), "clock_ghz_max": float(ghz.max()),
-                "tile_us_median": float(np.median(secs) * 1e6)}
+        cyc = (a[:, 1] - a[:, 0]).astype(np.float64)
+        kloop = (a[:, 5] - a[:, 4]).astype(np.float64)
+        r = {"workgroups": int(a.shape[0]), "clock_ghz_median": float(np.median(ghz)),
+             "clock_ghz_min": float(ghz.min()), "clock_ghz_max": float(ghz.max()),
+             "tile_us_median": float(np.median(secs) * 1e6),
+             "tile_cycles_median": float(np.median(cyc)),
+             "prologue_share": float(np.median((a[:, 4] - a[:, 0]) / cyc)),
+             "k_loop_share": float(np.median(kloop / cyc)),
+             "epilogue_share": float(np.median((a[:, 1] - a[:, 5]) / cyc))}
+        if mfma_cycles > 0:
+            r["mfma_busy_in_tile"] = float(mfma_cycles / np.median(cyc))
+            r["mfma_busy_in_k_loop"] = float(mfma_cycles / np.median(kloop))
+        return r
 
     def weights_changed(self):
         """kf_weights_changed: B was rewritten in place; the next call repacks it."""

@@ -1329,9 +1329,10 @@ def test_copy_probe():
 @pytest.mark.parametrize("name,kw", [("C2", dict(M=520, N=776, K=256)), ("C5", dict(M=512, N=1024, K=512))])
 def test_gemm_clock_stamps(name, kw):
     """kf_set_clock_stamps: every workgroup of the 256x256 kernel writes its
-    four counters, the shader clock they give is a clock the device can run
-    at, the tile times add up to no more than the launch, the output bits do
-    not change, and NULL turns the stamps off; other plans refuse them."""
+    six counters, in order (start, end of the prologue, end of the K loop,
+    end), the shader clock they give is a clock the device can run at, the
+    output bits do not change, and NULL turns the stamps off; other plans
+    refuse them."""
     torch = _torch()
     cfg = inputs.config(name, **kw)
     t = inputs.generate(cfg, seed=63)
@@ -1340,15 +1341,17 @@ def test_gemm_clock_stamps(name, kw):
     ref = op.empty_output("cuda")
     op(ins, ref)
     tiles = -(-cfg["M"] // 256) * -(-cfg["N"] // 256)
-    buf = torch.zeros(4 * tiles + 4, dtype=torch.int64, device="cuda")
+    buf = torch.zeros(6 * tiles + 6, dtype=torch.int64, device="cuda")
     op.set_clock_stamps(buf)
     out = op.empty_output("cuda")
     op(ins, out)
     torch.cuda.synchronize()
     bits = (lambda x: x.view(torch.int16)) if ref.dtype == torch.bfloat16 else (lambda x: x)
     assert torch.equal(bits(ref), bits(out))
-    a = buf.cpu().numpy().reshape(-1, 4)
+    a = buf.cpu().numpy().reshape(-1, 6)
     assert np.all(a[:tiles, 1] > a[:tiles, 0]) and np.all(a[:tiles, 3] > a[:tiles, 2])
+    c0, c1, cp, ck = a[:tiles, 0], a[:tiles, 1], a[:tiles, 4], a[:tiles, 5]
+    assert np.all(c0 < cp) and np.all(cp < ck) and np.all(ck < c1)
     assert np.all(a[tiles:] == 0)           # room for one more workgroup than launched: untouched
     hz = kf.lib().kf_wall_clock_hz()
     ghz = (a[:tiles, 1] - a[:tiles, 0]) / ((a[:tiles, 3] - a[:tiles, 2]) / hz) * 1e-9
@@ -1358,9 +1361,14 @@ def test_gemm_clock_stamps(name, kw):
     op(ins, out)
     torch.cuda.synchronize()
     assert int(buf.abs().sum().item()) == 0
-    st = op.clock_stamps(lambda: op(ins, out), tiles, calls=3)
+    mfma = 2.0 * 256 * 256 * cfg["K"] / 4 / (2048 if cfg["in_dtype"] == "e4m3" else 1024)
+    st = op.clock_stamps(lambda: op(ins, out), tiles, calls=3, mfma_cycles=mfma)
     print(f"[gpu] {name} stamps {st}", flush=True)
     assert st["workgroups"] == tiles and 0.3 < st["clock_ghz_median"] < 2.6
+    shares = st["prologue_share"] + st["k_loop_share"] + st["epilogue_share"]
+    assert 0.9 < shares < 1.1, st
+    # the matrix cores cannot be busy for more cycles than the K loop has
+    assert 0 < st["mfma_busy_in_tile"] < st["mfma_busy_in_k_loop"] <= 1.02, st
     rows = kf.FusedOp.from_config(inputs.config("F4", M=64, N=2048))
     with pytest.raises(kf.KFError) as e:
         rows.set_clock_stamps(buf)
