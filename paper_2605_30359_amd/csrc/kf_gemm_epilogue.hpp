@@ -545,29 +545,32 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     put_row(acc, bi, v);
   });
   row_combine<true>(c, mx, true);
-  // softmax keeps e^(h - max) in the accumulators for the store below
+  // e^(h - max) per row block; softmax stores each row block's values as soon
+  // as they are computed (the store needs the tile max, not the sum), so the
+  // output traffic starts while the next row blocks' exponentials are
+  // computed.  The sum runs over the same values in the same order either way.
   const bool softmax = row_op == KF_OP_ROW_SOFTMAX;
   float se[RB];
-  auto exp_sums = [&](auto KEEP_c) {
-    static_for<0, RB>([&](auto bi_c) {
-      constexpr int bi = decltype(bi_c)::value;
-      const float ml = mx[bi] * kLog2e;
-      float s = 0.0f;
+  static_for<0, RB>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    const float ml = mx[bi] * kLog2e;
+    Row v;
 #pragma unroll
-      for (int q = 0; q < 16; ++q)
+    for (int g = 0; g < 16; ++g) {
+      const f32x16& a = acc[bi][g >> 2];
+      const int o = (g & 3) * 4;
 #pragma unroll
-        for (int bj = 0; bj < 4; ++bj) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(acc_read(acc[bi][bj][q]), kLog2e, -ml));
-          if constexpr (decltype(KEEP_c)::value) acc[bi][bj][q] = e;
-          s += e;
-        }
-      se[bi] = s;
-    });
-  };
-  if (softmax)
-    exp_sums(std::true_type{});
-  else
-    exp_sums(std::false_type{});
+      for (int k = 0; k < 4; ++k) v[g][k] = __builtin_amdgcn_exp2f(fmaf(acc_read(a[o + k]), kLog2e, -ml));
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) s += v[bj * 4 + (q >> 2)][q & 3];  // = e of acc[bi][bj][q]
+    se[bi] = s;
+    // softmax: store e^(h - tile max); the row-finishing kernel rescales it
+    if (softmax) store_row(p, c, bi, v);
+  });
   row_combine<false>(c, se, true);
   if (c.lane < 32 && c.wn == 0) {
     float2* part = reinterpret_cast<float2*>(p.partials);
@@ -578,14 +581,6 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
       if (m < p.M) part[m * p.tiles_n + tn] = make_float2(mx[bi], se[bi]);
     }
   }
-  if (!softmax) return;  // logsumexp, cross-entropy: the finishing kernel writes
-  // softmax: store e^(h - tile max); the row-finishing kernel rescales it
-  static_for<0, RB>([&](auto bi_c) {
-    constexpr int bi = decltype(bi_c)::value;
-    Row v;
-    get_row(acc, bi, v);
-    store_row(p, c, bi, v);
-  });
 }
 
 
