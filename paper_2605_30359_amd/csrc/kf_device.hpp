@@ -132,6 +132,20 @@ __device__ __forceinline__ float f_erf_gelu(float x) {
 }
 // exact GELU: 0.5 x (1 + erf(x / sqrt 2))
 __device__ __forceinline__ float f_gelu_erf(float x) { return 0.5f * x * (1.0f + f_erf_gelu(x * 0.7071067811865476f)); }
+// exact GELU of an input in [-1, 1] (the output of a tanh), by the Maclaurin
+// series of erf: 0.5 x (1 + erf(x / sqrt 2)) = 0.5 x + x^2 sum_n e_n x^(2n),
+// e_n = 0.5 sqrt(2/pi) (-1)^n / (n! (2n+1) 2^n), summed through n = 6.  On
+// [-1, 1] the first omitted term is below 4.2e-8 and the fp32 evaluation is
+// within 1.3e-7 of the exact GELU: closer than the general form above, with
+// no exp and no reciprocal.
+__device__ __forceinline__ float f_gelu_erf_unit(float x) {
+  constexpr float e0 = 0.3989422804014327f, e1 = -0.06649038006690546f, e2 = 0.009973557010035817f,
+                  e3 = -0.0011873282154804545f, e4 = 0.00011543468761615529f, e5 = -9.444656259503615e-06f,
+                  e6 = 6.659693516316651e-07f;
+  const float u = x * x;
+  const float s = fmaf(u, fmaf(u, fmaf(u, fmaf(u, fmaf(u, fmaf(u, e6, e5), e4), e3), e2), e1), e0);
+  return fmaf(u, s, 0.5f * x);
+}
 
 // One element-wise op (kinds that need no tensor and no reduction).
 __device__ __forceinline__ float apply_elementwise(int kind, float p0, float p1, float x) {

@@ -159,6 +159,13 @@ __device__ __forceinline__ void row_combine(const EpiCtx& c, float (&v)[RB], boo
   __syncthreads();
 }
 
+// Epilogue-internal op kind: a GELU_ERF whose input is the output of a TANH
+// (the op before it in the list), so in [-1, 1].
+constexpr int kOpGeluErfUnit = 1000;
+__host__ __device__ constexpr int epi_kind(int kind, int prev) {
+  return kind == KF_OP_GELU_ERF && prev == KF_OP_TANH ? kOpGeluErfUnit : kind;
+}
+
 // One element-wise / tensor-reading op (kind, at position o of the list) on
 // one row block.  With a compile-time kind the switch folds away.
 __device__ __forceinline__ void apply_op(const GemmArgs& p, const EpiCtx& c, int bi, int kind, int o, Row& v) {
@@ -209,6 +216,7 @@ __device__ __forceinline__ void apply_op(const GemmArgs& p, const EpiCtx& c, int
       KF_EW_CASE(KF_OP_RELU, fmaxf(x, 0.0f))
       KF_EW_CASE(KF_OP_GELU_TANH, f_gelu_tanh(x))
       KF_EW_CASE(KF_OP_GELU_ERF, f_gelu_erf(x))
+      KF_EW_CASE(kOpGeluErfUnit, f_gelu_erf_unit(x))
       KF_EW_CASE(KF_OP_SWISH, f_swish(x))
       KF_EW_CASE(KF_OP_SIGMOID, f_sigmoid(x))
       KF_EW_CASE(KF_OP_TANH, f_tanh(x))
@@ -222,16 +230,18 @@ __device__ __forceinline__ void apply_op(const GemmArgs& p, const EpiCtx& c, int
 }
 
 // Ops oi..oe-1 of chain CH on one row block: interpreted (chain 0), or
-// unrolled over the chain's compile-time op kinds.
+// unrolled over the chain's compile-time op kinds.  Either way a GELU_ERF
+// right after a TANH takes the bounded-input form (the same bits).
 template <int CH>
 __device__ __forceinline__ void apply_phase(const GemmArgs& p, const EpiCtx& c, int bi, int oi, int oe, Row& v) {
   if constexpr (CH == 0) {
 #pragma nounroll
-    for (int o = oi; o < oe; ++o) apply_op(p, c, bi, op_kind(c.ops, o), o, v);
+    for (int o = oi; o < oe; ++o) apply_op(p, c, bi, epi_kind(op_kind(c.ops, o), o > 0 ? op_kind(c.ops, o - 1) : 0), o, v);
   } else {
     static_for<0, kChainLen[CH]>([&](auto O_c) {
       constexpr int o = decltype(O_c)::value;
-      if (o >= oi && o < oe) apply_op(p, c, bi, kChainOps[CH][o], o, v);
+      constexpr int kind = epi_kind(kChainOps[CH][o], o > 0 ? kChainOps[CH][o > 0 ? o - 1 : 0] : 0);
+      if (o >= oi && o < oe) apply_op(p, c, bi, kind, o, v);
     });
   }
 }
