@@ -932,6 +932,36 @@ def test_residual_aligned_k_steps(name, kw):
         assert torch.equal(ref.view(torch.int16), out.view(torch.int16)), (name, v)
 
 
+@pytest.mark.parametrize("ops,tol", [
+    ([("tanh",), ("gelu_erf",)], 1e-6),   # input from a tanh: the polynomial form
+    ([("gelu_erf",)], 3e-6),              # general input: the rational erf approximation
+    ([("tanh",), ("relu",), ("gelu_erf",)], 3e-6),  # not right after the tanh: general form
+])
+def test_gelu_erf_accuracy_on_device(ops, tol):
+    """The epilogue's GELU(erf) against the exact function of the device's own
+    fp32 contraction output: the same inputs run once with no ops and once
+    with the ops, and the exact (fp64, math.erf) ops applied to the first
+    output must match the second to `tol` (fp32 rounding of tanh and GELU)."""
+    import math
+    _torch()
+    cfg0 = inputs.config("F1", M=256, N=512, K=64, out_dtype="f32", ops=[])
+    t = inputs.generate(cfg0, seed=71)
+    _, h = run_gpu(cfg0, t)
+    cfg1 = inputs.config("F1", M=256, N=512, K=64, out_dtype="f32", ops=ops)
+    _, y = run_gpu(cfg1, {k: t[k] for k in ("a", "b")})
+    x = to_host_f64(h)
+    for o in ops:
+        if o[0] == "tanh":
+            x = np.tanh(x)
+        elif o[0] == "relu":
+            x = np.maximum(x, 0.0)
+        else:
+            x = 0.5 * x * (1.0 + np.vectorize(math.erf)(x / math.sqrt(2.0)))
+    err = float(np.max(np.abs(to_host_f64(y) - x)))
+    print(f"[gpu] gelu_erf {[o[0] for o in ops]} max |err| {err:.3e} (|h| up to {np.max(np.abs(to_host_f64(h))):.2f})")
+    assert err < tol, err
+
+
 # ------------------------------------- specialised vs interpreted epilogues
 
 @pytest.mark.parametrize("name,kw", [
