@@ -39,6 +39,16 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 template <int RB>
 using AccT = f32x16[RB][4];
 
+// Whether the row reduction of compile-time chain `ch` comes right after a
+// HARDTANH (whose upper bound then serves as the tile's row offset, when
+// its bounds are at most kRowOffsetSpan apart).
+constexpr float kRowOffsetSpan = 64.0f;
+constexpr bool chain_row_after_hardtanh(int ch) {
+  for (int o = 1; o < kChainLen[ch]; ++o)
+    if (is_row_op(kChainOps[ch][o])) return kChainOps[ch][o - 1] == KF_OP_HARDTANH;
+  return false;
+}
+
 // The row softmax / logsumexp op of a compile-time chain (0: none, or chain 0).
 constexpr int chain_row_op(int ch) {
   for (int o = 0; o < kChainLen[ch]; ++o)
@@ -505,16 +515,28 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
     return;
   }
 
-  // kEpiRow: tile-row max, then the sum of e^(h - max); the (max, sum) pair of
-  // this 256-column tile goes to the partials buffer.
+  // kEpiRow: the tile's row offset mu (normally the tile-row max), then the
+  // sum of e^(h - mu); the (mu, sum) pair of this 256-column tile goes to the
+  // partials buffer, and softmax stores e^(h - mu).  Any offset gives the
+  // same softmax and logsumexp after the finishing kernel (it rescales by
+  // e^(mu_t - max_t mu_t) / S); the max only keeps e^(h - mu) from
+  // overflowing.  When the op right before the row op is a HARDTANH with
+  // bounds (lo, hi), hi - lo <= 64, every h is at most hi and e^(h - hi) is at
+  // least e^-64: hi is a safe offset, and the tile takes one pass over its
+  // accumulators with no max and no cross-wave max exchange.
   const int row_op = chain_row_op(CH) ? chain_row_op(CH) : op_kind(c.ops, r);
   const bool ce = row_op == KF_OP_ROW_CROSS_ENTROPY;
+  const bool softmax = row_op == KF_OP_ROW_SOFTMAX;
   rd.template issue<0, kRes>();
   res_wait(c);
-  float mx[RB];
-  static_for<0, RB>([&](auto bi_c) {
+  // (a compiled chain with that shape is only planned when the bounds
+  // qualify, so there the choice is made at compile time)
+  const bool bounded = chain_row_after_hardtanh(CH) ||
+                       (CH == 0 && r > 0 && op_kind(c.ops, r - 1) == KF_OP_HARDTANH &&
+                        op_p1(c.ops, r - 1) - op_p0(c.ops, r - 1) <= kRowOffsetSpan);
+  // the ops before the row op on one row block; columns past N become -inf
+  auto prep = [&](auto bi_c, Row& v) {
     constexpr int bi = decltype(bi_c)::value;
-    Row v;
     get_row(acc, bi, v);
 #pragma unroll
     for (int g = 0; g < 16; ++g) v[g] *= FP8 ? p.scale : 1.0f;  // the bf16 path skips the multiply
@@ -548,38 +570,51 @@ __device__ __forceinline__ void run_epilogue(const GemmArgs& p, const EpiCtx& c,
         for (int q = 0; q < 4; ++q) v[g][q] = (n + q < N) ? v[g][q] : -INFINITY;
       }
     }
-    float m = -INFINITY;
-#pragma unroll
-    for (int g = 0; g < 16; ++g) m = fmaxf(m, max4(v[g]));
-    mx[bi] = m;
-    put_row(acc, bi, v);
-  });
-  row_combine<true>(c, mx, true);
-  // e^(h - max) per row block; softmax stores each row block's values as soon
-  // as they are computed (the store needs the tile max, not the sum), so the
-  // output traffic starts while the next row blocks' exponentials are
-  // computed.  The sum runs over the same values in the same order either way.
-  const bool softmax = row_op == KF_OP_ROW_SOFTMAX;
-  float se[RB];
-  static_for<0, RB>([&](auto bi_c) {
+  };
+  // e^(h - mu) of one row block in place and its sum (in the order of the
+  // accumulators: block bj, element q); softmax stores the values as soon as
+  // they are computed (the store needs mu, not the sum), so the output
+  // traffic overlaps the remaining row blocks' work.
+  auto exp_store = [&](auto bi_c, Row& v, float mu) {
     constexpr int bi = decltype(bi_c)::value;
-    const float ml = mx[bi] * kLog2e;
-    Row v;
+    const float ml = mu * kLog2e;
 #pragma unroll
-    for (int g = 0; g < 16; ++g) {
-      const f32x16& a = acc[bi][g >> 2];
-      const int o = (g & 3) * 4;
+    for (int g = 0; g < 16; ++g)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) v[g][k] = __builtin_amdgcn_exp2f(fmaf(acc_read(a[o + k]), kLog2e, -ml));
-    }
+      for (int k = 0; k < 4; ++k) v[g][k] = __builtin_amdgcn_exp2f(fmaf(v[g][k], kLog2e, -ml));
     float s = 0.0f;
 #pragma unroll
     for (int q = 0; q < 16; ++q)
 #pragma unroll
-      for (int bj = 0; bj < 4; ++bj) s += v[bj * 4 + (q >> 2)][q & 3];  // = e of acc[bi][bj][q]
-    se[bi] = s;
-    // softmax: store e^(h - tile max); the row-finishing kernel rescales it
+      for (int bj = 0; bj < 4; ++bj) s += v[bj * 4 + (q >> 2)][q & 3];
     if (softmax) store_row(p, c, bi, v);
+    return s;
+  };
+  float mx[RB], se[RB];
+  const float hi = bounded ? op_p1(c.ops, r - 1) : 0.0f;
+  if (!bounded) {
+    static_for<0, RB>([&](auto bi_c) {
+      constexpr int bi = decltype(bi_c)::value;
+      Row v;
+      prep(bi_c, v);
+      float m = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < 16; ++g) m = fmaxf(m, max4(v[g]));
+      mx[bi] = m;
+      put_row(acc, bi, v);
+    });
+    row_combine<true>(c, mx, true);
+  }
+  static_for<0, RB>([&](auto bi_c) {
+    constexpr int bi = decltype(bi_c)::value;
+    Row v;
+    if (bounded) {
+      prep(bi_c, v);
+      mx[bi] = hi;
+    } else {
+      get_row(acc, bi, v);
+    }
+    se[bi] = exp_store(bi_c, v, mx[bi]);
   });
   row_combine<false>(c, se, true);
   if (c.lane < 32 && c.wn == 0) {

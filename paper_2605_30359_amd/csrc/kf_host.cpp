@@ -115,14 +115,23 @@ struct kf_desc {
 namespace {
 
 // The compile-time chain whose op kinds equal the spec's and which belongs to
-// the spec's contraction (chain 1, no ops, to every one), else 0.
+// the spec's contraction (chain 1, no ops, to every one), else 0.  A GEMM
+// chain whose row reduction follows a HARDTANH is compiled for that
+// HARDTANH's upper bound as the row offset, valid for bounds at most 64
+// apart; with wider bounds the op runs interpreted.
 int match_chain(const kf_op_spec* s) {
   const int family = s->contraction == KF_CONV2D_3X3 ? 2 : s->contraction == KF_CONV3D_3X3X3 ? 3 : 1;
   for (int ch = 1; ch < kf::kNumChains; ++ch) {
     if ((kf::kChainFamily[ch] != 0 && kf::kChainFamily[ch] != family) || kf::kChainLen[ch] != s->n_ops) continue;
     bool same = true;
     for (int o = 0; o < s->n_ops; ++o) same = same && s->ops[o].kind == kf::kChainOps[ch][o];
-    if (same) return ch;
+    if (!same) continue;
+    if (s->contraction == KF_GEMM)
+      for (int o = 1; o < s->n_ops; ++o)
+        if (kf::is_row_op(s->ops[o].kind) && s->ops[o - 1].kind == KF_OP_HARDTANH &&
+            !(s->ops[o - 1].p1 - s->ops[o - 1].p0 <= 64.0f))
+          return 0;
+    return ch;
   }
   return 0;
 }

@@ -962,6 +962,30 @@ def test_gelu_erf_accuracy_on_device(ops, tol):
     assert err < tol, err
 
 
+@pytest.mark.parametrize("name,kw", [
+    # a row reduction right after a HARDTANH with bounds at most 64 apart takes
+    # the upper bound as the row offset (one pass, no max exchange)
+    ("C5", dict(M=300, N=1040, K=128, ops=[("bias",), ("hardtanh", -30.0, 30.0), ("row_softmax",)])),
+    ("C5", dict(M=300, N=1040, K=128, ops=[("bias",), ("hardtanh", -0.25, 0.5), ("row_softmax",)])),
+    # wider bounds: planned on the interpreted epilogue with the tile-row max
+    ("C5", dict(M=300, N=1040, K=128, ops=[("bias",), ("hardtanh", -100.0, 100.0), ("row_softmax",)])),
+    # interpreted chains with the bounded offset
+    ("C5", dict(M=300, N=1040, K=128, ops=[("bias",), ("scale", 4.0), ("hardtanh", -2.0, 2.0), ("row_softmax",)])),
+    ("C2", dict(M=200, N=1040, K=96, ops=[("bias",), ("hardtanh", -4.0, 4.0), ("row_logsumexp",)])),
+    ("F6", dict(M=200, N=1040, K=96, ops=[("bias",), ("hardtanh", -3.0, 3.0), ("row_cross_entropy",)])),
+])
+def test_row_reduction_after_hardtanh(name, kw):
+    """Row softmax / logsumexp / cross-entropy after a HARDTANH, with bounds
+    narrow enough for the one-pass offset and too wide for it, compiled and
+    interpreted, ragged N: the oracle's result."""
+    _torch()
+    cfg = inputs.config(name, **kw)
+    t = inputs.generate(cfg, seed=77)
+    _, out = run_gpu(cfg, t)
+    err = check(cfg, t, out)
+    print(f"[gpu] {name} {kw['ops']} err {err:.3e}")
+
+
 # ------------------------------------- specialised vs interpreted epilogues
 
 @pytest.mark.parametrize("name,kw", [
